@@ -1,0 +1,230 @@
+"""Seeded synthetic inputs for the Polestar layer step.
+
+This module only draws random numbers and stores them in the run dtype; it
+holds none of the method's arithmetic, so the HIP path and the CPU oracle can
+both be fed from it.  Every array is generated on the host in float32 with
+`numpy.random.default_rng(seed)` and rounded once to the run dtype (round to
+nearest, ties to even).  bf16 arrays are returned as their uint16 bit
+patterns, fp32 arrays as float32.
+
+Seeds: seed = 1000 * config + 10 * subrun + stream, with streams
+  0 weights, 1 base hidden states, 2 drift noise, 3 planted (heavy) set,
+  4 logits, 5 drift history, 6 logit spikes.
+Weights and base hidden states depend on the configuration only.
+
+The workloads follow the shapes of LLaDA-8B (d=4096, 32 MHA heads of 128,
+vocab 126464) and Dream-7B (d=3584, 28 query / 4 KV heads of 128, vocab
+152064) and the decoding structure of the paper: a prompt followed by the
+generated region, the active block of B positions right after the prompt.
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+
+@dataclass(frozen=True)
+class LayerConfig:
+    """Shape and noise recipe of one synthetic single-layer workload."""
+    index: int
+    name: str
+    dtype: str            # "fp32" or "bf16"
+    batch: int
+    d: int
+    n_heads: int
+    n_kv_heads: int
+    head_dim: int
+    prompt_len: int
+    seq: int
+    block_len: int
+    vocab: int
+    logit_std: float
+    heavy_fracs: tuple    # heavy fraction of each sub-run (or chained step)
+    chained: bool = False     # sub-runs are consecutive steps of one run
+    clustered: bool = False   # heavy positions in contiguous runs
+    weight_std: float = 0.02
+    light_std: float = 0.01
+    heavy_std: float = 0.5
+    hist_depth: int = 5
+    tau_s: float = 0.9
+    alpha: float = 10.0
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def block_start(self) -> int:
+        return self.prompt_len
+
+    @property
+    def cached_positions(self) -> int:
+        return self.seq - self.block_len
+
+    def tokens_per_step(self) -> int:
+        return self.batch * self.block_len
+
+
+CONFIGS = {
+    0: LayerConfig(0, "tiny-fp32", "fp32", batch=1, d=256, n_heads=4, n_kv_heads=4,
+                   head_dim=64, prompt_len=64, seq=96, block_len=32, vocab=1024,
+                   logit_std=3.0, heavy_fracs=(0.10,)),
+    1: LayerConfig(1, "llada8b-layer-b1-s768", "bf16", batch=1, d=4096, n_heads=32,
+                   n_kv_heads=32, head_dim=128, prompt_len=512, seq=768, block_len=32,
+                   vocab=126464, logit_std=4.0, heavy_fracs=(0.05, 0.15, 0.25)),
+    2: LayerConfig(2, "llada8b-layer-b8-s1536", "bf16", batch=8, d=4096, n_heads=32,
+                   n_kv_heads=32, head_dim=128, prompt_len=1024, seq=1536, block_len=32,
+                   vocab=126464, logit_std=4.0, heavy_fracs=(0.02, 0.10, 0.30),
+                   chained=True),
+    3: LayerConfig(3, "dream7b-gqa-layer-b4-s2048", "bf16", batch=4, d=3584, n_heads=28,
+                   n_kv_heads=4, head_dim=128, prompt_len=1536, seq=2048, block_len=64,
+                   vocab=152064, logit_std=4.0, heavy_fracs=(0.10,), clustered=True),
+}
+
+
+def seed_of(config: int, subrun: int, stream: int) -> int:
+    return 1000 * config + 10 * subrun + stream
+
+
+def rng(config: int, subrun: int, stream: int) -> np.random.Generator:
+    return np.random.default_rng(seed_of(config, subrun, stream))
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bit patterns, round to nearest, ties to even."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    bias = 0x7FFF + ((u >> 16) & 1)
+    return ((u + bias) >> 16).astype(np.uint16)
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def store(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Round a float32 array to the run dtype: uint16 bits for bf16."""
+    if dtype == "fp32":
+        return np.ascontiguousarray(x, dtype=np.float32)
+    if dtype == "bf16":
+        return f32_to_bf16_bits(x)
+    raise ValueError(dtype)
+
+
+def load_f32(x: np.ndarray, dtype: str) -> np.ndarray:
+    """The float32 values of a stored array (exact for both dtypes)."""
+    return bf16_bits_to_f32(x) if dtype == "bf16" else np.asarray(x, dtype=np.float32)
+
+
+def normal(g: np.random.Generator, shape, std: float) -> np.ndarray:
+    return g.standard_normal(size=shape, dtype=np.float32) * np.float32(std)
+
+
+def planted_uniform(cfg: LayerConfig, subrun: int, frac: float) -> np.ndarray:
+    """[batch][seq] bool: round(frac*seq) positions per sequence, uniform."""
+    g = rng(cfg.index, subrun, 3)
+    n = int(round(frac * cfg.seq))
+    out = np.zeros((cfg.batch, cfg.seq), dtype=bool)
+    for b in range(cfg.batch):
+        out[b, g.choice(cfg.seq, size=n, replace=False)] = True
+    return out
+
+
+def planted_runs(cfg: LayerConfig, subrun: int, frac: float) -> np.ndarray:
+    """[batch][seq] bool: non-overlapping contiguous runs of length U{8..64}
+    placed uniformly among cached positions until they cover
+    ceil(frac * cached) positions (the last run is truncated)."""
+    g = rng(cfg.index, subrun, 3)
+    bs, bl = cfg.block_start, cfg.block_len
+    target = int(math.ceil(frac * cfg.cached_positions))
+    out = np.zeros((cfg.batch, cfg.seq), dtype=bool)
+    for b in range(cfg.batch):
+        covered = 0
+        while covered < target:
+            length = int(g.integers(8, 65))
+            start = int(g.integers(0, cfg.seq - length + 1))
+            span = np.arange(start, start + length)
+            if np.any((span >= bs) & (span < bs + bl)) or out[b, span].any():
+                continue
+            # keep a gap of one position so that runs stay separate
+            lo, hi = max(0, start - 1), min(cfg.seq, start + length + 1)
+            if out[b, lo:hi].any():
+                continue
+            take = min(length, target - covered)
+            out[b, start:start + take] = True
+            covered += take
+    return out
+
+
+def weights(cfg: LayerConfig) -> dict:
+    """W_q [H*hd][d], W_k and W_v [Hkv*hd][d], N(0, weight_std)."""
+    g = rng(cfg.index, 0, 0)
+    qd = cfg.n_heads * cfg.head_dim
+    kvd = cfg.n_kv_heads * cfg.head_dim
+    w_q = normal(g, (qd, cfg.d), cfg.weight_std)
+    w_k = normal(g, (kvd, cfg.d), cfg.weight_std)
+    w_v = normal(g, (kvd, cfg.d), cfg.weight_std)
+    return {k: store(v, cfg.dtype) for k, v in (("w_q", w_q), ("w_k", w_k), ("w_v", w_v))}
+
+
+def base_states(cfg: LayerConfig) -> np.ndarray:
+    """h_prev of the first step: [batch][seq][d], N(0, 1)."""
+    g = rng(cfg.index, 0, 1)
+    return store(normal(g, (cfg.batch, cfg.seq, cfg.d), 1.0), cfg.dtype)
+
+
+def perturb(cfg: LayerConfig, h_prev: np.ndarray, subrun: int, planted: np.ndarray) -> np.ndarray:
+    """h_cur = h_prev + N(0, light) everywhere + N(0, heavy) on planted rows."""
+    g = rng(cfg.index, subrun, 2)
+    base = load_f32(h_prev, cfg.dtype)
+    light = normal(g, base.shape, cfg.light_std)
+    heavy = normal(g, base.shape, cfg.heavy_std) * planted[:, :, None].astype(np.float32)
+    return store(base + light + heavy, cfg.dtype)
+
+
+def logits(cfg: LayerConfig, subrun: int) -> np.ndarray:
+    g = rng(cfg.index, subrun, 4)
+    return store(normal(g, (cfg.batch, cfg.block_len, cfg.vocab), cfg.logit_std), cfg.dtype)
+
+
+def history(cfg: LayerConfig, subrun: int, light_kl: float = 5e-5) -> np.ndarray:
+    """Drift history [batch][h][block_len] fp32: positive values around the
+    drift that light noise gives (KL ~ light_std**2 / 2), spread 10%."""
+    g = rng(cfg.index, subrun, 5)
+    x = light_kl * (1.0 + 0.1 * g.standard_normal(
+        size=(cfg.batch, cfg.hist_depth, cfg.block_len), dtype=np.float32))
+    return np.abs(x).astype(np.float32)
+
+
+def spike_rows(cfg: LayerConfig, subrun: int, fraction: float = 0.25) -> np.ndarray:
+    """[batch][block_len] bool: which tokens receive a logit spike."""
+    g = rng(cfg.index, subrun, 6)
+    n = max(1, int(round(fraction * cfg.block_len)))
+    out = np.zeros((cfg.batch, cfg.block_len), dtype=bool)
+    for b in range(cfg.batch):
+        out[b, g.choice(cfg.block_len, size=n, replace=False)] = True
+    return out
+
+
+def layer_inputs(cfg: LayerConfig, subrun: int = 0) -> dict:
+    """All inputs of one step of a single-layer workload.
+
+    For a chained configuration, sub-run s is step s: its h_prev is the h_cur
+    of step s-1 (step 0 starts from the base states)."""
+    h_prev = base_states(cfg)
+    steps = range(subrun + 1) if cfg.chained else [subrun]
+    for s in steps:
+        frac = cfg.heavy_fracs[s]
+        planted = (planted_runs if cfg.clustered else planted_uniform)(cfg, s, frac)
+        h_cur = perturb(cfg, h_prev, s, planted)
+        if s != steps[-1]:
+            h_prev = h_cur
+    bs, bl = cfg.block_start, cfg.block_len
+    cached = np.ones(cfg.seq, dtype=bool)
+    cached[bs:bs + bl] = False
+    k = int((planted & cached[None, :]).sum(axis=1).max())
+    out = dict(h_prev=h_prev, h_cur=h_cur, planted=planted, k=k,
+               logits=logits(cfg, subrun), hist=history(cfg, subrun),
+               hist_len=np.full(cfg.batch, cfg.hist_depth, dtype=np.int32),
+               masked=np.ones((cfg.batch, cfg.block_len), dtype=np.uint8))
+    out.update(weights(cfg))
+    return out
