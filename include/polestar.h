@@ -1,0 +1,224 @@
+/*
+ * polestar.h -- C ABI of the MI355X (gfx950) hot path of Polestar's cached
+ * denoising step (arxiv 2607.14107): drift -> select -> sparse K/V refresh ->
+ * bidirectional attention -> Polestar-Commit, for one layer of a masked
+ * diffusion LLM.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All array arguments are DEVICE pointers (HIP device memory of the
+ *    current device); scalars are passed by value.  The caller owns every
+ *    buffer.  The library allocates nothing and keeps no mutable global
+ *    state; calls are reentrant.
+ *  - Arrays are dense and row-major in the index order written next to them,
+ *    e.g. [batch][seq][d] means element (b, i, c) is at ((b*seq)+i)*d + c.
+ *  - `dtype` selects the element type of the hidden states, weights, caches,
+ *    Q/out buffers and logits: POLESTAR_FP32 (float) or POLESTAR_BF16
+ *    (bfloat16 stored as uint16 bit patterns).  Reductions and softmax
+ *    arithmetic are fp32; results stored in bf16 are rounded to nearest even.
+ *  - Every call validates its arguments on the host first and returns
+ *    POLESTAR_ERR_INVALID_ARGUMENT (nothing enqueued) for a NULL required
+ *    pointer, a negative or zero size where a positive one is required, or
+ *    inconsistent sizes; POLESTAR_ERR_UNSUPPORTED for shapes or alignments the
+ *    kernels do not handle (all array pointers must be 16-byte aligned; bf16
+ *    rows of d elements need d % 8 == 0, fp32 rows d % 4 == 0;
+ *    head_dim must be 64 or 128).  It then enqueues its kernels on `stream`
+ *    and returns without synchronising.  POLESTAR_ERR_LAUNCH reports a failed
+ *    launch.  Faults inside kernels surface at the caller's next
+ *    synchronisation.
+ *  - Entry points with a `workspace` take caller-provided device scratch of
+ *    at least the size returned by the matching *_workspace_size function
+ *    for the same shape (POLESTAR_ERR_WORKSPACE if smaller).  Its contents
+ *    need no initialisation and are garbage after the call; two calls in
+ *    flight at once need two workspaces.
+ */
+#ifndef POLESTAR_H
+#define POLESTAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    POLESTAR_OK = 0,
+    POLESTAR_ERR_INVALID_ARGUMENT = 1,
+    POLESTAR_ERR_UNSUPPORTED = 2,
+    POLESTAR_ERR_LAUNCH = 3,
+    POLESTAR_ERR_WORKSPACE = 4
+} polestar_status;
+
+typedef enum { POLESTAR_FP32 = 0, POLESTAR_BF16 = 1 } polestar_dtype;
+
+/* Version of this ABI: major*10000 + minor*100 + patch. */
+int polestar_version(void);
+
+/* Static, human-readable name of a status code. */
+const char* polestar_status_string(polestar_status s);
+
+/*
+ * polestar_drift -- token representation drift (Sec. 3, eq. "drift").
+ *
+ * The paper measures a token's drift as KL(current || previous) of its
+ * distribution at two consecutive denoising steps.  Here the distribution of
+ * token (b, i) is the softmax of its layer-input hidden state over the d
+ * channels, so, in nats,
+ *     drift[b][i] = KL( softmax(h_cur[b][i][:]) || softmax(h_prev[b][i][:]) ).
+ * It is evaluated in fp32 in the form
+ *     sum_c p_c*dlt_c - log1p( sum_c q_c*expm1(dlt_c) ),  dlt = h_cur - h_prev,
+ * which is exactly 0 for identical rows.  Tiny negative results of rounding
+ * are returned as they are.
+ *
+ *   h_cur, h_prev : [batch][seq][d] dtype   current / cached hidden states
+ *   drift         : [batch][seq] float      output
+ * Requires batch, seq, d > 0.
+ */
+polestar_status polestar_drift(polestar_dtype dtype, int batch, int seq, int d,
+                               const void* h_cur, const void* h_prev, float* drift,
+                               hipStream_t stream);
+
+/*
+ * polestar_select -- stale-position selection (Alg. 1, TopK of the drift).
+ *
+ * Candidates of sequence b are the cached positions I = J \ J_b (Sec. 2,
+ * block-wise KV caching: positions outside the active block
+ * [block_start, block_start + block_len)) for which eligible[b][i] != 0
+ * (eligible == NULL: every cached position).  The k candidates with the
+ * largest drift are chosen; equal drift values (+0.0 and -0.0 are equal)
+ * rank the lower position first.  The chosen positions are written in
+ * ascending order.
+ *
+ *   drift       : [batch][seq] float (NaN is outside the contract)
+ *   eligible    : [batch][seq] uint8 or NULL
+ *   k           : per-sequence budget, 0 <= k <= seq
+ *   stale_idx   : [batch][k] int32 output, ascending, padded with -1
+ *   stale_count : [batch] int32 output, min(k, number of candidates)
+ * Requires batch, seq > 0, 0 <= block_start, block_len >= 0,
+ * block_start + block_len <= seq; stale_idx may be NULL only when k == 0.
+ */
+polestar_status polestar_select(int batch, int seq, const float* drift,
+                                const uint8_t* eligible, int block_start, int block_len,
+                                int k, int32_t* stale_idx, int32_t* stale_count,
+                                hipStream_t stream);
+
+/*
+ * polestar_refresh_kv -- sparse K/V refresh (Sec. 4.1, "Measuring Drift and
+ * Layer-wise KV Updates"; Corollary 1 of App. B).
+ *
+ * For every row r of R_b = {stale_idx[b][0 .. stale_count[b]-1]} U J_b
+ * (the active block is recomputed every step, Sec. 2):
+ *     k_cache[b][r] = W_k h_cur[b][r],   v_cache[b][r] = W_v h_cur[b][r]
+ * with fp32 accumulation, rounded to the cache dtype.  Rows outside R_b
+ * keep their bytes.  A stale index inside J_b is legal (the row is written
+ * twice with the same value).
+ *
+ *   h_cur          : [batch][seq][d] dtype
+ *   stale_idx      : [batch][k_max] int32, entries 0 .. stale_count[b]-1 in
+ *                    [0, seq) (values outside are undefined behaviour)
+ *   stale_count    : [batch] int32, each in [0, k_max]
+ *   w_k, w_v       : [n_kv_heads*head_dim][d] dtype (output x input)
+ *   k_cache, v_cache : [batch][seq][n_kv_heads][head_dim] dtype, in/out
+ *   workspace      : >= polestar_refresh_kv_workspace_size(...) bytes
+ * Requires batch, seq, d, n_kv_heads > 0, k_max >= 0, block_len >= 0,
+ * block_start + block_len <= seq.  stale_idx/stale_count may be NULL only
+ * when k_max == 0.
+ */
+size_t polestar_refresh_kv_workspace_size(polestar_dtype dtype, int batch, int d,
+                                          int n_kv_heads, int head_dim,
+                                          int k_max, int block_len);
+polestar_status polestar_refresh_kv(polestar_dtype dtype, int batch, int seq, int d,
+                                    int n_kv_heads, int head_dim, const void* h_cur,
+                                    const int32_t* stale_idx, const int32_t* stale_count,
+                                    int k_max, int block_start, int block_len,
+                                    const void* w_k, const void* w_v,
+                                    void* k_cache, void* v_cache,
+                                    void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream);
+
+/*
+ * polestar_attend -- bidirectional attention of the active block over the
+ * whole cache (Sec. 2, eq. 3; App. B setup).
+ *
+ * If w_q != NULL the queries are first projected, Q = W_q h_cur[b][J_b],
+ * into q_buf (fp32 accumulation, rounded to dtype); if w_q == NULL, q_buf
+ * already holds Q and h_cur is not read.  Then for every query head h,
+ * with KV head g = h / (n_heads / n_kv_heads) (consecutive query heads share
+ * a KV head):
+ *     l_j = scale * q . k_cache[b][j][g],  a = softmax_j(l),
+ *     out = sum_j a_j v_cache[b][j][g]      over all seq positions j
+ * with no causal or padding mask.  scale <= 0 selects 1/sqrt(head_dim).
+ * lse (optional) receives the natural-log log-sum-exp of the l_j.
+ *
+ *   h_cur   : [batch][seq][d] dtype (read when w_q != NULL)
+ *   w_q     : [n_heads*head_dim][d] dtype or NULL
+ *   q_buf   : [batch][block_len][n_heads][head_dim] dtype (out if w_q, else in)
+ *   k_cache, v_cache : [batch][seq][n_kv_heads][head_dim] dtype
+ *   out     : [batch][block_len][n_heads][head_dim] dtype
+ *   lse     : [batch][n_heads][block_len] float or NULL
+ *   workspace : >= polestar_attend_workspace_size(...) bytes
+ * Requires n_heads % n_kv_heads == 0, block_len > 0,
+ * block_start + block_len <= seq.
+ */
+size_t polestar_attend_workspace_size(polestar_dtype dtype, int batch, int seq, int d,
+                                      int n_heads, int n_kv_heads, int head_dim,
+                                      int block_len);
+polestar_status polestar_attend(polestar_dtype dtype, int batch, int seq, int d,
+                                int n_heads, int n_kv_heads, int head_dim,
+                                int block_start, int block_len,
+                                const void* h_cur, const void* w_q, void* q_buf,
+                                const void* k_cache, const void* v_cache, float scale,
+                                void* out, float* lse,
+                                void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
+/*
+ * polestar_commit -- Polestar-Commit for the current block (Sec. 4.2,
+ * Alg. 1; confidence of Sec. 2 and eq. 1).
+ *
+ * For every block position j of sequence b:
+ *   token[b][j] = argmax over v != mask_token_id of logits[b][j][v]
+ *                 (equal logits: lowest id; mask_token_id < 0: none excluded)
+ *   conf[b][j]  = exp(l_token - m) / sum_v exp(l_v - m), m = max_v l_v
+ *                 (softmax over the whole vocabulary)
+ * and for masked positions (masked[b][j] != 0), in fp32 with this order:
+ *   n     = h > 0 ? hist_len[b] : 0
+ *   mu    = n > 0 ? (((hist[b][0][j] + hist[b][1][j]) + ...) + hist[b][n-1][j]) / n : 0
+ *   D     = dlt_j - mu,  dlt_j = drift[b][block_start + j] (0 if drift == NULL)
+ *   t     = tau_s - conf;  tau_d = (alpha * t) * t
+ *   commit[b][j] = conf > tau_s || D > tau_d
+ * (drift == NULL turns the drift branch off: commit = conf > tau_s).
+ * If force_one != 0 and no masked position of b commits, the masked position
+ * with the largest conf (lowest j on ties) commits.  Unmasked positions never
+ * commit.  Finally, when h > 0 and drift != NULL, dlt is pushed into the
+ * history: entries stay oldest first, at most h are kept
+ * (hist_len[b] = min(n + 1, h)).
+ *
+ *   logits   : [batch][block_len][vocab] dtype
+ *   masked   : [batch][block_len] uint8
+ *   drift    : [batch][seq] float or NULL
+ *   hist     : [batch][h][block_len] float, in/out (may be NULL if h == 0)
+ *   hist_len : [batch] int32, in/out, values in [0, h] (NULL if h == 0)
+ *   token, conf, commit : [batch][block_len] int32 / float / uint8 outputs
+ *   workspace : >= polestar_commit_workspace_size(...) bytes
+ * Requires block_len, vocab > 0, h >= 0, mask_token_id < vocab, and
+ * block_start + block_len <= seq when drift != NULL.
+ */
+size_t polestar_commit_workspace_size(polestar_dtype dtype, int batch, int block_len,
+                                      int vocab);
+polestar_status polestar_commit(polestar_dtype dtype, int batch, int block_len, int vocab,
+                                const void* logits, const uint8_t* masked,
+                                const float* drift, int seq, int block_start,
+                                float* hist, int32_t* hist_len, int h,
+                                int mask_token_id, float tau_s, float alpha, int force_one,
+                                int32_t* token, float* conf, uint8_t* commit,
+                                void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* POLESTAR_H */

@@ -1,0 +1,275 @@
+// polestar_commit: Polestar-Commit for the current block (Sec. 4.2, Alg. 1)
+// on top of the confidence of Sec. 2 / eq. 1.
+//
+// Kernel 1 scans the logits, an HBM-bound stream: workgroup (split, j, b)
+// reduces one slice of the vocabulary of token (b, j) to
+//   (m, s, best value, best id):  m = max_v l_v,  s = sum_v exp(l_v - m),
+//   best = argmax over v != mask id (lowest id on ties)
+// with 16-byte loads, per-lane running values and wavefront shuffles.
+// Kernel 2 (one workgroup per sequence, one thread per block position)
+// merges the slices in order, forms conf = exp(best - m) / s, applies the
+// fp32 commit rule with the operation order of the header (no contraction),
+// the force-one fallback and the history push.
+#include "common.hpp"
+#include "host_common.hpp"
+
+namespace ps {
+namespace {
+
+constexpr int kScanBlock = 256;
+
+struct ScanPart {
+    float m;
+    float s;
+    float best;
+    int idx;
+};
+
+__device__ __forceinline__ void better(float& bv, int& bi, float v, int i) {
+    if (v > bv || (v == bv && i < bi)) {
+        bv = v;
+        bi = i;
+    }
+}
+
+__device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2) {
+    const float mn = fmaxf(m, m2);
+    if (mn == -INFINITY) return;
+    s = s * fast_exp2((m - mn) * kLog2e) + s2 * fast_exp2((m2 - mn) * kLog2e);
+    m = mn;
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(kScanBlock) void scan_kernel(const char* __restrict__ logits, int vocab,
+                                                          int nq, int chunk, int splits, int mask_id,
+                                                          ScanPart* __restrict__ parts) {
+    using T = Elem<BF16>;
+    constexpr int ES = T::kBytes;
+    constexpr int G = 4;   // 16-byte chunks per lane kept in flight
+    __shared__ float sm[4], ss[4], sb[4];
+    __shared__ int si[4];
+    const int split = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const size_t tok = static_cast<size_t>(b) * nq + j;
+    const int v0 = split * chunk;
+    const int v1 = min(vocab, v0 + chunk);
+    const char* row = logits + tok * vocab * ES;
+
+    float m = -INFINITY, s = 0.f, bv = -INFINITY;
+    int bi = 0x7fffffff;
+    // elements [v0, v1) in 16-byte chunks; chunk c starts at element v0 + c*E
+    const int nchunks = (v1 - v0) / T::E;
+    for (int c0 = 0; c0 < nchunks; c0 += kScanBlock * G) {
+        uint4 r[G];
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq) {
+            const int c = c0 + gq * kScanBlock + threadIdx.x;
+            r[gq] = c < nchunks ? ld16(row + static_cast<size_t>(v0 + c * T::E) * ES) : zero16();
+        }
+        float lm = -INFINITY;
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq) {
+            const int c = c0 + gq * kScanBlock + threadIdx.x;
+            if (c >= nchunks) continue;
+            float f[T::E];
+            T::unpack(r[gq], f);
+            const int vb = v0 + c * T::E;
+#pragma unroll
+            for (int e = 0; e < T::E; ++e) {
+                lm = fmaxf(lm, f[e]);
+                if (vb + e != mask_id) better(bv, bi, f[e], vb + e);
+            }
+        }
+        if (lm == -INFINITY) continue;
+        const float mn = fmaxf(m, lm);
+        float ls = 0.f;
+        const float mnl = mn * kLog2e;
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq) {
+            const int c = c0 + gq * kScanBlock + threadIdx.x;
+            if (c >= nchunks) continue;
+            float f[T::E];
+            T::unpack(r[gq], f);
+#pragma unroll
+            for (int e = 0; e < T::E; ++e) ls += fast_exp2(fmaf(f[e], kLog2e, -mnl));
+        }
+        s = (m == -INFINITY ? 0.f : s * fast_exp2((m - mn) * kLog2e)) + ls;
+        m = mn;
+    }
+    // wavefront reduction
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float m2 = __shfl_xor(m, o), s2 = __shfl_xor(s, o);
+        const float b2 = __shfl_xor(bv, o);
+        const int i2 = __shfl_xor(bi, o);
+        merge_ms(m, s, m2, s2);
+        better(bv, bi, b2, i2);
+    }
+    if (lane == 0) {
+        sm[w] = m; ss[w] = s; sb[w] = bv; si[w] = bi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int q = 1; q < 4; ++q) {
+            merge_ms(m, s, sm[q], ss[q]);
+            better(bv, bi, sb[q], si[q]);
+        }
+        parts[tok * splits + split] = ScanPart{m, s, bv, bi};
+    }
+}
+
+// The fp32 rule, written without contraction so that the operation order is
+// the documented one.
+#pragma clang fp contract(off)
+__device__ bool commit_rule(float c, float dlt, bool use_drift, const float* hist_col, int hstride,
+                            int n, float tau_s, float alpha) {
+    if (c > tau_s) return true;
+    if (!use_drift) return false;
+    float mu = 0.f;
+    if (n > 0) {
+        float s = 0.f;
+        for (int r = 0; r < n; ++r) s = s + hist_col[r * hstride];
+        mu = s / static_cast<float>(n);
+    }
+    const float D = dlt - mu;
+    const float t = tau_s - c;
+    const float tau_d = (alpha * t) * t;
+    return D > tau_d;
+}
+#pragma clang fp contract(on)
+
+__global__ __launch_bounds__(1024) void finalize_kernel(const ScanPart* __restrict__ parts, int splits,
+                                                        int nq, const uint8_t* __restrict__ masked,
+                                                        const float* __restrict__ drift, int seq,
+                                                        int block_start, float* hist, int32_t* hist_len,
+                                                        int h, float tau_s, float alpha, int force_one,
+                                                        int32_t* __restrict__ token,
+                                                        float* __restrict__ conf,
+                                                        uint8_t* __restrict__ commit) {
+    __shared__ int any_commit;
+    __shared__ unsigned long long best_key;
+    const int b = blockIdx.x;
+    const int j = threadIdx.x;
+    if (j == 0) {
+        any_commit = 0;
+        best_key = 0ull;
+    }
+    const int n = (h > 0 && hist_len) ? min(max(hist_len[b], 0), h) : 0;
+    __syncthreads();
+    const bool inb = j < nq;
+    const size_t tok = static_cast<size_t>(b) * nq + j;
+    float c = 0.f, dlt = 0.f;
+    bool is_masked = false, cm = false;
+    if (inb) {
+        const ScanPart* p = parts + tok * splits;
+        float m = p[0].m, s = p[0].s, bv = p[0].best;
+        int bi = p[0].idx;
+        for (int q = 1; q < splits; ++q) {
+            merge_ms(m, s, p[q].m, p[q].s);
+            better(bv, bi, p[q].best, p[q].idx);
+        }
+        c = fast_exp2((bv - m) * kLog2e) / s;
+        token[tok] = bi;
+        conf[tok] = c;
+        is_masked = masked[tok] != 0;
+        if (drift) dlt = drift[static_cast<size_t>(b) * seq + block_start + j];
+        const float* hcol = hist ? hist + static_cast<size_t>(b) * h * nq + j : nullptr;
+        cm = is_masked && commit_rule(c, dlt, drift != nullptr, hcol, nq, n, tau_s, alpha);
+        if (cm) atomicOr(&any_commit, 1);
+    }
+    __syncthreads();
+    if (force_one && !any_commit && inb && is_masked) {
+        // largest confidence, then lowest position: key = (conf bits, ~j)
+        const unsigned long long key =
+            (static_cast<unsigned long long>(__float_as_uint(c)) << 32) | (0xffffffffu - j);
+        atomicMax(&best_key, key);
+    }
+    __syncthreads();
+    if (force_one && !any_commit && inb && is_masked && best_key != 0ull &&
+        static_cast<int>(0xffffffffu - static_cast<uint32_t>(best_key & 0xffffffffull)) == j)
+        cm = true;
+    if (inb) commit[tok] = cm ? 1 : 0;
+    // history push (all block positions), entries oldest first
+    if (inb && h > 0 && drift && hist) {
+        float* hcol = hist + static_cast<size_t>(b) * h * nq + j;
+        if (n < h) {
+            hcol[n * nq] = dlt;
+        } else {
+            for (int r = 0; r + 1 < h; ++r) hcol[r * nq] = hcol[(r + 1) * nq];
+            hcol[(h - 1) * nq] = dlt;
+        }
+    }
+    __syncthreads();
+    if (j == 0 && h > 0 && drift && hist_len) hist_len[b] = min(n + 1, h);
+}
+
+struct CommitPlan {
+    int splits;
+    int chunk;
+    size_t ws_bytes;
+};
+
+CommitPlan commit_plan(bool bf16, int batch, int nq, int vocab) {
+    CommitPlan p{};
+    const int e = bf16 ? 8 : 4;
+    const long toks = static_cast<long>(batch) * nq;
+    int splits = static_cast<int>((512 + toks - 1) / toks);
+    const int max_splits = ceil_div(vocab, 2048);
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    p.chunk = ceil_div(ceil_div(vocab, splits), e) * e;
+    p.splits = ceil_div(vocab, p.chunk);
+    p.ws_bytes = static_cast<size_t>(toks) * p.splits * sizeof(ScanPart);
+    return p;
+}
+
+}  // namespace
+}  // namespace ps
+
+extern "C" size_t polestar_commit_workspace_size(polestar_dtype dtype, int batch, int block_len,
+                                                 int vocab) {
+    using namespace ps;
+    if (!dtype_ok(dtype) || batch <= 0 || block_len <= 0 || vocab <= 0) return 0;
+    return commit_plan(dtype == POLESTAR_BF16, batch, block_len, vocab).ws_bytes;
+}
+
+extern "C" polestar_status polestar_commit(polestar_dtype dtype, int batch, int block_len, int vocab,
+                                           const void* logits, const uint8_t* masked,
+                                           const float* drift, int seq, int block_start,
+                                           float* hist, int32_t* hist_len, int h,
+                                           int mask_token_id, float tau_s, float alpha,
+                                           int force_one, int32_t* token, float* conf,
+                                           uint8_t* commit, void* workspace,
+                                           size_t workspace_bytes, hipStream_t stream) {
+    using namespace ps;
+    if (!dtype_ok(dtype) || batch <= 0 || block_len <= 0 || vocab <= 0 || h < 0 || !logits ||
+        !masked || !token || !conf || !commit || mask_token_id >= vocab ||
+        (h > 0 && drift && (!hist || !hist_len)) ||
+        (drift && (seq <= 0 || block_start < 0 || block_start > seq - block_len)))
+        return POLESTAR_ERR_INVALID_ARGUMENT;
+    if (!row_ok(dtype, vocab) || !aligned16(logits) || block_len > 1024 || batch > 65535 ||
+        block_len > 65535)
+        return POLESTAR_ERR_UNSUPPORTED;
+    const bool bf16 = dtype == POLESTAR_BF16;
+    const CommitPlan p = commit_plan(bf16, batch, block_len, vocab);
+    if (workspace_bytes < p.ws_bytes || !workspace) return POLESTAR_ERR_WORKSPACE;
+    ScanPart* parts = static_cast<ScanPart*>(workspace);
+    dim3 grid(p.splits, block_len, batch);
+    if (bf16)
+        hipLaunchKernelGGL((scan_kernel<true>), grid, dim3(kScanBlock), 0, stream,
+                           static_cast<const char*>(logits), vocab, block_len, p.chunk, p.splits,
+                           mask_token_id, parts);
+    else
+        hipLaunchKernelGGL((scan_kernel<false>), grid, dim3(kScanBlock), 0, stream,
+                           static_cast<const char*>(logits), vocab, block_len, p.chunk, p.splits,
+                           mask_token_id, parts);
+    polestar_status st = launch_status();
+    if (st != POLESTAR_OK) return st;
+    const int threads = ceil_div(block_len, 64) * 64;
+    const bool use_hist = h > 0 && drift;
+    hipLaunchKernelGGL(finalize_kernel, dim3(batch), dim3(threads), 0, stream, parts, p.splits,
+                       block_len, masked, drift, seq, block_start, use_hist ? hist : nullptr,
+                       use_hist ? hist_len : nullptr, use_hist ? h : 0, tau_s, alpha, force_one,
+                       token, conf, commit);
+    return launch_status();
+}

@@ -1,0 +1,52 @@
+// Skinny "gather rows -> MFMA GEMM -> scatter rows" used by the K/V refresh
+// (stale rows plus the active block, scattered into the caches) and by the
+// Q projection of the active block (dense output).  Internal to the library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "polestar.h"
+
+namespace ps {
+
+enum GemmMode : int { kGemmRefresh = 0, kGemmBlockRows = 1 };
+
+// Y[m][n] = sum_k X[row(m)][k] * W[n][k], W = w0 for n < n0, else w1 (row n - n0).
+struct GemmArgs {
+    const char* x;        // [batch][seq][K] input rows
+    const char* w0;
+    const char* w1;
+    int n0;
+    int N, K;
+    int mode;
+    int batch, seq;
+    const int32_t* stale_idx;    // refresh mode: [batch][k_max]
+    const int32_t* stale_count;  // refresh mode: [batch]
+    int k_max;
+    int block_start, block_len;
+    char* out0;   // refresh: k_cache (row pitch n0); block rows: [rows][N]
+    char* out1;   // refresh: v_cache (row pitch N - n0)
+    float* ws;    // split-K partials [ksplit][m_max][N]
+    int m_max;
+    int ksplit;
+    int steps_per_split;
+};
+
+struct GemmPlan {
+    int mt;             // 16-row MFMA tiles per workgroup
+    int row_tiles;
+    int col_tiles;
+    int ksplit;
+    int steps_per_split;
+    size_t ws_bytes;    // fp32 partials, 0 when ksplit == 1
+};
+
+GemmPlan gemm_plan(bool bf16, long m_max, int N, int K);
+
+// Enqueue the GEMM (and the split-K reduction when the plan splits K).
+// `g.ws` must hold plan.ws_bytes.  Returns POLESTAR_OK or a launch error.
+polestar_status gemm_run(bool bf16, const GemmPlan& plan, GemmArgs g, hipStream_t stream);
+
+}  // namespace ps

@@ -9,7 +9,7 @@ patterns, fp32 arrays as float32.
 
 Seeds: seed = 1000 * config + 10 * subrun + stream, with streams
   0 weights, 1 base hidden states, 2 drift noise, 3 planted (heavy) set,
-  4 logits, 5 drift history, 6 logit spikes.
+  4 logits, 5 drift history, 6 logit spikes, 7 stand-in K/V cache.
 Weights and base hidden states depend on the configuration only.
 
 The workloads follow the shapes of LLaDA-8B (d=4096, 32 MHA heads of 128,
@@ -228,3 +228,14 @@ def layer_inputs(cfg: LayerConfig, subrun: int = 0) -> dict:
                masked=np.ones((cfg.batch, cfg.block_len), dtype=np.uint8))
     out.update(weights(cfg))
     return out
+
+
+def random_cache(cfg: LayerConfig, subrun: int = 0) -> tuple[np.ndarray, np.ndarray]:
+    """A stand-in prior K/V cache [batch][seq][kv_heads][head_dim] with the
+    spread of a projection of N(0,1) states by N(0, weight_std) weights
+    (std weight_std * sqrt(d)), for workloads where re-projecting every row
+    on the host would take minutes."""
+    g = rng(cfg.index, subrun, 7)
+    shape = (cfg.batch, cfg.seq, cfg.n_kv_heads, cfg.head_dim)
+    std = cfg.weight_std * math.sqrt(cfg.d)
+    return store(normal(g, shape, std), cfg.dtype), store(normal(g, shape, std), cfg.dtype)

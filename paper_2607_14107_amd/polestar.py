@@ -1,0 +1,277 @@
+"""Thin Python binding of libpolestar.so (the C ABI of include/polestar.h).
+
+Argument marshalling only: tensors provide device memory (`data_ptr()`) and
+the current HIP stream; every step of the computation runs in the library's
+HIP kernels.  There is no CPU fallback: if the library is not built, or a
+tensor is not on the GPU, the call raises.
+
+Names follow the C entry points: drift, select, refresh_kv, attend, commit.
+`Step` preallocates the buffers of one layer step and runs the five calls
+back to back on one stream.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libpolestar.so")
+
+OK = 0
+STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "launch failed", 4: "workspace too small"}
+FP32, BF16 = 0, 1
+
+# hyperparameter defaults (table of default hyperparameters, App. D)
+DEFAULT_TAU_S = 0.9
+DEFAULT_ALPHA = 10.0
+DEFAULT_HISTORY = 5
+
+_lib = None
+
+
+class PolestarError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: {STATUS.get(status, status)} (status {status})")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load libpolestar.so once and declare its signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built: run paper_2607_14107_amd.build.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I, F, Z, S = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t, ctypes.c_int
+    L.polestar_version.restype = I
+    L.polestar_version.argtypes = []
+    L.polestar_status_string.restype = ctypes.c_char_p
+    L.polestar_status_string.argtypes = [I]
+    L.polestar_drift.restype = S
+    L.polestar_drift.argtypes = [I, I, I, I, P, P, P, P]
+    L.polestar_select.restype = S
+    L.polestar_select.argtypes = [I, I, P, P, I, I, I, P, P, P]
+    L.polestar_refresh_kv_workspace_size.restype = Z
+    L.polestar_refresh_kv_workspace_size.argtypes = [I, I, I, I, I, I, I]
+    L.polestar_refresh_kv.restype = S
+    L.polestar_refresh_kv.argtypes = [I, I, I, I, I, I, P, P, P, I, I, I, P, P, P, P, P, Z, P]
+    L.polestar_attend_workspace_size.restype = Z
+    L.polestar_attend_workspace_size.argtypes = [I, I, I, I, I, I, I, I]
+    L.polestar_attend.restype = S
+    L.polestar_attend.argtypes = [I, I, I, I, I, I, I, I, I, P, P, P, P, P, F, P, P, P, Z, P]
+    L.polestar_commit_workspace_size.restype = Z
+    L.polestar_commit_workspace_size.argtypes = [I, I, I, I]
+    L.polestar_commit.restype = S
+    L.polestar_commit.argtypes = [I, I, I, I, P, P, P, I, I, P, P, I, I, F, F, I, P, P, P, P, Z, P]
+    _lib = L
+    return L
+
+
+def _check(fn: str, status: int) -> None:
+    if status != OK:
+        raise PolestarError(fn, status)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return FP32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t: torch.Tensor | None, dtype: torch.dtype | None = None) -> int | None:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"expected {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _workspace(nbytes: int, device, ws: torch.Tensor | None) -> torch.Tensor | None:
+    if nbytes == 0:
+        return ws
+    if ws is not None and ws.numel() * ws.element_size() >= nbytes:
+        return ws
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------------------
+# entry points
+# ---------------------------------------------------------------------------
+
+def drift(h_cur: torch.Tensor, h_prev: torch.Tensor, out: torch.Tensor | None = None,
+          stream=None) -> torch.Tensor:
+    """KL(softmax(h_cur[b,i]) || softmax(h_prev[b,i])) -> [batch][seq] float32."""
+    b, s, d = h_cur.shape
+    if h_prev.shape != h_cur.shape or h_prev.dtype != h_cur.dtype:
+        raise ValueError("h_cur and h_prev differ in shape or dtype")
+    if out is None:
+        out = torch.empty((b, s), dtype=torch.float32, device=h_cur.device)
+    _check("polestar_drift", lib().polestar_drift(_dtype_code(h_cur), b, s, d, _ptr(h_cur), _ptr(h_prev),
+                                                 _ptr(out, torch.float32), _stream(stream)))
+    return out
+
+
+def select(drift_vals: torch.Tensor, k: int, block_start: int, block_len: int,
+           eligible: torch.Tensor | None = None, stale_idx: torch.Tensor | None = None,
+           stale_count: torch.Tensor | None = None, stream=None):
+    """TopK of the drift over cached positions -> (stale_idx [batch][k] int32, stale_count [batch])."""
+    b, s = drift_vals.shape
+    dev = drift_vals.device
+    if stale_idx is None:
+        stale_idx = torch.empty((b, max(k, 0)), dtype=torch.int32, device=dev)
+    if stale_count is None:
+        stale_count = torch.empty((b,), dtype=torch.int32, device=dev)
+    _check("polestar_select", lib().polestar_select(
+        b, s, _ptr(drift_vals, torch.float32), _ptr(eligible, torch.uint8), block_start, block_len, k,
+        _ptr(stale_idx, torch.int32) if k > 0 else None, _ptr(stale_count, torch.int32), _stream(stream)))
+    return stale_idx, stale_count
+
+
+def refresh_kv_workspace_size(dtype: int, batch: int, d: int, n_kv_heads: int, head_dim: int,
+                              k_max: int, block_len: int) -> int:
+    return lib().polestar_refresh_kv_workspace_size(dtype, batch, d, n_kv_heads, head_dim, k_max, block_len)
+
+
+def refresh_kv(h_cur: torch.Tensor, stale_idx: torch.Tensor | None, stale_count: torch.Tensor | None,
+               block_start: int, block_len: int, w_k: torch.Tensor, w_v: torch.Tensor,
+               k_cache: torch.Tensor, v_cache: torch.Tensor, workspace: torch.Tensor | None = None,
+               stream=None) -> None:
+    """Re-project rows stale U J_b into k_cache / v_cache in place."""
+    b, s, d = h_cur.shape
+    _, _, kvh, hd = k_cache.shape
+    dt = _dtype_code(h_cur)
+    k_max = 0 if stale_idx is None else stale_idx.shape[1]
+    ws = _workspace(refresh_kv_workspace_size(dt, b, d, kvh, hd, k_max, block_len), h_cur.device, workspace)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("polestar_refresh_kv", lib().polestar_refresh_kv(
+        dt, b, s, d, kvh, hd, _ptr(h_cur),
+        _ptr(stale_idx, torch.int32) if k_max > 0 else None,
+        _ptr(stale_count, torch.int32) if k_max > 0 else None, k_max, block_start, block_len,
+        _ptr(w_k, h_cur.dtype), _ptr(w_v, h_cur.dtype), _ptr(k_cache, h_cur.dtype),
+        _ptr(v_cache, h_cur.dtype), _ptr(ws), nbytes, _stream(stream)))
+
+
+def attend_workspace_size(dtype: int, batch: int, seq: int, d: int, n_heads: int, n_kv_heads: int,
+                          head_dim: int, block_len: int) -> int:
+    return lib().polestar_attend_workspace_size(dtype, batch, seq, d, n_heads, n_kv_heads, head_dim, block_len)
+
+
+def attend(h_cur: torch.Tensor | None, w_q: torch.Tensor | None, k_cache: torch.Tensor,
+           v_cache: torch.Tensor, block_start: int, block_len: int, n_heads: int,
+           q_buf: torch.Tensor | None = None, out: torch.Tensor | None = None,
+           lse: torch.Tensor | None = None, scale: float = 0.0,
+           workspace: torch.Tensor | None = None, stream=None):
+    """Bidirectional attention of the active block over the whole cache.
+
+    With w_q, Q = W_q h_cur[:, J_b] is projected into q_buf first; without,
+    q_buf must hold Q.  Returns (out, q_buf)."""
+    b, s, kvh, hd = k_cache.shape
+    dt = _dtype_code(k_cache)
+    dev = k_cache.device
+    d = h_cur.shape[2] if h_cur is not None else n_heads * hd
+    if q_buf is None:
+        q_buf = torch.empty((b, block_len, n_heads, hd), dtype=k_cache.dtype, device=dev)
+    if out is None:
+        out = torch.empty((b, block_len, n_heads, hd), dtype=k_cache.dtype, device=dev)
+    ws = _workspace(attend_workspace_size(dt, b, s, d, n_heads, kvh, hd, block_len), dev, workspace)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("polestar_attend", lib().polestar_attend(
+        dt, b, s, d, n_heads, kvh, hd, block_start, block_len,
+        _ptr(h_cur) if w_q is not None else None, _ptr(w_q), _ptr(q_buf, k_cache.dtype),
+        _ptr(k_cache), _ptr(v_cache, k_cache.dtype), float(scale), _ptr(out, k_cache.dtype),
+        _ptr(lse, torch.float32), _ptr(ws), nbytes, _stream(stream)))
+    return out, q_buf
+
+
+def commit_workspace_size(dtype: int, batch: int, block_len: int, vocab: int) -> int:
+    return lib().polestar_commit_workspace_size(dtype, batch, block_len, vocab)
+
+
+def commit(logits: torch.Tensor, masked: torch.Tensor, drift_vals: torch.Tensor | None,
+           block_start: int, hist: torch.Tensor | None, hist_len: torch.Tensor | None,
+           mask_token_id: int = -1, tau_s: float = DEFAULT_TAU_S, alpha: float = DEFAULT_ALPHA,
+           force_one: bool = False, token: torch.Tensor | None = None,
+           conf: torch.Tensor | None = None, commit_out: torch.Tensor | None = None,
+           workspace: torch.Tensor | None = None, stream=None):
+    """Polestar-Commit of the current block -> (token int32, conf float32, commit uint8)."""
+    b, nq, vocab = logits.shape
+    dt = _dtype_code(logits)
+    dev = logits.device
+    seq = drift_vals.shape[1] if drift_vals is not None else 0
+    h = hist.shape[1] if hist is not None else 0
+    if token is None:
+        token = torch.empty((b, nq), dtype=torch.int32, device=dev)
+    if conf is None:
+        conf = torch.empty((b, nq), dtype=torch.float32, device=dev)
+    if commit_out is None:
+        commit_out = torch.empty((b, nq), dtype=torch.uint8, device=dev)
+    ws = _workspace(commit_workspace_size(dt, b, nq, vocab), dev, workspace)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("polestar_commit", lib().polestar_commit(
+        dt, b, nq, vocab, _ptr(logits), _ptr(masked, torch.uint8), _ptr(drift_vals, torch.float32), seq,
+        block_start, _ptr(hist, torch.float32), _ptr(hist_len, torch.int32), h, mask_token_id,
+        float(tau_s), float(alpha), int(bool(force_one)), _ptr(token, torch.int32),
+        _ptr(conf, torch.float32), _ptr(commit_out, torch.uint8), _ptr(ws), nbytes, _stream(stream)))
+    return token, conf, commit_out
+
+
+# ---------------------------------------------------------------------------
+# one layer step with preallocated buffers
+# ---------------------------------------------------------------------------
+
+class Step:
+    """drift -> select -> refresh_kv -> attend -> commit for one layer, on
+    buffers allocated once.  All five calls go to the current stream."""
+
+    def __init__(self, *, batch: int, seq: int, d: int, n_heads: int, n_kv_heads: int,
+                 head_dim: int, block_start: int, block_len: int, vocab: int, k: int,
+                 dtype: torch.dtype, hist_depth: int = DEFAULT_HISTORY, device="cuda"):
+        self.shape = dict(batch=batch, seq=seq, d=d, n_heads=n_heads, n_kv_heads=n_kv_heads,
+                          head_dim=head_dim, block_start=block_start, block_len=block_len,
+                          vocab=vocab, k=k)
+        dt = FP32 if dtype == torch.float32 else BF16
+        dev = torch.device(device)
+        f = dict(device=dev)
+        self.drift = torch.empty((batch, seq), dtype=torch.float32, **f)
+        self.stale_idx = torch.empty((batch, k), dtype=torch.int32, **f) if k > 0 else None
+        self.stale_count = torch.empty((batch,), dtype=torch.int32, **f)
+        self.q_buf = torch.empty((batch, block_len, n_heads, head_dim), dtype=dtype, **f)
+        self.out = torch.empty((batch, block_len, n_heads, head_dim), dtype=dtype, **f)
+        self.lse = torch.empty((batch, n_heads, block_len), dtype=torch.float32, **f)
+        self.token = torch.empty((batch, block_len), dtype=torch.int32, **f)
+        self.conf = torch.empty((batch, block_len), dtype=torch.float32, **f)
+        self.commit = torch.empty((batch, block_len), dtype=torch.uint8, **f)
+        self.ws_refresh = _workspace(refresh_kv_workspace_size(dt, batch, d, n_kv_heads, head_dim, k, block_len), dev, None)
+        self.ws_attend = _workspace(attend_workspace_size(dt, batch, seq, d, n_heads, n_kv_heads, head_dim, block_len), dev, None)
+        self.ws_commit = _workspace(commit_workspace_size(dt, batch, block_len, vocab), dev, None)
+
+    def run(self, h_cur, h_prev, w_q, w_k, w_v, k_cache, v_cache, logits, masked, hist, hist_len,
+            *, mask_token_id=-1, tau_s=DEFAULT_TAU_S, alpha=DEFAULT_ALPHA, force_one=False,
+            eligible=None):
+        s = self.shape
+        drift(h_cur, h_prev, out=self.drift)
+        if s["k"] > 0:
+            select(self.drift, s["k"], s["block_start"], s["block_len"], eligible,
+                   self.stale_idx, self.stale_count)
+        refresh_kv(h_cur, self.stale_idx, self.stale_count, s["block_start"], s["block_len"],
+                   w_k, w_v, k_cache, v_cache, workspace=self.ws_refresh)
+        attend(h_cur, w_q, k_cache, v_cache, s["block_start"], s["block_len"], s["n_heads"],
+               q_buf=self.q_buf, out=self.out, lse=self.lse, workspace=self.ws_attend)
+        commit(logits, masked, self.drift, s["block_start"], hist, hist_len, mask_token_id,
+               tau_s, alpha, force_one, self.token, self.conf, self.commit, workspace=self.ws_commit)
+        return self

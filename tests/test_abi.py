@@ -1,0 +1,129 @@
+"""CPU tests of the boundary: the library loads, exports every symbol the
+header declares, and rejects bad arguments on the host before launching
+anything (fake pointers below never reach a kernel)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from tests._util import ROOT, ensure_built
+from paper_2607_14107_amd import polestar as ps
+
+INVALID, UNSUPPORTED, WORKSPACE = 1, 2, 4
+FAKE = 0x10000          # 16-byte aligned, never dereferenced
+MISALIGNED = 0x10004
+
+
+@pytest.fixture(scope="module")
+def L():
+    return ensure_built()
+
+
+def _header_functions():
+    with open(os.path.join(ROOT, "include", "polestar.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(polestar_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _header_functions()
+    assert len(names) == 10, names
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version_and_status_strings(L):
+    assert L.polestar_version() == 10000
+    for code in range(5):
+        assert L.polestar_status_string(code)
+    assert L.polestar_status_string(99) == b"unknown status"
+
+
+def test_drift_validation(L):
+    f = L.polestar_drift
+    assert f(1, 1, 4, 8, None, FAKE, FAKE, None) == INVALID
+    assert f(1, 0, 4, 8, FAKE, FAKE, FAKE, None) == INVALID
+    assert f(2, 1, 4, 8, FAKE, FAKE, FAKE, None) == INVALID          # unknown dtype
+    assert f(1, 1, 4, 12, FAKE, FAKE, FAKE, None) == UNSUPPORTED     # bf16 rows need d % 8 == 0
+    assert f(0, 1, 4, 6, FAKE, FAKE, FAKE, None) == UNSUPPORTED      # fp32 rows need d % 4 == 0
+    assert f(1, 1, 4, 8, MISALIGNED, FAKE, FAKE, None) == UNSUPPORTED
+    assert f(1, 1, 4, 16384, FAKE, FAKE, FAKE, None) == UNSUPPORTED  # above the register budget
+
+
+def test_select_validation(L):
+    f = L.polestar_select
+    assert f(1, 10, None, None, 0, 2, 3, FAKE, FAKE, None) == INVALID
+    assert f(1, 10, FAKE, None, 0, 2, 11, FAKE, FAKE, None) == INVALID       # k > seq
+    assert f(1, 10, FAKE, None, 9, 2, 3, FAKE, FAKE, None) == INVALID        # block past the end
+    assert f(1, 10, FAKE, None, 0, 2, 3, None, FAKE, None) == INVALID        # k > 0 needs stale_idx
+    assert f(1, 10, FAKE, None, -1, 2, 3, FAKE, FAKE, None) == INVALID
+    assert f(1, 40000, FAKE, None, 0, 2, 3, FAKE, FAKE, None) == UNSUPPORTED
+
+
+def test_refresh_validation_and_workspace(L):
+    f = L.polestar_refresh_kv
+    ws = ps.refresh_kv_workspace_size(ps.BF16, 1, 4096, 32, 128, 115, 32)
+    assert ws > 0
+    args = [1, 1, 768, 4096, 32, 128, FAKE, FAKE, FAKE, 115, 512, 32, FAKE, FAKE, FAKE, FAKE, FAKE, ws, None]
+    a = list(args); a[6] = None
+    assert f(*a) == INVALID                                   # h_cur
+    a = list(args); a[10] = 760
+    assert f(*a) == INVALID                                   # block past the end
+    a = list(args); a[7] = None
+    assert f(*a) == INVALID                                   # k_max > 0 needs stale_idx
+    a = list(args); a[5] = 96
+    assert f(*a) == UNSUPPORTED                               # head_dim
+    a = list(args); a[14] = MISALIGNED
+    assert f(*a) == UNSUPPORTED
+    a = list(args); a[17] = ws - 1
+    assert f(*a) == WORKSPACE
+    # nothing to refresh: returns OK without launching
+    a = list(args); a[9] = 0; a[11] = 0; a[7] = None; a[8] = None
+    assert f(*a) == 0
+    assert ps.refresh_kv_workspace_size(ps.BF16, 1, 4096, 32, 128, -1, 32) == 0
+
+
+def test_attend_validation_and_workspace(L):
+    f = L.polestar_attend
+    ws = ps.attend_workspace_size(ps.BF16, 1, 768, 4096, 32, 32, 128, 32)
+    assert ws > 0
+    args = [1, 1, 768, 4096, 32, 32, 128, 512, 32, FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, None, FAKE, ws, None]
+    a = list(args); a[5] = 5
+    assert f(*a) == INVALID                                   # heads % kv_heads
+    a = list(args); a[8] = 0
+    assert f(*a) == INVALID                                   # empty block
+    a = list(args); a[9] = None
+    assert f(*a) == INVALID                                   # w_q without h_cur
+    a = list(args); a[6] = 256
+    assert f(*a) == UNSUPPORTED
+    a = list(args); a[18] = ws - 1
+    assert f(*a) == WORKSPACE
+
+
+def test_commit_validation_and_workspace(L):
+    f = L.polestar_commit
+    ws = ps.commit_workspace_size(ps.BF16, 1, 32, 126464)
+    assert ws > 0
+    args = [1, 1, 32, 126464, FAKE, FAKE, FAKE, 768, 512, FAKE, FAKE, 5, -1, 0.9, 10.0, 1,
+            FAKE, FAKE, FAKE, FAKE, ws, None]
+    a = list(args); a[4] = None
+    assert f(*a) == INVALID
+    a = list(args); a[12] = 126464
+    assert f(*a) == INVALID                                   # mask id beyond the vocabulary
+    a = list(args); a[9] = None
+    assert f(*a) == INVALID                                   # h > 0 with drift needs hist
+    a = list(args); a[8] = 740
+    assert f(*a) == INVALID                                   # block past the end of drift rows
+    a = list(args); a[3] = 126465
+    assert f(*a) == UNSUPPORTED                               # rows of 16-byte chunks
+    a = list(args); a[20] = ws - 1
+    assert f(*a) == WORKSPACE
+
+
+def test_binding_fails_loudly_without_gpu_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(1, 4, 8)
+    with pytest.raises(ValueError):
+        ps.drift(x, x)
