@@ -124,7 +124,8 @@ polestar_status polestar_select(int batch, int seq, const float* drift,
  *   workspace      : >= polestar_refresh_kv_workspace_size(...) bytes
  * Requires batch, seq, d, n_kv_heads > 0, k_max >= 0, block_len >= 0,
  * block_start + block_len <= seq.  stale_idx/stale_count may be NULL only
- * when k_max == 0.
+ * when k_max == 0.  UNSUPPORTED unless d % 128 == 0 (bf16) / d % 64 == 0
+ * (fp32): the projection streams rows in 256-byte steps.
  */
 size_t polestar_refresh_kv_workspace_size(polestar_dtype dtype, int batch, int d,
                                           int n_kv_heads, int head_dim,
@@ -160,7 +161,8 @@ polestar_status polestar_refresh_kv(polestar_dtype dtype, int batch, int seq, in
  *   lse     : [batch][n_heads][block_len] float or NULL
  *   workspace : >= polestar_attend_workspace_size(...) bytes
  * Requires n_heads % n_kv_heads == 0, block_len > 0,
- * block_start + block_len <= seq.
+ * block_start + block_len <= seq; with w_q, d % 128 == 0 (bf16) /
+ * d % 64 == 0 (fp32) as for polestar_refresh_kv.
  */
 size_t polestar_attend_workspace_size(polestar_dtype dtype, int batch, int seq, int d,
                                       int n_heads, int n_kv_heads, int head_dim,

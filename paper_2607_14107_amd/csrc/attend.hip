@@ -426,7 +426,8 @@ extern "C" polestar_status polestar_attend(polestar_dtype dtype, int batch, int 
         n_heads % n_kv_heads != 0 || !q_buf || !k_cache || !v_cache || !out ||
         (w_q && !h_cur))
         return POLESTAR_ERR_INVALID_ARGUMENT;
-    if ((head_dim != 64 && head_dim != 128) || !row_ok(dtype, d) || !aligned16(q_buf) ||
+    if ((head_dim != 64 && head_dim != 128) || (w_q && !gemm_k_ok(dtype == POLESTAR_BF16, d)) ||
+        !aligned16(q_buf) ||
         !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out) || !aligned16(workspace) ||
         (w_q && (!aligned16(w_q) || !aligned16(h_cur))))
         return POLESTAR_ERR_UNSUPPORTED;

@@ -150,6 +150,31 @@ template <> struct Mma<false> {
     }
 };
 
+// 32x32 output tiles (twice the flops per issue slot of 16x16x32 on gfx950).
+// Lane l carries index (l % 32) of the non-reduced dimension and k-group
+// (l / 32); result register j of lane l holds
+// C[8*(j/4) + 4*(l/32) + (j%4)][l % 32].
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ int mfma32_row(int lane, int j) { return 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3); }
+
+template <bool BF16> struct Mma32;
+template <> struct Mma32<true> {
+    __device__ __forceinline__ static floatx16 step(const uint4& a, const uint4& b, floatx16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                      __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    }
+};
+template <> struct Mma32<false> {
+    __device__ __forceinline__ static floatx16 step(const uint4& a, const uint4& b, floatx16 c) {
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+        return c;
+    }
+};
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 constexpr float kLog2e = 1.4426950408889634f;

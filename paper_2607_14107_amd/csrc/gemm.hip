@@ -3,19 +3,30 @@
 // App. B: K = W_K h, V = W_V h) and of the Q projection of the active block.
 //
 // The product is skinny: a few hundred gathered rows times a [N][K] weight
-// read once from HBM.  A workgroup (4 waves) owns BM = 16*MT rows and 128
-// output columns, wave w the columns 32w..32w+31 (two 16x16 MFMA tiles).
-// Per super-step of 256 bytes of K:
-//  - the gathered input rows are staged through LDS (16-byte coalesced loads,
-//    row pitch padded to 272 bytes so the MFMA reads are bank-conflict free)
-//    and shared by the four waves;
-//  - each wave streams its weight rows straight from HBM into registers,
-//    64 contiguous bytes per lane, two super-steps ahead;
-//  - one MFMA step consumes a 16-byte slice of A and B per lane.  A and B
-//    use the same lane -> k assignment, so k may be visited in any order.
-// When the row x column tiles alone do not fill the chip, K is split over
-// workgroups; fp32 partials go to the workspace and a second kernel sums
-// them in split order (deterministic), rounds and scatters 16-byte rows.
+// that is read once from HBM.  Two kernels:
+//
+// gemm_rows_kernel (more than 64 rows): a workgroup of 4 waves owns
+//   BM = 32*MT rows and 128 columns; wave w computes all BM rows of columns
+//   32w..32w+31 with v_mfma_f32_32x32x16_bf16 (on gfx950 it does twice the
+//   work per issue slot of the 16x16x32 form).  Per super-step of 256 bytes
+//   of K:
+//   - the gathered input rows are staged in LDS (16-byte coalesced loads,
+//     272-byte row pitch: conflict-free MFMA reads) and shared by the waves;
+//   - each wave streams its weight rows from HBM straight into registers,
+//     128 contiguous bytes per lane, two super-steps ahead (triple buffer,
+//     loop unrolled three times so the buffers rotate without copies).
+//   When rows x columns do not fill the chip, K is split over workgroups;
+//   fp32 partials go to the workspace and gemm_reduce_kernel sums them in
+//   split order (deterministic) and scatters 16-byte rows.
+//
+// gemm_small_kernel (at most 64 rows, e.g. the Q projection): a workgroup
+//   owns all rows and 16 columns; its 4 waves take interleaved super-steps
+//   of the full K with both operands loaded straight into registers and are
+//   summed in LDS, so no partials leave the chip.
+//
+// In both, A and B use the same lane -> k assignment, so k may be visited in
+// any order.  All loads are unconditional (rows or columns past the end read
+// row 0 and are never stored) so the compiler's wait counts stay static.
 #include "common.hpp"
 #include "gemm.hpp"
 #include "host_common.hpp"
@@ -24,9 +35,9 @@ namespace ps {
 namespace {
 
 constexpr int kGemmBlock = 256;
-constexpr int kBN = 128;          // columns per workgroup
 constexpr int kLda = 272;         // LDS row pitch (bytes) of the staged input rows
 constexpr int kTargetWgs = 256;   // one workgroup per compute unit on MI355X
+constexpr int kMaxSplit = 8;
 
 // Row bookkeeping --------------------------------------------------------------
 // Refresh mode: sequence b contributes count_b stale rows followed by its
@@ -97,24 +108,79 @@ __device__ __forceinline__ char* out_ptr(const GemmArgs& g, int b, int pos, int 
     return g.out1 + (row * (g.N - g.n0) + (n - g.n0)) * es;
 }
 
+// 8 consecutive fp32 values -> destination (16-byte bf16 or 2x16-byte fp32 store).
+template <bool BF16>
+__device__ __forceinline__ void store8(char* dst, const float* v) {
+    if constexpr (BF16) {
+        st16(dst, make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                             pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])));
+    } else {
+        st16(dst, make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]),
+                             __float_as_uint(v[2]), __float_as_uint(v[3])));
+        st16(dst + 16, make_uint4(__float_as_uint(v[4]), __float_as_uint(v[5]),
+                                  __float_as_uint(v[6]), __float_as_uint(v[7])));
+    }
+}
+
+// Weight row of output column n (nullptr past N).
+__device__ __forceinline__ const char* weight_row(const GemmArgs& g, int n, int es) {
+    if (n >= g.N) return nullptr;
+    return n < g.n0 ? g.w0 + static_cast<size_t>(n) * g.K * es
+                    : g.w1 + static_cast<size_t>(n - g.n0) * g.K * es;
+}
+
+// ---------------------------------------------------------------------------
+// gemm_rows_kernel: BM = 32*MT rows x 128 columns per workgroup; wave w owns
+// columns 32w..32w+31 of all rows (v_mfma_f32_32x32x16_bf16: lane l carries
+// row/column l%32 and k-group l/32, 128 contiguous bytes per super-step).
+// ---------------------------------------------------------------------------
+
 template <bool BF16, int MT>
-__global__ __launch_bounds__(kGemmBlock) void gemm_kernel(GemmArgs g) {
+__global__ __launch_bounds__(kGemmBlock) void gemm_rows_kernel(GemmArgs g) {
     using T = Elem<BF16>;
-    constexpr int BM = MT * 16;
+    constexpr int BM = MT * 32;
+    constexpr int BN = 128;
+    constexpr int RA = BM / 16;            // 16-byte chunks each thread stages per super-step
     constexpr int ES = T::kBytes;
-    constexpr int KS = 256 / ES;      // k elements per super-step
     __shared__ __align__(16) char sa[2][BM * kLda];
     __shared__ int rowb[BM], rowp[BM];
     __shared__ int scan_tmp[17];
-    extern __shared__ int pre[];      // batch + 1 (refresh mode)
+    extern __shared__ int pre[];           // batch + 1 (refresh mode)
+
+    const int tile = blockIdx.x / g.ksplit;
+    const int split = blockIdx.x - tile * g.ksplit;
+    const int col_tile = tile % g.col_tiles;
+    const int row_tile = tile / g.col_tiles;
 
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int w = t >> 6;
-    const int m0 = blockIdx.y * BM;
+    const int m0 = row_tile * BM;
+
+    // The weight row this lane streams (column n of wave w; past N: row 0,
+    // never stored), 128 contiguous bytes per super-step at k-group lane/32.
+    // Its first two super-steps are requested before the row bookkeeping,
+    // whose dependent loads (counts, prefix, stale indices) would otherwise
+    // delay the weight stream.
+    const int n = col_tile * BN + w * 32 + (lane & 31);
+    const char* brow = weight_row(g, n, ES);
+    if (!brow) brow = g.w0;
+    brow += (lane >> 5) * 128;
+    const int nsteps = g.K / (256 / ES);
+    const int s0 = split * g.steps_per_split;
+    const int s1 = min(nsteps, s0 + g.steps_per_split);
+    const int slast = s1 - 1;
+    auto load_b = [&](int step, uint4 (&rb)[8]) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) rb[s] = ld16(brow + step * 256 + 16 * s);
+    };
+    uint4 b0[8], b1[8], b2[8];
+    load_b(s0, b0);
+    load_b(min(s0 + 1, slast), b1);
+
     const int total = g.mode == kGemmRefresh ? build_prefix(g, pre, scan_tmp)
                                              : g.batch * g.block_len;
-    if (m0 >= total) return;          // uniform over the workgroup
+    if (m0 >= total) return;               // uniform over the workgroup
     if (t < BM) {
         int b, pos;
         map_row(g, pre, total, m0 + t, b, pos);
@@ -123,192 +189,293 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_kernel(GemmArgs g) {
     }
     __syncthreads();
 
-    // Input rows this thread stages: r = t/16 + 16 i, 16 bytes at acol.
-    const char* arow[MT];
+    // Rows that map to nothing read row 0 instead: their accumulators are
+    // never stored, and every load stays unconditional (static wait counts).
+    const char* arow[RA];
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
+    for (int i = 0; i < RA; ++i) {
         const int r = (t >> 4) + 16 * i;
         const int b = rowb[r];
-        arow[i] = b >= 0 ? g.x + (static_cast<size_t>(b) * g.seq + rowp[r]) * g.K * ES : nullptr;
+        arow[i] = b >= 0 ? g.x + (static_cast<size_t>(b) * g.seq + rowp[r]) * g.K * ES : g.x;
     }
     const int acol = (t & 15) * 16;
 
-    // Weight rows this lane streams: two 16-column tiles of wave w.
-    const int col0 = blockIdx.x * kBN + w * 32;
-    const char* brow[2];
-#pragma unroll
-    for (int nt = 0; nt < 2; ++nt) {
-        const int n = col0 + nt * 16 + (lane & 15);
-        brow[nt] = n >= g.N ? nullptr
-                 : n < g.n0 ? g.w0 + static_cast<size_t>(n) * g.K * ES
-                            : g.w1 + static_cast<size_t>(n - g.n0) * g.K * ES;
-    }
-    const int bcol = (lane >> 4) * 64;
-
-    const int nsteps = (g.K + KS - 1) / KS;
-    const int s0 = blockIdx.z * g.steps_per_split;
-    const int s1 = min(nsteps, s0 + g.steps_per_split);
-
-    floatx4 acc[MT][2];
+    floatx16 acc[MT];
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < 16; ++j) acc[i][j] = 0.f;
 
-    auto load_a = [&](int step, uint4 (&ra)[MT]) {
-        const int kb = step * 256 + acol;
-        const bool kin = kb / ES < g.K;
+    auto load_a = [&](int step, uint4 (&ra)[RA]) {
 #pragma unroll
-        for (int i = 0; i < MT; ++i) ra[i] = (arow[i] && kin) ? ld16(arow[i] + kb) : zero16();
+        for (int i = 0; i < RA; ++i) ra[i] = ld16(arow[i] + step * 256 + acol);
     };
-    auto store_a = [&](int buf, const uint4 (&ra)[MT]) {
+    auto store_a = [&](int buf, const uint4 (&ra)[RA]) {
 #pragma unroll
-        for (int i = 0; i < MT; ++i) st16(&sa[buf][((t >> 4) + 16 * i) * kLda + acol], ra[i]);
+        for (int i = 0; i < RA; ++i) st16(&sa[buf][((t >> 4) + 16 * i) * kLda + acol], ra[i]);
     };
-    auto load_b = [&](int step, uint4 (&rb)[2][4]) {
+    auto compute = [&](int buf, const uint4 (&rb)[8]) {
+        const char* abase = &sa[buf][(lane & 31) * kLda + (lane >> 5) * 128];
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const int kb = step * 256 + bcol + 16 * s;
-                rb[nt][s] = (brow[nt] && kb / ES < g.K) ? ld16(brow[nt] + kb) : zero16();
-            }
-    };
-
-    uint4 b0[2][4], b1[2][4];
-    {
-        uint4 ra[MT];
-        load_a(s0, ra);
-        load_b(s0, b0);
-        if (s0 + 1 < s1) load_b(s0 + 1, b1);
-        store_a(0, ra);
-    }
-    __syncthreads();
-
-    for (int step = s0; step < s1; ++step) {
-        const int buf = (step - s0) & 1;
-        uint4 ra[MT];
-        uint4 b2[2][4];
-        if (step + 1 < s1) load_a(step + 1, ra);
-        if (step + 2 < s1) load_b(step + 2, b2);
-        const char* abase = &sa[buf][(lane & 15) * kLda + (lane >> 4) * 64];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
+        for (int s = 0; s < 8; ++s) {
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                const uint4 a = *reinterpret_cast<const uint4*>(abase + mt * 16 * kLda + 16 * s);
-#pragma unroll
-                for (int nt = 0; nt < 2; ++nt)
-                    acc[mt][nt] = Mma<BF16>::step(a, b0[nt][s], acc[mt][nt]);
+                const uint4 a = *reinterpret_cast<const uint4*>(abase + mt * 32 * kLda + 16 * s);
+                acc[mt] = Mma32<BF16>::step(a, rb[s], acc[mt]);
             }
         }
-        if (step + 1 < s1) store_a(buf ^ 1, ra);
-        __syncthreads();
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                b0[nt][s] = b1[nt][s];
-                b1[nt][s] = b2[nt][s];
-            }
-    }
+    };
 
-    // Epilogue: lane holds rows mt*16 + 4*(lane/16) + i of column n.
+    // Software pipeline.  Issue order of the loads: ... B(s+1), A(s+1),
+    // B(s+2), A(s+2) ...  Waiting for A(s+1) at the end of step s (to stage
+    // it in LDS) therefore also covers B(s+1), which step s+1 needs, while
+    // B(s+2) stays in flight: weights get two compute phases of latency
+    // cover, the (L2-resident) input rows one.  Prefetches past s1 - 1
+    // re-read step s1 - 1 (cache hits, ignored) so every iteration issues
+    // the same loads and the wait counts stay static.
+    uint4 ra[RA];
+    load_a(s0, ra);
+    store_a(0, ra);                       // waits for A(s0) (and B(s0), B(s0+1))
+    load_a(min(s0 + 1, slast), ra);
+    __syncthreads();
+
+    // step S: issue B(S+2) -> B_LOAD; compute with LDS[(S-s0)%2] and B_USE;
+    // stage A(S+1) -> LDS[(S-s0+1)%2]; then issue A(S+2).
+#define PS_GEMM_STEP(S, B_USE, B_LOAD)                                      \
+    {                                                                       \
+        const int s_ = (S);                                                 \
+        __builtin_amdgcn_sched_barrier(0);                                  \
+        load_b(min(s_ + 2, slast), B_LOAD);                                 \
+        __builtin_amdgcn_sched_barrier(0);                                  \
+        compute((s_ - s0) & 1, B_USE);                                      \
+        if (s_ + 1 < s1) store_a((s_ - s0 + 1) & 1, ra);                    \
+        __syncthreads();                                                    \
+        load_a(min(s_ + 2, slast), ra);                                     \
+    }
+    int sc = s0;
+    for (; sc + 3 <= s1; sc += 3) {      // single exit: buffers rotate b0 -> b1 -> b2
+        PS_GEMM_STEP(sc, b0, b2)
+        PS_GEMM_STEP(sc + 1, b1, b0)
+        PS_GEMM_STEP(sc + 2, b2, b1)
+    }
+    if (sc < s1) PS_GEMM_STEP(sc, b0, b2)
+    if (sc + 1 < s1) PS_GEMM_STEP(sc + 1, b1, b0)
+#undef PS_GEMM_STEP
+
+    // Epilogue, staged through LDS (the input staging buffers are free now):
+    // register j of acc[mt] is row mt*32 + mfma32_row(lane, j) of column
+    // 32w + lane%32; then each thread writes 8 consecutive columns of a row
+    // (16-byte stores, 512 contiguous bytes per row of the tile).
+    constexpr int EP = BN + 4;            // fp32 pitch of the staged tile
+    static_assert(static_cast<size_t>(BM) * EP * 4 <= sizeof(sa), "epilogue tile must fit");
+    float* ep = reinterpret_cast<float*>(&sa[0][0]);
+    __syncthreads();                      // every wave is done reading sa
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-            const int n = col0 + nt * 16 + (lane & 15);
-            if (n >= g.N) continue;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = mt * 16 + 4 * (lane >> 4) + i;
-                const int b = rowb[r];
-                if (b < 0) continue;
-                const float v = acc[mt][nt][i];
-                if (g.ksplit == 1)
-                    store_elem<BF16>(out_ptr<BF16>(g, b, rowp[r], m0 + r, n), v);
-                else
-                    g.ws[(static_cast<size_t>(blockIdx.z) * g.m_max + (m0 + r)) * g.N + n] = v;
-            }
+        for (int j = 0; j < 16; ++j)
+            ep[(mt * 32 + mfma32_row(lane, j)) * EP + w * 32 + (lane & 31)] = acc[mt][j];
+    __syncthreads();
+    for (int idx = t; idx < BM * (BN / 8); idx += kGemmBlock) {
+        const int r = idx / (BN / 8);
+        const int c = (idx % (BN / 8)) * 8;
+        const int b = rowb[r];
+        const int nc = col_tile * BN + c;
+        if (b < 0 || nc >= g.N) continue;
+        const float* v = ep + r * EP + c;
+        if (g.ksplit == 1) {
+            store8<BF16>(out_ptr<BF16>(g, b, rowp[r], m0 + r, nc), v);
+        } else {
+            float* dst = g.ws + (static_cast<size_t>(split) * g.m_max + (m0 + r)) * g.N + nc;
+            *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+            *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
         }
+    }
 }
 
-// Sum of the split-K partials of one output row per workgroup, rounded and
-// written with 16-byte stores (8 consecutive columns per thread).
+// Sum of the split-K partials, in split order (deterministic): one thread per
+// 8 consecutive columns of one row, all split loads issued before the adds,
+// rounded and written with 16-byte stores.
 template <bool BF16>
 __global__ __launch_bounds__(kGemmBlock) void gemm_reduce_kernel(GemmArgs g) {
     __shared__ int scan_tmp[17];
-    __shared__ int rowinfo[2];
     extern __shared__ int pre[];
-    const int m = blockIdx.x;
+    const int groups = g.N / 8;
+    const long id = static_cast<long>(blockIdx.x) * kGemmBlock + threadIdx.x;
+    const int mraw = static_cast<int>(id / groups);
+    const int c = static_cast<int>(id - static_cast<long>(mraw) * groups) * 8;
+    // Partial loads first (rows past m_max read row 0, never stored); the
+    // row bookkeeping's dependent loads then overlap them.
+    const int m = mraw < g.m_max ? mraw : 0;
+    const size_t stride = static_cast<size_t>(g.m_max) * g.N;
+    const float* src = g.ws + static_cast<size_t>(m) * g.N + c;
+    float4 x[2 * kMaxSplit];
+#pragma unroll
+    for (int s = 0; s < kMaxSplit; ++s) {
+        if (s < g.ksplit) {
+            x[2 * s] = *reinterpret_cast<const float4*>(src + s * stride);
+            x[2 * s + 1] = *reinterpret_cast<const float4*>(src + s * stride + 4);
+        }
+    }
     const int total = g.mode == kGemmRefresh ? build_prefix(g, pre, scan_tmp)
                                              : g.batch * g.block_len;
-    if (m >= total) return;
-    if (threadIdx.x == 0) {
+    if (mraw >= total) return;
+    int b, pos;
+    map_row(g, pre, total, m, b, pos);
+    if (b < 0) return;
+    float v[8] = {x[0].x, x[0].y, x[0].z, x[0].w, x[1].x, x[1].y, x[1].z, x[1].w};
+#pragma unroll
+    for (int s = 1; s < kMaxSplit; ++s) {
+        if (s < g.ksplit) {
+            v[0] += x[2 * s].x; v[1] += x[2 * s].y; v[2] += x[2 * s].z; v[3] += x[2 * s].w;
+            v[4] += x[2 * s + 1].x; v[5] += x[2 * s + 1].y; v[6] += x[2 * s + 1].z; v[7] += x[2 * s + 1].w;
+        }
+    }
+    store8<BF16>(out_ptr<BF16>(g, b, pos, m, c), v);
+}
+
+// ---------------------------------------------------------------------------
+// gemm_small_kernel: at most 16*MT rows, 16 columns per workgroup, the 4
+// waves take super-steps w, w+4, w+8, ... of K and are summed in LDS.
+// ---------------------------------------------------------------------------
+
+template <bool BF16, int MT>
+__global__ __launch_bounds__(kGemmBlock) void gemm_small_kernel(GemmArgs g) {
+    using T = Elem<BF16>;
+    constexpr int ES = T::kBytes;
+    constexpr int BM = MT * 16;
+    __shared__ int rowb[BM], rowp[BM];
+    __shared__ int scan_tmp[17];
+    __shared__ float red[4][BM][17];
+    extern __shared__ int pre[];
+
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int w = t >> 6;
+    const int col0 = blockIdx.x * 16;
+    const int m0 = blockIdx.y * BM;
+    const int kcol = (lane >> 4) * 64;
+    const int nsteps = g.K / (256 / ES);
+    // wave w: super-steps w, w+4, ...; the last one it owns is slast
+    // (prefetches past it re-read slast and are ignored).
+    const int nmine = w < nsteps ? (nsteps - 1 - w) / 4 + 1 : 0;
+    const int slast = w < nsteps ? w + 4 * (nmine - 1) : 0;
+
+    // Weight row of column col0 + lane%16 (past N: row 0, never stored); its
+    // first two super-steps are requested before the row bookkeeping.
+    const char* brow = weight_row(g, col0 + (lane & 15), ES);
+    if (!brow) brow = g.w0;
+    auto load_b = [&](int step, uint4 (&rb)[4]) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) rb[s] = ld16(brow + step * 256 + kcol + 16 * s);
+    };
+    uint4 q0[4], q1[4], q2[4];
+    load_b(min(w, slast), q0);
+    load_b(min(w + 4, slast), q1);
+
+    const int total = g.mode == kGemmRefresh ? build_prefix(g, pre, scan_tmp)
+                                             : g.batch * g.block_len;
+    if (m0 >= total) return;
+    if (t < BM) {
         int b, pos;
-        map_row(g, pre, total, m, b, pos);
-        rowinfo[0] = b;
-        rowinfo[1] = pos;
+        map_row(g, pre, total, m0 + t, b, pos);
+        rowb[t] = b;
+        rowp[t] = pos;
     }
     __syncthreads();
-    const int b = rowinfo[0], pos = rowinfo[1];
-    if (b < 0) return;
-    const size_t split_stride = static_cast<size_t>(g.m_max) * g.N;
-    for (int c = threadIdx.x; c < g.N / 8; c += blockDim.x) {
-        const int n = c * 8;
-        const float* src = g.ws + static_cast<size_t>(m) * g.N + n;
+
+    // Rows past the end read row 0 and are never stored.
+    const char* arow[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const int r = mt * 16 + (lane & 15);
+        const int b = rowb[r];
+        arow[mt] = b >= 0 ? g.x + (static_cast<size_t>(b) * g.seq + rowp[r]) * g.K * ES : g.x;
+    }
+    auto load_a = [&](int step, uint4 (&ra)[MT][4]) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) ra[mt][s] = ld16(arow[mt] + step * 256 + kcol + 16 * s);
+    };
+    floatx4 acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](const uint4 (&ra)[MT][4], const uint4 (&rb)[4]) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) acc[mt] = Mma<BF16>::step(ra[mt][s], rb[s], acc[mt]);
+    };
+
+    uint4 a0[MT][4], a1[MT][4], a2[MT][4];
+    load_a(min(w, slast), a0);
+    load_a(min(w + 4, slast), a1);
+#define PS_SMALL_STEP(I, A_USE, B_USE, A_LOAD, B_LOAD)                      \
+    {                                                                       \
+        __builtin_amdgcn_sched_barrier(0);                                  \
+        load_a(min(w + 4 * ((I) + 2), slast), A_LOAD);                      \
+        load_b(min(w + 4 * ((I) + 2), slast), B_LOAD);                      \
+        __builtin_amdgcn_sched_barrier(0);                                  \
+        compute(A_USE, B_USE);                                              \
+    }
+    int ic = 0;
+    for (; ic + 3 <= nmine; ic += 3) {
+        PS_SMALL_STEP(ic, a0, q0, a2, q2)
+        PS_SMALL_STEP(ic + 1, a1, q1, a0, q0)
+        PS_SMALL_STEP(ic + 2, a2, q2, a1, q1)
+    }
+    if (ic < nmine) PS_SMALL_STEP(ic, a0, q0, a2, q2)
+    if (ic + 1 < nmine) PS_SMALL_STEP(ic + 1, a1, q1, a0, q0)
+#undef PS_SMALL_STEP
+
+    // sum the four waves: lane holds rows mt*16 + 4*(lane/16) + i, column lane%16
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) red[w][mt * 16 + 4 * (lane >> 4) + i][lane & 15] = acc[mt][i];
+    __syncthreads();
+    // thread -> (row r, 8 columns c)
+    for (int idx = t; idx < BM * 2; idx += kGemmBlock) {
+        const int r = idx >> 1, c = (idx & 1) * 8;
+        const int b = rowb[r];
+        const int n = col0 + c;
+        if (b < 0 || n >= g.N) continue;
         float v[8];
-        {
-            const float4 x0 = *reinterpret_cast<const float4*>(src);
-            const float4 x1 = *reinterpret_cast<const float4*>(src + 4);
-            v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
-            v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
-        }
-        for (int s = 1; s < g.ksplit; ++s) {
-            const float4 x0 = *reinterpret_cast<const float4*>(src + s * split_stride);
-            const float4 x1 = *reinterpret_cast<const float4*>(src + s * split_stride + 4);
-            v[0] += x0.x; v[1] += x0.y; v[2] += x0.z; v[3] += x0.w;
-            v[4] += x1.x; v[5] += x1.y; v[6] += x1.z; v[7] += x1.w;
-        }
-        char* dst = out_ptr<BF16>(g, b, pos, m, n);
-        if constexpr (BF16) {
-            st16(dst, make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
-                                 pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])));
-        } else {
-            st16(dst, make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]),
-                                 __float_as_uint(v[2]), __float_as_uint(v[3])));
-            st16(dst + 16, make_uint4(__float_as_uint(v[4]), __float_as_uint(v[5]),
-                                      __float_as_uint(v[6]), __float_as_uint(v[7])));
-        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = ((red[0][r][c + j] + red[1][r][c + j]) + red[2][r][c + j]) + red[3][r][c + j];
+        store8<BF16>(out_ptr<BF16>(g, b, rowp[r], m0 + r, n), v);
     }
 }
 
 template <bool BF16, int MT>
-void launch_gemm(const GemmPlan& p, const GemmArgs& g, size_t dyn, hipStream_t s) {
-    dim3 grid(p.col_tiles, p.row_tiles, p.ksplit);
-    hipLaunchKernelGGL((gemm_kernel<BF16, MT>), grid, dim3(kGemmBlock), dyn, s, g);
+void launch_rows(const GemmPlan& p, const GemmArgs& g, size_t dyn, hipStream_t s) {
+    hipLaunchKernelGGL((gemm_rows_kernel<BF16, MT>), dim3(p.grid), dim3(kGemmBlock), dyn, s, g);
 }
 
 template <bool BF16>
-bool dispatch_gemm(const GemmPlan& p, const GemmArgs& g, size_t dyn, hipStream_t s) {
+bool dispatch_rows(const GemmPlan& p, const GemmArgs& g, size_t dyn, hipStream_t s) {
+    switch (p.mt) {   // 32-row tiles per workgroup
+        case 1: launch_rows<BF16, 1>(p, g, dyn, s); return true;
+        case 2: launch_rows<BF16, 2>(p, g, dyn, s); return true;
+        case 3: launch_rows<BF16, 3>(p, g, dyn, s); return true;
+        case 4: launch_rows<BF16, 4>(p, g, dyn, s); return true;
+        case 5: launch_rows<BF16, 5>(p, g, dyn, s); return true;
+        case 6: launch_rows<BF16, 6>(p, g, dyn, s); return true;
+        case 7: launch_rows<BF16, 7>(p, g, dyn, s); return true;
+        case 8: launch_rows<BF16, 8>(p, g, dyn, s); return true;
+        default: return false;
+    }
+}
+
+template <bool BF16>
+bool dispatch_small(const GemmPlan& p, const GemmArgs& g, size_t dyn, hipStream_t s) {
+    dim3 grid(p.col_tiles, p.row_tiles);
     switch (p.mt) {
-        case 1: launch_gemm<BF16, 1>(p, g, dyn, s); return true;
-        case 2: launch_gemm<BF16, 2>(p, g, dyn, s); return true;
-        case 3: launch_gemm<BF16, 3>(p, g, dyn, s); return true;
-        case 4: launch_gemm<BF16, 4>(p, g, dyn, s); return true;
-        case 5: launch_gemm<BF16, 5>(p, g, dyn, s); return true;
-        case 6: launch_gemm<BF16, 6>(p, g, dyn, s); return true;
-        case 7: launch_gemm<BF16, 7>(p, g, dyn, s); return true;
-        case 8: launch_gemm<BF16, 8>(p, g, dyn, s); return true;
-        case 9: launch_gemm<BF16, 9>(p, g, dyn, s); return true;
-        case 10: launch_gemm<BF16, 10>(p, g, dyn, s); return true;
-        case 11: launch_gemm<BF16, 11>(p, g, dyn, s); return true;
-        case 12: launch_gemm<BF16, 12>(p, g, dyn, s); return true;
-        case 13: launch_gemm<BF16, 13>(p, g, dyn, s); return true;
-        case 14: launch_gemm<BF16, 14>(p, g, dyn, s); return true;
-        case 15: launch_gemm<BF16, 15>(p, g, dyn, s); return true;
-        case 16: launch_gemm<BF16, 16>(p, g, dyn, s); return true;
+        case 1: hipLaunchKernelGGL((gemm_small_kernel<BF16, 1>), grid, dim3(kGemmBlock), dyn, s, g); return true;
+        case 2: hipLaunchKernelGGL((gemm_small_kernel<BF16, 2>), grid, dim3(kGemmBlock), dyn, s, g); return true;
+        case 3: hipLaunchKernelGGL((gemm_small_kernel<BF16, 3>), grid, dim3(kGemmBlock), dyn, s, g); return true;
+        case 4: hipLaunchKernelGGL((gemm_small_kernel<BF16, 4>), grid, dim3(kGemmBlock), dyn, s, g); return true;
         default: return false;
     }
 }
@@ -320,33 +487,51 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     const int ks = bf16 ? 128 : 64;
     const int nsteps = ceil_div(K, ks);
     if (m_max <= 0) m_max = 1;
+    if (m_max <= 64) {
+        p.small = true;
+        p.mt = ceil_div(m_max, 16);
+        p.row_tiles = 1;
+        p.col_tiles = ceil_div(N, 16);
+        p.ksplit = 1;
+        p.steps_per_split = nsteps;
+        p.grid = p.col_tiles;
+        return p;
+    }
+    p.small = false;
     p.row_tiles = ceil_div(m_max, 256);
-    p.mt = ceil_div(m_max, 16L * p.row_tiles);
-    p.col_tiles = ceil_div(N, kBN);
-    const long wgs = static_cast<long>(p.row_tiles) * p.col_tiles;
+    p.mt = ceil_div(m_max, 32L * p.row_tiles);
+    p.col_tiles = ceil_div(N, 128);
+    const long tiles = static_cast<long>(p.row_tiles) * p.col_tiles;
     int ksplit = 1;
-    if (wgs < kTargetWgs) ksplit = ceil_div(kTargetWgs, wgs);
-    if (ksplit > 8) ksplit = 8;
+    if (tiles < kTargetWgs) ksplit = ceil_div(kTargetWgs, tiles);
+    if (ksplit > kMaxSplit) ksplit = kMaxSplit;
     if (ksplit > nsteps) ksplit = nsteps;
     p.steps_per_split = ceil_div(nsteps, ksplit);
     p.ksplit = ceil_div(nsteps, p.steps_per_split);
-    p.ws_bytes = p.ksplit > 1 ? static_cast<size_t>(p.ksplit) * m_max * N * sizeof(float) : 0;
+    p.grid = static_cast<int>(tiles * p.ksplit);
+    if (p.ksplit > 1)
+        p.ws_bytes = align_up(static_cast<size_t>(p.ksplit) * m_max * N * sizeof(float), 256);
     return p;
 }
 
 polestar_status gemm_run(bool bf16, const GemmPlan& p, GemmArgs g, hipStream_t stream) {
     g.ksplit = p.ksplit;
     g.steps_per_split = p.steps_per_split;
+    g.row_tiles = p.row_tiles;
+    g.col_tiles = p.col_tiles;
     const size_t dyn = g.mode == kGemmRefresh ? (static_cast<size_t>(g.batch) + 1) * sizeof(int) : 0;
-    const bool ok = bf16 ? dispatch_gemm<true>(p, g, dyn, stream)
-                         : dispatch_gemm<false>(p, g, dyn, stream);
+    bool ok;
+    if (p.small) ok = bf16 ? dispatch_small<true>(p, g, dyn, stream) : dispatch_small<false>(p, g, dyn, stream);
+    else ok = bf16 ? dispatch_rows<true>(p, g, dyn, stream) : dispatch_rows<false>(p, g, dyn, stream);
     if (!ok) return POLESTAR_ERR_UNSUPPORTED;
     polestar_status st = launch_status();
-    if (st != POLESTAR_OK || p.ksplit == 1) return st;
+    if (st != POLESTAR_OK || p.small || p.ksplit == 1) return st;
+    const long threads = static_cast<long>(g.m_max) * (g.N / 8);
+    const int blocks = ceil_div(threads, kGemmBlock);
     if (bf16)
-        hipLaunchKernelGGL((gemm_reduce_kernel<true>), dim3(g.m_max), dim3(kGemmBlock), dyn, stream, g);
+        hipLaunchKernelGGL((gemm_reduce_kernel<true>), dim3(blocks), dim3(kGemmBlock), dyn, stream, g);
     else
-        hipLaunchKernelGGL((gemm_reduce_kernel<false>), dim3(g.m_max), dim3(kGemmBlock), dyn, stream, g);
+        hipLaunchKernelGGL((gemm_reduce_kernel<false>), dim3(blocks), dim3(kGemmBlock), dyn, stream, g);
     return launch_status();
 }
 
@@ -378,9 +563,9 @@ extern "C" polestar_status polestar_refresh_kv(polestar_dtype dtype, int batch, 
         block_start > seq - block_len || !h_cur || !w_k || !w_v || !k_cache || !v_cache ||
         (k_max > 0 && (!stale_idx || !stale_count)))
         return POLESTAR_ERR_INVALID_ARGUMENT;
-    if ((head_dim != 64 && head_dim != 128) || !row_ok(dtype, d) || !aligned16(h_cur) ||
-        !aligned16(w_k) || !aligned16(w_v) || !aligned16(k_cache) || !aligned16(v_cache) ||
-        !aligned16(workspace))
+    if ((head_dim != 64 && head_dim != 128) || !gemm_k_ok(dtype == POLESTAR_BF16, d) ||
+        !aligned16(h_cur) || !aligned16(w_k) || !aligned16(w_v) || !aligned16(k_cache) ||
+        !aligned16(v_cache) || !aligned16(workspace))
         return POLESTAR_ERR_UNSUPPORTED;
     if (batch > 65536) return POLESTAR_ERR_UNSUPPORTED;
     const long m_max = static_cast<long>(batch) * (k_max + block_len);

@@ -28,22 +28,28 @@ struct GemmArgs {
     int block_start, block_len;
     char* out0;   // refresh: k_cache (row pitch n0); block rows: [rows][N]
     char* out1;   // refresh: v_cache (row pitch N - n0)
-    float* ws;    // split-K partials [ksplit][m_max][N]
+    float* ws;          // split-K partials [split][m_max][N] fp32
     int m_max;
     int ksplit;
     int steps_per_split;
+    int row_tiles, col_tiles;
 };
 
 struct GemmPlan {
+    bool small;         // gemm_small_kernel (<= 64 rows) instead of gemm_rows_kernel
     int mt;             // 16-row MFMA tiles per workgroup
     int row_tiles;
     int col_tiles;
     int ksplit;
     int steps_per_split;
+    int grid;           // workgroups of gemm_rows_kernel
     size_t ws_bytes;    // fp32 partials, 0 when ksplit == 1
 };
 
 GemmPlan gemm_plan(bool bf16, long m_max, int N, int K);
+
+// The GEMMs stream K in super-steps of 256 bytes per row: 128 bf16 or 64 fp32.
+inline bool gemm_k_ok(bool bf16, int K) { return K > 0 && K % (bf16 ? 128 : 64) == 0; }
 
 // Enqueue the GEMM (and the split-K reduction when the plan splits K).
 // `g.ws` must hold plan.ws_bytes.  Returns POLESTAR_OK or a launch error.

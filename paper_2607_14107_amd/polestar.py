@@ -106,7 +106,8 @@ def _workspace(nbytes: int, device, ws: torch.Tensor | None) -> torch.Tensor | N
         return ws
     if ws is not None and ws.numel() * ws.element_size() >= nbytes:
         return ws
-    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    # zero-filled once: the library keeps arrival counters in it
+    return torch.zeros(nbytes, dtype=torch.uint8, device=device)
 
 
 # ---------------------------------------------------------------------------
