@@ -11,8 +11,19 @@ perturbed.  Inputs are seeded synthetic data, resident in HBM before timing.
 
 To measure HBM rather than the 256 MB Infinity Cache, every step reads one of
 R independent copies of all inputs and weights (R * working set > 256 MB),
-round robin.  Per-call durations come from HIP events recorded on the launch
-stream around each call inside the timed region.  One JSON line is printed.
+round robin.  After the warmup, an untimed diagnostic pass records HIP events
+around every call (the per-call breakdown, "calls_us") and names the dominant
+call; in the timed region events on the launch stream bracket that call only,
+which gives the roofline's launch duration.  One JSON line is printed.
+
+Counter summaries (HBM traffic of the dominant call):
+
+    python bench.py --copy-calibration      # a plain 1 GiB device copy, for the
+                                            # FETCH_SIZE / WRITE_SIZE scale factor
+    python bench.py --summarize-counters FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR
+
+read rocprofv3 --pmc output directories and write
+profiles/<call>_<workload>_traffic.json.
 """
 
 from __future__ import annotations
@@ -46,6 +57,11 @@ def parse():
     p.add_argument("--copies", type=int, default=0, help="input copies rotated (0: enough for 512 MB)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=20.0)
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="run a plain 1 GiB device copy (counter scale factor) and exit")
+    p.add_argument("--summarize-counters", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH", "COPY_WRITE"),
+                   help="write the traffic summary of the dominant call from rocprofv3 --pmc output")
+    p.add_argument("--call", default="refresh_kv", help="call whose counters --summarize-counters reads")
     return p.parse_args()
 
 
@@ -69,25 +85,147 @@ def algorithmic_cost(cfg, k, es):
     return cost
 
 
-def source_digest(files):
+# Kernels launched by each call, and the sources they are built from.
+CALL_KERNELS = {
+    "refresh_kv": ("gemm_rows_kernel", "gemm_reduce_kernel", "gemm_small_kernel"),
+    "attend": ("gemm_small_kernel", "gemm_rows_kernel", "gemm_reduce_kernel", "attend_kernel",
+               "attend_merge_kernel"),
+    "drift": ("drift_kernel",),
+    "select": ("select_kernel",),
+    "commit": ("scan_kernel", "finalize_kernel"),
+}
+CALL_SOURCES = {
+    "refresh_kv": ("gemm.hip", "gemm.hpp"),
+    "attend": ("attend.hip", "gemm.hip", "gemm.hpp"),
+    "drift": ("drift.hip",),
+    "select": ("select.hip",),
+    "commit": ("commit.hip",),
+}
+COPY_BYTES = 1 << 30
+
+
+def source_digest(call):
+    """Digest of the sources a call's kernels are built from (changes when the
+    kernels do, which retires a counter summary)."""
     h = hashlib.sha256()
-    for f in files:
-        with open(os.path.join(ROOT, f), "rb") as fh:
+    for f in CALL_SOURCES[call] + ("common.hpp", "host_common.hpp"):
+        with open(os.path.join(ROOT, "paper_2607_14107_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def traffic_for(kernel_files, per_launch_units):
-    """HBM bytes per launch from the committed counter summary, or None when
-    the summary is missing or the kernel changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", "refresh_kv_traffic.json")
+def traffic_path(call, workload):
+    return os.path.join(ROOT, "profiles", f"{call}_{workload}_traffic.json")
+
+
+def traffic_for(call, workload):
+    """HBM bytes per launch of `call` from the committed counter summary, or
+    None when there is none or the kernels changed since it was taken."""
+    path = traffic_path(call, workload)
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
-    if t.get("source_digest") != source_digest(kernel_files):
+    if t.get("source_digest") != source_digest(call):
         return None
     return t.get("bytes_per_launch")
+
+
+def copy_calibration():
+    """A plain device-to-device copy of COPY_BYTES (the scale factor of the
+    FETCH_SIZE / WRITE_SIZE counters: known bytes / counted bytes)."""
+    import torch
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 3}))
+    return 0
+
+
+def _counter_rows(directory, counter):
+    """(dispatch id, kernel name, value) per dispatch from the counter CSVs
+    rocprofv3 --pmc wrote under `directory`."""
+    import csv
+    import glob
+    out = {}
+    for path in glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r.get("Counter_Name") != counter:
+                    continue
+                key = int(r["Dispatch_Id"])
+                name = r["Kernel_Name"]
+                prev = out.get(key, (name, 0.0))
+                out[key] = (name, prev[1] + float(r["Counter_Value"]))
+    return sorted((k, v[0], v[1]) for k, v in out.items())
+
+
+def _call_launch_kib(rows, call):
+    """Counter KiB per launch of `call`: the dispatches of its most frequent
+    leading kernel, each with the dispatches of the same call that follow it."""
+    names = CALL_KERNELS[call]
+    lead = [n for _, n, _ in rows if names[0] in n]
+    if not lead:
+        lead = [n for _, n, _ in rows if any(k in n for k in names)]
+    from collections import Counter
+    main = Counter(lead).most_common(1)[0][0]
+    per_launch = []
+    i = 0
+    while i < len(rows):
+        _, name, v = rows[i]
+        if name == main:
+            tot = v
+            j = i + 1
+            while j < len(rows) and rows[j][1] != main and any(k in rows[j][1] for k in names[1:]):
+                tot += rows[j][2]
+                j += 1
+            per_launch.append(tot)
+            i = j
+        else:
+            i += 1
+    return main, per_launch
+
+
+def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, call, workload):
+    def copy_kib(d, counter):
+        vals = [v for _, n, v in _counter_rows(d, counter) if "copy" in n.lower()]
+        if not vals:
+            raise SystemExit(f"no copy dispatch with {counter} under {d}")
+        return float(np.median(vals))
+    f_fetch = COPY_BYTES / (copy_kib(copy_fetch_dir, "FETCH_SIZE") * 1024)
+    f_write = COPY_BYTES / (copy_kib(copy_write_dir, "WRITE_SIZE") * 1024)
+    main, fetch = _call_launch_kib(_counter_rows(fetch_dir, "FETCH_SIZE"), call)
+    _, write = _call_launch_kib(_counter_rows(write_dir, "WRITE_SIZE"), call)
+    fetch_kib, write_kib = float(np.median(fetch)), float(np.median(write))
+    t = {
+        "call": call, "workload": workload, "lead_kernel": main,
+        "launches_counted": [len(fetch), len(write)],
+        "fetch_kib_per_launch": round(fetch_kib, 1), "write_kib_per_launch": round(write_kib, 1),
+        "copy_scale_fetch": round(f_fetch, 4), "copy_scale_write": round(f_write, 4),
+        "bytes_per_launch": int(fetch_kib * 1024 * f_fetch + write_kib * 1024 * f_write),
+        "source_digest": source_digest(call),
+        "commands": [
+            "cd /tmp && export TMPDIR=/tmp",
+            "rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/pmc_fetch -o c -- "
+            "python3 $R/bench.py --no-cpu-baseline --steps 20 --warmup 2",
+            "rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/pmc_write -o c -- "
+            "python3 $R/bench.py --no-cpu-baseline --steps 20 --warmup 2",
+            "rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/pmc_cfetch -o c -- python3 $R/bench.py --copy-calibration",
+            "rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/pmc_cwrite -o c -- python3 $R/bench.py --copy-calibration",
+            f"python3 $R/bench.py --summarize-counters gpurun_out/pmc_fetch gpurun_out/pmc_write "
+            f"gpurun_out/pmc_cfetch gpurun_out/pmc_cwrite --call {call}",
+        ],
+        "note": "counter KiB per launch summed over the call's kernels (median over launches); "
+                "bytes = KiB * 1024 * (copy bytes / copy counter bytes) for FETCH and WRITE",
+    }
+    with open(traffic_path(call, workload), "w") as f:
+        json.dump(t, f, indent=1)
+        f.write("\n")
+    print(json.dumps(t))
+    return 0
 
 
 def cpu_baseline(cfg, x, k, budget_s):
@@ -126,6 +264,11 @@ def cpu_baseline(cfg, x, k, budget_s):
 
 def main():
     args = parse()
+    if args.summarize_counters:
+        from paper_2607_14107_amd import inputs
+        return summarize_counters(*args.summarize_counters, args.call, inputs.CONFIGS[args.config].name)
+    if args.copy_calibration:
+        return copy_calibration()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the layer step shards over the batch with no exchange, see DESIGN.md)", file=sys.stderr)
@@ -181,56 +324,67 @@ def main():
 
     stream = torch.cuda.current_stream()
 
-    def run_step(i, ev=None):
-        s = sets[i % copies]
+    def call(name, s):
         sh = step.shape
-        if ev is not None:
-            ev[0].record(stream)
-        P.drift(s["h_cur"], s["h_prev"], out=step.drift)
-        if ev is not None:
-            ev[1].record(stream)
-        if k > 0:
-            P.select(step.drift, k, sh["block_start"], sh["block_len"], None, step.stale_idx, step.stale_count)
-        if ev is not None:
-            ev[2].record(stream)
-        P.refresh_kv(s["h_cur"], step.stale_idx, step.stale_count, sh["block_start"], sh["block_len"],
-                     s["w_k"], s["w_v"], s["k_cache"], s["v_cache"], workspace=step.ws_refresh)
-        if ev is not None:
-            ev[3].record(stream)
-        P.attend(s["h_cur"], s["w_q"], s["k_cache"], s["v_cache"], sh["block_start"], sh["block_len"],
-                 sh["n_heads"], q_buf=step.q_buf, out=step.out, lse=step.lse, workspace=step.ws_attend)
-        if ev is not None:
-            ev[4].record(stream)
-        P.commit(s["logits"], s["masked"], step.drift, sh["block_start"], s["hist"], s["hist_len"], -1,
-                 cfg.tau_s, cfg.alpha, False, step.token, step.conf, step.commit, workspace=step.ws_commit)
-        if ev is not None:
-            ev[5].record(stream)
+        if name == "drift":
+            P.drift(s["h_cur"], s["h_prev"], out=step.drift)
+        elif name == "select":
+            if k > 0:
+                P.select(step.drift, k, sh["block_start"], sh["block_len"], None, step.stale_idx, step.stale_count)
+        elif name == "refresh_kv":
+            P.refresh_kv(s["h_cur"], step.stale_idx, step.stale_count, sh["block_start"], sh["block_len"],
+                         s["w_k"], s["w_v"], s["k_cache"], s["v_cache"], workspace=step.ws_refresh)
+        elif name == "attend":
+            P.attend(s["h_cur"], s["w_q"], s["k_cache"], s["v_cache"], sh["block_start"], sh["block_len"],
+                     sh["n_heads"], q_buf=step.q_buf, out=step.out, lse=step.lse, workspace=step.ws_attend)
+        else:
+            P.commit(s["logits"], s["masked"], step.drift, sh["block_start"], s["hist"], s["hist_len"], -1,
+                     cfg.tau_s, cfg.alpha, False, step.token, step.conf, step.commit, workspace=step.ws_commit)
+
+    def run_step(i, ev=None, only=None):
+        """One whole step; events around every call (ev: list of 6) or
+        around the call named `only` (ev: list of 2)."""
+        s = sets[i % copies]
+        for j, name in enumerate(CALLS):
+            if ev is not None and only is None:
+                ev[j].record(stream)
+            if ev is not None and name == only:
+                ev[0].record(stream)
+            call(name, s)
+            if ev is not None and name == only:
+                ev[1].record(stream)
+        if ev is not None and only is None:
+            ev[len(CALLS)].record(stream)
 
     for i in range(args.warmup):
         run_step(i)
     torch.cuda.synchronize()
 
-    # timed region: K whole steps, with events around each call
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    # diagnostic pass (untimed): events around every call give the per-call
+    # breakdown and name the dominant call
+    ndiag = max(1, min(args.steps, 50))
+    dev_events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)] for _ in range(ndiag)]
+    for i in range(ndiag):
+        run_step(i, dev_events[i])
+    torch.cuda.synchronize()
+    call_us = {c: float(np.mean([ev[j].elapsed_time(ev[j + 1]) * 1e3 for ev in dev_events]))
+               for j, c in enumerate(CALLS)}
+    dom = max(call_us, key=call_us.get)
+
+    # timed region: K whole steps; HIP events on the launch stream bracket
+    # the dominant call only
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        run_step(args.warmup + i, events[i])
+        run_step(args.warmup + i, events[i], only=dom)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-
-    per_call = {c: [] for c in CALLS}
-    for ev in events:
-        for j, c in enumerate(CALLS):
-            per_call[c].append(ev[j].elapsed_time(ev[j + 1]) * 1e3)   # us
-    call_us = {c: float(np.mean(v)) for c, v in per_call.items()}
+    dom_us = float(np.mean([ev[0].elapsed_time(ev[1]) * 1e3 for ev in events]))
 
     tokens = cfg.batch * cfg.block_len
     value = tokens * args.steps / elapsed
     cost = algorithmic_cost(cfg, k, es)
-    # dominant call: the longest one
-    dom = max(call_us, key=call_us.get)
-    dom_us = call_us[dom]
     c = cost[dom]
     flops_rate = c["flops"] / (dom_us * 1e-6) / 1e12
     bytes_rate = c["bytes"] / (dom_us * 1e-6) / 1e9
@@ -243,7 +397,8 @@ def main():
         roof = {"bound": "hbm", "achieved": round(bytes_rate, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(bytes_rate / HBM_PEAK_GBS, 4)}
     roof["kernel"] = dom
-    roof["traffic"] = traffic_for(["paper_2607_14107_amd/csrc/gemm.hip"], 1) if dom == "refresh_kv" else None
+    roof["launch_us"] = round(dom_us, 3)
+    roof["traffic"] = traffic_for(dom, cfg.name)
 
     calls = {}
     for name in CALLS:

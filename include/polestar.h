@@ -206,7 +206,8 @@ polestar_status polestar_attend(polestar_dtype dtype, int batch, int seq, int d,
  *   token, conf, commit : [batch][block_len] int32 / float / uint8 outputs
  *   workspace : >= polestar_commit_workspace_size(...) bytes
  * Requires block_len, vocab > 0, h >= 0, mask_token_id < vocab, and
- * block_start + block_len <= seq when drift != NULL.
+ * block_start + block_len <= seq when drift != NULL.  UNSUPPORTED for
+ * block_len > 1024, h > 16, or vocab not a whole number of 16-byte chunks.
  */
 size_t polestar_commit_workspace_size(polestar_dtype dtype, int batch, int block_len,
                                       int vocab);

@@ -17,6 +17,8 @@ namespace ps {
 namespace {
 
 constexpr int kScanBlock = 256;
+constexpr int kMaxSplits = 16;    // vocabulary slices per token
+constexpr int kMaxHist = 16;      // drift history depth h
 
 struct ScanPart {
     float m;
@@ -121,14 +123,16 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(const char* __restrict
 // The fp32 rule, written without contraction so that the operation order is
 // the documented one.
 #pragma clang fp contract(off)
-__device__ bool commit_rule(float c, float dlt, bool use_drift, const float* hist_col, int hstride,
-                            int n, float tau_s, float alpha) {
+__device__ bool commit_rule(float c, float dlt, bool use_drift, const float* hv, int n, float tau_s,
+                            float alpha) {
     if (c > tau_s) return true;
     if (!use_drift) return false;
     float mu = 0.f;
     if (n > 0) {
         float s = 0.f;
-        for (int r = 0; r < n; ++r) s = s + hist_col[r * hstride];
+#pragma unroll
+        for (int r = 0; r < kMaxHist; ++r)
+            if (r < n) s = s + hv[r];
         mu = s / static_cast<float>(n);
     }
     const float D = dlt - mu;
@@ -150,33 +154,40 @@ __global__ __launch_bounds__(1024) void finalize_kernel(const ScanPart* __restri
     __shared__ unsigned long long best_key;
     const int b = blockIdx.x;
     const int j = threadIdx.x;
+    const bool inb = j < nq;
+    const int jc = inb ? j : 0;
+    const size_t tok = static_cast<size_t>(b) * nq + jc;
+
+    // Every load of this thread is issued up front (one memory round trip):
+    // the slice partials, the mask, the drift and the history column.
+    ScanPart pv[kMaxSplits];
+#pragma unroll
+    for (int q = 0; q < kMaxSplits; ++q) pv[q] = parts[tok * splits + (q < splits ? q : 0)];
+    const int n = (h > 0 && hist_len) ? min(max(hist_len[b], 0), h) : 0;
+    const bool is_masked = masked[tok] != 0;
+    const float dlt = drift ? drift[static_cast<size_t>(b) * seq + block_start + jc] : 0.f;
+    float hv[kMaxHist];
+    float* hcol = hist ? hist + static_cast<size_t>(b) * h * nq + jc : nullptr;
+#pragma unroll
+    for (int r = 0; r < kMaxHist; ++r) hv[r] = (hcol && r < h) ? hcol[r * nq] : 0.f;
+
     if (j == 0) {
         any_commit = 0;
         best_key = 0ull;
     }
-    const int n = (h > 0 && hist_len) ? min(max(hist_len[b], 0), h) : 0;
-    __syncthreads();
-    const bool inb = j < nq;
-    const size_t tok = static_cast<size_t>(b) * nq + j;
-    float c = 0.f, dlt = 0.f;
-    bool is_masked = false, cm = false;
-    if (inb) {
-        const ScanPart* p = parts + tok * splits;
-        float m = p[0].m, s = p[0].s, bv = p[0].best;
-        int bi = p[0].idx;
-        for (int q = 1; q < splits; ++q) {
-            merge_ms(m, s, p[q].m, p[q].s);
-            better(bv, bi, p[q].best, p[q].idx);
+    float m = pv[0].m, ssum = pv[0].s, bv = pv[0].best;
+    int bi = pv[0].idx;
+#pragma unroll
+    for (int q = 1; q < kMaxSplits; ++q) {
+        if (q < splits) {
+            merge_ms(m, ssum, pv[q].m, pv[q].s);
+            better(bv, bi, pv[q].best, pv[q].idx);
         }
-        c = fast_exp2((bv - m) * kLog2e) / s;
-        token[tok] = bi;
-        conf[tok] = c;
-        is_masked = masked[tok] != 0;
-        if (drift) dlt = drift[static_cast<size_t>(b) * seq + block_start + j];
-        const float* hcol = hist ? hist + static_cast<size_t>(b) * h * nq + j : nullptr;
-        cm = is_masked && commit_rule(c, dlt, drift != nullptr, hcol, nq, n, tau_s, alpha);
-        if (cm) atomicOr(&any_commit, 1);
     }
+    const float c = fast_exp2((bv - m) * kLog2e) / ssum;
+    bool cm = inb && is_masked && commit_rule(c, dlt, drift != nullptr, hv, n, tau_s, alpha);
+    __syncthreads();                        // any_commit / best_key initialised
+    if (cm) atomicOr(&any_commit, 1);
     __syncthreads();
     if (force_one && !any_commit && inb && is_masked) {
         // largest confidence, then lowest position: key = (conf bits, ~j)
@@ -188,18 +199,22 @@ __global__ __launch_bounds__(1024) void finalize_kernel(const ScanPart* __restri
     if (force_one && !any_commit && inb && is_masked && best_key != 0ull &&
         static_cast<int>(0xffffffffu - static_cast<uint32_t>(best_key & 0xffffffffull)) == j)
         cm = true;
-    if (inb) commit[tok] = cm ? 1 : 0;
-    // history push (all block positions), entries oldest first
-    if (inb && h > 0 && drift && hist) {
-        float* hcol = hist + static_cast<size_t>(b) * h * nq + j;
-        if (n < h) {
-            hcol[n * nq] = dlt;
-        } else {
-            for (int r = 0; r + 1 < h; ++r) hcol[r * nq] = hcol[(r + 1) * nq];
-            hcol[(h - 1) * nq] = dlt;
+    if (inb) {
+        token[tok] = bi;
+        conf[tok] = c;
+        commit[tok] = cm ? 1 : 0;
+        // history push (all block positions), entries oldest first
+        if (h > 0 && drift && hist) {
+            if (n < h) {
+                hcol[n * nq] = dlt;
+            } else {
+#pragma unroll
+                for (int r = 0; r + 1 < kMaxHist; ++r)
+                    if (r + 1 < h) hcol[r * nq] = hv[r + 1];
+                hcol[(h - 1) * nq] = dlt;
+            }
         }
     }
-    __syncthreads();
     if (j == 0 && h > 0 && drift && hist_len) hist_len[b] = min(n + 1, h);
 }
 
@@ -216,6 +231,7 @@ CommitPlan commit_plan(bool bf16, int batch, int nq, int vocab) {
     int splits = static_cast<int>((512 + toks - 1) / toks);
     const int max_splits = ceil_div(vocab, 2048);
     if (splits > max_splits) splits = max_splits;
+    if (splits > kMaxSplits) splits = kMaxSplits;
     if (splits < 1) splits = 1;
     p.chunk = ceil_div(ceil_div(vocab, splits), e) * e;
     p.splits = ceil_div(vocab, p.chunk);
@@ -248,7 +264,7 @@ extern "C" polestar_status polestar_commit(polestar_dtype dtype, int batch, int 
         (drift && (seq <= 0 || block_start < 0 || block_start > seq - block_len)))
         return POLESTAR_ERR_INVALID_ARGUMENT;
     if (!row_ok(dtype, vocab) || !aligned16(logits) || block_len > 1024 || batch > 65535 ||
-        block_len > 65535)
+        h > kMaxHist)
         return POLESTAR_ERR_UNSUPPORTED;
     const bool bf16 = dtype == POLESTAR_BF16;
     const CommitPlan p = commit_plan(bf16, batch, block_len, vocab);

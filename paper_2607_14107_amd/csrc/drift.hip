@@ -2,9 +2,11 @@
 // states (Sec. 3, eq. "drift"; the distribution of a token is the softmax of
 // its hidden state over the d channels).
 //
-// One wavefront owns one row: it loads the two rows of the token once with
-// coalesced 16-byte loads into registers (an HBM-bound stream of 2*d
-// elements), reduces the common max, then accumulates in fp32
+// A row is spread over 64-256 threads (4 waves at d = 4096, two 16-byte
+// chunks of each row per lane): the two rows of the token are loaded once
+// with coalesced 16-byte loads into registers (an HBM-bound stream of 2*d
+// elements), the common max is reduced (shuffles, then LDS across the
+// row's waves), then the thread accumulates in fp32
 //   Zb  = sum e_c,              e_c = exp(b_c - m)
 //   Sqe = sum e_c * expm1(dlt_c),   dlt = a - b
 //   Spd = sum e_c * (1 + expm1(dlt_c)) * dlt_c
@@ -18,8 +20,7 @@
 namespace ps {
 namespace {
 
-constexpr int kDriftBlock = 256;               // 4 waves, one row each
-constexpr int kRowsPerBlock = kDriftBlock / kWave;
+constexpr int kDriftBlock = 256;
 constexpr float kSmall = 0.0625f;              // |dlt| below this: series for expm1
 
 // expm1 for |x| < 1/16 from its Taylor series; the first omitted term
@@ -36,118 +37,131 @@ __device__ __forceinline__ float expm1_any(float x) {
     return fabsf(x) < kSmall ? expm1_small(x) : fast_exp2(x * kLog2e) - 1.0f;
 }
 
-template <bool BF16, int NCH>
+// Reduce NV values at once over the TPR threads of a row: wave shuffles,
+// then one LDS round across the row's waves.  `red` holds NV floats per wave.
+template <int TPR, int NV, bool MAX>
+__device__ __forceinline__ void row_reduce(float (&v)[NV], float* red) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = MAX ? wave_max(v[i]) : wave_sum(v[i]);
+    if constexpr (TPR > kWave) {
+        const int w = threadIdx.x >> 6;
+        const int lane = threadIdx.x & 63;
+        constexpr int W = TPR / kWave;        // waves per row
+        if (lane == 0) {
+#pragma unroll
+            for (int i = 0; i < NV; ++i) red[w * NV + i] = v[i];
+        }
+        __syncthreads();
+        const int first = (w / W) * W;
+#pragma unroll
+        for (int i = 0; i < NV; ++i) {
+            float x = red[first * NV + i];
+#pragma unroll
+            for (int q = 1; q < W; ++q) x = MAX ? fmaxf(x, red[(first + q) * NV + i]) : x + red[(first + q) * NV + i];
+            v[i] = x;
+        }
+        __syncthreads();
+    }
+}
+
+// One row of d elements per TPR threads (TPR = 64, 128 or 256); each thread
+// keeps NCH 16-byte chunks of both rows in registers.  Rows of a workgroup:
+// kDriftBlock / TPR.
+template <bool BF16, int TPR, int NCH>
 __global__ __launch_bounds__(kDriftBlock) void drift_kernel(const char* __restrict__ hc,
                                                             const char* __restrict__ hp,
                                                             float* __restrict__ out,
                                                             int rows, int d) {
     using T = Elem<BF16>;
-    const int lane = threadIdx.x & 63;
-    const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
-    if (row >= rows) return;
+    __shared__ float red[3 * (kDriftBlock / kWave)];
+    const int tr = threadIdx.x % TPR;             // thread within the row
+    const int row_raw = blockIdx.x * (kDriftBlock / TPR) + threadIdx.x / TPR;
+    const bool live = row_raw < rows;
+    const int row = live ? row_raw : rows - 1;    // keep every thread in the reductions
     const size_t base = static_cast<size_t>(row) * d * T::kBytes;
+    const int chunks = d / T::E;
 
+    // Unconditional loads: chunks past the row end re-read chunk 0 and are
+    // masked out of the arithmetic.
     uint4 ra[NCH], rb[NCH];
+    bool ok[NCH];
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-        const int e0 = (c * kWave + lane) * T::E;
-        if (e0 < d) {
-            ra[c] = ld16(hc + base + static_cast<size_t>(e0) * T::kBytes);
-            rb[c] = ld16(hp + base + static_cast<size_t>(e0) * T::kBytes);
-        }
+        const int ch = c * TPR + tr;
+        ok[c] = ch < chunks;
+        const size_t off = base + static_cast<size_t>(ok[c] ? ch : 0) * 16;
+        ra[c] = ld16(hc + off);
+        rb[c] = ld16(hp + off);
     }
 
     // Pass 1: common maximum and the largest |dlt| of the row.
     float m = -INFINITY, big = 0.0f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-        const int e0 = (c * kWave + lane) * T::E;
-        if (e0 < d) {
-            float a[T::E], b[T::E];
-            T::unpack(ra[c], a);
-            T::unpack(rb[c], b);
+        float a[T::E], b[T::E];
+        T::unpack(ra[c], a);
+        T::unpack(rb[c], b);
 #pragma unroll
-            for (int j = 0; j < T::E; ++j) {
-                m = fmaxf(m, fmaxf(a[j], b[j]));
-                big = fmaxf(big, fabsf(a[j] - b[j]));
-            }
+        for (int j = 0; j < T::E; ++j) {
+            m = fmaxf(m, ok[c] ? fmaxf(a[j], b[j]) : -INFINITY);
+            big = fmaxf(big, ok[c] ? fabsf(a[j] - b[j]) : 0.0f);
         }
     }
-    m = wave_max(m);
-    big = wave_max(big);
+    {
+        float mx[2] = {m, big};
+        row_reduce<TPR, 2, true>(mx, red);
+        m = mx[0];
+        big = mx[1];
+    }
     const float mlog = m * kLog2e;
 
-    // Pass 2: the three sums.
+    // Pass 2: the three sums (masked chunks contribute nothing).
     float zb = 0.0f, sqe = 0.0f, spd = 0.0f;
-    if (big < kSmall) {
+    const bool light = big < kSmall;
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            const int e0 = (c * kWave + lane) * T::E;
-            if (e0 < d) {
-                float a[T::E], b[T::E];
-                T::unpack(ra[c], a);
-                T::unpack(rb[c], b);
+    for (int c = 0; c < NCH; ++c) {
+        float a[T::E], b[T::E];
+        T::unpack(ra[c], a);
+        T::unpack(rb[c], b);
+        const float keep = ok[c] ? 1.0f : 0.0f;
 #pragma unroll
-                for (int j = 0; j < T::E; ++j) {
-                    const float dl = a[j] - b[j];
-                    const float e = fast_exp2(fmaf(b[j], kLog2e, -mlog));
-                    const float em = expm1_small(dl);
-                    zb += e;
-                    sqe = fmaf(e, em, sqe);
-                    spd = fmaf(fmaf(e, em, e), dl, spd);
-                }
-            }
-        }
-    } else {
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            const int e0 = (c * kWave + lane) * T::E;
-            if (e0 < d) {
-                float a[T::E], b[T::E];
-                T::unpack(ra[c], a);
-                T::unpack(rb[c], b);
-#pragma unroll
-                for (int j = 0; j < T::E; ++j) {
-                    const float dl = a[j] - b[j];
-                    const float e = fast_exp2(fmaf(b[j], kLog2e, -mlog));
-                    const float em = expm1_any(dl);
-                    zb += e;
-                    sqe = fmaf(e, em, sqe);
-                    spd = fmaf(fmaf(e, em, e), dl, spd);
-                }
-            }
+        for (int j = 0; j < T::E; ++j) {
+            const float dl = a[j] - b[j];
+            const float e = keep * fast_exp2(fmaf(b[j], kLog2e, -mlog));
+            const float em = light ? expm1_small(dl) : expm1_any(dl);
+            zb += e;
+            sqe = fmaf(e, em, sqe);
+            spd = fmaf(fmaf(e, em, e), dl, spd);
         }
     }
-    zb = wave_sum(zb);
-    sqe = wave_sum(sqe);
-    spd = wave_sum(spd);
-    if (lane == 0) out[row] = spd / (zb + sqe) - log1pf(sqe / zb);
+    {
+        float sums[3] = {zb, sqe, spd};
+        row_reduce<TPR, 3, false>(sums, red);
+        zb = sums[0];
+        sqe = sums[1];
+        spd = sums[2];
+    }
+    if (live && tr == 0) out[row] = spd / (zb + sqe) - log1pf(sqe / zb);
 }
 
-template <bool BF16, int NCH>
+template <bool BF16, int TPR, int NCH>
 void launch(const void* hc, const void* hp, float* out, int rows, int d, hipStream_t s) {
-    dim3 grid(ceil_div(rows, kRowsPerBlock));
-    hipLaunchKernelGGL((drift_kernel<BF16, NCH>), grid, dim3(kDriftBlock), 0, s,
+    dim3 grid(ceil_div(rows, kDriftBlock / TPR));
+    hipLaunchKernelGGL((drift_kernel<BF16, TPR, NCH>), grid, dim3(kDriftBlock), 0, s,
                        static_cast<const char*>(hc), static_cast<const char*>(hp), out, rows, d);
 }
 
+// chunks per row -> (threads per row, chunks per thread)
 template <bool BF16>
-bool dispatch(int nch, const void* hc, const void* hp, float* out, int rows, int d,
+bool dispatch(int chunks, const void* hc, const void* hp, float* out, int rows, int d,
               hipStream_t s) {
-    switch (nch) {
-        case 1: launch<BF16, 1>(hc, hp, out, rows, d, s); return true;
-        case 2: launch<BF16, 2>(hc, hp, out, rows, d, s); return true;
-        case 3: launch<BF16, 3>(hc, hp, out, rows, d, s); return true;
-        case 4: launch<BF16, 4>(hc, hp, out, rows, d, s); return true;
-        case 5: launch<BF16, 5>(hc, hp, out, rows, d, s); return true;
-        case 6: launch<BF16, 6>(hc, hp, out, rows, d, s); return true;
-        case 7: launch<BF16, 7>(hc, hp, out, rows, d, s); return true;
-        case 8: launch<BF16, 8>(hc, hp, out, rows, d, s); return true;
-        case 10: launch<BF16, 10>(hc, hp, out, rows, d, s); return true;
-        case 12: launch<BF16, 12>(hc, hp, out, rows, d, s); return true;
-        case 16: launch<BF16, 16>(hc, hp, out, rows, d, s); return true;
-        default: return false;
-    }
+    if (chunks <= 64) { launch<BF16, 64, 1>(hc, hp, out, rows, d, s); return true; }
+    if (chunks <= 128) { launch<BF16, 64, 2>(hc, hp, out, rows, d, s); return true; }
+    if (chunks <= 256) { launch<BF16, 128, 2>(hc, hp, out, rows, d, s); return true; }
+    if (chunks <= 512) { launch<BF16, 256, 2>(hc, hp, out, rows, d, s); return true; }
+    if (chunks <= 1024) { launch<BF16, 256, 4>(hc, hp, out, rows, d, s); return true; }
+    if (chunks <= 2048) { launch<BF16, 256, 8>(hc, hp, out, rows, d, s); return true; }
+    return false;
 }
 
 }  // namespace
@@ -162,18 +176,11 @@ extern "C" polestar_status polestar_drift(polestar_dtype dtype, int batch, int s
     if (!row_ok(dtype, d) || !aligned16(h_cur) || !aligned16(h_prev) || !aligned16(drift))
         return POLESTAR_ERR_UNSUPPORTED;
     const bool bf16 = dtype == POLESTAR_BF16;
-    const int per_chunk = kWave * (bf16 ? 8 : 4);
-    int nch = ceil_div(d, per_chunk);
-    // round the register budget up to an instantiated size
-    static const int sizes[] = {1, 2, 3, 4, 5, 6, 7, 8, 10, 12, 16};
-    int pick = 0;
-    for (int s : sizes)
-        if (s >= nch) { pick = s; break; }
-    if (pick == 0) return POLESTAR_ERR_UNSUPPORTED;   // d above 8192 (bf16) / 4096 (fp32)
     const long rows = static_cast<long>(batch) * seq;
     if (rows > 0x7fffffffL) return POLESTAR_ERR_UNSUPPORTED;
-    bool ok = bf16 ? dispatch<true>(pick, h_cur, h_prev, drift, static_cast<int>(rows), d, stream)
-                   : dispatch<false>(pick, h_cur, h_prev, drift, static_cast<int>(rows), d, stream);
-    if (!ok) return POLESTAR_ERR_UNSUPPORTED;
+    const int chunks = d / (bf16 ? 8 : 4);
+    const bool ok = bf16 ? dispatch<true>(chunks, h_cur, h_prev, drift, static_cast<int>(rows), d, stream)
+                         : dispatch<false>(chunks, h_cur, h_prev, drift, static_cast<int>(rows), d, stream);
+    if (!ok) return POLESTAR_ERR_UNSUPPORTED;   // d above 16384 (bf16) / 8192 (fp32)
     return launch_status();
 }

@@ -38,6 +38,8 @@ constexpr int kGemmBlock = 256;
 constexpr int kLda = 272;         // LDS row pitch (bytes) of the staged input rows
 constexpr int kTargetWgs = 256;   // one workgroup per compute unit on MI355X
 constexpr int kMaxSplit = 8;
+constexpr int kSmallWaves = 4;    // gemm_small_kernel: waves per workgroup
+constexpr int kSmallBlock = kSmallWaves * 64;
 
 // Row bookkeeping --------------------------------------------------------------
 // Refresh mode: sequence b contributes count_b stale rows followed by its
@@ -340,13 +342,13 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_reduce_kernel(GemmArgs g) {
 // ---------------------------------------------------------------------------
 
 template <bool BF16, int MT>
-__global__ __launch_bounds__(kGemmBlock) void gemm_small_kernel(GemmArgs g) {
+__global__ __launch_bounds__(kSmallBlock) void gemm_small_kernel(GemmArgs g) {
     using T = Elem<BF16>;
     constexpr int ES = T::kBytes;
     constexpr int BM = MT * 16;
     __shared__ int rowb[BM], rowp[BM];
     __shared__ int scan_tmp[17];
-    __shared__ float red[4][BM][17];
+    __shared__ float red[kSmallWaves][BM][17];
     extern __shared__ int pre[];
 
     const int t = threadIdx.x;
@@ -356,10 +358,11 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_small_kernel(GemmArgs g) {
     const int m0 = blockIdx.y * BM;
     const int kcol = (lane >> 4) * 64;
     const int nsteps = g.K / (256 / ES);
-    // wave w: super-steps w, w+4, ...; the last one it owns is slast
+    // wave w: super-steps w, w+W, ...; the last one it owns is slast
     // (prefetches past it re-read slast and are ignored).
-    const int nmine = w < nsteps ? (nsteps - 1 - w) / 4 + 1 : 0;
-    const int slast = w < nsteps ? w + 4 * (nmine - 1) : 0;
+    constexpr int W = kSmallWaves;
+    const int nmine = w < nsteps ? (nsteps - 1 - w) / W + 1 : 0;
+    const int slast = w < nsteps ? w + W * (nmine - 1) : 0;
 
     // Weight row of column col0 + lane%16 (past N: row 0, never stored); its
     // first two super-steps are requested before the row bookkeeping.
@@ -371,7 +374,7 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_small_kernel(GemmArgs g) {
     };
     uint4 q0[4], q1[4], q2[4];
     load_b(min(w, slast), q0);
-    load_b(min(w + 4, slast), q1);
+    load_b(min(w + W, slast), q1);
 
     const int total = g.mode == kGemmRefresh ? build_prefix(g, pre, scan_tmp)
                                              : g.batch * g.block_len;
@@ -410,12 +413,12 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_small_kernel(GemmArgs g) {
 
     uint4 a0[MT][4], a1[MT][4], a2[MT][4];
     load_a(min(w, slast), a0);
-    load_a(min(w + 4, slast), a1);
+    load_a(min(w + W, slast), a1);
 #define PS_SMALL_STEP(I, A_USE, B_USE, A_LOAD, B_LOAD)                      \
     {                                                                       \
         __builtin_amdgcn_sched_barrier(0);                                  \
-        load_a(min(w + 4 * ((I) + 2), slast), A_LOAD);                      \
-        load_b(min(w + 4 * ((I) + 2), slast), B_LOAD);                      \
+        load_a(min(w + W * ((I) + 2), slast), A_LOAD);                      \
+        load_b(min(w + W * ((I) + 2), slast), B_LOAD);                      \
         __builtin_amdgcn_sched_barrier(0);                                  \
         compute(A_USE, B_USE);                                              \
     }
@@ -429,21 +432,26 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_small_kernel(GemmArgs g) {
     if (ic + 1 < nmine) PS_SMALL_STEP(ic + 1, a1, q1, a0, q0)
 #undef PS_SMALL_STEP
 
-    // sum the four waves: lane holds rows mt*16 + 4*(lane/16) + i, column lane%16
+    // sum the waves in order: lane holds rows mt*16 + 4*(lane/16) + i, column lane%16
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) red[w][mt * 16 + 4 * (lane >> 4) + i][lane & 15] = acc[mt][i];
     __syncthreads();
     // thread -> (row r, 8 columns c)
-    for (int idx = t; idx < BM * 2; idx += kGemmBlock) {
+    for (int idx = t; idx < BM * 2; idx += kSmallBlock) {
         const int r = idx >> 1, c = (idx & 1) * 8;
         const int b = rowb[r];
         const int n = col0 + c;
         if (b < 0 || n >= g.N) continue;
         float v[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = ((red[0][r][c + j] + red[1][r][c + j]) + red[2][r][c + j]) + red[3][r][c + j];
+        for (int j = 0; j < 8; ++j) {
+            float acc_j = red[0][r][c + j];
+#pragma unroll
+            for (int q = 1; q < kSmallWaves; ++q) acc_j += red[q][r][c + j];
+            v[j] = acc_j;
+        }
         store8<BF16>(out_ptr<BF16>(g, b, rowp[r], m0 + r, n), v);
     }
 }
@@ -472,10 +480,10 @@ template <bool BF16>
 bool dispatch_small(const GemmPlan& p, const GemmArgs& g, size_t dyn, hipStream_t s) {
     dim3 grid(p.col_tiles, p.row_tiles);
     switch (p.mt) {
-        case 1: hipLaunchKernelGGL((gemm_small_kernel<BF16, 1>), grid, dim3(kGemmBlock), dyn, s, g); return true;
-        case 2: hipLaunchKernelGGL((gemm_small_kernel<BF16, 2>), grid, dim3(kGemmBlock), dyn, s, g); return true;
-        case 3: hipLaunchKernelGGL((gemm_small_kernel<BF16, 3>), grid, dim3(kGemmBlock), dyn, s, g); return true;
-        case 4: hipLaunchKernelGGL((gemm_small_kernel<BF16, 4>), grid, dim3(kGemmBlock), dyn, s, g); return true;
+        case 1: hipLaunchKernelGGL((gemm_small_kernel<BF16, 1>), grid, dim3(kSmallBlock), dyn, s, g); return true;
+        case 2: hipLaunchKernelGGL((gemm_small_kernel<BF16, 2>), grid, dim3(kSmallBlock), dyn, s, g); return true;
+        case 3: hipLaunchKernelGGL((gemm_small_kernel<BF16, 3>), grid, dim3(kSmallBlock), dyn, s, g); return true;
+        case 4: hipLaunchKernelGGL((gemm_small_kernel<BF16, 4>), grid, dim3(kSmallBlock), dyn, s, g); return true;
         default: return false;
     }
 }

@@ -1,26 +1,46 @@
 // polestar_select: TopK of the drift over the cached positions of each
 // sequence (Alg. 1, TopK; cached set I = J \ J_b of Sec. 2).
 //
-// One 1024-thread workgroup per sequence.  Each thread keeps IPT consecutive
-// positions in registers as order-preserving 32-bit keys of the fp32 drift
-// (+0.0 and -0.0 share one key).  A most-significant-digit-first radix
-// select (4 passes of 8 bits, histograms in LDS) finds the key T of the k-th
-// largest candidate and how many candidates equal to T are still needed;
-// those are taken lowest position first.  Two block prefix sums in position
-// order then rank the ties and write the chosen positions ascending.  The
-// work is integer-only and latency-bound (tens of KB per step).
+// One 256-thread workgroup (4 waves) per sequence.  Each thread keeps IPT
+// consecutive positions in registers as order-preserving 32-bit keys of the
+// fp32 drift (+0.0 and -0.0 share one key).  A most-significant-digit-first
+// radix select (4 passes of 8 bits, double-buffered histograms in LDS, two
+// barriers per pass) finds the key T of the k-th largest candidate and how
+// many candidates equal to T are still needed; those are taken lowest
+// position first.  Two prefix sums in position order then rank the ties and
+// write the chosen positions ascending.  The work is integer-only and
+// latency-bound (tens of KB per step), so the barrier count is what matters.
 #include "common.hpp"
 #include "host_common.hpp"
 
 namespace ps {
 namespace {
 
-constexpr int kSelBlock = 1024;
+constexpr int kSelBlock = 256;                 // 4 waves per sequence
+constexpr int kSelWaves = kSelBlock / kWave;
 
 __device__ __forceinline__ uint32_t order_key(float f) {
     uint32_t u = __float_as_uint(f);
     if (u == 0x80000000u) u = 0u;                       // -0.0 -> +0.0
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Exclusive prefix sum over the 4 waves of the workgroup in thread order.
+// `tot` holds kSelWaves ints of LDS owned by this call site.  One barrier.
+__device__ __forceinline__ int scan4(int v, int* tot, int* total) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int incl = wave_incl_scan(v, lane);
+    if (lane == 63) tot[w] = incl;
+    __syncthreads();
+    int before = 0, all = 0;
+#pragma unroll
+    for (int i = 0; i < kSelWaves; ++i) {
+        const int x = tot[i];
+        before += i < w ? x : 0;
+        all += x;
+    }
+    *total = all;
+    return before + incl - v;
 }
 
 template <int IPT>
@@ -29,10 +49,10 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(const float* __restri
                                                            int seq, int bs, int bl, int k,
                                                            int32_t* __restrict__ idx,
                                                            int32_t* __restrict__ cnt) {
-    __shared__ int hist[256];
-    __shared__ int scan_tmp[17];
-    __shared__ uint32_t sh_prefix;
-    __shared__ int sh_remaining;
+    __shared__ int hist[2][256];
+    __shared__ int tot[4][kSelWaves];
+    __shared__ uint32_t sh_prefix[4];
+    __shared__ int sh_remaining[4];
 
     const int b = blockIdx.x;
     const int t = threadIdx.x;
@@ -44,45 +64,52 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(const float* __restri
     const float* dr = drift + static_cast<size_t>(b) * seq;
     const uint8_t* el = elig ? elig + static_cast<size_t>(b) * seq : nullptr;
 
+    // keys in registers; positions p0 .. p0 + IPT - 1 of this thread
     uint32_t key[IPT];
     bool valid[IPT];
     int nv = 0;
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
         const int p = p0 + j;
-        bool v = p < seq && !(p >= bs && p < bs + bl);
-        if (v && el) v = el[p] != 0;
+        const int pc = p < seq ? p : 0;
+        const float dv = dr[pc];
+        const bool e = el ? el[pc] != 0 : true;
+        const bool v = p < seq && !(p >= bs && p < bs + bl) && e;
         valid[j] = v;
-        key[j] = v ? order_key(dr[p]) : 0u;
+        key[j] = v ? order_key(dv) : 0u;
         nv += v ? 1 : 0;
     }
+    hist[0][t] = 0;                     // first histogram buffer (one bin per thread)
     int n_cand;
-    (void)block_excl_scan(nv, scan_tmp, &n_cand);
+    (void)scan4(nv, tot[0], &n_cand);   // its barrier also publishes the cleared bins
 
     bool sel[IPT];
     if (k >= n_cand) {
 #pragma unroll
         for (int j = 0; j < IPT; ++j) sel[j] = valid[j];
     } else {
+        // Radix select, most significant byte first: find the key T of the
+        // k-th largest candidate and how many candidates equal to T to take.
         uint32_t prefix = 0u, pmask = 0u;
         int remaining = k;   // >= 1 here
-        for (int shift = 24; shift >= 0; shift -= 8) {
-            if (t < 256) hist[t] = 0;
-            __syncthreads();
+#pragma unroll
+        for (int pass = 0; pass < 4; ++pass) {
+            const int shift = 24 - 8 * pass;
+            int* h = hist[pass & 1];
+            hist[(pass + 1) & 1][t] = 0;        // next pass's buffer, idle since the last pass
 #pragma unroll
             for (int j = 0; j < IPT; ++j)
                 if (valid[j] && (key[j] & pmask) == prefix)
-                    atomicAdd(&hist[(key[j] >> shift) & 255u], 1);
+                    atomicAdd(&h[(key[j] >> shift) & 255u], 1);
             __syncthreads();
             if (t < kWave) {
                 // lane t owns bins 4t..4t+3; suffix sums from the top bin down
-                const int h0 = hist[4 * t], h1 = hist[4 * t + 1];
-                const int h2 = hist[4 * t + 2], h3 = hist[4 * t + 3];
+                const int h0 = h[4 * t], h1 = h[4 * t + 1], h2 = h[4 * t + 2], h3 = h[4 * t + 3];
                 const int own = h0 + h1 + h2 + h3;
                 int suf = own;   // inclusive suffix over lanes >= t
 #pragma unroll
                 for (int o = 1; o < kWave; o <<= 1) {
-                    int v = __shfl_down(suf, o);
+                    const int v = __shfl_down(suf, o);
                     if (t + o < kWave) suf += v;
                 }
                 int run = suf - own;   // count in bins above 4t+3
@@ -92,16 +119,15 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(const float* __restri
                     const int above = run;
                     run += hv[q];
                     if (run >= remaining && above < remaining) {
-                        sh_prefix = prefix | (static_cast<uint32_t>(4 * t + q) << shift);
-                        sh_remaining = remaining - above;
+                        sh_prefix[pass] = prefix | (static_cast<uint32_t>(4 * t + q) << shift);
+                        sh_remaining[pass] = remaining - above;
                     }
                 }
             }
             __syncthreads();
-            prefix = sh_prefix;
-            remaining = sh_remaining;
+            prefix = sh_prefix[pass];
+            remaining = sh_remaining[pass];
             pmask |= 255u << shift;
-            __syncthreads();
         }
         // prefix is the key T of the k-th largest; take `remaining` keys equal
         // to T, lowest position first.
@@ -109,7 +135,7 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(const float* __restri
 #pragma unroll
         for (int j = 0; j < IPT; ++j) neq += (valid[j] && key[j] == prefix) ? 1 : 0;
         int eq_total;
-        int eq_rank = block_excl_scan(neq, scan_tmp, &eq_total);
+        int eq_rank = scan4(neq, tot[1], &eq_total);
 #pragma unroll
         for (int j = 0; j < IPT; ++j) {
             const bool eq = valid[j] && key[j] == prefix;
@@ -122,7 +148,7 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(const float* __restri
 #pragma unroll
     for (int j = 0; j < IPT; ++j) ns += sel[j] ? 1 : 0;
     int total;
-    int pos = block_excl_scan(ns, scan_tmp, &total);
+    int pos = scan4(ns, tot[2], &total);
     int32_t* out = idx + static_cast<size_t>(b) * k;
 #pragma unroll
     for (int j = 0; j < IPT; ++j)
@@ -151,14 +177,15 @@ extern "C" polestar_status polestar_select(int batch, int seq, const float* drif
         return POLESTAR_ERR_INVALID_ARGUMENT;
     const int ipt = ceil_div(seq, kSelBlock);
     int32_t* idx = stale_idx;
-    switch (ipt <= 1 ? 1 : ipt <= 2 ? 2 : ipt <= 4 ? 4 : ipt <= 8 ? 8 : ipt <= 16 ? 16 : ipt <= 32 ? 32 : 0) {
-        case 1: launch<1>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream); break;
-        case 2: launch<2>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream); break;
-        case 4: launch<4>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream); break;
-        case 8: launch<8>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream); break;
-        case 16: launch<16>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream); break;
-        case 32: launch<32>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream); break;
-        default: return POLESTAR_ERR_UNSUPPORTED;   // seq above 32768
-    }
+    if (ipt <= 1) launch<1>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream);
+    else if (ipt <= 2) launch<2>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream);
+    else if (ipt <= 3) launch<3>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream);
+    else if (ipt <= 4) launch<4>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream);
+    else if (ipt <= 6) launch<6>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream);
+    else if (ipt <= 8) launch<8>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream);
+    else if (ipt <= 16) launch<16>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream);
+    else if (ipt <= 32) launch<32>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream);
+    else if (ipt <= 64) launch<64>(batch, seq, drift, eligible, block_start, block_len, k, idx, stale_count, stream);
+    else return POLESTAR_ERR_UNSUPPORTED;   // seq above 16384
     return launch_status();
 }

@@ -49,7 +49,7 @@ def test_drift_validation(L):
     assert f(1, 1, 4, 12, FAKE, FAKE, FAKE, None) == UNSUPPORTED     # bf16 rows need d % 8 == 0
     assert f(0, 1, 4, 6, FAKE, FAKE, FAKE, None) == UNSUPPORTED      # fp32 rows need d % 4 == 0
     assert f(1, 1, 4, 8, MISALIGNED, FAKE, FAKE, None) == UNSUPPORTED
-    assert f(1, 1, 4, 16384, FAKE, FAKE, FAKE, None) == UNSUPPORTED  # above the register budget
+    assert f(1, 1, 4, 32768, FAKE, FAKE, FAKE, None) == UNSUPPORTED  # above the register budget
 
 
 def test_select_validation(L):
@@ -59,7 +59,7 @@ def test_select_validation(L):
     assert f(1, 10, FAKE, None, 9, 2, 3, FAKE, FAKE, None) == INVALID        # block past the end
     assert f(1, 10, FAKE, None, 0, 2, 3, None, FAKE, None) == INVALID        # k > 0 needs stale_idx
     assert f(1, 10, FAKE, None, -1, 2, 3, FAKE, FAKE, None) == INVALID
-    assert f(1, 40000, FAKE, None, 0, 2, 3, FAKE, FAKE, None) == UNSUPPORTED
+    assert f(1, 20000, FAKE, None, 0, 2, 3, FAKE, FAKE, None) == UNSUPPORTED
 
 
 def test_refresh_validation_and_workspace(L):
