@@ -3,8 +3,8 @@
     python bench.py [--steps K] [--warmup W] [--config 1] [--subrun 1]
 
 A step is the whole hot path over one batch: drift -> select -> sparse K/V
-refresh -> Q projection + bidirectional attention -> commit, five C-ABI calls
-on one stream.  The default workload is the LLaDA-8B-shaped layer (bf16,
+refresh -> Q projection of the active block -> bidirectional attention ->
+commit, six C-ABI calls on one stream.  The default workload is the LLaDA-8B-shaped layer (bf16,
 batch 1, d=4096, 32 heads of 128, sequence 768 = prompt 512 + 256 generated,
 active block 32, vocabulary 126464) with 15% of the positions heavily
 perturbed.  Inputs are seeded synthetic data, resident in HBM before timing.
@@ -44,7 +44,7 @@ METRIC = "denoise-step tokens/s per layer, LLaDA-8B shape; % of HBM/MFMA rooflin
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3
-CALLS = ("drift", "select", "refresh_kv", "attend", "commit")
+CALLS = ("drift", "select", "refresh_kv", "project_q", "attend", "commit")
 
 
 def parse():
@@ -77,8 +77,8 @@ def algorithmic_cost(cfg, k, es):
         "select": dict(bytes=4 * b * S + 4 * b * (k + 1), flops=0),
         "refresh_kv": dict(bytes=2 * kvd * d * es + R * d * es + R * 2 * kvd * es + 4 * b * (k + 1),
                            flops=2 * R * d * 2 * kvd),
-        "attend": dict(bytes=qd * d * es + b * B * d * es + 2 * b * S * kvd * es + 2 * b * B * qd * es,
-                       flops=2 * b * B * d * qd + 4 * b * H * B * S * hd),
+        "project_q": dict(bytes=qd * d * es + b * B * d * es + b * B * qd * es, flops=2 * b * B * d * qd),
+        "attend": dict(bytes=2 * b * S * kvd * es + 2 * b * B * qd * es, flops=4 * b * H * B * S * hd),
         "commit": dict(bytes=b * B * V * es + b * B * (4 + 4 + 1 + 1) + 4 * b * (cfg.hist_depth + 1) * B,
                        flops=0),
     }
@@ -88,15 +88,16 @@ def algorithmic_cost(cfg, k, es):
 # Kernels launched by each call, and the sources they are built from.
 CALL_KERNELS = {
     "refresh_kv": ("gemm_rows_kernel", "gemm_reduce_kernel", "gemm_small_kernel"),
-    "attend": ("gemm_small_kernel", "gemm_rows_kernel", "gemm_reduce_kernel", "attend_kernel",
-               "attend_merge_kernel"),
+    "project_q": ("gemm_small_kernel", "gemm_rows_kernel", "gemm_reduce_kernel"),
+    "attend": ("attend_kernel", "attend_merge_kernel"),
     "drift": ("drift_kernel",),
     "select": ("select_kernel",),
     "commit": ("scan_kernel", "finalize_kernel"),
 }
 CALL_SOURCES = {
     "refresh_kv": ("gemm.hip", "gemm.hpp"),
-    "attend": ("attend.hip", "gemm.hip", "gemm.hpp"),
+    "project_q": ("attend.hip", "gemm.hip", "gemm.hpp"),
+    "attend": ("attend.hip",),
     "drift": ("drift.hip",),
     "select": ("select.hip",),
     "commit": ("commit.hip",),
@@ -334,27 +335,35 @@ def main():
         elif name == "refresh_kv":
             P.refresh_kv(s["h_cur"], step.stale_idx, step.stale_count, sh["block_start"], sh["block_len"],
                          s["w_k"], s["w_v"], s["k_cache"], s["v_cache"], workspace=step.ws_refresh)
+        elif name == "project_q":
+            P.project_q(s["h_cur"], s["w_q"], sh["block_start"], sh["block_len"], sh["n_heads"],
+                        out=step.q_buf, workspace=step.ws_q)
         elif name == "attend":
-            P.attend(s["h_cur"], s["w_q"], s["k_cache"], s["v_cache"], sh["block_start"], sh["block_len"],
+            P.attend(None, None, s["k_cache"], s["v_cache"], sh["block_start"], sh["block_len"],
                      sh["n_heads"], q_buf=step.q_buf, out=step.out, lse=step.lse, workspace=step.ws_attend)
         else:
             P.commit(s["logits"], s["masked"], step.drift, sh["block_start"], s["hist"], s["hist_len"], -1,
                      cfg.tau_s, cfg.alpha, False, step.token, step.conf, step.commit, workspace=step.ws_commit)
 
-    def run_step(i, ev=None, only=None):
-        """One whole step; events around every call (ev: list of 6) or
-        around the call named `only` (ev: list of 2)."""
+    def run_serial(i, ev):
+        """One step with every call on the launch stream and events around
+        each (the per-call breakdown)."""
         s = sets[i % copies]
         for j, name in enumerate(CALLS):
-            if ev is not None and only is None:
-                ev[j].record(stream)
+            ev[j].record(stream)
+            call(name, s)
+        ev[len(CALLS)].record(stream)
+
+    def run_step(i, ev=None, only=None):
+        """One step, every call on the launch stream, events around the call
+        named `only`."""
+        s = sets[i % copies]
+        for name in CALLS:
             if ev is not None and name == only:
                 ev[0].record(stream)
             call(name, s)
             if ev is not None and name == only:
                 ev[1].record(stream)
-        if ev is not None and only is None:
-            ev[len(CALLS)].record(stream)
 
     for i in range(args.warmup):
         run_step(i)
@@ -365,7 +374,7 @@ def main():
     ndiag = max(1, min(args.steps, 50))
     dev_events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)] for _ in range(ndiag)]
     for i in range(ndiag):
-        run_step(i, dev_events[i])
+        run_serial(i, dev_events[i])
     torch.cuda.synchronize()
     call_us = {c: float(np.mean([ev[j].elapsed_time(ev[j + 1]) * 1e3 for ev in dev_events]))
                for j, c in enumerate(CALLS)}

@@ -140,6 +140,33 @@ polestar_status polestar_refresh_kv(polestar_dtype dtype, int batch, int seq, in
                                     hipStream_t stream);
 
 /*
+ * polestar_project_q -- query projection of the active block (Sec. 2, eq. 3:
+ * the queries of the active positions J_b).
+ *
+ *   q[b][j][h][:] = W_q[h*head_dim : (h+1)*head_dim] . h_cur[b][block_start + j]
+ * in fp32 accumulation, rounded to dtype (round to nearest even).  It reads
+ * neither cache, so it may run on a second stream while drift, select and
+ * the K/V refresh run; polestar_attend with w_q == NULL then consumes q.
+ *
+ *   h_cur : [batch][seq][d] dtype
+ *   w_q   : [n_heads*head_dim][d] dtype
+ *   q     : [batch][block_len][n_heads][head_dim] dtype (output)
+ *   workspace : >= polestar_project_q_workspace_size(...) bytes (0 when
+ *               batch*block_len <= 64; NULL is then allowed)
+ * Requires block_len > 0, block_start + block_len <= seq; UNSUPPORTED
+ * unless head_dim is 64 or 128, d % 128 == 0 (bf16) / d % 64 == 0 (fp32),
+ * batch <= 65535 and every pointer is 16-byte aligned.  The workspace needs
+ * no initialisation.
+ */
+size_t polestar_project_q_workspace_size(polestar_dtype dtype, int batch, int d,
+                                         int n_heads, int head_dim, int block_len);
+polestar_status polestar_project_q(polestar_dtype dtype, int batch, int seq, int d,
+                                   int n_heads, int head_dim, int block_start, int block_len,
+                                   const void* h_cur, const void* w_q, void* q,
+                                   void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/*
  * polestar_attend -- bidirectional attention of the active block over the
  * whole cache (Sec. 2, eq. 3; App. B setup).
  *

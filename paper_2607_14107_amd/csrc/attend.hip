@@ -391,6 +391,62 @@ struct AttendLayout {
     size_t total;
 };
 
+// Q = W_q h_cur[b][block rows] through the shared GEMM (block-rows mode).
+polestar_status run_q_projection(bool bf16, const GemmPlan& plan, int batch, int seq, int d, int H,
+                                 int hd, int block_start, int block_len, const void* h_cur,
+                                 const void* w_q, void* q, char* ws, hipStream_t stream) {
+    GemmArgs g{};
+    g.x = static_cast<const char*>(h_cur);
+    g.w0 = static_cast<const char*>(w_q);
+    g.w1 = nullptr;
+    g.n0 = H * hd;
+    g.N = H * hd;
+    g.K = d;
+    g.mode = kGemmBlockRows;
+    g.batch = batch;
+    g.seq = seq;
+    g.block_start = block_start;
+    g.block_len = block_len;
+    g.out0 = static_cast<char*>(q);
+    g.ws = reinterpret_cast<float*>(ws);
+    g.m_max = batch * block_len;
+    return gemm_run(bf16, plan, g, stream);
+}
+
+}  // namespace
+}  // namespace ps
+
+extern "C" size_t polestar_project_q_workspace_size(polestar_dtype dtype, int batch, int d,
+                                                    int n_heads, int head_dim, int block_len) {
+    using namespace ps;
+    if (!dtype_ok(dtype) || batch <= 0 || d <= 0 || n_heads <= 0 || head_dim <= 0 || block_len <= 0)
+        return 0;
+    return gemm_plan(dtype == POLESTAR_BF16, static_cast<long>(batch) * block_len, n_heads * head_dim, d)
+        .ws_bytes;
+}
+
+extern "C" polestar_status polestar_project_q(polestar_dtype dtype, int batch, int seq, int d,
+                                              int n_heads, int head_dim, int block_start,
+                                              int block_len, const void* h_cur, const void* w_q,
+                                              void* q, void* workspace, size_t workspace_bytes,
+                                              hipStream_t stream) {
+    using namespace ps;
+    if (!dtype_ok(dtype) || batch <= 0 || seq <= 0 || d <= 0 || n_heads <= 0 || head_dim <= 0 ||
+        block_len <= 0 || block_start < 0 || block_start > seq - block_len || !h_cur || !w_q || !q)
+        return POLESTAR_ERR_INVALID_ARGUMENT;
+    const bool bf16 = dtype == POLESTAR_BF16;
+    if ((head_dim != 64 && head_dim != 128) || !gemm_k_ok(bf16, d) || !aligned16(h_cur) ||
+        !aligned16(w_q) || !aligned16(q) || !aligned16(workspace) || batch > 65535 ||
+        static_cast<long>(batch) * block_len > 0x7fffffffL / 4)
+        return POLESTAR_ERR_UNSUPPORTED;
+    const GemmPlan plan = gemm_plan(bf16, static_cast<long>(batch) * block_len, n_heads * head_dim, d);
+    if (workspace_bytes < plan.ws_bytes || (plan.ws_bytes > 0 && !workspace)) return POLESTAR_ERR_WORKSPACE;
+    return run_q_projection(bf16, plan, batch, seq, d, n_heads, head_dim, block_start, block_len, h_cur,
+                            w_q, q, static_cast<char*>(workspace), stream);
+}
+
+namespace ps {
+namespace {
 AttendLayout attend_layout(bool bf16, int batch, int seq, int d, int H, int hd, int nq, bool project) {
     AttendLayout L{};
     if (project) L.qp = gemm_plan(bf16, static_cast<long>(batch) * nq, H * hd, d);
@@ -439,22 +495,8 @@ extern "C" polestar_status polestar_attend(polestar_dtype dtype, int batch, int 
     char* ws = static_cast<char*>(workspace);
 
     if (w_q) {
-        GemmArgs g{};
-        g.x = static_cast<const char*>(h_cur);
-        g.w0 = static_cast<const char*>(w_q);
-        g.w1 = nullptr;
-        g.n0 = n_heads * head_dim;
-        g.N = n_heads * head_dim;
-        g.K = d;
-        g.mode = kGemmBlockRows;
-        g.batch = batch;
-        g.seq = seq;
-        g.block_start = block_start;
-        g.block_len = block_len;
-        g.out0 = static_cast<char*>(q_buf);
-        g.ws = reinterpret_cast<float*>(ws);
-        g.m_max = batch * block_len;
-        polestar_status st = gemm_run(bf16, L.qp, g, stream);
+        polestar_status st = run_q_projection(bf16, L.qp, batch, seq, d, n_heads, head_dim, block_start,
+                                              block_len, h_cur, w_q, q_buf, ws, stream);
         if (st != POLESTAR_OK) return st;
     }
 

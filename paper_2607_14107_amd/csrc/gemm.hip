@@ -12,12 +12,17 @@
 //   of K:
 //   - the gathered input rows are staged in LDS (16-byte coalesced loads,
 //     272-byte row pitch: conflict-free MFMA reads) and shared by the waves;
+//     a wave reads the fragments of the next 16-k chunk while the MFMAs of
+//     the current one run;
 //   - each wave streams its weight rows from HBM straight into registers,
 //     128 contiguous bytes per lane, two super-steps ahead (triple buffer,
 //     loop unrolled three times so the buffers rotate without copies).
 //   When rows x columns do not fill the chip, K is split over workgroups;
-//   fp32 partials go to the workspace and gemm_reduce_kernel sums them in
-//   split order (deterministic) and scatters 16-byte rows.
+//   each writes its fp32 partial tile as one contiguous block of the
+//   workspace ([split][column tile][row][128]: long DRAM bursts, not 512-byte
+//   pieces 32 KB apart), the row map goes next to it, and gemm_reduce_kernel
+//   sums the partials in split order (deterministic) and scatters 16-byte
+//   rows.
 //
 // gemm_small_kernel (at most 64 rows, e.g. the Q projection): a workgroup
 //   owns all rows and 16 columns; its 4 waves take interleaved super-steps
@@ -182,6 +187,13 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_rows_kernel(GemmArgs g) {
 
     const int total = g.mode == kGemmRefresh ? build_prefix(g, pre, scan_tmp)
                                              : g.batch * g.block_len;
+    // Split K: the first workgroup of each row tile publishes its rows'
+    // (sequence, position) for the reduce kernel (-1: row maps to nothing).
+    if (g.ksplit > 1 && split == 0 && col_tile == 0 && t < BM && m0 + t < g.m_max) {
+        int b, pos;
+        map_row(g, pre, total, m0 + t, b, pos);
+        *reinterpret_cast<int2*>(g.rowmap + 2 * (m0 + t)) = make_int2(b, pos);
+    }
     if (m0 >= total) return;               // uniform over the workgroup
     if (t < BM) {
         int b, pos;
@@ -216,25 +228,37 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_rows_kernel(GemmArgs g) {
 #pragma unroll
         for (int i = 0; i < RA; ++i) st16(&sa[buf][((t >> 4) + 16 * i) * kLda + acol], ra[i]);
     };
+    // The MT fragments of chunk s+1 are read from LDS while the MFMAs of
+    // chunk s run (two register sets; the scheduling barriers keep that
+    // order), so LDS latency is not exposed per MFMA.
     auto compute = [&](int buf, const uint4 (&rb)[8]) {
         const char* abase = &sa[buf][(lane & 31) * kLda + (lane >> 5) * 128];
+        uint4 af[2][MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) af[0][mt] = *reinterpret_cast<const uint4*>(abase + mt * 32 * kLda);
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
+            __builtin_amdgcn_sched_barrier(0);
+            if (s + 1 < 8) {
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                const uint4 a = *reinterpret_cast<const uint4*>(abase + mt * 32 * kLda + 16 * s);
-                acc[mt] = Mma32<BF16>::step(a, rb[s], acc[mt]);
+                for (int mt = 0; mt < MT; ++mt)
+                    af[(s + 1) & 1][mt] = *reinterpret_cast<const uint4*>(abase + mt * 32 * kLda + 16 * (s + 1));
             }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) acc[mt] = Mma32<BF16>::step(af[s & 1][mt], rb[s], acc[mt]);
         }
+        __builtin_amdgcn_sched_barrier(0);
     };
 
     // Software pipeline.  Issue order of the loads: ... B(s+1), A(s+1),
     // B(s+2), A(s+2) ...  Waiting for A(s+1) at the end of step s (to stage
     // it in LDS) therefore also covers B(s+1), which step s+1 needs, while
     // B(s+2) stays in flight: weights get two compute phases of latency
-    // cover, the (L2-resident) input rows one.  Prefetches past s1 - 1
-    // re-read step s1 - 1 (cache hits, ignored) so every iteration issues
-    // the same loads and the wait counts stay static.
+    // cover, the (L2-resident) input rows one.  (Two phases for the input
+    // rows too, with a second register buffer, measured no faster.)
+    // Prefetches past s1 - 1 re-read step s1 - 1 (cache hits, ignored) so
+    // every iteration issues the same loads and the wait counts stay static.
     uint4 ra[RA];
     load_a(s0, ra);
     store_a(0, ra);                       // waits for A(s0) (and B(s0), B(s0+1))
@@ -288,29 +312,28 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_rows_kernel(GemmArgs g) {
         if (g.ksplit == 1) {
             store8<BF16>(out_ptr<BF16>(g, b, rowp[r], m0 + r, nc), v);
         } else {
-            float* dst = g.ws + (static_cast<size_t>(split) * g.m_max + (m0 + r)) * g.N + nc;
+            float* dst = g.ws + ((static_cast<size_t>(split) * g.col_tiles + col_tile) * g.m_max + (m0 + r)) * BN + c;
             *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
             *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
         }
     }
 }
 
-// Sum of the split-K partials, in split order (deterministic): one thread per
-// 8 consecutive columns of one row, all split loads issued before the adds,
-// rounded and written with 16-byte stores.
+// Sum of the split-K partials, in split order (deterministic): thread ->
+// (column tile, row, 8 columns) so that consecutive threads read consecutive
+// 32-byte pieces of the contiguous partial tiles; the partial and row-map
+// loads are independent, then one rounded 16-byte store.
 template <bool BF16>
 __global__ __launch_bounds__(kGemmBlock) void gemm_reduce_kernel(GemmArgs g) {
-    __shared__ int scan_tmp[17];
-    extern __shared__ int pre[];
-    const int groups = g.N / 8;
     const long id = static_cast<long>(blockIdx.x) * kGemmBlock + threadIdx.x;
-    const int mraw = static_cast<int>(id / groups);
-    const int c = static_cast<int>(id - static_cast<long>(mraw) * groups) * 8;
-    // Partial loads first (rows past m_max read row 0, never stored); the
-    // row bookkeeping's dependent loads then overlap them.
-    const int m = mraw < g.m_max ? mraw : 0;
-    const size_t stride = static_cast<size_t>(g.m_max) * g.N;
-    const float* src = g.ws + static_cast<size_t>(m) * g.N + c;
+    const long per_tile = static_cast<long>(g.m_max) * 16;
+    const int ct = static_cast<int>(id / per_tile);
+    if (ct >= g.col_tiles) return;
+    const int rem = static_cast<int>(id - ct * per_tile);
+    const int m = rem >> 4;
+    const int c = (rem & 15) * 8;
+    const size_t stride = static_cast<size_t>(g.col_tiles) * g.m_max * 128;   // one split
+    const float* src = g.ws + (static_cast<size_t>(ct) * g.m_max + m) * 128 + c;
     float4 x[2 * kMaxSplit];
 #pragma unroll
     for (int s = 0; s < kMaxSplit; ++s) {
@@ -319,12 +342,9 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_reduce_kernel(GemmArgs g) {
             x[2 * s + 1] = *reinterpret_cast<const float4*>(src + s * stride + 4);
         }
     }
-    const int total = g.mode == kGemmRefresh ? build_prefix(g, pre, scan_tmp)
-                                             : g.batch * g.block_len;
-    if (mraw >= total) return;
-    int b, pos;
-    map_row(g, pre, total, m, b, pos);
-    if (b < 0) return;
+    const int2 mp = *reinterpret_cast<const int2*>(g.rowmap + 2 * m);
+    const int n = ct * 128 + c;
+    if (mp.x < 0 || n >= g.N) return;
     float v[8] = {x[0].x, x[0].y, x[0].z, x[0].w, x[1].x, x[1].y, x[1].z, x[1].w};
 #pragma unroll
     for (int s = 1; s < kMaxSplit; ++s) {
@@ -333,7 +353,7 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_reduce_kernel(GemmArgs g) {
             v[4] += x[2 * s + 1].x; v[5] += x[2 * s + 1].y; v[6] += x[2 * s + 1].z; v[7] += x[2 * s + 1].w;
         }
     }
-    store8<BF16>(out_ptr<BF16>(g, b, pos, m, c), v);
+    store8<BF16>(out_ptr<BF16>(g, mp.x, mp.y, m, n), v);
 }
 
 // ---------------------------------------------------------------------------
@@ -490,6 +510,11 @@ bool dispatch_small(const GemmPlan& p, const GemmArgs& g, size_t dyn, hipStream_
 
 }  // namespace
 
+// Partial tiles of a split-K plan, [ksplit][col_tiles][m_max][128] fp32.
+static size_t partial_bytes(const GemmPlan& p, long m_max) {
+    return align_up(static_cast<size_t>(p.ksplit) * p.col_tiles * m_max * 128 * sizeof(float), 256);
+}
+
 GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     GemmPlan p{};
     const int ks = bf16 ? 128 : 64;
@@ -518,11 +543,13 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     p.ksplit = ceil_div(nsteps, p.steps_per_split);
     p.grid = static_cast<int>(tiles * p.ksplit);
     if (p.ksplit > 1)
-        p.ws_bytes = align_up(static_cast<size_t>(p.ksplit) * m_max * N * sizeof(float), 256);
+        p.ws_bytes = partial_bytes(p, m_max) + align_up(static_cast<size_t>(m_max) * 2 * sizeof(int), 256);
     return p;
 }
 
 polestar_status gemm_run(bool bf16, const GemmPlan& p, GemmArgs g, hipStream_t stream) {
+    g.rowmap = p.ksplit > 1 ? reinterpret_cast<int*>(reinterpret_cast<char*>(g.ws) + partial_bytes(p, g.m_max))
+                            : nullptr;
     g.ksplit = p.ksplit;
     g.steps_per_split = p.steps_per_split;
     g.row_tiles = p.row_tiles;
@@ -534,12 +561,12 @@ polestar_status gemm_run(bool bf16, const GemmPlan& p, GemmArgs g, hipStream_t s
     if (!ok) return POLESTAR_ERR_UNSUPPORTED;
     polestar_status st = launch_status();
     if (st != POLESTAR_OK || p.small || p.ksplit == 1) return st;
-    const long threads = static_cast<long>(g.m_max) * (g.N / 8);
+    const long threads = static_cast<long>(g.col_tiles) * g.m_max * 16;
     const int blocks = ceil_div(threads, kGemmBlock);
     if (bf16)
-        hipLaunchKernelGGL((gemm_reduce_kernel<true>), dim3(blocks), dim3(kGemmBlock), dyn, stream, g);
+        hipLaunchKernelGGL((gemm_reduce_kernel<true>), dim3(blocks), dim3(kGemmBlock), 0, stream, g);
     else
-        hipLaunchKernelGGL((gemm_reduce_kernel<false>), dim3(blocks), dim3(kGemmBlock), dyn, stream, g);
+        hipLaunchKernelGGL((gemm_reduce_kernel<false>), dim3(blocks), dim3(kGemmBlock), 0, stream, g);
     return launch_status();
 }
 

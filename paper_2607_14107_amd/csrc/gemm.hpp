@@ -28,7 +28,8 @@ struct GemmArgs {
     int block_start, block_len;
     char* out0;   // refresh: k_cache (row pitch n0); block rows: [rows][N]
     char* out1;   // refresh: v_cache (row pitch N - n0)
-    float* ws;          // split-K partials [split][m_max][N] fp32
+    float* ws;          // split-K partials [split][col_tile][m_max][128] fp32
+    int* rowmap;        // split-K: [m_max][2] (sequence, position) of row m, -1: none
     int m_max;
     int ksplit;
     int steps_per_split;
@@ -43,7 +44,7 @@ struct GemmPlan {
     int ksplit;
     int steps_per_split;
     int grid;           // workgroups of gemm_rows_kernel
-    size_t ws_bytes;    // fp32 partials, 0 when ksplit == 1
+    size_t ws_bytes;    // fp32 partials + row map, 0 when ksplit == 1
 };
 
 GemmPlan gemm_plan(bool bf16, long m_max, int N, int K);

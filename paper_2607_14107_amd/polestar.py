@@ -59,6 +59,10 @@ def lib() -> ctypes.CDLL:
     L.polestar_refresh_kv_workspace_size.argtypes = [I, I, I, I, I, I, I]
     L.polestar_refresh_kv.restype = S
     L.polestar_refresh_kv.argtypes = [I, I, I, I, I, I, P, P, P, I, I, I, P, P, P, P, P, Z, P]
+    L.polestar_project_q_workspace_size.restype = Z
+    L.polestar_project_q_workspace_size.argtypes = [I, I, I, I, I, I]
+    L.polestar_project_q.restype = S
+    L.polestar_project_q.argtypes = [I, I, I, I, I, I, I, I, P, P, P, P, Z, P]
     L.polestar_attend_workspace_size.restype = Z
     L.polestar_attend_workspace_size.argtypes = [I, I, I, I, I, I, I, I]
     L.polestar_attend.restype = S
@@ -106,8 +110,8 @@ def _workspace(nbytes: int, device, ws: torch.Tensor | None) -> torch.Tensor | N
         return ws
     if ws is not None and ws.numel() * ws.element_size() >= nbytes:
         return ws
-    # zero-filled once: the library keeps arrival counters in it
-    return torch.zeros(nbytes, dtype=torch.uint8, device=device)
+    # the library needs no initialised workspace
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
 # ---------------------------------------------------------------------------
@@ -165,6 +169,28 @@ def refresh_kv(h_cur: torch.Tensor, stale_idx: torch.Tensor | None, stale_count:
         _ptr(stale_count, torch.int32) if k_max > 0 else None, k_max, block_start, block_len,
         _ptr(w_k, h_cur.dtype), _ptr(w_v, h_cur.dtype), _ptr(k_cache, h_cur.dtype),
         _ptr(v_cache, h_cur.dtype), _ptr(ws), nbytes, _stream(stream)))
+
+
+def project_q_workspace_size(dtype: int, batch: int, d: int, n_heads: int, head_dim: int,
+                             block_len: int) -> int:
+    return lib().polestar_project_q_workspace_size(dtype, batch, d, n_heads, head_dim, block_len)
+
+
+def project_q(h_cur: torch.Tensor, w_q: torch.Tensor, block_start: int, block_len: int, n_heads: int,
+              out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+              stream=None) -> torch.Tensor:
+    """Q = W_q h_cur[:, J_b] -> [batch][block_len][n_heads][head_dim]."""
+    b, s, d = h_cur.shape
+    hd = w_q.shape[0] // n_heads
+    dt = _dtype_code(h_cur)
+    if out is None:
+        out = torch.empty((b, block_len, n_heads, hd), dtype=h_cur.dtype, device=h_cur.device)
+    ws = _workspace(project_q_workspace_size(dt, b, d, n_heads, hd, block_len), h_cur.device, workspace)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("polestar_project_q", lib().polestar_project_q(
+        dt, b, s, d, n_heads, hd, block_start, block_len, _ptr(h_cur), _ptr(w_q, h_cur.dtype),
+        _ptr(out, h_cur.dtype), _ptr(ws), nbytes, _stream(stream)))
+    return out
 
 
 def attend_workspace_size(dtype: int, batch: int, seq: int, d: int, n_heads: int, n_kv_heads: int,
@@ -236,8 +262,13 @@ def commit(logits: torch.Tensor, masked: torch.Tensor, drift_vals: torch.Tensor 
 # ---------------------------------------------------------------------------
 
 class Step:
-    """drift -> select -> refresh_kv -> attend -> commit for one layer, on
-    buffers allocated once.  All five calls go to the current stream."""
+    """One layer step on buffers allocated once, every call on the current
+    stream: drift -> select -> refresh_kv -> project_q -> attend -> commit.
+
+    (The query projection reads only h_cur and W_q and could run on a second
+    stream; measured on MI355X, the cross-stream event waits cost more than
+    the overlap saves at these sizes, so the step stays on one stream.)
+    """
 
     def __init__(self, *, batch: int, seq: int, d: int, n_heads: int, n_kv_heads: int,
                  head_dim: int, block_start: int, block_len: int, vocab: int, k: int,
@@ -258,6 +289,7 @@ class Step:
         self.conf = torch.empty((batch, block_len), dtype=torch.float32, **f)
         self.commit = torch.empty((batch, block_len), dtype=torch.uint8, **f)
         self.ws_refresh = _workspace(refresh_kv_workspace_size(dt, batch, d, n_kv_heads, head_dim, k, block_len), dev, None)
+        self.ws_q = _workspace(project_q_workspace_size(dt, batch, d, n_heads, head_dim, block_len), dev, None)
         self.ws_attend = _workspace(attend_workspace_size(dt, batch, seq, d, n_heads, n_kv_heads, head_dim, block_len), dev, None)
         self.ws_commit = _workspace(commit_workspace_size(dt, batch, block_len, vocab), dev, None)
 
@@ -271,7 +303,9 @@ class Step:
                    self.stale_idx, self.stale_count)
         refresh_kv(h_cur, self.stale_idx, self.stale_count, s["block_start"], s["block_len"],
                    w_k, w_v, k_cache, v_cache, workspace=self.ws_refresh)
-        attend(h_cur, w_q, k_cache, v_cache, s["block_start"], s["block_len"], s["n_heads"],
+        project_q(h_cur, w_q, s["block_start"], s["block_len"], s["n_heads"], out=self.q_buf,
+                  workspace=self.ws_q)
+        attend(None, None, k_cache, v_cache, s["block_start"], s["block_len"], s["n_heads"],
                q_buf=self.q_buf, out=self.out, lse=self.lse, workspace=self.ws_attend)
         commit(logits, masked, self.drift, s["block_start"], hist, hist_len, mask_token_id,
                tau_s, alpha, force_one, self.token, self.conf, self.commit, workspace=self.ws_commit)

@@ -29,7 +29,7 @@ def _header_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = _header_functions()
-    assert len(names) == 10, names
+    assert len(names) == 12, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -99,6 +99,28 @@ def test_attend_validation_and_workspace(L):
     a = list(args); a[6] = 256
     assert f(*a) == UNSUPPORTED
     a = list(args); a[18] = ws - 1
+    assert f(*a) == WORKSPACE
+
+
+def test_project_q_validation_and_workspace(L):
+    f = L.polestar_project_q
+    assert ps.project_q_workspace_size(ps.BF16, 1, 4096, 32, 128, 32) == 0      # 32 rows: no partials
+    ws = ps.project_q_workspace_size(ps.BF16, 8, 4096, 32, 128, 32)
+    assert ws > 0                                                                # 256 rows: split-K
+    args = [1, 8, 1536, 4096, 32, 128, 1024, 32, FAKE, FAKE, FAKE, FAKE, ws, None]
+    a = list(args); a[8] = None
+    assert f(*a) == INVALID                                   # h_cur
+    a = list(args); a[6] = 1510
+    assert f(*a) == INVALID                                   # block past the end
+    a = list(args); a[7] = 0
+    assert f(*a) == INVALID                                   # empty block
+    a = list(args); a[3] = 4000
+    assert f(*a) == UNSUPPORTED                               # d % 128
+    a = list(args); a[5] = 96
+    assert f(*a) == UNSUPPORTED                               # head_dim
+    a = list(args); a[10] = MISALIGNED
+    assert f(*a) == UNSUPPORTED
+    a = list(args); a[12] = ws - 1
     assert f(*a) == WORKSPACE
 
 

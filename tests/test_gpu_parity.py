@@ -244,6 +244,38 @@ def test_attend_matches_oracle(P, cfg_index):
     np.testing.assert_allclose(from_dev(lse), lse_want, rtol=10 * rtol, atol=10 * rtol)
 
 
+@pytest.mark.parametrize("cfg_index", [0, 1, 2, 3])
+def test_project_q_matches_oracle_and_attend(P, cfg_index):
+    """The stand-alone projection equals the oracle's and, bit for bit, the
+    projection polestar_attend makes itself (same kernels, same plan)."""
+    L = layer(cfg_index)
+    cfg, x, dec = L["cfg"], L["x"], L["dec"]
+    h = to_dev(x["h_cur"], cfg.dtype)
+    wq = to_dev(x["w_q"], cfg.dtype)
+    q = P.project_q(h, wq, cfg.block_start, cfg.block_len, cfg.n_heads)
+    want = ref.q_project(dec["h_cur"], dec["w_q"], cfg.block_start, cfg.block_len, cfg.n_heads, cfg.head_dim)
+    assert_rows_close(ref.decode(from_dev(q), cfg.dtype), want, RTOL[cfg.dtype], "Q")
+    _, q_att = P.attend(h, wq, to_dev(L["kc"], cfg.dtype), to_dev(L["vc"], cfg.dtype),
+                        cfg.block_start, cfg.block_len, cfg.n_heads)
+    assert np.array_equal(from_dev(q), from_dev(q_att))
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("batch,seq,bs,bl,d,H,hd", [(1, 40, 7, 33, 256, 2, 64), (3, 70, 60, 10, 512, 1, 128),
+                                                    (5, 20, 0, 20, 1024, 4, 64)])
+def test_project_q_ragged_shapes(P, dtype, batch, seq, bs, bl, d, H, hd):
+    """Row tiles with a ragged tail, more than 64 rows (split-K path), and a
+    block at the start of the sequence."""
+    if dtype == "fp32" and d % 64:
+        pytest.skip("fp32 rows need d % 64 == 0")
+    g = np.random.default_rng(batch * 1000 + seq)
+    h = inputs.store(g.standard_normal((batch, seq, d), dtype=np.float32), dtype)
+    wq = inputs.store(0.05 * g.standard_normal((H * hd, d), dtype=np.float32), dtype)
+    q = P.project_q(to_dev(h, dtype), to_dev(wq, dtype), bs, bl, H)
+    want = ref.q_project(ref.decode(h, dtype), ref.decode(wq, dtype), bs, bl, H, hd)
+    assert_rows_close(ref.decode(from_dev(q), dtype), want, RTOL[dtype], "Q")
+
+
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 @pytest.mark.parametrize("batch,seq,bs,bl,H,Hkv,hd", [(2, 50, 10, 20, 4, 2, 64), (1, 300, 0, 45, 3, 1, 128),
                                                       (3, 129, 97, 32, 2, 2, 128), (1, 1, 0, 1, 2, 1, 64)])
