@@ -72,13 +72,16 @@ __global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
     const char* vbase = a.v + (static_cast<size_t>(b) * a.seq * a.Hkv + kvh) * HD * ES;
 
     // Q fragments (B operand of S^T): query 16u + (lane & 15), d in [DPL g, DPL g + DPL).
+    // All loads are unconditional: queries past nq and keys past seq read the
+    // last row (finite values whose results are masked or never stored), so
+    // no load sits behind an exec mask and the wait counts stay static.
     uint4 qf[2][NC];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-        const int q = qg * kQG + 16 * u + (lane & 15);
+        const int q = min(qg * kQG + 16 * u + (lane & 15), a.nq - 1);
         const char* qp = a.q + ((static_cast<size_t>(b) * a.nq + q) * a.H + h) * HD * ES + g * DPL * ES;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) qf[u][c] = q < a.nq ? ld16(qp + 16 * c) : zero16();
+        for (int c = 0; c < NC; ++c) qf[u][c] = ld16(qp + 16 * c);
     }
 
     floatx4 o[DT][2];
@@ -90,40 +93,50 @@ __global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
     const int ntiles = (a.seq + kKT - 1) / kKT;
     const int t_begin = split * a.tiles_per_split;
     const int t_end = min(ntiles, t_begin + a.tiles_per_split);
+    // Each wave stages and reads only its own V^T region, so no workgroup
+    // barrier is needed until the waves are merged.
     char* myvt = vt[w];
+    const int wu = __builtin_amdgcn_readfirstlane(w);   // wave-uniform tile choice
 
     for (int base = t_begin; base < t_end; base += 4) {
-        const int tile = base + w;
-        const bool active = tile < t_end;
-        const int key0 = tile * kKT;
-        floatx4 st[2][2];
-        if (active) {
+        const int tile = base + wu;
+        if (tile < t_end) {
+            const int key0 = tile * kKT;
+            floatx4 st[2][2];
             // K fragments (A operand): key key0 + 16 t + (lane & 15).
             uint4 kf[2][NC];
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
-                const int key = key0 + 16 * t + (lane & 15);
+                const int key = min(key0 + 16 * t + (lane & 15), a.seq - 1);
                 const char* kp = kbase + static_cast<size_t>(key) * krow + g * DPL * ES;
 #pragma unroll
-                for (int c = 0; c < NC; ++c) kf[t][c] = key < a.seq ? ld16(kp + 16 * c) : zero16();
+                for (int c = 0; c < NC; ++c) kf[t][c] = ld16(kp + 16 * c);
             }
-            // V tile -> LDS, transposed to [d][key slot].
+            // V tile -> LDS, transposed to [d][key slot].  Every V load of
+            // the tile is issued before any packing (compile-time trip count).
             if constexpr (BF16) {
-                // 8 groups of 4 keys x HD/8 chunks of 8 d; lane: chunk lane%16 (+16 per pass)
+                // 8 groups of 4 keys x HD/8 chunks of 8 d; item pr = lane + 64 it
                 constexpr int DC = HD / 8;
-                for (int pr = lane; pr < DC * 8; pr += 64) {
+                constexpr int IT = DC * 8 / 64;
+                uint4 vv[IT][4];
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int pr = lane + 64 * it;
                     const int dc = pr % DC, kg = pr / DC;
-                    uint4 vv[4];
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
-                        const int key = key0 + 4 * kg + j;
-                        vv[j] = key < a.seq ? ld16(vbase + static_cast<size_t>(key) * krow + dc * 16)
-                                            : zero16();
+                        const int key = min(key0 + 4 * kg + j, a.seq - 1);
+                        vv[it][j] = ld16(vbase + static_cast<size_t>(key) * krow + dc * 16);
                     }
-                    const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vv[0]);
-                    const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vv[1]);
-                    const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vv[2]);
-                    const uint32_t* x3 = reinterpret_cast<const uint32_t*>(&vv[3]);
+                }
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int pr = lane + 64 * it;
+                    const int dc = pr % DC, kg = pr / DC;
+                    const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vv[it][0]);
+                    const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vv[it][1]);
+                    const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vv[it][2]);
+                    const uint32_t* x3 = reinterpret_cast<const uint32_t*>(&vv[it][3]);
                     const int slot = vslot(4 * kg);
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
@@ -138,19 +151,26 @@ __global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
                 }
             } else {
                 constexpr int DC = HD / 4;
-                for (int pr = lane; pr < DC * 8; pr += 64) {
+                constexpr int IT = DC * 8 / 64;
+                uint4 vv[IT][4];
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int pr = lane + 64 * it;
                     const int dc = pr % DC, kg = pr / DC;
-                    uint4 vv[4];
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
-                        const int key = key0 + 4 * kg + j;
-                        vv[j] = key < a.seq ? ld16(vbase + static_cast<size_t>(key) * krow + dc * 16)
-                                            : zero16();
+                        const int key = min(key0 + 4 * kg + j, a.seq - 1);
+                        vv[it][j] = ld16(vbase + static_cast<size_t>(key) * krow + dc * 16);
                     }
-                    const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vv[0]);
-                    const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vv[1]);
-                    const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vv[2]);
-                    const uint32_t* x3 = reinterpret_cast<const uint32_t*>(&vv[3]);
+                }
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int pr = lane + 64 * it;
+                    const int dc = pr % DC, kg = pr / DC;
+                    const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vv[it][0]);
+                    const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vv[it][1]);
+                    const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vv[it][2]);
+                    const uint32_t* x3 = reinterpret_cast<const uint32_t*>(&vv[it][3]);
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         *reinterpret_cast<uint4*>(myvt + (dc * 4 + e) * VP + 16 * kg) =
@@ -167,9 +187,6 @@ __global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
                     for (int c = 0; c < NC; ++c) s = Mma<BF16>::step(kf[t][c], qf[u][c], s);
                     st[t][u] = s;
                 }
-        }
-        __syncthreads();   // V^T of every wave is in LDS
-        if (active) {
             float p[2][2][4];   // [t][u][i]
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
@@ -232,7 +249,6 @@ __global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
                 }
             }
         }
-        __syncthreads();   // before the next tile overwrites V^T
     }
 
     // Merge the four waves.  Lane holds O^T[d = 16 dt + 4 g + i][q = 16 u + (lane & 15)].
@@ -310,10 +326,14 @@ __global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
 }
 
 // Combine the key splits of one (b, h, q) row: one wave per row, lanes over d.
+// Splits are taken eight at a time with every load of the chunk issued
+// before any arithmetic (indices clamped, extra splits weighted zero), and
+// merged in split order with a running maximum.
 template <bool BF16, int HD>
 __global__ __launch_bounds__(256) void attend_merge_kernel(AttArgs a) {
     constexpr int ES = Elem<BF16>::kBytes;
     constexpr int PL = HD / 64;   // d values per lane (1 or 2)
+    constexpr int CH = 8;         // splits per chunk
     const int lane = threadIdx.x & 63;
     const long rowid = static_cast<long>(blockIdx.x) * 4 + (threadIdx.x >> 6);   // over [b][h][q]
     const long nrows = static_cast<long>(a.batch) * a.H * a.nq;
@@ -323,18 +343,30 @@ __global__ __launch_bounds__(256) void attend_merge_kernel(AttArgs a) {
     const int h = static_cast<int>(bh % a.H);
     const int b = static_cast<int>(bh / a.H);
     const size_t prow0 = static_cast<size_t>(rowid) * a.splits;
-    float M = -INFINITY;
-    for (int s = 0; s < a.splits; ++s) M = fmaxf(M, a.part_ml[(prow0 + s) * 2]);
-    const float Mref = M == -INFINITY ? 0.f : M;
-    float L = 0.f, acc[PL];
+    float M = -INFINITY, L = 0.f, acc[PL];
 #pragma unroll
     for (int j = 0; j < PL; ++j) acc[j] = 0.f;
-    for (int s = 0; s < a.splits; ++s) {
-        const float wgt = fast_exp2(a.part_ml[(prow0 + s) * 2] - Mref);
-        L += a.part_ml[(prow0 + s) * 2 + 1] * wgt;
-        const float* po = a.part_o + (prow0 + s) * HD + lane * PL;
+    for (int s0 = 0; s0 < a.splits; s0 += CH) {
+        float2 ml[CH];
+        float po[CH][PL];
 #pragma unroll
-        for (int j = 0; j < PL; ++j) acc[j] += po[j] * wgt;
+        for (int c = 0; c < CH; ++c) {
+            const size_t pr = prow0 + min(s0 + c, a.splits - 1);
+            ml[c] = *reinterpret_cast<const float2*>(a.part_ml + pr * 2);
+#pragma unroll
+            for (int j = 0; j < PL; ++j) po[c][j] = a.part_o[pr * HD + lane * PL + j];
+        }
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const float m = s0 + c < a.splits ? ml[c].x : -INFINITY;
+            const float mn = fmaxf(M, m);
+            const float mref = mn == -INFINITY ? 0.f : mn;
+            const float wold = fast_exp2(M - mref), wnew = fast_exp2(m - mref);
+            L = L * wold + ml[c].y * wnew;
+#pragma unroll
+            for (int j = 0; j < PL; ++j) acc[j] = acc[j] * wold + po[c][j] * wnew;
+            M = mn;
+        }
     }
     const float inv = 1.f / L;
     const size_t row = (static_cast<size_t>(b) * a.nq + q) * a.H + h;

@@ -27,17 +27,19 @@ struct ScanPart {
     int idx;
 };
 
-__device__ __forceinline__ void better(float& bv, int& bi, float v, int i) {
-    if (v > bv || (v == bv && i < bi)) {
-        bv = v;
-        bi = i;
-    }
+// Argmax step: (v, i) replaces (bv, bi) if larger, or equal with a lower id.
+// Written as selects so that it compiles to straight-line code.
+__device__ __forceinline__ void better(float& bv, int& bi, float v, int i, bool valid = true) {
+    const bool take = valid & ((v > bv) | ((v == bv) & (i < bi)));   // no short-circuit: no branches
+    bv = take ? v : bv;
+    bi = take ? i : bi;
 }
 
+// (m, s) <- merge with (m2, s2), s = sum exp(l - m); all -inf stays (-inf, 0).
 __device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2) {
     const float mn = fmaxf(m, m2);
-    if (mn == -INFINITY) return;
-    s = s * fast_exp2((m - mn) * kLog2e) + s2 * fast_exp2((m2 - mn) * kLog2e);
+    const float mref = mn == -INFINITY ? 0.f : mn;
+    s = s * fast_exp2((m - mref) * kLog2e) + s2 * fast_exp2((m2 - mref) * kLog2e);
     m = mn;
 }
 
@@ -59,43 +61,49 @@ __global__ __launch_bounds__(kScanBlock) void scan_kernel(const char* __restrict
 
     float m = -INFINITY, s = 0.f, bv = -INFINITY;
     int bi = 0x7fffffff;
-    // elements [v0, v1) in 16-byte chunks; chunk c starts at element v0 + c*E
+    // Elements [v0, v1) in 16-byte chunks; chunk c starts at element v0 + c*E.
+    // Straight-line code: chunks past the slice re-read chunk 0 and count as
+    // -inf (no exp contribution, never the argmax); the mask id takes part in
+    // the softmax but not in the argmax.
     const int nchunks = (v1 - v0) / T::E;
     for (int c0 = 0; c0 < nchunks; c0 += kScanBlock * G) {
         uint4 r[G];
+        bool ok[G];
 #pragma unroll
         for (int gq = 0; gq < G; ++gq) {
             const int c = c0 + gq * kScanBlock + threadIdx.x;
-            r[gq] = c < nchunks ? ld16(row + static_cast<size_t>(v0 + c * T::E) * ES) : zero16();
+            ok[gq] = c < nchunks;
+            r[gq] = ld16(row + static_cast<size_t>(v0 + (ok[gq] ? c : 0) * T::E) * ES);
         }
+        __builtin_amdgcn_sched_barrier(0);   // all G loads in flight before any use
         float lm = -INFINITY;
 #pragma unroll
         for (int gq = 0; gq < G; ++gq) {
-            const int c = c0 + gq * kScanBlock + threadIdx.x;
-            if (c >= nchunks) continue;
+            const int vb = v0 + (c0 + gq * kScanBlock + threadIdx.x) * T::E;
             float f[T::E];
             T::unpack(r[gq], f);
-            const int vb = v0 + c * T::E;
 #pragma unroll
             for (int e = 0; e < T::E; ++e) {
-                lm = fmaxf(lm, f[e]);
-                if (vb + e != mask_id) better(bv, bi, f[e], vb + e);
+                const float x = ok[gq] ? f[e] : -INFINITY;
+                lm = fmaxf(lm, x);
+                better(bv, bi, x, vb + e, ok[gq] & (vb + e != mask_id));
             }
         }
-        if (lm == -INFINITY) continue;
         const float mn = fmaxf(m, lm);
+        const float mref = mn == -INFINITY ? 0.f : mn;
+        const float mnl = mref * kLog2e;
         float ls = 0.f;
-        const float mnl = mn * kLog2e;
 #pragma unroll
         for (int gq = 0; gq < G; ++gq) {
-            const int c = c0 + gq * kScanBlock + threadIdx.x;
-            if (c >= nchunks) continue;
             float f[T::E];
             T::unpack(r[gq], f);
 #pragma unroll
-            for (int e = 0; e < T::E; ++e) ls += fast_exp2(fmaf(f[e], kLog2e, -mnl));
+            for (int e = 0; e < T::E; ++e) {
+                const float x = ok[gq] ? f[e] : -INFINITY;
+                ls += fast_exp2(fmaf(x, kLog2e, -mnl));
+            }
         }
-        s = (m == -INFINITY ? 0.f : s * fast_exp2((m - mn) * kLog2e)) + ls;
+        s = s * fast_exp2((m - mref) * kLog2e) + ls;
         m = mn;
     }
     // wavefront reduction

@@ -33,8 +33,13 @@ __device__ __forceinline__ float expm1_small(float x) {
     return x * p;
 }
 
+// expm1 on either branch, chosen by a bitwise select so that the code stays
+// straight-line (no per-element exec-mask branches); both sides are cheap.
 __device__ __forceinline__ float expm1_any(float x) {
-    return fabsf(x) < kSmall ? expm1_small(x) : fast_exp2(x * kLog2e) - 1.0f;
+    const float series = expm1_small(x);
+    const float direct = fast_exp2(x * kLog2e) - 1.0f;
+    const uint32_t pick = 0u - static_cast<uint32_t>(fabsf(x) < kSmall);
+    return __uint_as_float((__float_as_uint(series) & pick) | (__float_as_uint(direct) & ~pick));
 }
 
 // Reduce NV values at once over the TPR threads of a row: wave shuffles,
@@ -93,31 +98,27 @@ __global__ __launch_bounds__(kDriftBlock) void drift_kernel(const char* __restri
         ra[c] = ld16(hc + off);
         rb[c] = ld16(hp + off);
     }
+    __builtin_amdgcn_sched_barrier(0);    // every load in flight before any use
 
-    // Pass 1: common maximum and the largest |dlt| of the row.
-    float m = -INFINITY, big = 0.0f;
+    // Pass 1: common maximum of the row.
+    float m = -INFINITY;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         float a[T::E], b[T::E];
         T::unpack(ra[c], a);
         T::unpack(rb[c], b);
 #pragma unroll
-        for (int j = 0; j < T::E; ++j) {
-            m = fmaxf(m, ok[c] ? fmaxf(a[j], b[j]) : -INFINITY);
-            big = fmaxf(big, ok[c] ? fabsf(a[j] - b[j]) : 0.0f);
-        }
+        for (int j = 0; j < T::E; ++j) m = fmaxf(m, ok[c] ? fmaxf(a[j], b[j]) : -INFINITY);
     }
     {
-        float mx[2] = {m, big};
-        row_reduce<TPR, 2, true>(mx, red);
+        float mx[1] = {m};
+        row_reduce<TPR, 1, true>(mx, red);
         m = mx[0];
-        big = mx[1];
     }
     const float mlog = m * kLog2e;
 
     // Pass 2: the three sums (masked chunks contribute nothing).
     float zb = 0.0f, sqe = 0.0f, spd = 0.0f;
-    const bool light = big < kSmall;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         float a[T::E], b[T::E];
@@ -128,7 +129,7 @@ __global__ __launch_bounds__(kDriftBlock) void drift_kernel(const char* __restri
         for (int j = 0; j < T::E; ++j) {
             const float dl = a[j] - b[j];
             const float e = keep * fast_exp2(fmaf(b[j], kLog2e, -mlog));
-            const float em = light ? expm1_small(dl) : expm1_any(dl);
+            const float em = expm1_any(dl);
             zb += e;
             sqe = fmaf(e, em, sqe);
             spd = fmaf(fmaf(e, em, e), dl, spd);

@@ -64,19 +64,29 @@ __global__ __launch_bounds__(kSelBlock) void select_kernel(const float* __restri
     const float* dr = drift + static_cast<size_t>(b) * seq;
     const uint8_t* el = elig ? elig + static_cast<size_t>(b) * seq : nullptr;
 
-    // keys in registers; positions p0 .. p0 + IPT - 1 of this thread
+    // keys in registers; positions p0 .. p0 + IPT - 1 of this thread.  Every
+    // load is issued before any is used (positions past seq re-read 0).
+    float dv[IPT];
+    uint8_t ev[IPT];
+#pragma unroll
+    for (int j = 0; j < IPT; ++j) dv[j] = dr[min(p0 + j, seq - 1)];
+    if (el) {                           // uniform branch, outside the element loop
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) ev[j] = el[min(p0 + j, seq - 1)];
+    } else {
+#pragma unroll
+        for (int j = 0; j < IPT; ++j) ev[j] = 1;
+    }
+    __builtin_amdgcn_sched_barrier(0);
     uint32_t key[IPT];
     bool valid[IPT];
     int nv = 0;
 #pragma unroll
     for (int j = 0; j < IPT; ++j) {
         const int p = p0 + j;
-        const int pc = p < seq ? p : 0;
-        const float dv = dr[pc];
-        const bool e = el ? el[pc] != 0 : true;
-        const bool v = p < seq && !(p >= bs && p < bs + bl) && e;
+        const bool v = (p < seq) & !((p >= bs) & (p < bs + bl)) & (ev[j] != 0);
         valid[j] = v;
-        key[j] = v ? order_key(dv) : 0u;
+        key[j] = v ? order_key(dv[j]) : 0u;
         nv += v ? 1 : 0;
     }
     hist[0][t] = 0;                     // first histogram buffer (one bin per thread)
