@@ -4,17 +4,20 @@
 
 A step is the whole hot path over one batch: drift -> select -> sparse K/V
 refresh -> Q projection of the active block -> bidirectional attention ->
-commit, six C-ABI calls on one stream.  The default workload is the LLaDA-8B-shaped layer (bf16,
+commit, one polestar_step call on one stream (five launch groups: the
+select, the Q projection and the vocabulary scan share one launch, the
+attention merge and the commit finalize another).  The default workload is the LLaDA-8B-shaped layer (bf16,
 batch 1, d=4096, 32 heads of 128, sequence 768 = prompt 512 + 256 generated,
 active block 32, vocabulary 126464) with 15% of the positions heavily
 perturbed.  Inputs are seeded synthetic data, resident in HBM before timing.
 
 To measure HBM rather than the 256 MB Infinity Cache, every step reads one of
 R independent copies of all inputs and weights (R * working set > 256 MB),
-round robin.  After the warmup, an untimed diagnostic pass records HIP events
-around every call (the per-call breakdown, "calls_us") and names the dominant
-call; in the timed region events on the launch stream bracket that call only,
-which gives the roofline's launch duration.  One JSON line is printed.
+round robin.  After the warmup, an untimed diagnostic pass runs the six calls one
+by one with HIP events around each (the per-call breakdown, "calls_us"); in
+the timed region polestar_step records events on the launch stream around
+its refresh launches, the dominant kernels, which gives the roofline's launch
+duration.  One JSON line is printed.
 
 Counter summaries (HBM traffic of the dominant call):
 
@@ -354,39 +357,47 @@ def main():
             call(name, s)
         ev[len(CALLS)].record(stream)
 
-    def run_step(i, ev=None, only=None):
-        """One step, every call on the launch stream, events around the call
-        named `only`."""
-        s = sets[i % copies]
-        for name in CALLS:
-            if ev is not None and name == only:
-                ev[0].record(stream)
-            call(name, s)
-            if ev is not None and name == only:
-                ev[1].record(stream)
+    # the step as it runs in the timed region: polestar_step, with its
+    # arguments built once per input copy
+    prepared = [step.prepare(c["h_cur"], c["h_prev"], c["w_q"], c["w_k"], c["w_v"], c["k_cache"],
+                             c["v_cache"], c["logits"], c["masked"], c["hist"], c["hist_len"],
+                             tau_s=cfg.tau_s, alpha=cfg.alpha) for c in sets]
+
+    def run_step(i, ev=None):
+        step.launch(prepared[i % copies], ev)
 
     for i in range(args.warmup):
         run_step(i)
     torch.cuda.synchronize()
 
-    # diagnostic pass (untimed): events around every call give the per-call
-    # breakdown and name the dominant call
+    # diagnostic pass (untimed): the six calls one by one with events around
+    # each give the per-call breakdown
+    # each give the per-call breakdown.  A device-side spin enqueued first
+    # lets the host queue the whole pass ahead of the GPU, so the events time
+    # the kernels back to back rather than the Python launch path.
     ndiag = max(1, min(args.steps, 50))
     dev_events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)] for _ in range(ndiag)]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(100_000_000)
     for i in range(ndiag):
         run_serial(i, dev_events[i])
     torch.cuda.synchronize()
     call_us = {c: float(np.mean([ev[j].elapsed_time(ev[j + 1]) * 1e3 for ev in dev_events]))
                for j, c in enumerate(CALLS)}
-    dom = max(call_us, key=call_us.get)
+    dom = "refresh_kv"   # the step's dominant launch group; polestar_step brackets it with events
 
-    # timed region: K whole steps; HIP events on the launch stream bracket
-    # the dominant call only
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    # timed region: K whole steps through polestar_step; its refresh launches
+    # are bracketed by HIP events recorded on the launch stream
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    for ev in events:             # create the events before timing
+        ev[0].record(stream)
+        ev[1].record(stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        run_step(args.warmup + i, events[i], only=dom)
+        run_step(args.warmup + i, events[i])
+    enqueued = time.perf_counter() - t0
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     dom_us = float(np.mean([ev[0].elapsed_time(ev[1]) * 1e3 for ev in events]))
@@ -438,6 +449,7 @@ def main():
                    "global_batch": cfg.batch, "seq_len": cfg.seq, "block": cfg.block_len,
                    "stale_rows": k, "input_copies": copies},
         "roofline": roof,
+        "host_enqueue_us_per_step": round(enqueued / args.steps * 1e6, 2),
         "calls_us": calls,
     }
     if not args.no_cpu_baseline:

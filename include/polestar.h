@@ -247,6 +247,70 @@ polestar_status polestar_commit(polestar_dtype dtype, int batch, int block_len, 
                                 void* workspace, size_t workspace_bytes,
                                 hipStream_t stream);
 
+/*
+ * polestar_step -- one whole layer step: polestar_drift, polestar_select,
+ * polestar_refresh_kv, polestar_project_q, polestar_attend (queries from q)
+ * and polestar_commit (with the drift branch on), with exactly their
+ * definitions and results, on one stream.
+ *
+ * Work that does not depend on the previous launch shares launches: the
+ * per-sequence select runs beside the Q projection and the vocabulary scan,
+ * and the attention's split merge beside the commit's finalize step, so the
+ * latency-bound pieces overlap bandwidth-bound ones.  Shapes outside the
+ * fused kernels (seq > 2048, batch * block_len > 64, block_len > 256) run
+ * the six calls one after another instead, with the same results.
+ *
+ * All fields of polestar_step_args keep the meaning, layout and
+ * requirements they have in the stand-alone calls above; eligible may be
+ * NULL, lse may be NULL, h may be 0 (hist, hist_len then unused), scale <= 0
+ * selects 1/sqrt(head_dim), k = 0 refreshes the active block only.
+ *   workspace : >= polestar_step_workspace_size(args) bytes, no initialisation
+ *   refresh_begin, refresh_end : optional events (NULL: none) recorded on the
+ *       stream right before and right after the refresh launches, so that a
+ *       caller can time the K/V refresh inside the step.
+ * Returns the first non-OK status of the pieces; as with the stand-alone
+ * calls, argument errors are found on the host before anything is enqueued
+ * (for the fused path: every check of every piece).
+ */
+typedef struct polestar_step_args {
+    polestar_dtype dtype;
+    int batch, seq, d;
+    int n_heads, n_kv_heads, head_dim;
+    int block_start, block_len;
+    int vocab;
+    int k;               /* stale rows per sequence */
+    int h;               /* drift history depth */
+    int mask_token_id;
+    int force_one;
+    float tau_s, alpha, scale;
+    const void* h_cur;   /* [batch][seq][d] */
+    const void* h_prev;  /* [batch][seq][d] */
+    const uint8_t* eligible;   /* [batch][seq] or NULL */
+    const void* w_q;     /* [n_heads*head_dim][d] */
+    const void* w_k;     /* [n_kv_heads*head_dim][d] */
+    const void* w_v;     /* [n_kv_heads*head_dim][d] */
+    void* k_cache;       /* [batch][seq][n_kv_heads][head_dim], in/out */
+    void* v_cache;       /* [batch][seq][n_kv_heads][head_dim], in/out */
+    const void* logits;  /* [batch][block_len][vocab] */
+    const uint8_t* masked;     /* [batch][block_len] */
+    float* hist;         /* [batch][h][block_len], in/out */
+    int32_t* hist_len;   /* [batch], in/out */
+    float* drift;        /* out [batch][seq] */
+    int32_t* stale_idx;  /* out [batch][k] */
+    int32_t* stale_count;     /* out [batch] */
+    void* q;             /* out [batch][block_len][n_heads][head_dim] */
+    void* out;           /* out [batch][block_len][n_heads][head_dim] */
+    float* lse;          /* out [batch][n_heads][block_len] or NULL */
+    int32_t* token;      /* out [batch][block_len] */
+    float* conf;         /* out [batch][block_len] */
+    uint8_t* commit;     /* out [batch][block_len] */
+} polestar_step_args;
+
+size_t polestar_step_workspace_size(const polestar_step_args* args);
+polestar_status polestar_step(const polestar_step_args* args, void* workspace,
+                              size_t workspace_bytes, hipEvent_t refresh_begin,
+                              hipEvent_t refresh_end, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

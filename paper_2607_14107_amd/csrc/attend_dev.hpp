@@ -1,0 +1,456 @@
+// Device side of polestar_attend, shared by attend.hip and the fused step.
+//
+// Bidirectional attention of the active block over the whole
+// cache (Sec. 2, eq. 3: queries of J_b attend to the cached K/V of I and the
+// recomputed K/V of J_b, here all held in the refreshed cache; App. B setup:
+// l = q.k / sqrt(d_h), a = softmax(l), o = sum a v).  No causal mask.
+//
+// The queries come from the Q projection (the shared skinny GEMM of
+// gemm.hip).  Split-key flash attention:
+//  - workgroup = (sequence b, query head h, group of 32 queries, key split);
+//    its 4 waves take 32-key tiles in turn and keep an online softmax;
+//  - S^T = K Q^T on MFMA with K as the A operand, so each lane ends up with
+//    the scores of one query for 8 keys -- exactly the B-operand slice of
+//    O^T = V^T P^T.  V^T is staged in LDS with its keys in the same order;
+//  - the 4 waves are merged in LDS; with one split the workgroup writes the
+//    output directly, otherwise (m, l, O) partials go to the workspace and a
+//    merge kernel combines the splits in order with their log-sum-exp.
+// Scores are kept in base-2 units (scale * log2 e folded in) for exp2.
+#pragma once
+
+#include "common.hpp"
+#include "host_common.hpp"
+
+namespace ps {
+namespace {
+
+constexpr int kAttBlock = 256;   // 4 waves
+constexpr int kQG = 32;          // queries per workgroup
+constexpr int kKT = 32;          // keys per tile
+
+struct AttArgs {
+    const char* q;       // [batch][nq][H][hd]
+    const char* k;       // [batch][seq][Hkv][hd]
+    const char* v;
+    char* out;           // [batch][nq][H][hd]
+    float* lse;          // [batch][H][nq] or null
+    float* part_o;       // [batch][H][nq][splits][hd]
+    float* part_ml;      // [batch][H][nq][splits][2]
+    int batch, seq, nq, H, Hkv;
+    int splits, tiles_per_split;
+    float scale_log2;    // scale * log2(e)
+};
+
+// Position of key kk (0..31) of a tile in the LDS row of V^T: lane group g
+// reads slots 8g..8g+7 = keys 4g..4g+3 and 16+4g..16+4g+3 (bf16 path).
+__device__ __forceinline__ int vslot(int kk) {
+    return kk < 16 ? 8 * (kk >> 2) + (kk & 3) : 8 * ((kk - 16) >> 2) + 4 + (kk & 3);
+}
+
+template <bool BF16, int HD>
+__global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
+    using T = Elem<BF16>;
+    constexpr int ES = T::kBytes;
+    constexpr int NC = HD * ES / 64;        // 16-byte chunks of one lane's d-range
+    constexpr int DPL = HD / 4;             // d values per lane group
+    constexpr int DT = HD / 16;             // 16-row d tiles of O^T
+    // V^T rows: bf16 32 keys (64 B) + 16 B pad; fp32 32 keys (128 B) + 16 B pad
+    constexpr int VP = BF16 ? 80 : 144;
+    __shared__ __align__(16) char vt[4][HD * VP];
+    __shared__ float wm[4][kQG], wl[4][kQG];
+    __shared__ __align__(16) float wo[4][kQG][HD + 4];
+
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    const int g = lane >> 4;
+    const int split = blockIdx.x;
+    const int qgroups = (a.nq + kQG - 1) / kQG;
+    const int h = blockIdx.y / qgroups;
+    const int qg = blockIdx.y - h * qgroups;
+    const int b = blockIdx.z;
+    const int kvh = h / (a.H / a.Hkv);
+
+    const size_t krow = static_cast<size_t>(a.Hkv) * HD * ES;   // bytes per cache row
+    const char* kbase = a.k + (static_cast<size_t>(b) * a.seq * a.Hkv + kvh) * HD * ES;
+    const char* vbase = a.v + (static_cast<size_t>(b) * a.seq * a.Hkv + kvh) * HD * ES;
+
+    // Q fragments (B operand of S^T): query 16u + (lane & 15), d in [DPL g, DPL g + DPL).
+    // All loads are unconditional: queries past nq and keys past seq read the
+    // last row (finite values whose results are masked or never stored), so
+    // no load sits behind an exec mask and the wait counts stay static.
+    uint4 qf[2][NC];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int q = min(qg * kQG + 16 * u + (lane & 15), a.nq - 1);
+        const char* qp = a.q + ((static_cast<size_t>(b) * a.nq + q) * a.H + h) * HD * ES + g * DPL * ES;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) qf[u][c] = ld16(qp + 16 * c);
+    }
+
+    floatx4 o[DT][2];
+#pragma unroll
+    for (int i = 0; i < DT; ++i) o[i][0] = o[i][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float mrun[2] = {-INFINITY, -INFINITY};
+    float lrun[2] = {0.f, 0.f};
+
+    const int ntiles = (a.seq + kKT - 1) / kKT;
+    const int t_begin = split * a.tiles_per_split;
+    const int t_end = min(ntiles, t_begin + a.tiles_per_split);
+    // Each wave stages and reads only its own V^T region, so no workgroup
+    // barrier is needed until the waves are merged.
+    char* myvt = vt[w];
+    const int wu = __builtin_amdgcn_readfirstlane(w);   // wave-uniform tile choice
+
+    for (int base = t_begin; base < t_end; base += 4) {
+        const int tile = base + wu;
+        if (tile < t_end) {
+            const int key0 = tile * kKT;
+            floatx4 st[2][2];
+            // K fragments (A operand): key key0 + 16 t + (lane & 15).
+            uint4 kf[2][NC];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const int key = min(key0 + 16 * t + (lane & 15), a.seq - 1);
+                const char* kp = kbase + static_cast<size_t>(key) * krow + g * DPL * ES;
+#pragma unroll
+                for (int c = 0; c < NC; ++c) kf[t][c] = ld16(kp + 16 * c);
+            }
+            // V tile -> LDS, transposed to [d][key slot].  Every V load of
+            // the tile is issued before any packing (compile-time trip count).
+            if constexpr (BF16) {
+                // 8 groups of 4 keys x HD/8 chunks of 8 d; item pr = lane + 64 it
+                constexpr int DC = HD / 8;
+                constexpr int IT = DC * 8 / 64;
+                uint4 vv[IT][4];
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int pr = lane + 64 * it;
+                    const int dc = pr % DC, kg = pr / DC;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int key = min(key0 + 4 * kg + j, a.seq - 1);
+                        vv[it][j] = ld16(vbase + static_cast<size_t>(key) * krow + dc * 16);
+                    }
+                }
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int pr = lane + 64 * it;
+                    const int dc = pr % DC, kg = pr / DC;
+                    const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vv[it][0]);
+                    const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vv[it][1]);
+                    const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vv[it][2]);
+                    const uint32_t* x3 = reinterpret_cast<const uint32_t*>(&vv[it][3]);
+                    const int slot = vslot(4 * kg);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int sh = (e & 1) * 16;
+                        const uint32_t k0 = (x0[e >> 1] >> sh) & 0xffffu;
+                        const uint32_t k1 = (x1[e >> 1] >> sh) & 0xffffu;
+                        const uint32_t k2 = (x2[e >> 1] >> sh) & 0xffffu;
+                        const uint32_t k3 = (x3[e >> 1] >> sh) & 0xffffu;
+                        uint2 pk = make_uint2(k0 | (k1 << 16), k2 | (k3 << 16));
+                        *reinterpret_cast<uint2*>(myvt + (dc * 8 + e) * VP + slot * 2) = pk;
+                    }
+                }
+            } else {
+                constexpr int DC = HD / 4;
+                constexpr int IT = DC * 8 / 64;
+                uint4 vv[IT][4];
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int pr = lane + 64 * it;
+                    const int dc = pr % DC, kg = pr / DC;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int key = min(key0 + 4 * kg + j, a.seq - 1);
+                        vv[it][j] = ld16(vbase + static_cast<size_t>(key) * krow + dc * 16);
+                    }
+                }
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    const int pr = lane + 64 * it;
+                    const int dc = pr % DC, kg = pr / DC;
+                    const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vv[it][0]);
+                    const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vv[it][1]);
+                    const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vv[it][2]);
+                    const uint32_t* x3 = reinterpret_cast<const uint32_t*>(&vv[it][3]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        *reinterpret_cast<uint4*>(myvt + (dc * 4 + e) * VP + 16 * kg) =
+                            make_uint4(x0[e], x1[e], x2[e], x3[e]);
+                }
+            }
+            // S^T tiles: st[t][u] = K_t Q_u^T.
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    floatx4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) s = Mma<BF16>::step(kf[t][c], qf[u][c], s);
+                    st[t][u] = s;
+                }
+            float p[2][2][4];   // [t][u][i]
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                float mx = -INFINITY;
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int key = key0 + 16 * t + 4 * g + i;
+                        const float s = key < a.seq ? st[t][u][i] * a.scale_log2 : -INFINITY;
+                        p[t][u][i] = s;
+                        mx = fmaxf(mx, s);
+                    }
+                mx = fmaxf(mx, __shfl_xor(mx, 16));
+                mx = fmaxf(mx, __shfl_xor(mx, 32));
+                const float mnew = fmaxf(mrun[u], mx);
+                const float mref = mnew == -INFINITY ? 0.f : mnew;
+                const float alpha = fast_exp2(mrun[u] - mref);
+                float sum = 0.f;
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float e = fast_exp2(p[t][u][i] - mref);
+                        p[t][u][i] = e;
+                        sum += e;
+                    }
+                sum += __shfl_xor(sum, 16);
+                sum += __shfl_xor(sum, 32);
+                lrun[u] = lrun[u] * alpha + sum;
+                mrun[u] = mnew;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) o[dt][u] *= alpha;
+            }
+            // O^T += V^T P^T
+            if constexpr (BF16) {
+                uint4 pf[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+                    pf[u] = make_uint4(pack_bf16x2(p[0][u][0], p[0][u][1]), pack_bf16x2(p[0][u][2], p[0][u][3]),
+                                       pack_bf16x2(p[1][u][0], p[1][u][1]), pack_bf16x2(p[1][u][2], p[1][u][3]));
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    const uint4 va = *reinterpret_cast<const uint4*>(myvt + (dt * 16 + (lane & 15)) * VP + g * 16);
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) o[dt][u] = mfma_bf16(va, pf[u], o[dt][u]);
+                }
+            } else {
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    const float* vrow = reinterpret_cast<const float*>(myvt + (dt * 16 + (lane & 15)) * VP);
+#pragma unroll
+                    for (int t = 0; t < 2; ++t)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float va = vrow[16 * t + 4 * g + i];
+#pragma unroll
+                            for (int u = 0; u < 2; ++u) o[dt][u] = mfma_f32(va, p[t][u][i], o[dt][u]);
+                        }
+                }
+            }
+        }
+    }
+
+    // Merge the four waves.  Lane holds O^T[d = 16 dt + 4 g + i][q = 16 u + (lane & 15)].
+    if (lane < 16) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            wm[w][16 * u + lane] = mrun[u];
+            wl[w][16 * u + lane] = lrun[u];
+        }
+    }
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) wo[w][16 * u + (lane & 15)][dt * 16 + 4 * g + i] = o[dt][u][i];
+    __syncthreads();
+
+    // Each thread finishes 32*HD/256 outputs: query qi, d range.
+    constexpr int PER = kQG * HD / kAttBlock;   // 8 (HD 64) or 16 (HD 128)
+    const int qi = threadIdx.x / (HD / PER);
+    const int d0 = (threadIdx.x % (HD / PER)) * PER;
+    const int q = qg * kQG + qi;
+    float M = -INFINITY;
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww) M = fmaxf(M, wm[ww][qi]);
+    const float Mref = M == -INFINITY ? 0.f : M;
+    float wgt[4], L = 0.f;
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww) {
+        wgt[ww] = fast_exp2(wm[ww][qi] - Mref);
+        L += wl[ww][qi] * wgt[ww];
+    }
+    float acc[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        float s = 0.f;
+#pragma unroll
+        for (int ww = 0; ww < 4; ++ww) s += wo[ww][qi][d0 + j] * wgt[ww];
+        acc[j] = s;
+    }
+    if (q >= a.nq) return;
+    const size_t row = (static_cast<size_t>(b) * a.nq + q) * a.H + h;   // [b][q][h]
+    if (a.splits == 1) {
+        const float inv = 1.f / L;
+        char* op = a.out + (row * HD + d0) * ES;
+#pragma unroll
+        for (int j = 0; j < PER; j += 8) {
+            if constexpr (BF16) {
+                st16(op + 2 * j, make_uint4(pack_bf16x2(acc[j] * inv, acc[j + 1] * inv),
+                                            pack_bf16x2(acc[j + 2] * inv, acc[j + 3] * inv),
+                                            pack_bf16x2(acc[j + 4] * inv, acc[j + 5] * inv),
+                                            pack_bf16x2(acc[j + 6] * inv, acc[j + 7] * inv)));
+            } else {
+                float* fp = reinterpret_cast<float*>(op) + j;
+                *reinterpret_cast<float4*>(fp) = make_float4(acc[j] * inv, acc[j + 1] * inv,
+                                                             acc[j + 2] * inv, acc[j + 3] * inv);
+                *reinterpret_cast<float4*>(fp + 4) = make_float4(acc[j + 4] * inv, acc[j + 5] * inv,
+                                                                 acc[j + 6] * inv, acc[j + 7] * inv);
+            }
+        }
+        if (a.lse && d0 == 0)
+            a.lse[(static_cast<size_t>(b) * a.H + h) * a.nq + q] = (M + __log2f(L)) * kLn2;
+    } else {
+        const size_t prow = ((static_cast<size_t>(b) * a.H + h) * a.nq + q) * a.splits + split;
+        float* po = a.part_o + prow * HD + d0;
+#pragma unroll
+        for (int j = 0; j < PER; j += 4)
+            *reinterpret_cast<float4*>(po + j) = make_float4(acc[j], acc[j + 1], acc[j + 2], acc[j + 3]);
+        if (d0 == 0) {
+            a.part_ml[prow * 2] = M;
+            a.part_ml[prow * 2 + 1] = L;
+        }
+    }
+}
+
+// Combine the key splits of one (b, h, q) row: one wave per row, lanes over d.
+// Splits are taken eight at a time with every load of the chunk issued
+// before any arithmetic (indices clamped, extra splits weighted zero), and
+// merged in split order with a running maximum.
+template <bool BF16, int HD>
+__device__ __forceinline__ void merge_body(const AttArgs& a, int blk) {
+    constexpr int ES = Elem<BF16>::kBytes;
+    constexpr int PL = HD / 64;   // d values per lane (1 or 2)
+    constexpr int CH = 8;         // splits per chunk
+    const int lane = threadIdx.x & 63;
+    const long rowid = static_cast<long>(blk) * 4 + (threadIdx.x >> 6);   // over [b][h][q]
+    const long nrows = static_cast<long>(a.batch) * a.H * a.nq;
+    if (rowid >= nrows) return;
+    const int q = static_cast<int>(rowid % a.nq);
+    const long bh = rowid / a.nq;
+    const int h = static_cast<int>(bh % a.H);
+    const int b = static_cast<int>(bh / a.H);
+    const size_t prow0 = static_cast<size_t>(rowid) * a.splits;
+    float M = -INFINITY, L = 0.f, acc[PL];
+#pragma unroll
+    for (int j = 0; j < PL; ++j) acc[j] = 0.f;
+    for (int s0 = 0; s0 < a.splits; s0 += CH) {
+        float2 ml[CH];
+        float po[CH][PL];
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const size_t pr = prow0 + min(s0 + c, a.splits - 1);
+            ml[c] = *reinterpret_cast<const float2*>(a.part_ml + pr * 2);
+#pragma unroll
+            for (int j = 0; j < PL; ++j) po[c][j] = a.part_o[pr * HD + lane * PL + j];
+        }
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const float m = s0 + c < a.splits ? ml[c].x : -INFINITY;
+            const float mn = fmaxf(M, m);
+            const float mref = mn == -INFINITY ? 0.f : mn;
+            const float wold = fast_exp2(M - mref), wnew = fast_exp2(m - mref);
+            L = L * wold + ml[c].y * wnew;
+#pragma unroll
+            for (int j = 0; j < PL; ++j) acc[j] = acc[j] * wold + po[c][j] * wnew;
+            M = mn;
+        }
+    }
+    const float inv = 1.f / L;
+    const size_t row = (static_cast<size_t>(b) * a.nq + q) * a.H + h;
+    char* op = a.out + (row * HD + lane * PL) * ES;
+    if constexpr (BF16) {
+        if constexpr (PL == 2) *reinterpret_cast<uint32_t*>(op) = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+        else *reinterpret_cast<uint16_t*>(op) = static_cast<uint16_t>(f32_to_bf16_bits(acc[0] * inv));
+    } else {
+#pragma unroll
+        for (int j = 0; j < PL; ++j) reinterpret_cast<float*>(op)[j] = acc[j] * inv;
+    }
+    if (a.lse && lane == 0) a.lse[(static_cast<size_t>(b) * a.H + h) * a.nq + q] = (M + __log2f(L)) * kLn2;
+}
+
+struct AttPlan {
+    int splits;
+    int tiles_per_split;
+    size_t part_bytes;   // partial O + (m, l)
+};
+
+inline AttPlan att_plan(int batch, int seq, int H, int nq, int hd) {
+    AttPlan p{};
+    const int ntiles = ceil_div(seq, kKT);
+    const long base = static_cast<long>(batch) * H * ceil_div(nq, kQG);
+    int splits = static_cast<int>((512 + base - 1) / base);
+    const int max_splits = ceil_div(ntiles, 4);      // at least one tile per wave
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    p.tiles_per_split = ceil_div(ntiles, splits);
+    p.splits = ceil_div(ntiles, p.tiles_per_split);
+    if (p.splits > 1) {
+        const size_t rows = static_cast<size_t>(batch) * H * nq * p.splits;
+        p.part_bytes = align_up(rows * hd * sizeof(float), 256) + align_up(rows * 2 * sizeof(float), 256);
+    }
+    return p;
+}
+
+template <bool BF16, int HD>
+void launch_att(const AttPlan& p, const AttArgs& a, hipStream_t s) {
+    dim3 grid(p.splits, a.H * ceil_div(a.nq, kQG), a.batch);
+    hipLaunchKernelGGL((attend_kernel<BF16, HD>), grid, dim3(kAttBlock), 0, s, a);
+}
+
+template <bool BF16, int HD>
+__global__ __launch_bounds__(256) void attend_merge_kernel(AttArgs a) {
+    merge_body<BF16, HD>(a, blockIdx.x);
+}
+
+template <bool BF16, int HD>
+void launch_merge(const AttArgs& a, hipStream_t s) {
+    const long rows = static_cast<long>(a.batch) * a.H * a.nq;
+    hipLaunchKernelGGL((attend_merge_kernel<BF16, HD>), dim3(ceil_div(rows, 4)), dim3(256), 0, s, a);
+}
+
+// Attention arguments for a plan; `part` is the plan's partial buffer (null
+// when the plan has one split).
+inline AttArgs att_args(const AttPlan& p, int batch, int seq, int nq, int H, int Hkv, int hd,
+                        const void* q, const void* k, const void* v, void* out, float* lse,
+                        float scale, char* part) {
+    AttArgs a{};
+    a.q = static_cast<const char*>(q);
+    a.k = static_cast<const char*>(k);
+    a.v = static_cast<const char*>(v);
+    a.out = static_cast<char*>(out);
+    a.lse = lse;
+    a.batch = batch;
+    a.seq = seq;
+    a.nq = nq;
+    a.H = H;
+    a.Hkv = Hkv;
+    a.splits = p.splits;
+    a.tiles_per_split = p.tiles_per_split;
+    const float sc = scale > 0.f ? scale : 1.0f / sqrtf(static_cast<float>(hd));
+    a.scale_log2 = sc * kLog2e;
+    if (p.splits > 1) {
+        const size_t rows = static_cast<size_t>(batch) * H * nq * p.splits;
+        a.part_o = reinterpret_cast<float*>(part);
+        a.part_ml = reinterpret_cast<float*>(part + align_up(rows * hd * sizeof(float), 256));
+    }
+    return a;
+}
+
+}  // namespace
+}  // namespace ps

@@ -38,6 +38,18 @@ class PolestarError(RuntimeError):
         self.status = status
 
 
+class StepArgs(ctypes.Structure):
+    """Mirror of polestar_step_args (include/polestar.h), field for field."""
+    _fields_ = [(n, ctypes.c_int) for n in (
+        "dtype", "batch", "seq", "d", "n_heads", "n_kv_heads", "head_dim", "block_start", "block_len",
+        "vocab", "k", "h", "mask_token_id", "force_one")] + \
+        [(n, ctypes.c_float) for n in ("tau_s", "alpha", "scale")] + \
+        [(n, ctypes.c_void_p) for n in (
+            "h_cur", "h_prev", "eligible", "w_q", "w_k", "w_v", "k_cache", "v_cache", "logits", "masked",
+            "hist", "hist_len", "drift", "stale_idx", "stale_count", "q", "out", "lse", "token", "conf",
+            "commit")]
+
+
 def lib() -> ctypes.CDLL:
     """Load libpolestar.so once and declare its signatures."""
     global _lib
@@ -67,6 +79,10 @@ def lib() -> ctypes.CDLL:
     L.polestar_attend_workspace_size.argtypes = [I, I, I, I, I, I, I, I]
     L.polestar_attend.restype = S
     L.polestar_attend.argtypes = [I, I, I, I, I, I, I, I, I, P, P, P, P, P, F, P, P, P, Z, P]
+    L.polestar_step_workspace_size.restype = Z
+    L.polestar_step_workspace_size.argtypes = [ctypes.POINTER(StepArgs)]
+    L.polestar_step.restype = S
+    L.polestar_step.argtypes = [ctypes.POINTER(StepArgs), P, Z, P, P, P]
     L.polestar_commit_workspace_size.restype = Z
     L.polestar_commit_workspace_size.argtypes = [I, I, I, I]
     L.polestar_commit.restype = S
@@ -261,9 +277,67 @@ def commit(logits: torch.Tensor, masked: torch.Tensor, drift_vals: torch.Tensor 
 # one layer step with preallocated buffers
 # ---------------------------------------------------------------------------
 
+def _event_handle(ev) -> int | None:
+    """Raw hipEvent_t of a torch.cuda.Event (created by recording it once)."""
+    if ev is None:
+        return None
+    if not ev.cuda_event:
+        ev.record()
+    return ev.cuda_event
+
+
+def step_args(*, h_cur, h_prev, w_q, w_k, w_v, k_cache, v_cache, logits, masked, hist, hist_len,
+              drift_out, stale_idx, stale_count, q, out, lse, token, conf, commit_out, k: int,
+              block_start: int, block_len: int, n_heads: int, eligible=None, mask_token_id: int = -1,
+              tau_s: float = DEFAULT_TAU_S, alpha: float = DEFAULT_ALPHA, force_one: bool = False,
+              scale: float = 0.0) -> StepArgs:
+    """polestar_step_args for one layer step (checks dtypes and devices)."""
+    b, seq, d = h_cur.shape
+    _, _, kvh, hd = k_cache.shape
+    dt = h_cur.dtype
+    a = StepArgs()
+    a.dtype = _dtype_code(h_cur)
+    a.batch, a.seq, a.d = b, seq, d
+    a.n_heads, a.n_kv_heads, a.head_dim = n_heads, kvh, hd
+    a.block_start, a.block_len = block_start, block_len
+    a.vocab = logits.shape[2]
+    a.k = k
+    a.h = hist.shape[1] if hist is not None else 0
+    a.mask_token_id = mask_token_id
+    a.force_one = int(bool(force_one))
+    a.tau_s, a.alpha, a.scale = float(tau_s), float(alpha), float(scale)
+    a.h_cur, a.h_prev = _ptr(h_cur), _ptr(h_prev, dt)
+    a.eligible = _ptr(eligible, torch.uint8)
+    a.w_q, a.w_k, a.w_v = _ptr(w_q, dt), _ptr(w_k, dt), _ptr(w_v, dt)
+    a.k_cache, a.v_cache = _ptr(k_cache, dt), _ptr(v_cache, dt)
+    a.logits, a.masked = _ptr(logits, dt), _ptr(masked, torch.uint8)
+    a.hist, a.hist_len = _ptr(hist, torch.float32), _ptr(hist_len, torch.int32)
+    a.drift = _ptr(drift_out, torch.float32)
+    a.stale_idx = _ptr(stale_idx, torch.int32) if k > 0 else None
+    a.stale_count = _ptr(stale_count, torch.int32)
+    a.q, a.out = _ptr(q, dt), _ptr(out, dt)
+    a.lse = _ptr(lse, torch.float32)
+    a.token, a.conf, a.commit = _ptr(token, torch.int32), _ptr(conf, torch.float32), _ptr(commit_out, torch.uint8)
+    return a
+
+
+def step_workspace_size(args: StepArgs) -> int:
+    return lib().polestar_step_workspace_size(ctypes.byref(args))
+
+
+def step(args: StepArgs, workspace: torch.Tensor, refresh_events=None, stream=None) -> None:
+    """polestar_step: the whole layer step; refresh_events = (begin, end)
+    torch.cuda.Event pair recorded around the K/V refresh, or None."""
+    ev0, ev1 = refresh_events if refresh_events is not None else (None, None)
+    nbytes = workspace.numel() * workspace.element_size()
+    _check("polestar_step", lib().polestar_step(ctypes.byref(args), _ptr(workspace), nbytes,
+                                                _event_handle(ev0), _event_handle(ev1), _stream(stream)))
+
+
 class Step:
-    """One layer step on buffers allocated once, every call on the current
-    stream: drift -> select -> refresh_kv -> project_q -> attend -> commit.
+    """One layer step on buffers allocated once, on the current stream:
+    drift -> select -> refresh_kv -> project_q -> attend -> commit, through
+    polestar_step (run) or as six separate calls (run_calls).
 
     (The query projection reads only h_cur and W_q and could run on a second
     stream; measured on MI355X, the cross-stream event waits cost more than
@@ -292,15 +366,48 @@ class Step:
         self.ws_q = _workspace(project_q_workspace_size(dt, batch, d, n_heads, head_dim, block_len), dev, None)
         self.ws_attend = _workspace(attend_workspace_size(dt, batch, seq, d, n_heads, n_kv_heads, head_dim, block_len), dev, None)
         self.ws_commit = _workspace(commit_workspace_size(dt, batch, block_len, vocab), dev, None)
+        self.ws_step = None
+
+    def prepare(self, h_cur, h_prev, w_q, w_k, w_v, k_cache, v_cache, logits, masked, hist, hist_len,
+                *, mask_token_id=-1, tau_s=DEFAULT_TAU_S, alpha=DEFAULT_ALPHA, force_one=False,
+                eligible=None) -> StepArgs:
+        """polestar_step_args for these inputs and this step's outputs (build
+        once, launch many times while the tensors stay the same)."""
+        s = self.shape
+        args = step_args(h_cur=h_cur, h_prev=h_prev, w_q=w_q, w_k=w_k, w_v=w_v, k_cache=k_cache,
+                         v_cache=v_cache, logits=logits, masked=masked, hist=hist, hist_len=hist_len,
+                         drift_out=self.drift, stale_idx=self.stale_idx, stale_count=self.stale_count,
+                         q=self.q_buf, out=self.out, lse=self.lse, token=self.token, conf=self.conf,
+                         commit_out=self.commit, k=s["k"], block_start=s["block_start"],
+                         block_len=s["block_len"], n_heads=s["n_heads"], eligible=eligible,
+                         mask_token_id=mask_token_id, tau_s=tau_s, alpha=alpha, force_one=force_one)
+        need = step_workspace_size(args)
+        if self.ws_step is None or self.ws_step.numel() < need:
+            self.ws_step = _workspace(need, self.drift.device, None)
+        return args
+
+    def launch(self, args: StepArgs, refresh_events=None):
+        """polestar_step on prepared arguments."""
+        step(args, self.ws_step, refresh_events)
+        return self
 
     def run(self, h_cur, h_prev, w_q, w_k, w_v, k_cache, v_cache, logits, masked, hist, hist_len,
             *, mask_token_id=-1, tau_s=DEFAULT_TAU_S, alpha=DEFAULT_ALPHA, force_one=False,
-            eligible=None):
+            eligible=None, refresh_events=None):
+        """The step through polestar_step (fused launches)."""
+        args = self.prepare(h_cur, h_prev, w_q, w_k, w_v, k_cache, v_cache, logits, masked, hist, hist_len,
+                            mask_token_id=mask_token_id, tau_s=tau_s, alpha=alpha, force_one=force_one,
+                            eligible=eligible)
+        return self.launch(args, refresh_events)
+
+    def run_calls(self, h_cur, h_prev, w_q, w_k, w_v, k_cache, v_cache, logits, masked, hist, hist_len,
+                  *, mask_token_id=-1, tau_s=DEFAULT_TAU_S, alpha=DEFAULT_ALPHA, force_one=False,
+                  eligible=None):
+        """The same step as six separate calls."""
         s = self.shape
         drift(h_cur, h_prev, out=self.drift)
-        if s["k"] > 0:
-            select(self.drift, s["k"], s["block_start"], s["block_len"], eligible,
-                   self.stale_idx, self.stale_count)
+        select(self.drift, s["k"], s["block_start"], s["block_len"], eligible, self.stale_idx,
+               self.stale_count)
         refresh_kv(h_cur, self.stale_idx, self.stale_count, s["block_start"], s["block_len"],
                    w_k, w_v, k_cache, v_cache, workspace=self.ws_refresh)
         project_q(h_cur, w_q, s["block_start"], s["block_len"], s["n_heads"], out=self.q_buf,

@@ -29,7 +29,7 @@ def _header_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = _header_functions()
-    assert len(names) == 12, names
+    assert len(names) == 14, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -142,6 +142,37 @@ def test_commit_validation_and_workspace(L):
     assert f(*a) == UNSUPPORTED                               # rows of 16-byte chunks
     a = list(args); a[20] = ws - 1
     assert f(*a) == WORKSPACE
+
+
+def test_step_validation_and_workspace(L):
+    a = ps.StepArgs()
+    a.dtype, a.batch, a.seq, a.d = 1, 1, 768, 4096
+    a.n_heads, a.n_kv_heads, a.head_dim = 32, 32, 128
+    a.block_start, a.block_len, a.vocab, a.k, a.h = 512, 32, 126464, 106, 5
+    a.mask_token_id, a.tau_s, a.alpha = -1, 0.9, 10.0
+    ws = ps.step_workspace_size(a)
+    assert ws > 0
+    # sum of the pieces' workspaces (refresh, attention partials, scan partials)
+    parts = (ps.refresh_kv_workspace_size(1, 1, 4096, 32, 128, 106, 32)
+             + ps.attend_workspace_size(1, 1, 768, 4096, 32, 32, 128, 32)
+             + ps.commit_workspace_size(1, 1, 32, 126464))
+    assert parts <= ws <= parts + 4 * 256
+    f = L.polestar_step
+    assert f(ctypes.byref(a), FAKE, ws, None, None, None) == INVALID      # pointers missing
+    for name in ("h_cur", "h_prev", "w_q", "w_k", "w_v", "k_cache", "v_cache", "logits", "masked", "hist",
+                 "hist_len", "drift", "stale_idx", "stale_count", "q", "out", "token", "conf", "commit"):
+        setattr(a, name, FAKE)
+    assert f(ctypes.byref(a), FAKE, ws - 1, None, None, None) == WORKSPACE
+    a.block_start = 740
+    assert f(ctypes.byref(a), FAKE, ws, None, None, None) == INVALID      # block past the end
+    a.block_start = 512
+    a.n_kv_heads = 5
+    assert f(ctypes.byref(a), FAKE, 1 << 30, None, None, None) == INVALID  # heads % kv heads
+    a.n_kv_heads = 32
+    a.h_cur = MISALIGNED
+    assert f(ctypes.byref(a), FAKE, ws, None, None, None) == UNSUPPORTED
+    assert L.polestar_step(None, FAKE, ws, None, None, None) == INVALID
+    assert L.polestar_step_workspace_size(None) == 0
 
 
 def test_binding_fails_loudly_without_gpu_tensors():

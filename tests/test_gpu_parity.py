@@ -480,3 +480,102 @@ def test_layer_step_end_to_end_and_deterministic(P, cfg_index, subrun):
     token, conf = ref.confidence(ref.decode(x["logits"], cfg.dtype), -1)
     assert np.array_equal(a["token"], token)
     np.testing.assert_allclose(a["conf"], conf, rtol=1e-4)
+
+
+# ---------------------------------------------------------------------------
+# fused step == the six calls
+# ---------------------------------------------------------------------------
+
+def _step_inputs(cfg, x, kc, vc):
+    torch = _torch()
+    dev = {n: to_dev(x[n], cfg.dtype) for n in ("h_cur", "h_prev", "w_q", "w_k", "w_v", "logits")}
+    dev["k_cache"], dev["v_cache"] = to_dev(kc, cfg.dtype), to_dev(vc, cfg.dtype)
+    dev["masked"] = torch.from_numpy(x["masked"]).cuda()
+    dev["hist"] = torch.from_numpy(x["hist"].copy()).cuda()
+    dev["hist_len"] = torch.from_numpy(x["hist_len"].copy()).cuda()
+    return dev
+
+
+def _run_both(P, cfg, x, kc, vc, k, force_one=True):
+    """Outputs of Step.run (polestar_step) and Step.run_calls on identical inputs."""
+    torch = _torch()
+    dt = torch.float32 if cfg.dtype == "fp32" else torch.bfloat16
+    res = []
+    for fused in (True, False):
+        st = P.Step(batch=cfg.batch, seq=cfg.seq, d=cfg.d, n_heads=cfg.n_heads, n_kv_heads=cfg.n_kv_heads,
+                    head_dim=cfg.head_dim, block_start=cfg.block_start, block_len=cfg.block_len,
+                    vocab=cfg.vocab, k=k, dtype=dt)
+        v = _step_inputs(cfg, x, kc, vc)
+        run = st.run if fused else st.run_calls
+        run(v["h_cur"], v["h_prev"], v["w_q"], v["w_k"], v["w_v"], v["k_cache"], v["v_cache"], v["logits"],
+            v["masked"], v["hist"], v["hist_len"], force_one=force_one)
+        torch.cuda.synchronize()
+        out = dict(drift=st.drift, cnt=st.stale_count, q=st.q_buf, out=st.out, lse=st.lse, token=st.token,
+                   conf=st.conf, commit=st.commit, kc=v["k_cache"], vc=v["v_cache"], hist=v["hist"],
+                   hist_len=v["hist_len"])
+        if k > 0:
+            out["idx"] = st.stale_idx
+        res.append({n: from_dev(t) for n, t in out.items()})
+    return res
+
+
+def _assert_same(a, b):
+    for n in a:
+        assert np.array_equal(a[n].view(np.uint8) if a[n].dtype != np.uint8 else a[n],
+                              b[n].view(np.uint8) if b[n].dtype != np.uint8 else b[n]), f"fused step differs in {n}"
+
+
+@pytest.mark.parametrize("cfg_index,subrun", [(0, 0), (1, 1), (2, 0), (3, 0)])
+def test_step_fused_equals_calls_on_configs(P, cfg_index, subrun):
+    """Configs 0-1 take the fused launches, 2-3 (more than 64 query rows) the
+    six-call fallback; either way the results equal the six calls bit for bit."""
+    L = layer(cfg_index, subrun)
+    a, b = _run_both(P, L["cfg"], L["x"], L["kc"], L["vc"], int(L["x"]["k"]))
+    _assert_same(a, b)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("batch,seq,bs,bl,d,H,Hkv,hd,vocab,k", [
+    (1, 100, 40, 30, 256, 2, 1, 64, 1000, 9),       # 1 key per thread, ragged block, GQA
+    (2, 700, 600, 32, 256, 4, 4, 64, 2048, 70),     # 3 keys per thread, 64 query rows (MT 4)
+    (1, 1500, 1400, 20, 512, 2, 2, 128, 4096, 0),   # 6 keys per thread, no stale rows
+    (3, 2048, 0, 16, 256, 1, 1, 128, 512, 200),     # 8 keys per thread, block at the start
+])
+def test_step_fused_equals_calls_small_shapes(P, dtype, batch, seq, bs, bl, d, H, Hkv, hd, vocab, k):
+    from types import SimpleNamespace
+    g = np.random.default_rng(seq + 31 * k)
+    cfg = SimpleNamespace(dtype=dtype, batch=batch, seq=seq, d=d, n_heads=H, n_kv_heads=Hkv, head_dim=hd,
+                          block_start=bs, block_len=bl, vocab=vocab)
+    base = g.standard_normal((batch, seq, d), dtype=np.float32)
+    hp = base.copy()
+    hc = base.copy()
+    heavy = g.random((batch, seq)) < 0.2
+    hc[heavy] += 0.5 * g.standard_normal((int(heavy.sum()), d), dtype=np.float32)
+    x = dict(h_cur=inputs.store(hc, dtype), h_prev=inputs.store(hp, dtype),
+             w_q=inputs.store(0.03 * g.standard_normal((H * hd, d), dtype=np.float32), dtype),
+             w_k=inputs.store(0.03 * g.standard_normal((Hkv * hd, d), dtype=np.float32), dtype),
+             w_v=inputs.store(0.03 * g.standard_normal((Hkv * hd, d), dtype=np.float32), dtype),
+             logits=inputs.store(3.0 * g.standard_normal((batch, bl, vocab), dtype=np.float32), dtype),
+             masked=(g.random((batch, bl)) < 0.7).astype(np.uint8),
+             hist=(1e-4 * g.random((batch, 5, bl))).astype(np.float32),
+             hist_len=g.integers(0, 6, size=batch).astype(np.int32))
+    kc = inputs.store(0.1 * g.standard_normal((batch, seq, Hkv, hd), dtype=np.float32), dtype)
+    vc = inputs.store(0.1 * g.standard_normal((batch, seq, Hkv, hd), dtype=np.float32), dtype)
+    a, b = _run_both(P, cfg, x, kc, vc, k, force_one=bool(k % 2))
+    _assert_same(a, b)
+
+
+def test_step_refresh_events_bracket_the_refresh(P):
+    torch = _torch()
+    L = layer(1, 1)
+    cfg, x = L["cfg"], L["x"]
+    st = P.Step(batch=cfg.batch, seq=cfg.seq, d=cfg.d, n_heads=cfg.n_heads, n_kv_heads=cfg.n_kv_heads,
+                head_dim=cfg.head_dim, block_start=cfg.block_start, block_len=cfg.block_len, vocab=cfg.vocab,
+                k=int(x["k"]), dtype=torch.bfloat16)
+    v = _step_inputs(cfg, x, L["kc"], L["vc"])
+    ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    st.run(v["h_cur"], v["h_prev"], v["w_q"], v["w_k"], v["w_v"], v["k_cache"], v["v_cache"], v["logits"],
+           v["masked"], v["hist"], v["hist_len"], refresh_events=ev)
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1])
+    assert 0.0 < ms < 50.0
