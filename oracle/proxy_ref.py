@@ -28,7 +28,8 @@ Readings where the paper leaves the detail open (also listed in the design doc):
        of rank floor(j*n/K).  A fixed number of iterations (default 10):
        assign each point to the centroid of largest cosine (ties: lowest
        cluster), then each centroid becomes the normalised sum of its
-       members' directions; a cluster left empty keeps its centroid.
+       members' directions; a cluster left empty keeps its centroid.  The
+       returned labels are the assignment to the final centroids.
   P-3  The proxy token of a cluster is the mean of its members' hidden
        states (not the unit centroid, whose scale would flatten attention),
        rounded to the activation dtype like any hidden state; its query is
@@ -58,7 +59,8 @@ def spherical_kmeans(h_win: np.ndarray, n_clusters: int, iters: int = 10):
     """h_win: [n][d] hidden states of the window positions (in position order).
 
     Returns (labels [n] int, centroids [K][d] unit vectors) after `iters`
-    rounds of assignment and update (readings P-1, P-2)."""
+    rounds of assignment and update; the labels assign every point to its
+    nearest final centroid (readings P-1, P-2)."""
     n = h_win.shape[0]
     x = h_win / np.linalg.norm(h_win, axis=1, keepdims=True)          # directions (P-1)
     z = np.stack([x[(j * n) // n_clusters] for j in range(n_clusters)])   # deterministic start (P-2)
@@ -72,6 +74,7 @@ def spherical_kmeans(h_win: np.ndarray, n_clusters: int, iters: int = 10):
                 continue                                # empty: keep the centroid (P-2)
             s = members.sum(axis=0)
             z[k] = s / np.linalg.norm(s)
+    labels = np.argmax(x @ z.T, axis=1)                 # the final centroids' assignment (P-2)
     return labels, z
 
 
