@@ -232,6 +232,45 @@ def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, cal
     return 0
 
 
+def measure_proxy(P, torch, cfg, s, stream, es, n_clusters=8, k_top=4, reps=50):
+    """The paper's clustered drift estimator on the same layer (untimed for
+    the headline): block-entry K-means of the window (2B before the block, B
+    after), then per step proxy drift + cluster select.  HIP events on the
+    launch stream, behind a device spin so the GPU runs the calls back to back."""
+    win = P.window_positions(cfg.seq, cfg.block_start, cfg.block_len, 2 * cfg.block_len, cfg.block_len)
+    widx = torch.tensor([win] * cfg.batch, dtype=torch.int32, device=s["h_cur"].device)
+    scores = torch.empty((cfg.batch, n_clusters, cfg.n_heads, cfg.seq), dtype=torch.float32, device=widx.device)
+    lse = torch.empty((cfg.batch, n_clusters, cfg.n_heads), dtype=torch.float32, device=widx.device)
+    dt = P.BF16 if cfg.dtype == "bf16" else P.FP32
+    ws = torch.empty(P.proxy_drift_workspace_size(dt, cfg.batch, cfg.seq, cfg.d, cfg.n_heads, cfg.head_dim,
+                                                  n_clusters), dtype=torch.uint8, device=widx.device)
+    drift_c = torch.empty((cfg.batch, n_clusters), dtype=torch.float32, device=widx.device)
+    idx = torch.empty((cfg.batch, len(win)), dtype=torch.int32, device=widx.device)
+    cnt = torch.empty((cfg.batch,), dtype=torch.int32, device=widx.device)
+    labels, sums, counts, _ = P.cluster(s["h_prev"], widx, n_clusters)
+    P.proxy_drift(sums, counts, s["w_q"], s["k_cache"], cfg.n_heads, scores, lse, True, drift_c, workspace=ws)
+    torch.cuda.synchronize()
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    torch.cuda._sleep(50_000_000)
+    e[0].record(stream)
+    for _ in range(5):
+        P.cluster(s["h_prev"], widx, n_clusters)
+    e[1].record(stream)
+    for _ in range(reps):
+        P.proxy_drift(sums, counts, s["w_q"], s["k_cache"], cfg.n_heads, scores, lse, False, drift_c, workspace=ws)
+        P.cluster_select(labels, drift_c, k_top, len(win), idx, cnt)
+    e[2].record(stream)
+    torch.cuda.synchronize()
+    step_us = e[1].elapsed_time(e[2]) * 1e3 / reps
+    kv_bytes = cfg.batch * cfg.seq * cfg.n_kv_heads * cfg.head_dim * es
+    sc_bytes = 3 * cfg.batch * n_clusters * cfg.n_heads * cfg.seq * 4
+    alg = cfg.n_heads * cfg.head_dim * cfg.d * es + kv_bytes + sc_bytes
+    return {"window": len(win), "clusters": n_clusters, "top_clusters": k_top,
+            "block_entry_kmeans_us": round(e[0].elapsed_time(e[1]) * 1e3 / 5, 2),
+            "step_us": round(step_us, 3), "step_bytes": int(alg),
+            "step_GB_s": round(alg / (step_us * 1e-6) / 1e9, 1)}
+
+
 def cpu_baseline(cfg, x, k, budget_s):
     """The oracle as it stands, timed on the host on whole steps of the same
     workload until about budget_s seconds of CPU work are done."""
@@ -402,6 +441,8 @@ def main():
     elapsed = time.perf_counter() - t0
     dom_us = float(np.mean([ev[0].elapsed_time(ev[1]) * 1e3 for ev in events]))
 
+    proxy = measure_proxy(P, torch, cfg, sets[0], stream, es)
+
     tokens = cfg.batch * cfg.block_len
     value = tokens * args.steps / elapsed
     cost = algorithmic_cost(cfg, k, es)
@@ -449,6 +490,7 @@ def main():
                    "global_batch": cfg.batch, "seq_len": cfg.seq, "block": cfg.block_len,
                    "stale_rows": k, "input_copies": copies},
         "roofline": roof,
+        "proxy_drift": proxy,
         "host_enqueue_us_per_step": round(enqueued / args.steps * 1e6, 2),
         "calls_us": calls,
     }

@@ -248,6 +248,98 @@ polestar_status polestar_commit(polestar_dtype dtype, int batch, int block_len, 
                                 hipStream_t stream);
 
 /*
+ * Clustered proxy drift -- Polestar's own drift estimator (Sec. 4.1 "Cluster
+ * and Quantize Hidden States" and "Measuring Drift and Layer-wise KV
+ * Updates"; Alg. 1: SphericalKMeans at block entry, ProxyAttn, KL and TopK
+ * per step).  The window's hidden states are clustered once per block; at
+ * every step each cluster's proxy token attends over the cache, its drift is
+ * the KL between this step's and the last step's proxy distributions, and
+ * the members of the top-k clusters are the rows to refresh.  An alternative
+ * to polestar_drift + polestar_select; the refresh and everything after it
+ * are unchanged.
+ *
+ * polestar_cluster -- spherical K-means of h[b][win_idx[b][i]] (i < n_win):
+ * points are the directions h/|h|; centroid j starts at the point of window
+ * rank floor(j*n_win/K); `iters` rounds of (assign each point to the centroid
+ * of largest cosine, lowest cluster on ties; centroid = normalised sum of its
+ * members' directions, an empty cluster keeps its centroid); then every point
+ * is assigned to its nearest final centroid.
+ *   h         : [batch][seq][d] dtype
+ *   win_idx   : [batch][n_win] int32 window positions (entries are clamped
+ *               into [0, seq); positions should be distinct)
+ *   labels    : out [batch][seq] int32, the cluster of each window position,
+ *               -1 elsewhere
+ *   sums      : out [batch][K][d] float, sum of the members' hidden states
+ *   counts    : out [batch][K] int32, members per cluster
+ *   centroids : out [batch][K][d] float, the unit centroids
+ * K = n_clusters.  UNSUPPORTED for K > 16, n_win > 2048, K*d > 32768,
+ * d not a multiple of 512 (bf16) / 256 (fp32), or h, sums, centroids not
+ * 16-byte aligned.
+ * Runs once per block: one workgroup per sequence.
+ */
+polestar_status polestar_cluster(polestar_dtype dtype, int batch, int seq, int d, const void* h,
+                                 const int32_t* win_idx, int n_win, int n_clusters, int iters,
+                                 int32_t* labels, float* sums, int32_t* counts, float* centroids,
+                                 hipStream_t stream);
+
+/*
+ * polestar_proxy_drift -- per step: proxy token t_k = sums[b][k] / counts[b][k]
+ * rounded to dtype (zero for an empty cluster); query q = W_q t_k rounded to
+ * dtype; per head h (KV head g = h / (n_heads / n_kv_heads))
+ *     s_(k,h,j) = scale * q_(k,h) . k_cache[b][j][g]   for every j < seq;
+ * and drift[b][k] = (1/n_heads) sum_h KL(softmax_j s_(k,h,.) ||
+ * softmax_j s'_(k,h,.)) in nats, s' the previous step's scores.  The new
+ * scores and their log-sum-exp then replace the previous ones.
+ *   sums, counts : the cluster state (polestar_cluster / _update)
+ *   w_q          : [n_heads*head_dim][d] dtype
+ *   k_cache      : [batch][seq][n_kv_heads][head_dim] dtype (the refreshed cache)
+ *   scores       : in/out [batch][K][n_heads][seq] float
+ *   lse          : in/out [batch][K][n_heads] float (natural log)
+ *   first        : nonzero at block entry: no previous scores are read,
+ *                  drift is 0, the scores and lse are stored
+ *   drift        : out [batch][K] float
+ *   workspace    : >= polestar_proxy_drift_workspace_size(...) bytes
+ * scale <= 0 selects 1/sqrt(head_dim).  UNSUPPORTED unless head_dim is 64 or
+ * 128, d % 128 == 0 (bf16) / d % 64 == 0 (fp32), K <= 16,
+ * K * (seq + head_dim) <= 36864 (one head's scores of every cluster are held
+ * on chip), and sums, W_q, k_cache and the workspace are 16-byte aligned.
+ */
+size_t polestar_proxy_drift_workspace_size(polestar_dtype dtype, int batch, int seq, int d,
+                                           int n_heads, int head_dim, int n_clusters);
+polestar_status polestar_proxy_drift(polestar_dtype dtype, int batch, int seq, int d, int n_heads,
+                                     int n_kv_heads, int head_dim, int n_clusters, const float* sums,
+                                     const int32_t* counts, const void* w_q, const void* k_cache,
+                                     float scale, float* scores, float* lse, int first, float* drift,
+                                     void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * polestar_cluster_select -- the k_top clusters of largest drift (equal
+ * drift: lower cluster first) of each sequence; their member positions
+ * (labels[b][p] selected) go to stale_idx[b][0..count) in ascending order,
+ * the rest of the row is -1, stale_count[b] = count (at most k_max: a row
+ * with more members keeps the first k_max).  Feeds polestar_refresh_kv.
+ *   labels : [batch][seq] int32 (polestar_cluster), drift : [batch][K] float
+ *   stale_idx : out [batch][k_max] int32, stale_count : out [batch] int32
+ */
+polestar_status polestar_cluster_select(int batch, int seq, const int32_t* labels, int n_clusters,
+                                        const float* drift, int k_top, int32_t* stale_idx, int k_max,
+                                        int32_t* stale_count, hipStream_t stream);
+
+/*
+ * polestar_cluster_update -- after the refresh of the rows in
+ * stale_idx[b][0..stale_count[b]): sums[b][labels[b][p]] += h_new[b][p] -
+ * h_old[b][p] for each of them that lies in the window (labels >= 0),
+ * accumulated in list order (deterministic).  Labels and counts stay.
+ *   h_new, h_old : [batch][seq][d] dtype;  sums : in/out [batch][K][d] float
+ * UNSUPPORTED unless d % 4 == 0 and K <= 16.
+ */
+polestar_status polestar_cluster_update(polestar_dtype dtype, int batch, int seq, int d,
+                                        const void* h_new, const void* h_old, const int32_t* labels,
+                                        int n_clusters, const int32_t* stale_idx,
+                                        const int32_t* stale_count, int k_max, float* sums,
+                                        hipStream_t stream);
+
+/*
  * polestar_step -- one whole layer step: polestar_drift, polestar_select,
  * polestar_refresh_kv, polestar_project_q, polestar_attend (queries from q)
  * and polestar_commit (with the drift branch on), with exactly their

@@ -21,7 +21,8 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpolestar.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "drift.hip", "select.hip", "gemm.hip", "attend.hip", "commit.hip", "step.hip"]
+SOURCES = ["api.hip", "drift.hip", "select.hip", "gemm.hip", "attend.hip", "commit.hip", "step.hip",
+           "proxy.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

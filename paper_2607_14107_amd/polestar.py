@@ -79,6 +79,16 @@ def lib() -> ctypes.CDLL:
     L.polestar_attend_workspace_size.argtypes = [I, I, I, I, I, I, I, I]
     L.polestar_attend.restype = S
     L.polestar_attend.argtypes = [I, I, I, I, I, I, I, I, I, P, P, P, P, P, F, P, P, P, Z, P]
+    L.polestar_cluster.restype = S
+    L.polestar_cluster.argtypes = [I, I, I, I, P, P, I, I, I, P, P, P, P, P]
+    L.polestar_proxy_drift_workspace_size.restype = Z
+    L.polestar_proxy_drift_workspace_size.argtypes = [I, I, I, I, I, I, I]
+    L.polestar_proxy_drift.restype = S
+    L.polestar_proxy_drift.argtypes = [I, I, I, I, I, I, I, I, P, P, P, P, F, P, P, I, P, P, Z, P]
+    L.polestar_cluster_select.restype = S
+    L.polestar_cluster_select.argtypes = [I, I, P, I, P, I, P, I, P, P]
+    L.polestar_cluster_update.restype = S
+    L.polestar_cluster_update.argtypes = [I, I, I, I, P, P, P, I, P, P, I, P, P]
     L.polestar_step_workspace_size.restype = Z
     L.polestar_step_workspace_size.argtypes = [ctypes.POINTER(StepArgs)]
     L.polestar_step.restype = S
@@ -276,6 +286,90 @@ def commit(logits: torch.Tensor, masked: torch.Tensor, drift_vals: torch.Tensor 
 # ---------------------------------------------------------------------------
 # one layer step with preallocated buffers
 # ---------------------------------------------------------------------------
+
+# ---------------------------------------------------------------------------
+# clustered proxy drift
+# ---------------------------------------------------------------------------
+
+def window_positions(seq: int, block_start: int, block_len: int, prefix: int, suffix: int) -> list:
+    """The local window around the active block: [start - prefix, start) and
+    [end, end + suffix), clipped to the sequence."""
+    lo, hi = max(0, block_start - prefix), min(seq, block_start + block_len + suffix)
+    return list(range(lo, block_start)) + list(range(block_start + block_len, hi))
+
+
+def cluster(h: torch.Tensor, win_idx: torch.Tensor, n_clusters: int, iters: int = 10, stream=None):
+    """Spherical K-means of the window's hidden states -> (labels [b][seq],
+    sums [b][K][d], counts [b][K], centroids [b][K][d])."""
+    b, seq, d = h.shape
+    dev = h.device
+    n_win = win_idx.shape[1]
+    labels = torch.empty((b, seq), dtype=torch.int32, device=dev)
+    sums = torch.empty((b, n_clusters, d), dtype=torch.float32, device=dev)
+    counts = torch.empty((b, n_clusters), dtype=torch.int32, device=dev)
+    cents = torch.empty((b, n_clusters, d), dtype=torch.float32, device=dev)
+    _check("polestar_cluster", lib().polestar_cluster(
+        _dtype_code(h), b, seq, d, _ptr(h), _ptr(win_idx, torch.int32), n_win, n_clusters, iters,
+        _ptr(labels), _ptr(sums), _ptr(counts), _ptr(cents), _stream(stream)))
+    return labels, sums, counts, cents
+
+
+def proxy_drift_workspace_size(dtype: int, batch: int, seq: int, d: int, n_heads: int, head_dim: int,
+                               n_clusters: int) -> int:
+    return lib().polestar_proxy_drift_workspace_size(dtype, batch, seq, d, n_heads, head_dim, n_clusters)
+
+
+def proxy_drift(sums: torch.Tensor, counts: torch.Tensor, w_q: torch.Tensor, k_cache: torch.Tensor,
+                n_heads: int, scores: torch.Tensor, lse: torch.Tensor, first: bool,
+                drift_out: torch.Tensor | None = None, scale: float = 0.0,
+                workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Drift per cluster [b][K]; scores [b][K][H][seq] and lse [b][K][H] are
+    the previous step's on entry and this step's on return."""
+    b, K, d = sums.shape
+    _, seq, kvh, hd = k_cache.shape
+    dt = _dtype_code(k_cache)
+    if drift_out is None:
+        drift_out = torch.empty((b, K), dtype=torch.float32, device=sums.device)
+    ws = _workspace(proxy_drift_workspace_size(dt, b, seq, d, n_heads, hd, K), sums.device, workspace)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("polestar_proxy_drift", lib().polestar_proxy_drift(
+        dt, b, seq, d, n_heads, kvh, hd, K, _ptr(sums, torch.float32), _ptr(counts, torch.int32),
+        _ptr(w_q, k_cache.dtype), _ptr(k_cache), float(scale), _ptr(scores, torch.float32),
+        _ptr(lse, torch.float32), int(bool(first)), _ptr(drift_out, torch.float32), _ptr(ws), nbytes,
+        _stream(stream)))
+    return drift_out
+
+
+def cluster_select(labels: torch.Tensor, drift_vals: torch.Tensor, k_top: int, k_max: int,
+                   stale_idx: torch.Tensor | None = None, stale_count: torch.Tensor | None = None,
+                   stream=None):
+    """Members of the k_top clusters of largest drift -> (stale_idx [b][k_max], stale_count [b])."""
+    b, seq = labels.shape
+    K = drift_vals.shape[1]
+    dev = labels.device
+    if stale_idx is None:
+        stale_idx = torch.empty((b, k_max), dtype=torch.int32, device=dev)
+    if stale_count is None:
+        stale_count = torch.empty((b,), dtype=torch.int32, device=dev)
+    _check("polestar_cluster_select", lib().polestar_cluster_select(
+        b, seq, _ptr(labels, torch.int32), K, _ptr(drift_vals, torch.float32), k_top,
+        _ptr(stale_idx, torch.int32) if k_max > 0 else None, k_max, _ptr(stale_count, torch.int32),
+        _stream(stream)))
+    return stale_idx, stale_count
+
+
+def cluster_update(h_new: torch.Tensor, h_old: torch.Tensor, labels: torch.Tensor,
+                   stale_idx: torch.Tensor, stale_count: torch.Tensor, sums: torch.Tensor,
+                   stream=None) -> None:
+    """sums[label(p)] += h_new[p] - h_old[p] for the refreshed window rows."""
+    b, seq, d = h_new.shape
+    K = sums.shape[1]
+    k_max = stale_idx.shape[1]
+    _check("polestar_cluster_update", lib().polestar_cluster_update(
+        _dtype_code(h_new), b, seq, d, _ptr(h_new), _ptr(h_old, h_new.dtype), _ptr(labels, torch.int32), K,
+        _ptr(stale_idx, torch.int32) if k_max > 0 else None, _ptr(stale_count, torch.int32), k_max,
+        _ptr(sums, torch.float32), _stream(stream)))
+
 
 def _event_handle(ev) -> int | None:
     """Raw hipEvent_t of a torch.cuda.Event (created by recording it once)."""

@@ -29,7 +29,7 @@ def _header_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = _header_functions()
-    assert len(names) == 14, names
+    assert len(names) == 19, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -173,6 +173,37 @@ def test_step_validation_and_workspace(L):
     assert f(ctypes.byref(a), FAKE, ws, None, None, None) == UNSUPPORTED
     assert L.polestar_step(None, FAKE, ws, None, None, None) == INVALID
     assert L.polestar_step_workspace_size(None) == 0
+
+
+def test_proxy_calls_validation(L):
+    c = L.polestar_cluster
+    args = [1, 1, 768, 4096, FAKE, FAKE, 96, 8, 10, FAKE, FAKE, FAKE, FAKE, None]
+    a = list(args); a[4] = None
+    assert c(*a) == INVALID
+    a = list(args); a[7] = 97
+    assert c(*a) == INVALID                                   # more clusters than points
+    a = list(args); a[7] = 17
+    a[6] = 200
+    assert c(*a) == UNSUPPORTED                               # K above 16
+    a = list(args); a[3] = 8192
+    assert c(*a) == UNSUPPORTED                               # K * d above the LDS budget
+    ws = ps.proxy_drift_workspace_size(1, 1, 768, 4096, 32, 128, 8)
+    assert ws > 0
+    f = L.polestar_proxy_drift
+    pa = [1, 1, 768, 4096, 32, 32, 128, 8, FAKE, FAKE, FAKE, FAKE, 0.0, FAKE, FAKE, 0, FAKE, FAKE, ws, None]
+    a = list(pa); a[5] = 5
+    assert f(*a) == INVALID                                   # heads % kv heads
+    a = list(pa); a[6] = 96
+    assert f(*a) == UNSUPPORTED
+    a = list(pa); a[18] = ws - 1
+    assert f(*a) == WORKSPACE
+    s = L.polestar_cluster_select
+    assert s(1, 768, FAKE, 8, FAKE, 4, None, 10, FAKE, None) == INVALID        # k_max > 0 needs stale_idx
+    assert s(1, 768, FAKE, 17, FAKE, 4, FAKE, 10, FAKE, None) == UNSUPPORTED
+    u = L.polestar_cluster_update
+    assert u(1, 1, 768, 4096, FAKE, FAKE, FAKE, 8, FAKE, FAKE, 10, None, None) == INVALID   # sums
+    assert u(1, 1, 768, 4094, FAKE, FAKE, FAKE, 8, FAKE, FAKE, 10, FAKE, None) == UNSUPPORTED
+    assert u(1, 1, 768, 4096, FAKE, FAKE, FAKE, 8, FAKE, FAKE, 0, FAKE, None) == 0         # nothing refreshed
 
 
 def test_binding_fails_loudly_without_gpu_tensors():
