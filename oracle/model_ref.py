@@ -1,0 +1,290 @@
+"""CPU oracle of Polestar's denoising loop on a whole layer stack.
+
+TEST INFRASTRUCTURE ONLY, like `polestar_ref`: the slow plain reference that
+the GPU loop is checked against; only the tests, the package's smoke check and
+the benchmark's `cpu_baseline` leg may use it, and it never consumes a value
+produced by the HIP path except where a test feeds it the GPU's layer inputs
+on purpose (replay).  float64 NumPy; the per-layer hot path is composed from
+`polestar_ref` (drift, select, refresh_kv, attend, confidence, commit_rule).
+
+The model (a masked-diffusion LM of the shape the paper evaluates, Sec. 5.1;
+readings where the paper gives no detail, also listed in the design doc):
+  M-1  Pre-norm layers: x += W_o Attn(h), h = RMSNorm(x); then
+       x += W_down (silu(W_gate g) * W_up g), g = RMSNorm(x).  Attention is
+       bidirectional over every cache slot (eq. 3).
+  M-2  RMSNorm(x) = x / sqrt(mean(x^2) + eps) with unit gain, eps = 1e-5.
+  M-3  Positions enter as an absolute position table added to the token
+       embedding (no rotary embedding): with random weights it only has to
+       make positions distinguishable, and it keeps K/V a plain projection of
+       the cached hidden state.
+  M-4  Rounding: the residual stream x is kept in fp32 (here: exact); every
+       other stored tensor is rounded to the activation dtype: h, g, q, K, V,
+       the attention output, W_o's output, the gate/up outputs, the SwiGLU
+       product, W_down's output and the logits.
+  M-5  The layer's hidden state H (whose drift is measured, from which K/V
+       are projected and which is cached) is h = RMSNorm(x) of the layer input.
+  M-6  Logits = W_lm RMSNorm(x_final); mask id = vocab - 1.
+
+The loop (Alg. 1 with the window-forward reading of the per-token drift):
+  M-7  Block b: J_b = the block's 32 positions; local window
+       Omega_b = [start - 2B, end + B) minus J_b, clipped to the sequence;
+       R = Omega_b u J_b (a contiguous range).
+  M-8  Block entry: even b -> forward every position (all K/V and H
+       rewritten); odd b -> forward R against the cache (K/V and H of all of
+       R rewritten).  Then the confidence-only commit of J_b (no fallback),
+       and the drift history is emptied.
+  M-9  Within the block, a step refreshes when the tokens committed since
+       the last refreshing forward exceed tau_upd (Sec. 4.1 "Update
+       Schedule"); the block entry counts as refreshing.  A refreshing step
+       forwards R: per layer drift on R's rows, the top ceil(|Omega|/2) of
+       Omega refreshed (K/V and H) along with J_b, queries from all of R.  A
+       plain step forwards J_b only (its K/V and H rewritten).  After the last
+       layer: logits of J_b, delta_j = drift of J_b at the last layer, the
+       Polestar-Commit rule (force_one), then the suffix commit of the
+       suffix rows that the last layer refreshed (Sec. 4.2).
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from oracle import polestar_ref as ref
+
+EPS = 1e-5
+
+
+# ---------------------------------------------------------------------------
+# model pieces
+# ---------------------------------------------------------------------------
+
+def rmsnorm(x: np.ndarray, eps: float = EPS) -> np.ndarray:
+    """M-2: x / sqrt(mean over the last axis of x^2 + eps)."""
+    x = np.asarray(x, dtype=np.float64)
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps)
+
+
+def silu(x: np.ndarray) -> np.ndarray:
+    """x * sigmoid(x)."""
+    return x / (1.0 + np.exp(-x))
+
+
+@dataclass
+class Shape:
+    n_layers: int
+    d: int
+    n_heads: int
+    head_dim: int
+    ffn: int
+    vocab: int
+    seq: int
+    dtype: str = "bf16"
+
+    @property
+    def mask_id(self) -> int:
+        return self.vocab - 1                                   # M-6
+
+
+def embed(tok_emb: np.ndarray, pos_emb: np.ndarray, ids: np.ndarray, lo: int, hi: int) -> np.ndarray:
+    """M-3: x[b][r] = tok_emb[ids[b][lo + r]] + pos_emb[lo + r] for r < hi - lo."""
+    return tok_emb[ids[:, lo:hi]] + pos_emb[None, lo:hi]
+
+
+@dataclass
+class LayerState:
+    """The cached state of one layer: K/V caches [b][S][H][hd] and the cached
+    hidden states H [b][S][d], all float64 holding dtype values."""
+    k: np.ndarray
+    v: np.ndarray
+    h: np.ndarray
+
+
+def layer_forward(x_rows: np.ndarray, lo: int, w: dict, st: LayerState, *, mode: str, block: tuple[int, int],
+                  shape: Shape, k_top: int = 0) -> dict:
+    """One layer over the rows R = [lo, lo + m) of every sequence (M-1, M-5, M-9).
+
+    mode: "all"     -- every K/V and H row of R rewritten (block entry);
+          "refresh" -- drift on R, the top k_top of R minus the block
+                       (eligible = Omega) and the block rewritten;
+          "plain"   -- only the block rewritten (R must be the block).
+    Returns a dict with the new state (st is not modified), the drift on R,
+    the stale set, and x_out for the rows of R."""
+    dt = shape.dtype
+    b, m, d = x_rows.shape
+    seq = st.h.shape[1]
+    bs, bl = block
+    h_rows = ref.round_to(rmsnorm(x_rows), dt)                               # M-5
+    # drift against the cached hidden states, on the rows of R
+    drift = np.zeros((b, seq))
+    drift[:, lo:lo + m] = ref.drift(h_rows, st.h[:, lo:lo + m])
+    if mode == "all":
+        rows = list(range(lo, lo + m))
+        idx = np.zeros((b, 0), np.int32)
+        cnt = np.zeros(b, np.int32)
+        kk, vv, _ = ref.refresh_kv(_place(h_rows, lo, st.h), w["w_k"], w["w_v"], st.k, st.v, idx, cnt, lo, m)
+    else:
+        eligible = np.zeros((b, seq), bool)
+        if mode == "refresh":
+            eligible[:, lo:lo + m] = True
+            eligible[:, bs:bs + bl] = False
+            idx, cnt = ref.select(drift, k_top, bs, bl, eligible)
+        else:
+            assert (lo, m) == (bs, bl)
+            idx, cnt = np.zeros((b, 0), np.int32), np.zeros(b, np.int32)
+        kk, vv, rows = ref.refresh_kv(_place(h_rows, lo, st.h), w["w_k"], w["w_v"], st.k, st.v, idx, cnt, bs, bl)
+    new_h = np.array(st.h, copy=True)
+    full_h = _place(h_rows, lo, st.h)
+    if mode == "all":
+        new_h[:, lo:lo + m] = h_rows
+    else:
+        for s in range(b):
+            r = np.asarray(rows[s], np.int64)
+            new_h[s, r] = full_h[s, r]
+    new = LayerState(ref.round_to(kk, dt), ref.round_to(vv, dt), new_h)
+    # attention of every row of R over the whole (updated) cache
+    q = ref.round_to(h_rows @ w["w_q"].T, dt).reshape(b, m, shape.n_heads, shape.head_dim)
+    o, _ = ref.attend(q, new.k, new.v)
+    o = ref.round_to(o, dt).reshape(b, m, shape.n_heads * shape.head_dim)
+    x = x_rows + ref.round_to(o @ w["w_o"].T, dt)
+    g = ref.round_to(rmsnorm(x), dt)
+    gu = ref.round_to(g @ w["w_gu"].T, dt)
+    f = shape.ffn
+    a = ref.round_to(silu(gu[..., :f]) * gu[..., f:], dt)
+    x = x + ref.round_to(a @ w["w_down"].T, dt)
+    return dict(state=new, drift=drift, stale_idx=idx, stale_count=cnt, h=h_rows, x_out=x)
+
+
+def _place(h_rows: np.ndarray, lo: int, h_all: np.ndarray) -> np.ndarray:
+    out = np.array(h_all, copy=True)
+    out[:, lo:lo + h_rows.shape[1]] = h_rows
+    return out
+
+
+def logits(x_rows: np.ndarray, w_lm: np.ndarray, dtype: str) -> np.ndarray:
+    """M-6: rounded W_lm RMSNorm(x) for the given rows."""
+    return ref.round_to(ref.round_to(rmsnorm(x_rows), dtype) @ w_lm.T, dtype)
+
+
+# ---------------------------------------------------------------------------
+# loop control (pure functions of the block index and the commit history)
+# ---------------------------------------------------------------------------
+
+def block_bounds(prompt_len: int, block_len: int, b: int) -> tuple[int, int]:
+    """J_b = [start, start + block_len)."""
+    s = prompt_len + b * block_len
+    return s, s + block_len
+
+
+def window(prompt_len: int, block_len: int, seq: int, b: int, prefix: int, suffix: int) -> tuple[int, int]:
+    """M-7: R = [max(0, start - prefix), min(seq, end + suffix))."""
+    s, e = block_bounds(prompt_len, block_len, b)
+    return max(0, s - prefix), min(seq, e + suffix)
+
+
+def window_top_k(lo: int, hi: int, block_len: int) -> int:
+    """M-9: ceil(|Omega| / 2), Omega = R minus the block."""
+    return int(math.ceil((hi - lo - block_len) / 2))
+
+
+def refreshes(committed_since: int, tau_upd: int) -> bool:
+    """M-9 / Sec. 4.1 "Update Schedule": refresh once more than tau_upd tokens
+    were decoded since the last refreshing forward."""
+    return committed_since > tau_upd
+
+
+# ---------------------------------------------------------------------------
+# the whole loop, free running (small sizes)
+# ---------------------------------------------------------------------------
+
+@dataclass
+class LoopParams:
+    prompt_len: int
+    gen_len: int
+    block_len: int = 32
+    prefix: int = 64
+    suffix: int = 32
+    tau_upd: int = 3
+    h: int = 5
+    alpha: float = 10.0
+    tau_s: float = 0.9
+    force_one: bool = True
+    suffix_commit: bool = True
+
+
+@dataclass
+class Trace:
+    forwards: list = field(default_factory=list)     # one dict per forward pass
+    committed: int = 0
+
+
+def generate(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams) -> tuple[np.ndarray, Trace]:
+    """Runs the loop of M-7..M-9 on prompt [b][prompt_len]; returns the final
+    token ids [b][seq] and the trace of forwards."""
+    b = prompt.shape[0]
+    seq = p.prompt_len + p.gen_len
+    assert seq == shape.seq
+    dt = shape.dtype
+    mask = shape.mask_id
+    y = np.full((b, seq), mask, np.int64)
+    y[:, :p.prompt_len] = prompt
+    hd = shape.head_dim
+    states = [LayerState(np.zeros((b, seq, shape.n_heads, hd)), np.zeros((b, seq, shape.n_heads, hd)),
+                         np.zeros((b, seq, shape.d))) for _ in range(shape.n_layers)]
+    tr = Trace()
+    n_blocks = p.gen_len // p.block_len
+    hist = np.zeros((b, max(p.h, 1), p.block_len), np.float32)
+    for blk in range(n_blocks):
+        bs, be = block_bounds(p.prompt_len, p.block_len, blk)
+        lo, hi = window(p.prompt_len, p.block_len, seq, blk, p.prefix, p.suffix)
+        # block entry (M-8)
+        elo, ehi = (0, seq) if blk % 2 == 0 else (lo, hi)
+        x = embed(weights["tok_emb"], weights["pos_emb"], y, elo, ehi)
+        for li in range(shape.n_layers):
+            r = layer_forward(x, elo, weights["layers"][li], states[li], mode="all", block=(bs, p.block_len),
+                              shape=shape)
+            states[li], x = r["state"], r["x_out"]
+        lg = logits(x[:, bs - elo:be - elo], weights["w_lm"], dt)
+        tok, conf = ref.confidence(lg, mask)
+        masked = y[:, bs:be] == mask
+        cm = masked & (conf.astype(np.float32) > np.float32(p.tau_s))
+        y[:, bs:be] = np.where(cm, tok, y[:, bs:be])
+        tr.forwards.append(dict(kind="entry_full" if blk % 2 == 0 else "entry_window", block=blk,
+                                rows=(elo, ehi), commit=cm, token=tok))
+        tr.committed += int(cm.sum())
+        since = int(cm.sum())                  # decoded after the entry's (refreshing) forward
+        hist_len = np.zeros(b, np.int32)
+        while (y[:, bs:be] == mask).any():
+            refresh = refreshes(since, p.tau_upd)
+            rlo, rhi = (lo, hi) if refresh else (bs, be)
+            kt = window_top_k(lo, hi, p.block_len) if refresh else 0
+            x = embed(weights["tok_emb"], weights["pos_emb"], y, rlo, rhi)
+            last = None
+            for li in range(shape.n_layers):
+                last = layer_forward(x, rlo, weights["layers"][li], states[li],
+                                     mode="refresh" if refresh else "plain", block=(bs, p.block_len),
+                                     shape=shape, k_top=kt)
+                states[li], x = last["state"], last["x_out"]
+            lg = logits(x[:, bs - rlo:be - rlo], weights["w_lm"], dt)
+            tok, conf = ref.confidence(lg, mask)
+            masked = y[:, bs:be] == mask
+            delta = last["drift"][:, bs:be].astype(np.float32)
+            cm, hist, hist_len = ref.commit_rule(conf.astype(np.float32), delta, masked, hist, hist_len, p.h,
+                                                 p.tau_s, p.alpha, p.force_one)
+            y[:, bs:be] = np.where(cm, tok, y[:, bs:be])
+            n_commit = int(cm.sum())
+            scm = None
+            if p.suffix_commit and refresh and be < hi:
+                el = ref.suffix_eligible(last["stale_idx"], last["stale_count"], be, hi - be)
+                slg = logits(x[:, be - rlo:hi - rlo], weights["w_lm"], dt)
+                stok, sconf = ref.confidence(slg, mask)
+                smask = y[:, be:hi] == mask
+                scm = ref.suffix_commit_rule(sconf.astype(np.float32), smask, el, p.tau_s)
+                y[:, be:hi] = np.where(scm, stok, y[:, be:hi])
+                n_commit += int(scm.sum())
+            tr.forwards.append(dict(kind="refresh" if refresh else "plain", block=blk, rows=(rlo, rhi),
+                                    commit=cm, token=tok, suffix_commit=scm))
+            tr.committed += n_commit
+            since = n_commit if refresh else since + n_commit
+    return y, tr

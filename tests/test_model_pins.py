@@ -1,0 +1,179 @@
+"""Pins of the whole-stack loop oracle (oracle/model_ref.py): closed forms of
+its pieces, a brute-force layer written from the definitions with plain
+loops, cache-consistency invariants of the sparse forwards, the schedule
+rules and invariants of the free-running loop.  CPU only."""
+
+import math
+
+import numpy as np
+import pytest
+
+from oracle import model_ref as mr
+from oracle import polestar_ref as ref
+
+
+def rand_weights(shape: mr.Shape, seed=0, std=0.3, lm_std=None):
+    g = np.random.default_rng(seed)
+    hdim = shape.n_heads * shape.head_dim
+
+    def w(*s, sd=std):
+        return ref.round_to(g.standard_normal(s) * sd, shape.dtype)
+
+    layers = [dict(w_q=w(hdim, shape.d), w_k=w(hdim, shape.d), w_v=w(hdim, shape.d), w_o=w(shape.d, hdim),
+                   w_gu=w(2 * shape.ffn, shape.d), w_down=w(shape.d, shape.ffn)) for _ in range(shape.n_layers)]
+    return dict(tok_emb=w(shape.vocab, shape.d, sd=1.0), pos_emb=w(shape.seq, shape.d, sd=1.0), layers=layers,
+                w_lm=w(shape.vocab, shape.d, sd=lm_std or std))
+
+
+def empty_state(b, shape):
+    return mr.LayerState(np.zeros((b, shape.seq, shape.n_heads, shape.head_dim)),
+                         np.zeros((b, shape.seq, shape.n_heads, shape.head_dim)),
+                         np.zeros((b, shape.seq, shape.d)))
+
+
+def test_rmsnorm_and_silu_closed_forms():
+    x = np.array([[3.0, 4.0]])
+    assert np.allclose(mr.rmsnorm(x, eps=0.0), x / math.sqrt(12.5), rtol=1e-15)
+    assert np.allclose(mr.rmsnorm(x), x / math.sqrt(12.5 + 1e-5), rtol=1e-15)
+    assert mr.silu(np.array(0.0)) == 0.0
+    assert mr.silu(np.array(math.log(3.0))) == pytest.approx(math.log(3.0) * 0.75, rel=1e-15)
+    assert mr.silu(np.array(-50.0)) == pytest.approx(0.0, abs=1e-18)
+
+
+def brute_layer_row(x_all, i, w, shape):
+    """Row i of a full-sequence layer forward, from M-1..M-5 with plain loops
+    (one sequence, fp64 throughout, rounding applied at the same points)."""
+    S, d = len(x_all), shape.d
+    H, hd, F = shape.n_heads, shape.head_dim, shape.ffn
+    rnd = lambda v: float(ref.round_to(np.array(v), shape.dtype))
+
+    def norm(vec):
+        ms = sum(t * t for t in vec) / len(vec)
+        return [rnd(t / math.sqrt(ms + mr.EPS)) for t in vec]
+
+    def mat(wm, vec):
+        return [sum(wm[r][c] * vec[c] for c in range(len(vec))) for r in range(len(wm))]
+
+    h = [norm(list(x_all[j])) for j in range(S)]
+    q = [rnd(t) for t in mat(w["w_q"], h[i])]
+    keys = [[rnd(t) for t in mat(w["w_k"], h[j])] for j in range(S)]
+    vals = [[rnd(t) for t in mat(w["w_v"], h[j])] for j in range(S)]
+    o = []
+    for hh in range(H):
+        sl = slice(hh * hd, (hh + 1) * hd)
+        sc = [sum(a * b for a, b in zip(q[sl], keys[j][sl])) / math.sqrt(hd) for j in range(S)]
+        m = max(sc)
+        e = [math.exp(s - m) for s in sc]
+        z = sum(e)
+        o += [rnd(sum(e[j] / z * vals[j][sl][c] for j in range(S))) for c in range(hd)]
+    x = [x_all[i][c] + rnd(t) for c, t in enumerate(mat(w["w_o"], o))]
+    g = norm(x)
+    gu = [rnd(t) for t in mat(w["w_gu"], g)]
+    a = [rnd(gu[f] / (1 + math.exp(-gu[f])) * gu[F + f]) for f in range(F)]
+    return [x[c] + rnd(t) for c, t in enumerate(mat(w["w_down"], a))]
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_layer_matches_brute_force(dtype):
+    shape = mr.Shape(n_layers=1, d=8, n_heads=2, head_dim=4, ffn=6, vocab=16, seq=5, dtype=dtype)
+    wts = rand_weights(shape, seed=3)
+    g = np.random.default_rng(4)
+    x = g.standard_normal((1, shape.seq, shape.d))
+    r = mr.layer_forward(x, 0, wts["layers"][0], empty_state(1, shape), mode="all", block=(0, shape.seq),
+                         shape=shape)
+    for i in range(shape.seq):
+        want = brute_layer_row(x[0], i, wts["layers"][0], shape)
+        np.testing.assert_allclose(r["x_out"][0, i], want, rtol=1e-9, atol=1e-12)
+
+
+def test_zero_output_projections_leave_the_residual():
+    shape = mr.Shape(n_layers=1, d=16, n_heads=2, head_dim=8, ffn=12, vocab=16, seq=6)
+    wts = rand_weights(shape)
+    w = dict(wts["layers"][0], w_o=np.zeros_like(wts["layers"][0]["w_o"]),
+             w_down=np.zeros_like(wts["layers"][0]["w_down"]))
+    x = np.random.default_rng(1).standard_normal((2, shape.seq, shape.d))
+    r = mr.layer_forward(x, 0, w, empty_state(2, shape), mode="all", block=(0, shape.seq), shape=shape)
+    assert np.array_equal(r["x_out"], x)
+
+
+def _full_then(shape, mode, lo, hi, bs, bl, seed=5):
+    """Full forward of a sequence, then a forward of rows [lo, hi) in `mode`
+    against the cache it left, with the same inputs."""
+    wts = rand_weights(shape, seed=seed)
+    g = np.random.default_rng(seed + 1)
+    x = g.standard_normal((2, shape.seq, shape.d))
+    full = mr.layer_forward(x, 0, wts["layers"][0], empty_state(2, shape), mode="all", block=(bs, bl),
+                            shape=shape)
+    part = mr.layer_forward(x[:, lo:hi], lo, wts["layers"][0], full["state"], mode=mode, block=(bs, bl),
+                            shape=shape, k_top=3)
+    return full, part
+
+
+@pytest.mark.parametrize("mode,lo,hi", [("all", 3, 15), ("refresh", 3, 15), ("plain", 8, 12)])
+def test_sparse_forward_against_a_consistent_cache_reproduces_the_full_forward(mode, lo, hi):
+    shape = mr.Shape(n_layers=1, d=16, n_heads=2, head_dim=8, ffn=12, vocab=16, seq=20)
+    full, part = _full_then(shape, mode, lo, hi, 8, 4)
+    np.testing.assert_array_equal(part["x_out"], full["x_out"][:, lo:hi])
+    for a, b in ((part["state"].k, full["state"].k), (part["state"].v, full["state"].v),
+                 (part["state"].h, full["state"].h)):
+        np.testing.assert_array_equal(a, b)
+    assert np.all(part["drift"] == 0.0)           # unchanged hidden states: zero drift
+
+
+def test_refresh_mode_selects_from_the_window_only_and_rewrites_what_it_selects():
+    shape = mr.Shape(n_layers=1, d=16, n_heads=2, head_dim=8, ffn=12, vocab=16, seq=20)
+    wts = rand_weights(shape, seed=7)
+    g = np.random.default_rng(8)
+    x = g.standard_normal((1, shape.seq, shape.d))
+    full = mr.layer_forward(x, 0, wts["layers"][0], empty_state(1, shape), mode="all", block=(8, 4),
+                            shape=shape)
+    x2 = x.copy()
+    x2[0, [4, 6, 13]] += 3.0 * g.standard_normal((3, shape.d))     # perturb three window rows
+    x2[0, 1] += 5.0                                                # and one outside the window
+    r = mr.layer_forward(x2[:, 3:15], 3, wts["layers"][0], full["state"], mode="refresh", block=(8, 4),
+                         shape=shape, k_top=3)
+    assert r["stale_idx"][0].tolist() == [4, 6, 13] and r["stale_count"][0] == 3
+    h_new = ref.round_to(mr.rmsnorm(x2[0]), shape.dtype)
+    for p in (4, 6, 13, 8, 9, 10, 11):
+        assert np.array_equal(r["state"].h[0, p], h_new[p])
+    for p in (1, 3, 5, 7, 12, 14):
+        assert np.array_equal(r["state"].h[0, p], full["state"].h[0, p])   # not refreshed
+
+
+def test_window_and_schedule_rules():
+    assert mr.block_bounds(512, 32, 0) == (512, 544)
+    assert mr.window(512, 32, 768, 0, 64, 32) == (448, 576)
+    assert mr.window(512, 32, 768, 7, 64, 32) == (672, 768)            # last block: no suffix
+    assert mr.window(8, 32, 72, 0, 64, 32) == (0, 72)                  # clipped at both ends
+    assert mr.window_top_k(448, 576, 32) == 48
+    assert mr.window_top_k(672, 768, 32) == 32
+    assert not mr.refreshes(3, 3) and mr.refreshes(4, 3) and mr.refreshes(1, 0)
+
+
+def test_free_running_loop_invariants():
+    shape = mr.Shape(n_layers=2, d=32, n_heads=2, head_dim=16, ffn=48, vocab=48, seq=40)
+    wts = rand_weights(shape, seed=11, lm_std=0.6)
+    g = np.random.default_rng(12)
+    prompt = g.integers(0, shape.vocab - 1, size=(2, 8))
+    p = mr.LoopParams(prompt_len=8, gen_len=32, block_len=8, prefix=16, suffix=8, tau_upd=1, h=2)
+    y, tr = mr.generate(wts, prompt, shape, p)
+    assert not (y == shape.mask_id).any()
+    assert np.array_equal(y[:, :8], prompt)
+    assert tr.committed == 2 * 32
+    kinds = [f["kind"] for f in tr.forwards]
+    entries = [f for f in tr.forwards if f["kind"].startswith("entry")]
+    assert [e["kind"] for e in entries] == ["entry_full", "entry_window"] * 2
+    assert kinds[0] == "entry_full"
+    # schedule: a step refreshes iff more than tau_upd tokens were committed
+    # since the last refreshing forward (entries included)
+    since = None
+    for f in tr.forwards:
+        n = int(f["commit"].sum()) + (0 if f.get("suffix_commit") is None else int(f["suffix_commit"].sum()))
+        if f["kind"].startswith("entry"):
+            since = n
+            continue
+        assert (f["kind"] == "refresh") == mr.refreshes(since, p.tau_upd)
+        since = n if f["kind"] == "refresh" else since + n
+        # force_one: every within-block step commits at least one token per unfinished sequence
+        assert f["commit"].any(axis=1).sum() >= 1
+    assert len(tr.forwards) < 2 * 32                 # some steps commit several tokens
