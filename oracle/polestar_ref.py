@@ -370,6 +370,32 @@ def commit_rule(conf32: np.ndarray, delta32: np.ndarray, masked: np.ndarray,
     return commit, new_hist, new_len
 
 
+def suffix_eligible(stale_idx: np.ndarray, stale_count: np.ndarray, suffix_start: int,
+                    suffix_len: int) -> np.ndarray:
+    """Suffix positions carried by the final layer's update packet (Sec. 4.2,
+    "Suffix Block Commit"; Alg. 1, the positions of the packet that fall in
+    the next block J_(b+1)): [batch][suffix_len] bool, True where position
+    suffix_start + r is among the first stale_count[b] entries of stale_idx[b]."""
+    batch = stale_idx.shape[0]
+    out = np.zeros((batch, suffix_len), dtype=bool)
+    for b in range(batch):
+        for r in range(int(stale_count[b])):
+            p = int(stale_idx[b, r])
+            if suffix_start <= p < suffix_start + suffix_len:
+                out[b, p - suffix_start] = True
+    return out
+
+
+def suffix_commit_rule(conf32: np.ndarray, masked: np.ndarray, eligible: np.ndarray,
+                       tau_s: float) -> np.ndarray:
+    """Suffix-block commit (Sec. 4.2, "Suffix Block Commit"): a suffix position
+    commits when it is still masked, the packet carries it (eligible) and its
+    confidence exceeds tau_s; compared in fp32, strictly, as in Alg. 1."""
+    f = np.float32
+    c = np.asarray(conf32, dtype=np.float32)
+    return np.asarray(masked, bool) & np.asarray(eligible, bool) & (c > f(tau_s))
+
+
 # ---------------------------------------------------------------------------
 # One whole layer step, for end-to-end checks.
 # ---------------------------------------------------------------------------

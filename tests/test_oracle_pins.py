@@ -469,3 +469,34 @@ def test_bf16_rounding_definition():
     x = np.random.default_rng(17).standard_normal(10000).astype(np.float32)
     bits = inputs.f32_to_bf16_bits(x)
     np.testing.assert_array_equal(ref.decode(bits, "bf16"), ref.round_to_bf16(x.astype(np.float64)))
+
+
+# ---------------------------------------------------------------------------
+# suffix-block commit (Sec. 4.2, "Suffix Block Commit")
+# ---------------------------------------------------------------------------
+
+def test_suffix_eligible_is_packet_within_suffix():
+    # packet rows 3, 40, 41, 47, 48 of a sequence with suffix window [40, 48)
+    idx = np.array([[3, 40, 41, 47, 48, -1], [44, -1, -1, -1, -1, -1]])
+    cnt = np.array([5, 1])
+    el = ref.suffix_eligible(idx, cnt, 40, 8)
+    assert el[0].tolist() == [True, True, False, False, False, False, False, True]
+    assert el[1].tolist() == [False] * 4 + [True] + [False] * 3
+    # entries past stale_count are ignored
+    assert not ref.suffix_eligible(idx, np.array([1, 0]), 40, 8).any()
+
+
+def test_suffix_commit_closed_form():
+    # two-token vocabularies with known softmax: conf = a / (a + 1) for logits (log a, 0)
+    a = np.array([19.0, 4.0, 19.0, 19.0, 99.0])              # conf 0.95, 0.8, 0.95, 0.95, 0.99
+    logits = np.stack([np.log(a), np.zeros_like(a)], axis=-1)[None]
+    token, conf = ref.confidence(logits, -1)
+    assert np.allclose(conf[0], a / (a + 1), rtol=1e-15) and (token == 0).all()
+    masked = np.array([[1, 1, 0, 1, 1]], bool)
+    eligible = np.array([[1, 1, 1, 0, 1]], bool)
+    got = ref.suffix_commit_rule(conf.astype(np.float32), masked, eligible, 0.9)
+    # conf high but unmasked (2) or not in the packet (3): no commit; low conf (1): no
+    assert got[0].tolist() == [True, False, False, False, True]
+    # strict comparison: conf equal to tau_s does not commit
+    c = np.array([[np.float32(0.9)]])
+    assert not ref.suffix_commit_rule(c, [[True]], [[True]], 0.9)[0, 0]
