@@ -248,6 +248,30 @@ polestar_status polestar_commit(polestar_dtype dtype, int batch, int block_len, 
                                 hipStream_t stream);
 
 /*
+ * polestar_suffix_commit -- suffix-block commit (Sec. 4.2 "Suffix Block
+ * Commit"; Alg. 1, the commit from the final layer's update packet).
+ *
+ * The rows are positions of the suffix window whose logits come from the
+ * final layer's update packet.  For every row j of sequence b, token and conf
+ * are as in polestar_commit, and
+ *   commit[b][j] = masked[b][j] && eligible[b][j] && conf > tau_s
+ * (drift decides which suffix positions are eligible, confidence which of
+ * them commit; no history, no forced commit).
+ *   logits   : [batch][n_rows][vocab] dtype
+ *   masked, eligible : [batch][n_rows] uint8
+ *   token, conf, commit : [batch][n_rows] int32 / float / uint8 outputs
+ *   workspace : >= polestar_commit_workspace_size(dtype, batch, n_rows, vocab)
+ * Requires n_rows, vocab > 0 and mask_token_id < vocab.  UNSUPPORTED for
+ * n_rows > 1024 or vocab not a whole number of 16-byte chunks.
+ */
+polestar_status polestar_suffix_commit(polestar_dtype dtype, int batch, int n_rows, int vocab,
+                                       const void* logits, const uint8_t* masked,
+                                       const uint8_t* eligible, int mask_token_id, float tau_s,
+                                       int32_t* token, float* conf, uint8_t* commit,
+                                       void* workspace, size_t workspace_bytes,
+                                       hipStream_t stream);
+
+/*
  * Clustered proxy drift -- Polestar's own drift estimator (Sec. 4.1 "Cluster
  * and Quantize Hidden States" and "Measuring Drift and Layer-wise KV
  * Updates"; Alg. 1: SphericalKMeans at block entry, ProxyAttn, KL and TopK

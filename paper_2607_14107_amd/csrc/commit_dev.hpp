@@ -152,9 +152,11 @@ __device__ bool commit_rule(float c, float dlt, bool use_drift, const float* hv,
 }
 #pragma clang fp contract(on)
 
-// Sequence b: one thread per block position j (blockDim.x >= nq).
+// Sequence b: one thread per block position j (blockDim.x >= nq).  `eligible`
+// (nullable) further restricts the positions that may commit.
 __device__ __forceinline__ void finalize_body(const ScanPart* __restrict__ parts, int splits, int nq,
                                               const uint8_t* __restrict__ masked,
+                                              const uint8_t* __restrict__ eligible,
                                               const float* __restrict__ drift, int seq,
                                               int block_start, float* hist, int32_t* hist_len, int h,
                                               float tau_s, float alpha, int force_one,
@@ -173,7 +175,8 @@ __device__ __forceinline__ void finalize_body(const ScanPart* __restrict__ parts
 #pragma unroll
     for (int q = 0; q < kMaxSplits; ++q) pv[q] = parts[tok * splits + (q < splits ? q : 0)];
     const int n = (h > 0 && hist_len) ? min(max(hist_len[b], 0), h) : 0;
-    const bool is_masked = masked[tok] != 0;
+    // a position may commit only if it is masked (and eligible, when a mask is given)
+    const bool is_masked = (masked[tok] != 0) & (eligible == nullptr || eligible[tok] != 0);
     const float dlt = drift ? drift[static_cast<size_t>(b) * seq + block_start + jc] : 0.f;
     float hv[kMaxHist];
     float* hcol = hist ? hist + static_cast<size_t>(b) * h * nq + jc : nullptr;

@@ -91,7 +91,7 @@ __global__ __launch_bounds__(kStepBlock) void back_kernel(BackArgs k) {
         merge_body<BF16, HD>(k.att, blockIdx.x);
         return;
     }
-    finalize_body(k.parts, k.splits, k.nq, k.masked, k.drift, k.seq, k.block_start, k.hist, k.hist_len,
+    finalize_body(k.parts, k.splits, k.nq, k.masked, nullptr, k.drift, k.seq, k.block_start, k.hist, k.hist_len,
                   k.h, k.tau_s, k.alpha, k.force_one, k.token, k.conf, k.commit,
                   blockIdx.x - k.n_merge);
 }

@@ -97,6 +97,8 @@ def lib() -> ctypes.CDLL:
     L.polestar_commit_workspace_size.argtypes = [I, I, I, I]
     L.polestar_commit.restype = S
     L.polestar_commit.argtypes = [I, I, I, I, P, P, P, I, I, P, P, I, I, F, F, I, P, P, P, P, Z, P]
+    L.polestar_suffix_commit.restype = S
+    L.polestar_suffix_commit.argtypes = [I, I, I, I, P, P, P, I, F, P, P, P, P, Z, P]
     _lib = L
     return L
 
@@ -280,6 +282,29 @@ def commit(logits: torch.Tensor, masked: torch.Tensor, drift_vals: torch.Tensor 
         block_start, _ptr(hist, torch.float32), _ptr(hist_len, torch.int32), h, mask_token_id,
         float(tau_s), float(alpha), int(bool(force_one)), _ptr(token, torch.int32),
         _ptr(conf, torch.float32), _ptr(commit_out, torch.uint8), _ptr(ws), nbytes, _stream(stream)))
+    return token, conf, commit_out
+
+
+def suffix_commit(logits: torch.Tensor, masked: torch.Tensor, eligible: torch.Tensor,
+                  mask_token_id: int = -1, tau_s: float = DEFAULT_TAU_S, token: torch.Tensor | None = None,
+                  conf: torch.Tensor | None = None, commit_out: torch.Tensor | None = None,
+                  workspace: torch.Tensor | None = None, stream=None):
+    """Suffix-block commit of the packet rows -> (token int32, conf float32, commit uint8)."""
+    b, n, vocab = logits.shape
+    dt = _dtype_code(logits)
+    dev = logits.device
+    if token is None:
+        token = torch.empty((b, n), dtype=torch.int32, device=dev)
+    if conf is None:
+        conf = torch.empty((b, n), dtype=torch.float32, device=dev)
+    if commit_out is None:
+        commit_out = torch.empty((b, n), dtype=torch.uint8, device=dev)
+    ws = _workspace(commit_workspace_size(dt, b, n, vocab), dev, workspace)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("polestar_suffix_commit", lib().polestar_suffix_commit(
+        dt, b, n, vocab, _ptr(logits), _ptr(masked, torch.uint8), _ptr(eligible, torch.uint8), mask_token_id,
+        float(tau_s), _ptr(token, torch.int32), _ptr(conf, torch.float32), _ptr(commit_out, torch.uint8),
+        _ptr(ws), nbytes, _stream(stream)))
     return token, conf, commit_out
 
 

@@ -29,7 +29,7 @@ def _header_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = _header_functions()
-    assert len(names) == 19, names
+    assert len(names) == 20, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -141,6 +141,22 @@ def test_commit_validation_and_workspace(L):
     a = list(args); a[3] = 126465
     assert f(*a) == UNSUPPORTED                               # rows of 16-byte chunks
     a = list(args); a[20] = ws - 1
+    assert f(*a) == WORKSPACE
+
+
+def test_suffix_commit_validation(L):
+    f = L.polestar_suffix_commit
+    ws = ps.commit_workspace_size(ps.BF16, 1, 32, 126464)
+    args = [1, 1, 32, 126464, FAKE, FAKE, FAKE, -1, 0.9, FAKE, FAKE, FAKE, FAKE, ws, None]
+    a = list(args); a[6] = None
+    assert f(*a) == INVALID                                   # eligibility mask required
+    a = list(args); a[7] = 126464
+    assert f(*a) == INVALID
+    a = list(args); a[2] = 1025
+    assert f(*a) == UNSUPPORTED
+    a = list(args); a[3] = 126465
+    assert f(*a) == UNSUPPORTED
+    a = list(args); a[13] = ws - 1
     assert f(*a) == WORKSPACE
 
 

@@ -439,6 +439,45 @@ def test_commit_plain_config_logits(P, cfg_index):
     assert np.array_equal(gm, (conf > cfg.tau_s) & x["masked"].astype(bool))
 
 
+@pytest.mark.parametrize("cfg_index", [0, 1, 2, 3])
+def test_suffix_commit(P, cfg_index):
+    """Suffix-block commit: the coverage logits stand for the final-layer packet
+    rows of the suffix window; the packet carries a seeded subset of it."""
+    torch = _torch()
+    cfg = inputs.CONFIGS[cfg_index]
+    lg_bits, token, conf, _, _, _, masked = coverage_inputs(cfg)
+    g = np.random.default_rng(inputs.seed_of(cfg.index, 0, 7))
+    s0 = cfg.block_start + cfg.block_len
+    n = cfg.block_len
+    k = cfg.block_len
+    idx = np.full((cfg.batch, 2 * k), -1, np.int64)
+    cnt = np.zeros(cfg.batch, np.int64)
+    hi = (conf > cfg.tau_s) & masked.astype(bool)
+    for b in range(cfg.batch):
+        # the packet: half of the confident masked suffix rows, a random third
+        # of the others, and rows outside the suffix window
+        h = np.flatnonzero(hi[b])
+        lo = np.flatnonzero(~hi[b])
+        inside = np.concatenate([h[: (len(h) + 1) // 2], g.choice(lo, size=len(lo) // 3, replace=False)])
+        outside = g.choice(np.arange(max(0, s0 - n), s0), size=min(n // 4, s0), replace=False)
+        rows = np.unique(np.concatenate([s0 + inside, outside]))
+        idx[b, :len(rows)], cnt[b] = rows, len(rows)
+    eligible = ref.suffix_eligible(idx, cnt, s0, n)
+    assert eligible.any() and (~eligible).any()
+    for mask_id in (-1, 3):
+        want_tok, want_conf = ref.confidence(ref.decode(lg_bits, cfg.dtype), mask_id)
+        gt, gc, gm = P.suffix_commit(to_dev(lg_bits, cfg.dtype), torch.from_numpy(masked).cuda(),
+                                     torch.from_numpy(eligible.astype(np.uint8)).cuda(), mask_id, cfg.tau_s)
+        gt, gc, gm = from_dev(gt), from_dev(gc), from_dev(gm).astype(bool)
+        assert np.array_equal(gt, want_tok)
+        np.testing.assert_allclose(gc, want_conf, rtol=1e-4)
+        want = ref.suffix_commit_rule(want_conf.astype(np.float32), masked.astype(bool), eligible, cfg.tau_s)
+        assert np.array_equal(gm, want)
+    # both outcomes among eligible masked rows
+    em = eligible & masked.astype(bool)
+    assert gm.any() and (em & ~gm).any()
+
+
 # ---------------------------------------------------------------------------
 # whole step
 # ---------------------------------------------------------------------------
