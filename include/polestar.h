@@ -364,6 +364,77 @@ polestar_status polestar_cluster_update(polestar_dtype dtype, int batch, int seq
                                         hipStream_t stream);
 
 /*
+ * The rest of a pre-norm layer stack, for running the denoising loop of
+ * Alg. 1 on a whole model (Sec. 5.1 evaluates LLaDA- and Dream-shaped
+ * models).  Layer: x += W_o Attn(RMSNorm(x)); x += W_down(silu(W_gate g) *
+ * W_up g), g = RMSNorm(x).  The residual stream x is fp32; everything else
+ * is stored in dtype (bf16 rounding is to nearest even).  Asynchronous on
+ * `stream`; the caller owns every buffer.
+ *
+ * polestar_embed -- x[b][r][:] = tok_emb[ids[b][lo + r]][:] + pos_emb[lo + r][:]
+ *   for r < n_rows (ids clamped into [0, vocab)).
+ *   ids : [batch][seq] int32; tok_emb : [vocab][d]; pos_emb : [seq][d] dtype;
+ *   x : out [batch][n_rows][d] float.  Requires lo + n_rows <= seq;
+ *   UNSUPPORTED unless d % 4 == 0 and x and the tables are 16-byte aligned.
+ */
+polestar_status polestar_embed(polestar_dtype dtype, int batch, int seq, int d, const int32_t* ids,
+                               int lo, int n_rows, const void* tok_emb, int vocab,
+                               const void* pos_emb, float* x, hipStream_t stream);
+
+/*
+ * polestar_rmsnorm -- out[b][out_start + r][:] = x[b][x_start + r][:] /
+ *   sqrt(mean_c x^2 + eps), unit gain, rounded to dtype, for r < n_rows.
+ *   x : [batch][x_seq][d] float;  out : [batch][out_seq][d] dtype.
+ * UNSUPPORTED unless d % 4 == 0, d <= 16384 and both are 16-byte aligned.
+ */
+polestar_status polestar_rmsnorm(polestar_dtype dtype, int batch, int n_rows, int d, const float* x,
+                                 int x_seq, int x_start, float eps, void* out, int out_seq,
+                                 int out_start, hipStream_t stream);
+
+/*
+ * polestar_linear -- y[b][r][:] = W x[b][row_start + r][:] for r < n_rows,
+ *   fp32 accumulation on MFMA, rounded to dtype (the GEMM of the K/V
+ *   refresh, dense rows in and out).
+ *   x : [batch][seq][n_in]; w : [n_out][n_in]; y : out [batch][n_rows][n_out]
+ *   workspace : >= polestar_linear_workspace_size(...) bytes (no init needed)
+ * UNSUPPORTED unless n_in % 128 == 0 (bf16) / % 64 (fp32), n_out % 16 == 0
+ * and every pointer is 16-byte aligned.
+ */
+size_t polestar_linear_workspace_size(polestar_dtype dtype, int batch, int n_rows, int n_out, int n_in);
+polestar_status polestar_linear(polestar_dtype dtype, int batch, int seq, int n_in, int n_out,
+                                int row_start, int n_rows, const void* x, const void* w, void* y,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * polestar_swiglu -- out[r][f] = silu(gate_up[r][f]) * gate_up[r][ffn + f],
+ *   silu(g) = g / (1 + e^-g), fp32, rounded to dtype.
+ *   gate_up : [rows][2*ffn] dtype; out : [rows][ffn] dtype.
+ * UNSUPPORTED unless ffn % 4 == 0 and both are 16-byte aligned.
+ */
+polestar_status polestar_swiglu(polestar_dtype dtype, long rows, int ffn, const void* gate_up,
+                                void* out, hipStream_t stream);
+
+/*
+ * polestar_residual_add -- x[i] += y[i] for i < n (float += dtype).
+ * UNSUPPORTED unless n % 4 == 0 and both are 16-byte aligned.
+ */
+polestar_status polestar_residual_add(polestar_dtype dtype, long n, float* x, const void* y,
+                                      hipStream_t stream);
+
+/*
+ * polestar_copy_rows -- dst[b][p][:] = src[b][p][:] for the rows that
+ *   polestar_refresh_kv rewrites: the first stale_count[b] entries of
+ *   stale_idx[b] (entries outside [0, seq) are skipped) and the block
+ *   [block_start, block_start + block_len).  Keeps the cached hidden states
+ *   H in step with the refreshed K/V (Alg. 1, Update of the cached states).
+ *   src, dst : [batch][seq][d] dtype, distinct buffers.
+ * UNSUPPORTED unless a row is a whole number of 16-byte chunks.
+ */
+polestar_status polestar_copy_rows(polestar_dtype dtype, int batch, int seq, int d, const void* src,
+                                   void* dst, const int32_t* stale_idx, const int32_t* stale_count,
+                                   int k_max, int block_start, int block_len, hipStream_t stream);
+
+/*
  * polestar_step -- one whole layer step: polestar_drift, polestar_select,
  * polestar_refresh_kv, polestar_project_q, polestar_attend (queries from q)
  * and polestar_commit (with the drift branch on), with exactly their

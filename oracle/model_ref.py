@@ -102,13 +102,15 @@ class LayerState:
 
 
 def layer_forward(x_rows: np.ndarray, lo: int, w: dict, st: LayerState, *, mode: str, block: tuple[int, int],
-                  shape: Shape, k_top: int = 0) -> dict:
+                  shape: Shape, k_top: int = 0, stale=None) -> dict:
     """One layer over the rows R = [lo, lo + m) of every sequence (M-1, M-5, M-9).
 
     mode: "all"     -- every K/V and H row of R rewritten (block entry);
           "refresh" -- drift on R, the top k_top of R minus the block
                        (eligible = Omega) and the block rewritten;
           "plain"   -- only the block rewritten (R must be the block).
+    stale = (idx, cnt) replaces the refresh mode's own selection (replay of a
+    selection taken elsewhere on the same drift).
     Returns a dict with the new state (st is not modified), the drift on R,
     the stale set, and x_out for the rows of R."""
     dt = shape.dtype
@@ -129,7 +131,7 @@ def layer_forward(x_rows: np.ndarray, lo: int, w: dict, st: LayerState, *, mode:
         if mode == "refresh":
             eligible[:, lo:lo + m] = True
             eligible[:, bs:bs + bl] = False
-            idx, cnt = ref.select(drift, k_top, bs, bl, eligible)
+            idx, cnt = ref.select(drift, k_top, bs, bl, eligible) if stale is None else stale
         else:
             assert (lo, m) == (bs, bl)
             idx, cnt = np.zeros((b, 0), np.int32), np.zeros(b, np.int32)

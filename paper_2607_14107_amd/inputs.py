@@ -239,3 +239,77 @@ def random_cache(cfg: LayerConfig, subrun: int = 0) -> tuple[np.ndarray, np.ndar
     shape = (cfg.batch, cfg.seq, cfg.n_kv_heads, cfg.head_dim)
     std = cfg.weight_std * math.sqrt(cfg.d)
     return store(normal(g, shape, std), cfg.dtype), store(normal(g, shape, std), cfg.dtype)
+
+
+# ---------------------------------------------------------------------------
+# Whole-stack workloads: the denoising loop over a pre-norm layer stack
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class StackConfig:
+    """Shape and weight recipe of a synthetic layer stack (random weights)."""
+    index: int
+    name: str
+    dtype: str
+    batch: int
+    n_layers: int
+    d: int
+    n_heads: int
+    head_dim: int
+    ffn: int
+    vocab: int
+    prompt_len: int
+    gen_len: int
+    block_len: int = 32
+    weight_std: float = 0.02
+    embed_std: float = 0.02
+    lm_std: float = 0.02
+
+    @property
+    def seq(self) -> int:
+        return self.prompt_len + self.gen_len
+
+
+STACKS = {
+    # LLaDA-8B-shaped stack: 32 layers, d 4096, 32x128 MHA, SwiGLU FFN 12288,
+    # vocab 126464 (mask id = vocab - 1), N(0, 0.02) weights everywhere,
+    # batch 16, prompt 512, 256 generated tokens in blocks of 32
+    4: StackConfig(4, "llada8b-stack-b16", "bf16", batch=16, n_layers=32, d=4096, n_heads=32, head_dim=128,
+                   ffn=12288, vocab=126464, prompt_len=512, gen_len=256),
+    # the same loop at sizes the float64 oracle replays in seconds; a wider
+    # LM head makes the confidences spread so that the commit rule decides
+    40: StackConfig(40, "tiny-stack-b2", "bf16", batch=2, n_layers=2, d=256, n_heads=4, head_dim=64, ffn=768,
+                    vocab=512, prompt_len=64, gen_len=64, embed_std=1.0, lm_std=0.25),
+}
+
+STACK_MATRICES = ("w_q", "w_k", "w_v", "w_o", "w_gu", "w_down")
+
+
+def _bf16_bits_fast(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bits, nearest, ties to even (finite values of modest
+    magnitude, where the 32-bit sum cannot carry out)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    return ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)).astype(np.uint16)
+
+
+def stack_tensor(cfg: StackConfig, name: str, layer: int = -1) -> np.ndarray:
+    """One weight of the stack in the run dtype, from its own seed
+    (config, layer, matrix).  Shapes: w_q/w_k/w_v [H*hd][d], w_o [d][H*hd],
+    w_gu [2*ffn][d] (gate rows then up rows), w_down [d][ffn],
+    tok_emb / w_lm [vocab][d], pos_emb [seq][d]."""
+    hd = cfg.n_heads * cfg.head_dim
+    shapes = dict(w_q=(hd, cfg.d), w_k=(hd, cfg.d), w_v=(hd, cfg.d), w_o=(cfg.d, hd), w_gu=(2 * cfg.ffn, cfg.d),
+                  w_down=(cfg.d, cfg.ffn), tok_emb=(cfg.vocab, cfg.d), pos_emb=(cfg.seq, cfg.d),
+                  w_lm=(cfg.vocab, cfg.d))
+    std = dict(tok_emb=cfg.embed_std, pos_emb=cfg.embed_std, w_lm=cfg.lm_std).get(name, cfg.weight_std)
+    names = STACK_MATRICES + ("tok_emb", "pos_emb", "w_lm")
+    g = np.random.default_rng(np.random.SeedSequence([cfg.index, layer + 1, names.index(name)]))
+    x = g.standard_normal(size=shapes[name], dtype=np.float32)
+    x *= np.float32(std)
+    return _bf16_bits_fast(x) if cfg.dtype == "bf16" else x
+
+
+def stack_prompt(cfg: StackConfig) -> np.ndarray:
+    """[batch][prompt_len] token ids in [0, vocab - 1) (never the mask id)."""
+    g = np.random.default_rng(np.random.SeedSequence([cfg.index, 0, 99]))
+    return g.integers(0, cfg.vocab - 1, size=(cfg.batch, cfg.prompt_len)).astype(np.int32)

@@ -99,6 +99,21 @@ def lib() -> ctypes.CDLL:
     L.polestar_commit.argtypes = [I, I, I, I, P, P, P, I, I, P, P, I, I, F, F, I, P, P, P, P, Z, P]
     L.polestar_suffix_commit.restype = S
     L.polestar_suffix_commit.argtypes = [I, I, I, I, P, P, P, I, F, P, P, P, P, Z, P]
+    Lg = ctypes.c_long
+    L.polestar_embed.restype = S
+    L.polestar_embed.argtypes = [I, I, I, I, P, I, I, P, I, P, P, P]
+    L.polestar_rmsnorm.restype = S
+    L.polestar_rmsnorm.argtypes = [I, I, I, I, P, I, I, F, P, I, I, P]
+    L.polestar_linear_workspace_size.restype = Z
+    L.polestar_linear_workspace_size.argtypes = [I, I, I, I, I]
+    L.polestar_linear.restype = S
+    L.polestar_linear.argtypes = [I, I, I, I, I, I, I, P, P, P, P, Z, P]
+    L.polestar_swiglu.restype = S
+    L.polestar_swiglu.argtypes = [I, Lg, I, P, P, P]
+    L.polestar_residual_add.restype = S
+    L.polestar_residual_add.argtypes = [I, Lg, P, P, P]
+    L.polestar_copy_rows.restype = S
+    L.polestar_copy_rows.argtypes = [I, I, I, I, P, P, P, P, I, I, I, P]
     _lib = L
     return L
 
@@ -306,6 +321,86 @@ def suffix_commit(logits: torch.Tensor, masked: torch.Tensor, eligible: torch.Te
         float(tau_s), _ptr(token, torch.int32), _ptr(conf, torch.float32), _ptr(commit_out, torch.uint8),
         _ptr(ws), nbytes, _stream(stream)))
     return token, conf, commit_out
+
+
+# ---------------------------------------------------------------------------
+# the rest of a layer stack (embedding, RMSNorm, projections, SwiGLU)
+# ---------------------------------------------------------------------------
+
+def embed(ids: torch.Tensor, lo: int, n_rows: int, tok_emb: torch.Tensor, pos_emb: torch.Tensor,
+          x: torch.Tensor, stream=None) -> torch.Tensor:
+    """x[b][r] = tok_emb[ids[b][lo + r]] + pos_emb[lo + r]; x is [batch][n_rows][d] float32."""
+    b, seq = ids.shape
+    vocab, d = tok_emb.shape
+    if tuple(x.shape) != (b, n_rows, d):
+        raise ValueError("x must be [batch][n_rows][d]")
+    _check("polestar_embed", lib().polestar_embed(
+        _dtype_code(tok_emb), b, seq, d, _ptr(ids, torch.int32), lo, n_rows, _ptr(tok_emb), vocab,
+        _ptr(pos_emb, tok_emb.dtype), _ptr(x, torch.float32), _stream(stream)))
+    return x
+
+
+def rmsnorm(x: torch.Tensor, x_start: int, n_rows: int, out: torch.Tensor, out_start: int,
+            eps: float = 1e-5, stream=None) -> torch.Tensor:
+    """out[b][out_start + r] = RMSNorm(x[b][x_start + r]) (unit gain), rounded to out's dtype."""
+    b, x_seq, d = x.shape
+    if out.shape[0] != b or out.shape[2] != d:
+        raise ValueError("x and out differ in batch or width")
+    _check("polestar_rmsnorm", lib().polestar_rmsnorm(
+        _dtype_code(out), b, n_rows, d, _ptr(x, torch.float32), x_seq, x_start, float(eps), _ptr(out),
+        out.shape[1], out_start, _stream(stream)))
+    return out
+
+
+def linear_workspace_size(dtype: int, batch: int, n_rows: int, n_out: int, n_in: int) -> int:
+    return lib().polestar_linear_workspace_size(dtype, batch, n_rows, n_out, n_in)
+
+
+def linear(x: torch.Tensor, row_start: int, n_rows: int, w: torch.Tensor, y: torch.Tensor,
+           workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """y[b][r] = W x[b][row_start + r]; x [batch][seq][n_in], w [n_out][n_in], y [batch][n_rows][n_out]."""
+    b, seq, n_in = x.shape
+    n_out = w.shape[0]
+    if tuple(y.shape) != (b, n_rows, n_out) or w.shape[1] != n_in:
+        raise ValueError("linear: shapes do not match")
+    dt = _dtype_code(x)
+    ws = _workspace(linear_workspace_size(dt, b, n_rows, n_out, n_in), x.device, workspace)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("polestar_linear", lib().polestar_linear(
+        dt, b, seq, n_in, n_out, row_start, n_rows, _ptr(x), _ptr(w, x.dtype), _ptr(y, x.dtype), _ptr(ws), nbytes,
+        _stream(stream)))
+    return y
+
+
+def swiglu(gate_up: torch.Tensor, out: torch.Tensor, stream=None) -> torch.Tensor:
+    """out[..., f] = silu(gate_up[..., f]) * gate_up[..., F + f], F = out.shape[-1]."""
+    f = out.shape[-1]
+    rows = out.numel() // f
+    if gate_up.numel() != 2 * out.numel():
+        raise ValueError("gate_up must hold 2*F values per row")
+    _check("polestar_swiglu", lib().polestar_swiglu(_dtype_code(out), rows, f, _ptr(gate_up, out.dtype),
+                                                   _ptr(out), _stream(stream)))
+    return out
+
+
+def residual_add(x: torch.Tensor, y: torch.Tensor, stream=None) -> torch.Tensor:
+    """x += y (float32 += dtype), same number of elements."""
+    if x.numel() != y.numel():
+        raise ValueError("residual_add: sizes differ")
+    _check("polestar_residual_add", lib().polestar_residual_add(
+        _dtype_code(y), x.numel(), _ptr(x, torch.float32), _ptr(y), _stream(stream)))
+    return x
+
+
+def copy_rows(src: torch.Tensor, dst: torch.Tensor, stale_idx: torch.Tensor | None,
+              stale_count: torch.Tensor | None, block_start: int, block_len: int, stream=None) -> None:
+    """dst rows = src rows for the stale set and the block (the rows refresh_kv rewrites)."""
+    b, seq, d = src.shape
+    k_max = 0 if stale_idx is None else stale_idx.shape[1]
+    _check("polestar_copy_rows", lib().polestar_copy_rows(
+        _dtype_code(src), b, seq, d, _ptr(src), _ptr(dst, src.dtype),
+        _ptr(stale_idx, torch.int32) if k_max > 0 else None,
+        _ptr(stale_count, torch.int32) if k_max > 0 else None, k_max, block_start, block_len, _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

@@ -29,7 +29,7 @@ def _header_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = _header_functions()
-    assert len(names) == 20, names
+    assert len(names) == 27, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -158,6 +158,32 @@ def test_suffix_commit_validation(L):
     assert f(*a) == UNSUPPORTED
     a = list(args); a[13] = ws - 1
     assert f(*a) == WORKSPACE
+
+
+def test_model_entry_validation(L):
+    # embed: rows past the sequence, width not a multiple of 4
+    assert L.polestar_embed(1, 2, 96, 256, FAKE, 90, 10, FAKE, 512, FAKE, FAKE, None) == INVALID
+    assert L.polestar_embed(1, 2, 96, 254, FAKE, 0, 10, FAKE, 512, FAKE, FAKE, None) == UNSUPPORTED
+    assert L.polestar_embed(1, 2, 96, 256, FAKE, 0, 10, FAKE, 512, FAKE, MISALIGNED, None) == UNSUPPORTED
+    # rmsnorm: destination rows past its sequence, negative eps, width too large
+    assert L.polestar_rmsnorm(1, 2, 10, 256, FAKE, 10, 0, 1e-5, FAKE, 12, 3, None) == INVALID
+    assert L.polestar_rmsnorm(1, 2, 10, 256, FAKE, 10, 0, -1.0, FAKE, 12, 0, None) == INVALID
+    assert L.polestar_rmsnorm(1, 2, 10, 16388, FAKE, 10, 0, 1e-5, FAKE, 12, 0, None) == UNSUPPORTED
+    # linear: K not a multiple of 128 (bf16), N not of 16, workspace
+    assert L.polestar_linear(1, 2, 50, 384, 272, 45, 10, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == INVALID
+    assert L.polestar_linear(1, 2, 50, 320, 272, 0, 10, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == UNSUPPORTED
+    assert L.polestar_linear(1, 2, 50, 384, 270, 0, 10, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == UNSUPPORTED
+    ws = ps.linear_workspace_size(ps.BF16, 2, 200, 256, 4096)
+    assert ws > 0
+    assert L.polestar_linear(1, 2, 200, 4096, 256, 0, 200, FAKE, FAKE, FAKE, FAKE, ws - 1, None) == WORKSPACE
+    # swiglu / residual add / copy rows
+    assert L.polestar_swiglu(1, 10, 6, FAKE, FAKE, None) == UNSUPPORTED
+    assert L.polestar_swiglu(1, 10, 8, None, FAKE, None) == INVALID
+    assert L.polestar_residual_add(1, 10, FAKE, FAKE, None) == UNSUPPORTED
+    assert L.polestar_residual_add(1, 0, None, None, None) == 0           # nothing to do
+    assert L.polestar_copy_rows(1, 2, 96, 256, FAKE, FAKE, None, None, 4, 0, 32, None) == INVALID
+    assert L.polestar_copy_rows(1, 2, 96, 4, FAKE, FAKE, None, None, 0, 0, 32, None) == UNSUPPORTED
+    assert L.polestar_copy_rows(1, 2, 96, 256, FAKE, FAKE, None, None, 0, 80, 32, None) == INVALID
 
 
 def test_step_validation_and_workspace(L):
