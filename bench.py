@@ -65,6 +65,9 @@ def parse():
     p.add_argument("--summarize-counters", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH", "COPY_WRITE"),
                    help="write the traffic summary of the dominant call from rocprofv3 --pmc output")
     p.add_argument("--call", default="refresh_kv", help="call whose counters --summarize-counters reads")
+    p.add_argument("--stack", type=int, default=None,
+                   help="run the denoising loop of a whole layer stack (4: LLaDA-8B-shaped, 32 layers, batch 16) "
+                        "once and print its tokens/s and tokens per forward instead of the layer-step benchmark")
     return p.parse_args()
 
 
@@ -305,6 +308,63 @@ def cpu_baseline(cfg, x, k, budget_s):
                       f"attention, commit) of the benchmarked workload, {t_total:.1f} s"}
 
 
+def stack_bench(index, P, torch):
+    """The loop of Alg. 1 on a whole stack with random weights: weights are
+    drawn on the host (one thread per matrix) and uploaded as they complete,
+    then one full generation is timed (wall clock around the loop, GPU time
+    per forward kind from HIP events)."""
+    import concurrent.futures as cf
+    from paper_2607_14107_amd import inputs, model
+    cfg = inputs.STACKS[index]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    t0 = time.perf_counter()
+
+    def up(a):
+        if cfg.dtype == "bf16":
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    jobs = [(n, -1) for n in ("tok_emb", "pos_emb", "w_lm")] + \
+        [(m, li) for li in range(cfg.n_layers) for m in inputs.STACK_MATRICES]
+    w = {"layers": [{} for _ in range(cfg.n_layers)]}
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(os.sched_getaffinity(0)))) as ex:
+        futs = {ex.submit(inputs.stack_tensor, cfg, n, li): (n, li) for n, li in jobs}
+        done = 0
+        for f in cf.as_completed(futs):
+            n, li = futs[f]
+            t = up(f.result())
+            if li < 0:
+                w[n] = t
+            else:
+                w["layers"][li][n] = t
+            done += 1
+            if done % 24 == 0:
+                print(f"weights {done}/{len(jobs)} ({time.perf_counter() - t0:.0f} s)", file=sys.stderr, flush=True)
+    shape = model.ModelShape(cfg.n_layers, cfg.d, cfg.n_heads, cfg.head_dim, cfg.ffn, cfg.vocab, cfg.seq)
+    lc = model.LoopConfig(prompt_len=cfg.prompt_len, gen_len=cfg.gen_len, block_len=cfg.block_len)
+    den = model.Denoiser(w, shape, cfg.batch, lc)
+    print(f"weights ready ({time.perf_counter() - t0:.0f} s); generating", file=sys.stderr, flush=True)
+    y, st = den.generate(inputs.stack_prompt(cfg), progress=lambda blk, f: print(
+        f"block {blk} done, {f} forwards ({time.perf_counter() - t0:.0f} s)", file=sys.stderr, flush=True))
+    assert not (y == shape.mask_id).any()
+    kinds = {"all": st["full_entries"] + st["window_entries"], "refresh": st["refreshing_steps"],
+             "plain": st["plain_steps"]}
+    per_fwd = {k: round(st["forward_gpu_ms"][k] / n, 3) for k, n in kinds.items() if n}
+    out = {"metric": "denoising-loop tokens/s, whole stack", "value": round(cfg.batch * cfg.gen_len / st["seconds"], 1),
+           "unit": "tokens/s", "n_gpus": 1, "higher_is_better": True, "dtype": cfg.dtype, "data": "synthetic",
+           "config": {"workload": f"{cfg.name}: {cfg.n_layers} layers, d {cfg.d}, {cfg.n_heads}x{cfg.head_dim} MHA, "
+                                  f"SwiGLU {cfg.ffn}, vocab {cfg.vocab}, batch {cfg.batch}, prompt {cfg.prompt_len}, "
+                                  f"{cfg.gen_len} generated in blocks of {cfg.block_len}, random N(0, 0.02) weights",
+                      "global_batch": cfg.batch, "seq_len": cfg.seq},
+           "tpf": round(st["tpf"], 3), "forwards": st["forwards"], "committed": st["committed"],
+           "suffix_committed": st["suffix_committed"], "seconds": round(st["seconds"], 3),
+           "forwards_by_kind": kinds, "gpu_ms_per_forward": per_fwd,
+           "gpu_ms_per_layer_forward": {k: round(v / cfg.n_layers, 4) for k, v in per_fwd.items()}}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main():
     args = parse()
     if args.summarize_counters:
@@ -328,6 +388,8 @@ def main():
         from paper_2607_14107_amd import build
         build.build(verbose=False)
     P.lib()
+    if args.stack is not None:
+        return stack_bench(args.stack, P, torch)
 
     cfg = inputs.CONFIGS[args.config]
     x = inputs.layer_inputs(cfg, args.subrun)

@@ -35,7 +35,8 @@ The loop (Alg. 1 with the window-forward reading of the per-token drift):
        and the drift history is emptied.
   M-9  Within the block, a step refreshes when the tokens committed since
        the last refreshing forward exceed tau_upd (Sec. 4.1 "Update
-       Schedule"); the block entry counts as refreshing.  A refreshing step
+       Schedule"); the block entry counts as refreshing.  The count is kept
+       per sequence and a batch refreshes when any of its sequences would.  A refreshing step
        forwards R: per layer drift on R's rows, the top ceil(|Omega|/2) of
        Omega refreshed (K/V and H) along with J_b, queries from all of R.  A
        plain step forwards J_b only (its K/V and H rewritten).  After the last
@@ -255,10 +256,10 @@ def generate(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams) -> 
         tr.forwards.append(dict(kind="entry_full" if blk % 2 == 0 else "entry_window", block=blk,
                                 rows=(elo, ehi), commit=cm, token=tok))
         tr.committed += int(cm.sum())
-        since = int(cm.sum())                  # decoded after the entry's (refreshing) forward
+        since = cm.sum(axis=1)                 # per sequence, decoded after the entry's (refreshing) forward
         hist_len = np.zeros(b, np.int32)
         while (y[:, bs:be] == mask).any():
-            refresh = refreshes(since, p.tau_upd)
+            refresh = refreshes(int(since.max()), p.tau_upd)
             rlo, rhi = (lo, hi) if refresh else (bs, be)
             kt = window_top_k(lo, hi, p.block_len) if refresh else 0
             x = embed(weights["tok_emb"], weights["pos_emb"], y, rlo, rhi)
@@ -275,7 +276,7 @@ def generate(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams) -> 
             cm, hist, hist_len = ref.commit_rule(conf.astype(np.float32), delta, masked, hist, hist_len, p.h,
                                                  p.tau_s, p.alpha, p.force_one)
             y[:, bs:be] = np.where(cm, tok, y[:, bs:be])
-            n_commit = int(cm.sum())
+            n_commit = cm.sum(axis=1)
             scm = None
             if p.suffix_commit and refresh and be < hi:
                 el = ref.suffix_eligible(last["stale_idx"], last["stale_count"], be, hi - be)
@@ -284,9 +285,9 @@ def generate(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams) -> 
                 smask = y[:, be:hi] == mask
                 scm = ref.suffix_commit_rule(sconf.astype(np.float32), smask, el, p.tau_s)
                 y[:, be:hi] = np.where(scm, stok, y[:, be:hi])
-                n_commit += int(scm.sum())
+                n_commit = n_commit + scm.sum(axis=1)
             tr.forwards.append(dict(kind="refresh" if refresh else "plain", block=blk, rows=(rlo, rhi),
                                     commit=cm, token=tok, suffix_commit=scm))
-            tr.committed += n_commit
+            tr.committed += int(n_commit.sum())
             since = n_commit if refresh else since + n_commit
     return y, tr

@@ -209,14 +209,31 @@ class Denoiser:
 
     # -- the loop -----------------------------------------------------------------------
 
-    def generate(self, prompt: np.ndarray, trace=None) -> tuple[np.ndarray, dict]:
+    def generate(self, prompt: np.ndarray, trace=None, capture=None, progress=None) -> tuple[np.ndarray, dict]:
+        """Runs the loop; returns the token ids [batch][seq] and statistics.
+
+        trace(event) receives, for every forward f of mode m ("all", "refresh",
+        "plain") with capture(f, m) true (all forwards when capture is None),
+        each layer's input, cache state before and after, drift and stale set,
+        and the logits of each commit; for the other forwards only the commit
+        decisions and their inputs.  progress(block, forwards) is called after
+        every block."""
         sh, cfg, b = self.shape, self.cfg, self.b
+        capture = (lambda f, m: True) if capture is None else capture
+        captured = set()
+
+        def full(f, m=None):
+            if m is not None and capture(f, m):
+                captured.add(f)
+            return f in captured
         S, B, mask = sh.seq, cfg.block_len, sh.mask_id
         y = np.full((b, S), mask, np.int32)
         y[:, :cfg.prompt_len] = prompt
         self.y.copy_(torch.from_numpy(y))
         stats = dict(forwards=0, committed=0, refreshing_steps=0, plain_steps=0, full_entries=0,
                      window_entries=0, suffix_committed=0)
+        gpu_ms = {"all": 0.0, "refresh": 0.0, "plain": 0.0}
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         fwd = 0
@@ -231,24 +248,30 @@ class Denoiser:
             # block entry
             elo, ehi = (0, S) if blk % 2 == 0 else (lo, hi)
             self.rows = ehi - elo
-            self.forward(elo, ehi, "all", (bs, B), trace=trace, fwd=fwd)
+            ev0.record()
+            self.forward(elo, ehi, "all", (bs, B), trace=trace if full(fwd, "all") else None, fwd=fwd)
+            ev1.record()
             stats["full_entries" if blk % 2 == 0 else "window_entries"] += 1
             lg = self.head(elo, bs, B)
             masked = torch.from_numpy((y[:, bs:be] == mask).astype(np.uint8)).to(self.dev)
             tok, conf, cm = P.commit(lg, masked, None, bs, None, None, mask, cfg.tau_s, cfg.alpha, False,
                                      _view(self.token, b, B), _view(self.conf, b, B), _view(self.commit, b, B),
                                      workspace=self.ws)
-            n = self._apply(y, bs, tok, cm, trace, fwd, "entry", lg, conf, masked)
-            stats["committed"] += n
+            n = self._apply(y, bs, tok, cm, trace, fwd, "entry", lg if full(fwd) else None, conf, masked)
+            gpu_ms["all"] += ev0.elapsed_time(ev1)
+            stats["committed"] += int(n.sum())
             fwd += 1
-            since = n
+            since = n                       # per sequence; a batch refreshes when any sequence would
             self.hist_len.zero_()
             while (y[:, bs:be] == mask).any():
-                refresh = since > cfg.tau_upd
+                refresh = int(since.max()) > cfg.tau_upd
                 rlo, rhi = (lo, hi) if refresh else (bs, be)
                 k_top = int(math.ceil((hi - lo - B) / 2)) if refresh else 0
                 self.rows = rhi - rlo
-                self.forward(rlo, rhi, "refresh" if refresh else "plain", (bs, B), k_top, trace=trace, fwd=fwd)
+                ev0.record()
+                mode = "refresh" if refresh else "plain"
+                self.forward(rlo, rhi, mode, (bs, B), k_top, trace=trace if full(fwd, mode) else None, fwd=fwd)
+                ev1.record()
                 stats["refreshing_steps" if refresh else "plain_steps"] += 1
                 lg = self.head(rlo, bs, B)
                 masked = torch.from_numpy((y[:, bs:be] == mask).astype(np.uint8)).to(self.dev)
@@ -256,35 +279,41 @@ class Denoiser:
                 tok, conf, cm = P.commit(lg, masked, self.drift, bs, self.hist, self.hist_len, mask, cfg.tau_s,
                                          cfg.alpha, cfg.force_one, _view(self.token, b, B), _view(self.conf, b, B),
                                          _view(self.commit, b, B), workspace=self.ws)
-                n = self._apply(y, bs, tok, cm, trace, fwd, "step", lg, conf, masked, hist_in)
+                n = self._apply(y, bs, tok, cm, trace, fwd, "step", lg if full(fwd) else None, conf, masked, hist_in)
+                gpu_ms["refresh" if refresh else "plain"] += ev0.elapsed_time(ev1)
                 if cfg.suffix_commit and refresh and be < hi:
-                    n_s = self._suffix(y, rlo, be, hi, k_top, trace, fwd)
-                    stats["suffix_committed"] += n_s
-                    n += n_s
-                stats["committed"] += n
+                    n_s = self._suffix(y, rlo, be, hi, k_top, trace, fwd, full(fwd))
+                    stats["suffix_committed"] += int(n_s.sum())
+                    n = n + n_s
+                stats["committed"] += int(n.sum())
                 fwd += 1
                 since = n if refresh else since + n
+            if progress is not None:
+                progress(blk, fwd)
         torch.cuda.synchronize()
         stats["seconds"] = time.perf_counter() - t0
         stats["forwards"] = fwd
-        stats["tpf"] = stats["committed"] / max(fwd, 1)
+        stats["tpf"] = stats["committed"] / max(fwd * b, 1)      # tokens per forward pass, per sequence
+        stats["forward_gpu_ms"] = {k: round(v, 3) for k, v in gpu_ms.items()}
         return y, stats
 
     def _apply(self, y, r0, tok, cm, trace, fwd, kind, lg, conf, masked, hist_in=None) -> int:
         """Copy the commit flags and tokens to the host, write committed
-        tokens into y (host and device); returns the number committed."""
+        tokens into y (host and device); returns the number committed per
+        sequence."""
         n_rows = tok.shape[1]
         t = tok.cpu().numpy()
         c = cm.cpu().numpy().astype(bool)
         y[:, r0:r0 + n_rows] = np.where(c, t, y[:, r0:r0 + n_rows])
         self.y[:, r0:r0 + n_rows].copy_(torch.from_numpy(y[:, r0:r0 + n_rows]))
         if trace is not None:
-            trace(dict(event="commit", forward=fwd, kind=kind, r0=r0, logits=lg.clone(), conf=conf.clone(),
+            trace(dict(event="commit", forward=fwd, kind=kind, r0=r0, logits=None if lg is None else lg.clone(),
+                       conf=conf.clone(),
                        token=tok.clone(), commit=cm.clone(), masked=masked.clone(), drift=self.drift.clone(),
                        hist_in=hist_in, hist_out=(self.hist.clone(), self.hist_len.clone())))
-        return int(c.sum())
+        return c.sum(axis=1)
 
-    def _suffix(self, y, rlo, be, hi, k_top, trace, fwd) -> int:
+    def _suffix(self, y, rlo, be, hi, k_top, trace, fwd, full=True) -> int:
         """Suffix commit of the suffix rows [be, hi) that the last layer refreshed."""
         b, mask = self.b, self.shape.mask_id
         n = hi - be
@@ -296,12 +325,12 @@ class Denoiser:
                 if be <= p < hi:
                     el[s, p - be] = 1
         if not el.any():
-            return 0
+            return np.zeros(b, np.int64)
         lg = self.head(rlo, be, n)
         masked = torch.from_numpy((y[:, be:hi] == mask).astype(np.uint8)).to(self.dev)
         elig = torch.from_numpy(el).to(self.dev)
         tok, conf, cm = P.suffix_commit(lg, masked, elig, mask, self.cfg.tau_s, _view(self.token, b, n),
                                         _view(self.conf, b, n), _view(self.commit, b, n), workspace=self.ws)
         if trace is not None:
-            trace(dict(event="suffix", forward=fwd, r0=be, eligible=elig.clone(), logits=lg.clone()))
-        return self._apply(y, be, tok, cm, trace, fwd, "suffix", lg, conf, masked)
+            trace(dict(event="suffix", forward=fwd, r0=be, eligible=elig.clone()))
+        return self._apply(y, be, tok, cm, trace, fwd, "suffix", lg if full else None, conf, masked)

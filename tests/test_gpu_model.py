@@ -117,39 +117,38 @@ def test_copy_rows(P):
 # the loop on a small stack, replayed against the oracle
 # ---------------------------------------------------------------------------
 
-def stack_weights(cfg):
+def stack_weights(cfg, oracle_embeddings=True):
     names = ("tok_emb", "pos_emb", "w_lm")
     host = {n: inputs.stack_tensor(cfg, n) for n in names}
     host["layers"] = [{m: inputs.stack_tensor(cfg, m, li) for m in inputs.STACK_MATRICES} for li in range(cfg.n_layers)]
     devw = {n: to_dev(host[n], cfg.dtype) for n in names}
     devw["layers"] = [{m: to_dev(l[m], cfg.dtype) for m in l} for l in host["layers"]]
-    ow = {n: ref.decode(host[n], cfg.dtype) for n in names}
+    ow = {n: ref.decode(host[n], cfg.dtype) for n in names if oracle_embeddings or n == "w_lm"}
     ow["layers"] = [{m: ref.decode(l[m], cfg.dtype) for m in l} for l in host["layers"]]
     return devw, ow
 
 
-def run_tiny(P, trace=True):
+def run_stack(P, index, trace=True, capture=None):
     from paper_2607_14107_amd import model
-    cfg = inputs.STACKS[40]
-    devw, ow = stack_weights(cfg)
+    cfg = inputs.STACKS[index]
+    devw, ow = stack_weights(cfg, oracle_embeddings=cfg.d <= 1024)
     shape = model.ModelShape(cfg.n_layers, cfg.d, cfg.n_heads, cfg.head_dim, cfg.ffn, cfg.vocab, cfg.seq)
     lc = model.LoopConfig(prompt_len=cfg.prompt_len, gen_len=cfg.gen_len, block_len=cfg.block_len)
     den = model.Denoiser(devw, shape, cfg.batch, lc)
     events = []
-    y, stats = den.generate(inputs.stack_prompt(cfg), trace=events.append if trace else None)
+    y, stats = den.generate(inputs.stack_prompt(cfg), trace=events.append if trace else None, capture=capture)
     return cfg, lc, ow, y, stats, events
 
 
-def test_tiny_stack_loop_replay(P):
-    cfg, lc, ow, y, stats, events = run_tiny(P)
+def replay(events, cfg, lc, ow, seqs=None):
+    """Checks every traced event against the oracle.  Value parity (layer
+    outputs, caches, logits, confidences) on the sequences in `seqs` (all by
+    default); selections and decisions on every sequence.  Returns the
+    number of layer events checked."""
     shape = mr.Shape(cfg.n_layers, cfg.d, cfg.n_heads, cfg.head_dim, cfg.ffn, cfg.vocab, cfg.seq, cfg.dtype)
     mask = shape.mask_id
     B = lc.block_len
-    # the loop finished: every generated position committed, the prompt intact
-    assert not (y == mask).any()
-    assert np.array_equal(y[:, :cfg.prompt_len], inputs.stack_prompt(cfg))
-    assert stats["committed"] == cfg.batch * cfg.gen_len
-    assert stats["refreshing_steps"] > 0 and stats["plain_steps"] > 0
+    sq = np.arange(cfg.batch) if seqs is None else np.asarray(seqs)
     last_x, last_stale, suffix_elig = {}, {}, {}
     n_layer_checks = 0
     for ev in events:
@@ -157,13 +156,13 @@ def test_tiny_stack_loop_replay(P):
             lo, hi, mode, li = ev["lo"], ev["hi"], ev["mode"], ev["layer"]
             bs, bl = ev["block"]
             bf, af = ev["before"], ev["after"]
-            st = mr.LayerState(dec(bf["k"]), dec(bf["v"]), dec(bf["h"]))
-            x_in = from_dev(bf["x"]).astype(np.float64)
-            h_gpu = dec(af["h_cur"])[:, lo:hi]
+            st = mr.LayerState(dec(bf["k"])[sq], dec(bf["v"])[sq], dec(bf["h"])[sq])
+            x_in = from_dev(bf["x"])[sq].astype(np.float64)
+            h_gpu = dec(af["h_cur"])[sq][:, lo:hi]
             assert_rows_close(h_gpu, ref.round_to(mr.rmsnorm(x_in), "bf16"), 2e-2, f"h rows, layer {li}")
             stale = None
             if mode == "refresh" or li == cfg.n_layers - 1:
-                gd = from_dev(af["drift"])[:, lo:hi]
+                gd = from_dev(af["drift"])[sq][:, lo:hi]
                 assert_drift_close(gd, ref.drift(h_gpu, st.h[:, lo:hi]))
             if mode == "refresh":
                 el = np.zeros((cfg.batch, cfg.seq), bool)
@@ -175,11 +174,11 @@ def test_tiny_stack_loop_replay(P):
                 assert np.array_equal(gidx, widx)
                 stale = (gidx, gcnt)
             r = mr.layer_forward(x_in, lo, ow["layers"][li], st, mode=mode, block=(bs, bl), shape=shape,
-                                 k_top=ev["k_top"], stale=stale)
-            assert_rows_close(from_dev(af["x"]), r["x_out"], 2e-2, f"x_out fwd {ev['forward']} layer {li}")
+                                 k_top=ev["k_top"], stale=None if stale is None else (stale[0][sq], stale[1][sq]))
+            assert_rows_close(from_dev(af["x"])[sq], r["x_out"], 2e-2, f"x_out fwd {ev['forward']} layer {li}")
             for nm in ("k", "v"):
-                assert_rows_close(dec(af[nm]), getattr(r["state"], nm), 2e-2, f"{nm} cache")
-            assert_rows_close(dec(af["h"]), r["state"].h, 2e-2, "cached H")
+                assert_rows_close(dec(af[nm])[sq], getattr(r["state"], nm), 2e-2, f"{nm} cache")
+            assert_rows_close(dec(af["h"])[sq], r["state"].h, 2e-2, "cached H")
             # rows the layer did not rewrite are bit-identical
             touched = np.zeros((cfg.batch, cfg.seq), bool)
             if mode == "all":
@@ -194,19 +193,19 @@ def test_tiny_stack_loop_replay(P):
                 assert np.array_equal(a[~touched], b0[~touched]), f"{nm}: untouched rows changed"
             n_layer_checks += 1
             if li == cfg.n_layers - 1:
-                last_x[ev["forward"]] = (lo, from_dev(af["x"]).astype(np.float64))
+                last_x[ev["forward"]] = (lo, from_dev(af["x"])[sq].astype(np.float64))
                 last_stale[ev["forward"]] = stale
         elif ev["event"] == "commit":
-            lo, xf = last_x[ev["forward"]]
             r0 = ev["r0"]
-            lg = from_dev(ev["logits"])
-            n = lg.shape[1]
-            assert_rows_close(ref.decode(lg, "bf16"), mr.logits(xf[:, r0 - lo:r0 - lo + n], ow["w_lm"], "bf16"),
-                              2e-2, "logits")
-            tok, conf = ref.confidence(ref.decode(lg, "bf16"), mask)
-            assert np.array_equal(from_dev(ev["token"]), tok)
             gconf = from_dev(ev["conf"])
-            np.testing.assert_allclose(gconf, conf, rtol=1e-4)
+            n = gconf.shape[1]
+            if ev["logits"] is not None:
+                lo, xf = last_x[ev["forward"]]
+                lg = ref.decode(from_dev(ev["logits"])[sq], "bf16")
+                assert_rows_close(lg, mr.logits(xf[:, r0 - lo:r0 - lo + n], ow["w_lm"], "bf16"), 2e-2, "logits")
+                tok, conf = ref.confidence(lg, mask)
+                assert np.array_equal(from_dev(ev["token"])[sq], tok)
+                np.testing.assert_allclose(gconf[sq], conf, rtol=1e-4)
             masked = from_dev(ev["masked"]).astype(bool)
             gcm = from_dev(ev["commit"]).astype(bool)
             if ev["kind"] == "entry":
@@ -221,27 +220,61 @@ def test_tiny_stack_loop_replay(P):
                 for s in range(cfg.batch):
                     assert np.array_equal(gh[s, :gl[s]], wh[s, :wl[s]])
             else:
-                gidx, gcnt = last_stale[ev["forward"]]
-                el = ref.suffix_eligible(gidx, gcnt, r0, n)
-                assert np.array_equal(el, suffix_elig[ev["forward"]])
+                el = suffix_elig[ev["forward"]]
+                if ev["forward"] in last_stale:
+                    gidx, gcnt = last_stale[ev["forward"]]
+                    assert np.array_equal(ref.suffix_eligible(gidx, gcnt, r0, n), el)
                 assert np.array_equal(gcm, ref.suffix_commit_rule(gconf, masked, el, lc.tau_s))
         elif ev["event"] == "suffix":           # precedes the suffix commit of its forward
             suffix_elig[ev["forward"]] = from_dev(ev["eligible"]).astype(bool)
-    assert n_layer_checks == cfg.n_layers * stats["forwards"]
+    return n_layer_checks
+
+
+def test_tiny_stack_loop_replay(P):
+    cfg, lc, ow, y, stats, events = run_stack(P, 40)
+    mask = cfg.vocab - 1
+    # the loop finished: every generated position committed, the prompt intact
+    assert not (y == mask).any()
+    assert np.array_equal(y[:, :cfg.prompt_len], inputs.stack_prompt(cfg))
+    assert stats["committed"] == cfg.batch * cfg.gen_len
+    assert stats["refreshing_steps"] > 0 and stats["plain_steps"] > 0
+    assert replay(events, cfg, lc, ow) == cfg.n_layers * stats["forwards"]
+
+
+def test_llada_width_stack_replay(P):
+    """The LLaDA-8B-shaped stack at full width and sequence length (d 4096,
+    FFN 12288, vocab 126464, batch 16, seq 768) with two layers and two
+    blocks: the first forward of each kind is traced and replayed on two of
+    the sixteen sequences; every decision of the run is replayed."""
+    firsts = set()
+
+    def capture(f, mode):
+        if mode in firsts:
+            return False
+        firsts.add(mode)
+        return True
+
+    cfg, lc, ow, y, stats, events = run_stack(P, 41, capture=capture)
+    assert not (y == cfg.vocab - 1).any()
+    assert stats["committed"] == cfg.batch * cfg.gen_len
+    assert stats["full_entries"] == 1 and stats["window_entries"] == 1
+    n = replay(events, cfg, lc, ow, seqs=[0, 11])
+    assert n == cfg.n_layers * len(firsts) and firsts == {"all", "refresh", "plain"}
 
 
 def test_tiny_stack_loop_schedule_and_determinism(P):
-    cfg, lc, _, y, stats, events = run_tiny(P)
-    _, _, _, y2, stats2, _ = run_tiny(P, trace=False)
+    cfg, lc, _, y, stats, events = run_stack(P, 40)
+    _, _, _, y2, stats2, _ = run_stack(P, 40, trace=False)
     assert np.array_equal(y, y2) and stats["forwards"] == stats2["forwards"]
     # the kinds of forward follow the schedule rule on the GPU's own commits
     forwards = {}
     for ev in events:
         if ev["event"] == "layer" and ev["layer"] == 0:
-            forwards[ev["forward"]] = dict(mode=ev["mode"], lo=ev["lo"], hi=ev["hi"], n=0, entry=None)
+            forwards[ev["forward"]] = dict(mode=ev["mode"], lo=ev["lo"], hi=ev["hi"], n=np.zeros(cfg.batch, int),
+                                           entry=None)
         elif ev["event"] == "commit":
             f = forwards[ev["forward"]]
-            f["n"] += int(from_dev(ev["commit"]).sum())
+            f["n"] = f["n"] + from_dev(ev["commit"]).sum(axis=1)
             f["entry"] = f["entry"] or ev["kind"] == "entry"
     since = None
     n_blocks = 0
@@ -253,7 +286,7 @@ def test_tiny_stack_loop_schedule_and_determinism(P):
             n_blocks += 1
             since = f["n"]
             continue
-        assert (f["mode"] == "refresh") == mr.refreshes(since, lc.tau_upd)
+        assert (f["mode"] == "refresh") == mr.refreshes(int(since.max()), lc.tau_upd)
         since = f["n"] if f["mode"] == "refresh" else since + f["n"]
     assert n_blocks == cfg.gen_len // lc.block_len
-    assert stats["tpf"] >= 1.0
+    assert stats["tpf"] == pytest.approx(stats["committed"] / (stats["forwards"] * cfg.batch))
