@@ -130,6 +130,29 @@ def proxy_kl(scores: np.ndarray, prev_scores: np.ndarray) -> np.ndarray:
     return kl.mean(axis=-1)
 
 
+def query_scores(q: np.ndarray, k_cache: np.ndarray, scale: float | None = None) -> np.ndarray:
+    """Attention logits of given queries over every cache position:
+    q [b][R][H][hd], k_cache [b][S][Hkv][hd] -> [b][R][H][S] =
+    scale * q_(r,h) . k_(j, kv head of h), scale 1/sqrt(hd) by default (eq. 3)."""
+    b, R, H, hd = q.shape
+    _, S, Hkv, _ = k_cache.shape
+    sc = 1.0 / np.sqrt(hd) if scale is None else scale
+    group = H // Hkv
+    out = np.empty((b, R, H, S))
+    for h in range(H):
+        keys = k_cache[:, :, h // group, :]                     # [b][S][hd]
+        out[:, :, h, :] = sc * np.einsum("brd,bsd->brs", q[:, :, h, :], keys)
+    return out
+
+
+def attention_drift(scores: np.ndarray, prev_scores: np.ndarray) -> np.ndarray:
+    """The commit drift of Alg. 1: for each query row, KL(A_t || A_(t-1)) of its
+    attention distributions over the positions, in nats, averaged over the
+    heads (the drift functional of Sec. 3 on the main attention of the last
+    layer).  scores, prev_scores [b][R][H][S] -> [b][R]."""
+    return proxy_kl(scores, prev_scores)
+
+
 def log_sum_exp(scores: np.ndarray) -> np.ndarray:
     """Natural-log normaliser of each distribution: [b][K][H]."""
     m = scores.max(axis=-1)

@@ -9,6 +9,7 @@ import math
 import numpy as np
 import pytest
 
+from oracle import polestar_ref as ref
 from oracle import proxy_ref as pr
 
 
@@ -165,3 +166,28 @@ def test_update_sums_equals_recomputing_the_window():
     upd = pr.update_sums(sums0[None], lab, stale, cnt, h_new, h_old)
     want, _ = pr.cluster_sums(h_new[0, win], lab_w, K)
     assert np.allclose(upd[0], want, atol=1e-12)
+
+
+def test_query_scores_closed_form_and_agreement_with_proxy_scores():
+    # the proxy scores are the scores of the proxy tokens' rounded queries
+    g = np.random.default_rng(9)
+    b, K, d, H, Hkv, hd, S = 2, 3, 16, 4, 2, 4, 7
+    tokens = g.standard_normal((b, K, d))
+    w_q = g.standard_normal((H * hd, d)) * 0.3
+    kc = g.standard_normal((b, S, Hkv, hd))
+    q = ref.round_to(tokens @ w_q.T, "bf16").reshape(b, K, H, hd)
+    assert np.allclose(pr.query_scores(q, kc), pr.proxy_scores(tokens, w_q, kc, H, "bf16"), rtol=1e-13)
+    # one query, one head, two keys: scores are the scaled dot products
+    q1 = np.array([1.0, 2.0]).reshape(1, 1, 1, 2)
+    k1 = np.array([[3.0, 1.0], [0.0, -1.0]]).reshape(1, 2, 1, 2)
+    assert np.allclose(pr.query_scores(q1, k1, scale=0.5)[0, 0, 0], [2.5, -1.0])
+
+
+def test_attention_drift_is_the_head_averaged_kl_of_each_query_row():
+    a, b = 0.7, 0.4
+    cur = np.log([[a, 1 - a], [0.5, 0.5]])[None, :, None, :]         # [1 seq][2 rows][1 head][2 pos]
+    prev = np.log([[b, 1 - b], [0.5, 0.5]])[None, :, None, :]
+    d = pr.attention_drift(cur, prev)
+    want = a * math.log(a / b) + (1 - a) * math.log((1 - a) / (1 - b))
+    assert d.shape == (1, 2)
+    assert d[0, 0] == pytest.approx(want, rel=1e-12) and d[0, 1] == 0.0
