@@ -337,6 +337,32 @@ polestar_status polestar_proxy_drift(polestar_dtype dtype, int batch, int seq, i
                                      void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * polestar_attention_drift -- drift of the attention distributions of given
+ * query rows between two steps (Alg. 1: the commit drift delta = KL of the
+ * last layer's main attention of the block's tokens against the previous
+ * step's; the drift functional of Sec. 3).  For every sequence b, row r and
+ * query head h (KV head h / (n_heads / n_kv_heads)):
+ *   s_j = scale * q[b][r][h] . k_cache[b][j][kv],  a = softmax_j(s),
+ *   KL_(r,h) = sum_j a_j (log a_j - log a'_j),  a' = softmax(previous scores)
+ *   drift[b][r] = mean over h of KL_(r,h)   (0 when first != 0)
+ * scores[b][r][h][:] and lse[b][r][h] hold the previous step's scores and
+ * natural-log normaliser on entry and this step's on return (first != 0:
+ * their contents on entry are ignored).  scale <= 0 selects 1/sqrt(head_dim).
+ *   q : [batch][n_rows][n_heads][head_dim] dtype;  k_cache : [batch][seq][n_kv_heads][head_dim]
+ *   scores : [batch][n_rows][n_heads][seq] float;  lse : [batch][n_rows][n_heads] float
+ *   drift : out [batch][n_rows] float
+ *   workspace : >= polestar_attention_drift_workspace_size(...) bytes (no init)
+ * UNSUPPORTED unless head_dim is 64 or 128, n_rows <= 64 and q, k_cache are
+ * 16-byte aligned.  polestar_proxy_drift runs the same kernels on its proxy
+ * queries.
+ */
+size_t polestar_attention_drift_workspace_size(int batch, int seq, int n_rows, int n_heads);
+polestar_status polestar_attention_drift(polestar_dtype dtype, int batch, int seq, int n_rows, int n_heads,
+                                         int n_kv_heads, int head_dim, const void* q, const void* k_cache,
+                                         float scale, float* scores, float* lse, int first, float* drift,
+                                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * polestar_cluster_select -- the k_top clusters of largest drift (equal
  * drift: lower cluster first) of each sequence; their member positions
  * (labels[b][p] selected) go to stale_idx[b][0..count) in ascending order,

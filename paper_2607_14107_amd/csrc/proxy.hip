@@ -30,7 +30,6 @@ constexpr int kKmWaves = kKmBlock / kWave;
 constexpr int kMaxClusters = 16;
 constexpr int kMaxWin = 2048;                // window positions per sequence
 constexpr int kMaxCentroidFloats = 32768;    // K * d held in LDS (128 KB)
-constexpr long kMaxProxyScores = 36864;      // K * (seq + head_dim) floats in LDS (144 KB)
 constexpr int kChunkGroup = 8;               // 16-byte chunks per lane loaded together in the K-means
 
 template <bool BF16>
@@ -279,6 +278,8 @@ __global__ __launch_bounds__(kKmBlock) void kmeans_kernel(const char* __restrict
 // ---------------------------------------------------------------------------
 // polestar_proxy_drift kernels
 // ---------------------------------------------------------------------------
+// polestar_proxy_drift kernels
+// ---------------------------------------------------------------------------
 
 // token[b][k][:] = dtype(sums / count), zero for an empty cluster; thread
 // per 4 channels (d % 4 == 0), workgroups over (cluster, channel range).
@@ -301,121 +302,249 @@ __global__ __launch_bounds__(256) void token_kernel(const float* __restrict__ su
         *reinterpret_cast<float4*>(tok + (static_cast<size_t>(bk) * d + c) * 4) = make_float4(x0, x1, x2, x3);
 }
 
-// Scores and drift of one (sequence b, head h), all K clusters at once:
-//   1. the K queries of head h go to LDS (fp32);
-//   2. thread j loads key row j (16-byte loads) and writes the K scores
-//      s_(k,j) to LDS (sc[k][j], fp32);
-//   3. wave w takes clusters w, w+4, ...: max and sum of exp over j (shuffles)
-//      give lse; then KL_(k,h) = sum_j p_j ((s_j - lse) - (s'_j - lse')) with
-//      the previous scores s' read from `prev`, which then receives s_j, and
-//      lse replaces lse'.
-// The per-head KL goes to kl[b][k][h]; head_mean_kernel averages it.
-constexpr int kPdBlock = 1024;
-constexpr int kPdPer = 16;                  // positions per lane per pass of the KL stage
+// ---------------------------------------------------------------------------
+// Scores of R query rows over every cache position and their KL against the
+// previous step's scores: the proxy drift of the clusters (R = K proxy
+// queries) and the commit drift of the block's queries.  S^T = K Q^T on
+// MFMA: a wave takes 16-key tiles, the query rows sit in registers as B
+// fragments.  Nothing is staged: each lane folds its scores into an online
+// (m, Z, W) per query row,
+//     Z = sum_j e^(s_j - m),   W = sum_j e^(s_j - m) (s_j - s'_j),
+// so that KL(p || p') = W / Z - (m + log Z) + lse' with p = softmax(s), and
+// each score replaces the previous one in place (read and written by the
+// same lane).  grid (key splits, heads, batch); the partials of a split go to
+// part[b][r][h][split][3] and qkl_merge_kernel combines them.
+// ---------------------------------------------------------------------------
+constexpr int kQkBlock = 256;
+constexpr int kQkWaves = kQkBlock / kWave;
+constexpr int kQkMaxRows = 64;              // four 16-row query tiles
+constexpr int kQkMaxSplits = 16;
 
-template <bool BF16, int HD>
-__global__ __launch_bounds__(kPdBlock) void proxy_kl_kernel(const char* __restrict__ q, const char* __restrict__ kc,
-                                                            int seq, int K, int H, int Hkv, float scale,
-                                                            float* __restrict__ prev, float* __restrict__ prev_lse,
-                                                            int first, float* __restrict__ kl) {
-    extern __shared__ float sm[];               // [K][HD] queries, then [K][seq] scores
-    float* qs = sm;
-    float* sc = sm + K * HD;
+struct QklArgs {
+    const char* q;        // [b][R][H][hd]
+    const char* kc;       // [b][S][Hkv][hd]
+    float* scores;        // [b][R][H][S], the previous step's in, this step's out
+    float* part;          // [b][R][H][splits][3]
+    int R, S, H, Hkv, splits, tiles_per_split, first;
+    float scale;
+};
+
+// (m, z, w) <- merge with (m2, z2, w2)
+__device__ __forceinline__ void mzw_merge(float& m, float& z, float& w, float m2, float z2, float w2) {
+    const float mn = fmaxf(m, m2);
+    const float f1 = m == mn ? 1.f : __expf(m - mn);
+    const float f2 = m2 == mn ? 1.f : __expf(m2 - mn);
+    z = z * f1 + z2 * f2;
+    w = w * f1 + w2 * f2;
+    m = mn;
+}
+
+template <bool BF16, int HD, int RT>
+__global__ __launch_bounds__(kQkBlock) void qkl_kernel(QklArgs a) {
     using T = Elem<BF16>;
     constexpr int ES = T::kBytes;
-    constexpr int E = T::E;
-    constexpr int NC = HD * ES / 16;            // 16-byte chunks of a key row
-    const int h = blockIdx.x, b = blockIdx.y;
-    const int g = h / (H / Hkv);
+    constexpr int E = T::E;                  // elements per 16-byte chunk
+    constexpr int NC = HD / (4 * E);         // chunks per row and lane (k-group g of each MFMA step)
+    constexpr int TB = RT * NC <= 8 ? 4 : (RT * NC <= 16 ? 2 : 1);   // key tiles loaded together
+    __shared__ float red[kQkWaves][RT * 16][3];
+    const int split = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-    for (int e = t; e < K * HD; e += kPdBlock) {
-        const int k = e / HD, c = e - k * HD;
-        qs[e] = load_elem<BF16>(q + ((static_cast<size_t>(b) * K + k) * H + h) * HD * ES, c);
+    const int g = lane >> 4, li = lane & 15;
+    const int kvh = h / (a.H / a.Hkv);
+
+    // query fragments: row 16 rt + li (rows past R repeat the last one and are
+    // never stored), chunk c holds elements [4E c + E g, +E)
+    uint4 qf[RT][NC];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+        const int r = min(16 * rt + li, a.R - 1);
+        const char* qrow = a.q + ((static_cast<size_t>(b) * a.R + r) * a.H + h) * HD * ES;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) qf[rt][c] = ld16(qrow + (c * 4 * E + g * E) * ES);
     }
-    __syncthreads();
-    // scores: thread per key; the key row's chunks are loaded together, then
-    // every cluster's dot product is accumulated chunk by chunk
-    for (int j = t; j < seq; j += kPdBlock) {
-        const char* kr = kc + ((static_cast<size_t>(b) * seq + j) * Hkv + g) * HD * ES;
-        float acc[kMaxClusters];
+    float pm[RT], pz[RT], pw[RT];
 #pragma unroll
-        for (int k = 0; k < kMaxClusters; ++k) acc[k] = 0.f;
-        constexpr int G = NC < 16 ? NC : 16;    // chunks held at once
-        uint4 raw[G];
+    for (int rt = 0; rt < RT; ++rt) { pm[rt] = -INFINITY; pz[rt] = 0.f; pw[rt] = 0.f; }
+
+    const int ntiles = (a.S + 15) / 16;
+    const int t0 = split * a.tiles_per_split;
+    const int t1 = min(ntiles, t0 + a.tiles_per_split);
+    const size_t krow = static_cast<size_t>(a.Hkv) * HD * ES;
+    const char* kbase = a.kc + (static_cast<size_t>(b) * a.S * a.Hkv + kvh) * HD * ES;
+    for (int tb = t0 + w; tb < t1; tb += kQkWaves * TB) {
+        // every load of this round first: key fragments of TB tiles and the
+        // previous scores the lane will fold in (clamped, unused when invalid)
+        uint4 kf[TB][NC];
+        float sp[TB][RT][4];
 #pragma unroll
-        for (int cc = 0; cc < NC; ++cc) {
-            if (cc % G == 0) {
+        for (int u = 0; u < TB; ++u) {
+            const int tile = min(tb + u * kQkWaves, t1 - 1);
+            const int key = min(tile * 16 + li, a.S - 1);
 #pragma unroll
-                for (int u = 0; u < G; ++u) raw[u] = ld16(kr + 16 * (cc + u));
+            for (int c = 0; c < NC; ++c) kf[u][c] = ld16(kbase + key * krow + (c * 4 * E + g * E) * ES);
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                const int r = min(16 * rt + li, a.R - 1);
+                const float* srow = a.scores + ((static_cast<size_t>(b) * a.R + r) * a.H + h) * a.S;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) sp[u][rt][i] = srow[min(tile * 16 + 4 * g + i, a.S - 1)];
             }
-            float kv[E];
-            T::unpack(raw[cc % G], kv);
+        }
 #pragma unroll
-            for (int k = 0; k < kMaxClusters; ++k) {
-                if (k < K) {
-                    const float4* qk = reinterpret_cast<const float4*>(qs + k * HD + cc * E);   // broadcast
+        for (int u = 0; u < TB; ++u) {
+            const int tile = tb + u * kQkWaves;
+            if (tile < t1) {
 #pragma unroll
-                    for (int e4 = 0; e4 < E / 4; ++e4) {
-                        const float4 qv = qk[e4];
-                        acc[k] = fmaf(qv.x, kv[4 * e4], acc[k]);
-                        acc[k] = fmaf(qv.y, kv[4 * e4 + 1], acc[k]);
-                        acc[k] = fmaf(qv.z, kv[4 * e4 + 2], acc[k]);
-                        acc[k] = fmaf(qv.w, kv[4 * e4 + 3], acc[k]);
+                for (int rt = 0; rt < RT; ++rt) {
+                    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) acc = Mma<BF16>::step(kf[u][c], qf[rt][c], acc);
+                    // lane holds S^T[key 16 tile + 4 g + i][query 16 rt + li]
+                    const int r = 16 * rt + li;
+                    float* srow = a.scores + ((static_cast<size_t>(b) * a.R + min(r, a.R - 1)) * a.H + h) * a.S;
+                    float sv[4];
+                    bool ok[4];
+                    float mx = pm[rt];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int key = tile * 16 + 4 * g + i;
+                        ok[i] = (r < a.R) & (key < a.S);
+                        sv[i] = acc[i] * a.scale;
+                        mx = ok[i] ? fmaxf(mx, sv[i]) : mx;
                     }
+                    const float f = pm[rt] == mx ? 1.f : __expf(pm[rt] - mx);
+                    float z = pz[rt] * f, ww = pw[rt] * f;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        if (ok[i]) {
+                            const float e = __expf(sv[i] - mx);
+                            z += e;
+                            ww = fmaf(e, sv[i] - sp[u][rt][i], ww);
+                            srow[tile * 16 + 4 * g + i] = sv[i];
+                        }
+                    }
+                    pm[rt] = mx;
+                    pz[rt] = z;
+                    pw[rt] = ww;
                 }
             }
         }
+    }
+    // lanes li, li+16, li+32, li+48 hold the same query rows: merge, then the waves
 #pragma unroll
-        for (int k = 0; k < kMaxClusters; ++k)
-            if (k < K) sc[k * seq + j] = acc[k] * scale;
+    for (int rt = 0; rt < RT; ++rt) {
+#pragma unroll
+        for (int off = 16; off <= 32; off <<= 1) {
+            const float m2 = __shfl_xor(pm[rt], off), z2 = __shfl_xor(pz[rt], off), w2 = __shfl_xor(pw[rt], off);
+            mzw_merge(pm[rt], pz[rt], pw[rt], m2, z2, w2);
+        }
+        if (g == 0) {
+            red[w][16 * rt + li][0] = pm[rt];
+            red[w][16 * rt + li][1] = pz[rt];
+            red[w][16 * rt + li][2] = pw[rt];
+        }
     }
     __syncthreads();
-    // KL per cluster: wave per cluster; the previous scores of a pass of
-    // kPdPer positions per lane are loaded before they are used
-    for (int k = w; k < K; k += kPdBlock / kWave) {
-        const float* srow = sc + k * seq;
-        float m = -INFINITY;
-        for (int j = lane; j < seq; j += kWave) m = fmaxf(m, srow[j]);
-        m = wave_max(m);
-        float z = 0.f;
-        for (int j = lane; j < seq; j += kWave) z += fast_exp2((srow[j] - m) * kLog2e);
-        z = wave_sum(z);
-        const float lse = m + logf(z);
-        const size_t rowid = (static_cast<size_t>(b) * K + k) * H + h;
-        const float lse_prev = prev_lse[rowid];
-        float* pr = prev + rowid * seq;
-        float acc = 0.f;
-        for (int j0 = 0; j0 < seq; j0 += kWave * kPdPer) {
-            float pv[kPdPer];
+    if (t < RT * 16 && t < a.R) {
+        float m = red[0][t][0], z = red[0][t][1], ww = red[0][t][2];
 #pragma unroll
-            for (int u = 0; u < kPdPer; ++u) pv[u] = pr[min(j0 + u * kWave + lane, seq - 1)];
-#pragma unroll
-            for (int u = 0; u < kPdPer; ++u) {
-                const int j = j0 + u * kWave + lane;
-                if (j < seq) {
-                    const float sj = srow[j];
-                    const float lp = sj - lse;
-                    acc = first ? acc : fmaf(fast_exp2(lp * kLog2e), lp - (pv[u] - lse_prev), acc);
-                    pr[j] = sj;
-                }
-            }
-        }
-        acc = wave_sum(acc);
-        if (lane == 0) {
-            kl[rowid] = first ? 0.f : acc;
-            prev_lse[rowid] = lse;
-        }
+        for (int q = 1; q < kQkWaves; ++q) mzw_merge(m, z, ww, red[q][t][0], red[q][t][1], red[q][t][2]);
+        float* pp = a.part + (((static_cast<size_t>(b) * a.R + t) * a.H + h) * a.splits + split) * 3;
+        pp[0] = m;
+        pp[1] = z;
+        pp[2] = ww;
     }
 }
 
-// drift[b][k] = mean over heads of kl[b][k][h], summed in head order.
-__global__ __launch_bounds__(256) void head_mean_kernel(const float* __restrict__ kl, int BK, int H,
+// One wave per (sequence, query row): lane h merges head h's splits, then
+//   lse = m + log Z,   KL = first ? 0 : W / Z - lse + lse_prev,
+// lse replaces lse_prev, and drift = the mean of KL over the heads.
+__global__ __launch_bounds__(256) void qkl_merge_kernel(const float* __restrict__ part, int BR, int H, int splits,
+                                                        int first, float* __restrict__ lse,
                                                         float* __restrict__ drift) {
-    const int bk = blockIdx.x * 256 + threadIdx.x;
-    if (bk >= BK) return;
-    float s = 0.f;
-    for (int h = 0; h < H; ++h) s += kl[static_cast<size_t>(bk) * H + h];
-    drift[bk] = s / static_cast<float>(H);
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (row >= BR) return;                              // uniform per wave
+    float acc = 0.f;
+    for (int h = lane; h < H; h += kWave) {
+        const float* pp = part + (static_cast<size_t>(row) * H + h) * splits * 3;
+        float v[kQkMaxSplits][3];
+#pragma unroll
+        for (int s = 0; s < kQkMaxSplits; ++s) {
+            const int sc = min(s, splits - 1);
+            v[s][0] = pp[3 * sc];
+            v[s][1] = pp[3 * sc + 1];
+            v[s][2] = pp[3 * sc + 2];
+        }
+        float m = v[0][0], z = v[0][1], w = v[0][2];
+#pragma unroll
+        for (int s = 1; s < kQkMaxSplits; ++s)
+            if (s < splits) mzw_merge(m, z, w, v[s][0], v[s][1], v[s][2]);
+        const size_t id = static_cast<size_t>(row) * H + h;
+        const float l = m + logf(z);
+        const float kl = first ? 0.f : w / z - l + lse[id];
+        lse[id] = l;
+        acc += kl;
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) drift[row] = acc / static_cast<float>(H);
+}
+
+struct QklPlan {
+    int splits, tiles_per_split;
+    size_t part_bytes;
+};
+
+QklPlan qkl_plan(int batch, int seq, int R, int H) {
+    QklPlan p{};
+    const int ntiles = ceil_div(seq, 16);
+    const long base = static_cast<long>(batch) * H;
+    int splits = static_cast<int>((256 + base - 1) / base);
+    splits = min(splits, max(1, ntiles / kQkWaves));
+    splits = max(1, min(splits, kQkMaxSplits));
+    p.tiles_per_split = ceil_div(ntiles, splits);
+    p.splits = ceil_div(ntiles, p.tiles_per_split);
+    p.part_bytes = align_up(static_cast<size_t>(batch) * R * H * p.splits * 3 * sizeof(float), 256);
+    return p;
+}
+
+template <bool BF16, int HD>
+void launch_qkl_rt(const QklArgs& a, int batch, hipStream_t s) {
+    const dim3 grid(a.splits, a.H, batch);
+    const int rt = ceil_div(a.R, 16);
+    if (rt == 1) hipLaunchKernelGGL((qkl_kernel<BF16, HD, 1>), grid, dim3(kQkBlock), 0, s, a);
+    else if (rt == 2) hipLaunchKernelGGL((qkl_kernel<BF16, HD, 2>), grid, dim3(kQkBlock), 0, s, a);
+    else if (rt == 3) hipLaunchKernelGGL((qkl_kernel<BF16, HD, 3>), grid, dim3(kQkBlock), 0, s, a);
+    else hipLaunchKernelGGL((qkl_kernel<BF16, HD, 4>), grid, dim3(kQkBlock), 0, s, a);
+}
+
+// scores + KL of R query rows, then the merge.  The caller has validated
+// shapes (R <= kQkMaxRows, hd 64 or 128, H % Hkv == 0) and sized `part`.
+polestar_status run_qkl(bool bf16, int batch, int seq, int R, int H, int Hkv, int hd, const char* q,
+                        const char* kc, float scale, float* scores, float* lse, int first, float* part,
+                        float* drift, hipStream_t stream) {
+    const QklPlan p = qkl_plan(batch, seq, R, H);
+    QklArgs a{};
+    a.q = q;
+    a.kc = kc;
+    a.scores = scores;
+    a.part = part;
+    a.R = R;
+    a.S = seq;
+    a.H = H;
+    a.Hkv = Hkv;
+    a.splits = p.splits;
+    a.tiles_per_split = p.tiles_per_split;
+    a.first = first;
+    a.scale = scale > 0.f ? scale : 1.0f / sqrtf(static_cast<float>(hd));
+    if (bf16) { if (hd == 128) launch_qkl_rt<true, 128>(a, batch, stream); else launch_qkl_rt<true, 64>(a, batch, stream); }
+    else { if (hd == 128) launch_qkl_rt<false, 128>(a, batch, stream); else launch_qkl_rt<false, 64>(a, batch, stream); }
+    polestar_status st = launch_status();
+    if (st != POLESTAR_OK) return st;
+    const int BR = batch * R;
+    hipLaunchKernelGGL(qkl_merge_kernel, dim3(ceil_div(BR, 4)), dim3(256), 0, stream, part, BR, H, p.splits, first,
+                       lse, drift);
+    return launch_status();
 }
 
 // ---------------------------------------------------------------------------
@@ -509,10 +638,10 @@ __global__ __launch_bounds__(256) void cluster_update_kernel(const char* __restr
 }
 
 // Workspace of polestar_proxy_drift: tokens, queries, the GEMM's partials,
-// the per-head KL.
+// the score/KL partials.
 struct ProxyLayout {
     GemmPlan qp;
-    size_t tok, q, gemm, kl, total;
+    size_t tok, q, gemm, part, total;
 };
 
 ProxyLayout proxy_layout(bool bf16, int batch, int seq, int d, int H, int hd, int K) {
@@ -522,8 +651,8 @@ ProxyLayout proxy_layout(bool bf16, int batch, int seq, int d, int H, int hd, in
     L.tok = 0;
     L.q = align_up(static_cast<size_t>(batch) * K * d * es, 256);
     L.gemm = L.q + align_up(static_cast<size_t>(batch) * K * H * hd * es, 256);
-    L.kl = L.gemm + align_up(L.qp.ws_bytes, 256);
-    L.total = L.kl + align_up(static_cast<size_t>(batch) * K * H * sizeof(float), 256);
+    L.part = L.gemm + align_up(L.qp.ws_bytes, 256);
+    L.total = L.part + qkl_plan(batch, seq, K, H).part_bytes;
     return L;
 }
 
@@ -579,8 +708,7 @@ extern "C" polestar_status polestar_proxy_drift(polestar_dtype dtype, int batch,
     const bool bf16 = dtype == POLESTAR_BF16;
     if ((head_dim != 64 && head_dim != 128) || !gemm_k_ok(bf16, d) || n_clusters > kMaxClusters ||
         !aligned16(w_q) || !aligned16(k_cache) || !aligned16(workspace) || !aligned16(sums) ||
-        batch > 65535 || n_heads > 65535 ||
-        static_cast<long>(n_clusters) * (seq + head_dim) > kMaxProxyScores)
+        batch > 65535 || n_heads > 65535)
         return POLESTAR_ERR_UNSUPPORTED;
     const ProxyLayout L = proxy_layout(bf16, batch, seq, d, n_heads, head_dim, n_clusters);
     if (workspace_bytes < L.total || !workspace) return POLESTAR_ERR_WORKSPACE;
@@ -608,24 +736,36 @@ extern "C" polestar_status polestar_proxy_drift(polestar_dtype dtype, int batch,
     g.m_max = BK;
     st = gemm_run(bf16, L.qp, g, stream);
     if (st != POLESTAR_OK) return st;
-    const float sc = scale > 0.f ? scale : 1.0f / sqrtf(static_cast<float>(head_dim));
-    const dim3 pgrid(n_heads, batch);
-    const size_t plds = (static_cast<size_t>(n_clusters) * head_dim + static_cast<size_t>(n_clusters) * seq) *
-                        sizeof(float);
-    float* kl = reinterpret_cast<float*>(ws + L.kl);
-    const char* qb = ws + L.q;
-    const char* kcb = static_cast<const char*>(k_cache);
-    if (bf16) {
-        if (head_dim == 128) hipLaunchKernelGGL((proxy_kl_kernel<true, 128>), pgrid, dim3(kPdBlock), plds, stream, qb, kcb, seq, n_clusters, n_heads, n_kv_heads, sc, scores, lse, first, kl);
-        else hipLaunchKernelGGL((proxy_kl_kernel<true, 64>), pgrid, dim3(kPdBlock), plds, stream, qb, kcb, seq, n_clusters, n_heads, n_kv_heads, sc, scores, lse, first, kl);
-    } else {
-        if (head_dim == 128) hipLaunchKernelGGL((proxy_kl_kernel<false, 128>), pgrid, dim3(kPdBlock), plds, stream, qb, kcb, seq, n_clusters, n_heads, n_kv_heads, sc, scores, lse, first, kl);
-        else hipLaunchKernelGGL((proxy_kl_kernel<false, 64>), pgrid, dim3(kPdBlock), plds, stream, qb, kcb, seq, n_clusters, n_heads, n_kv_heads, sc, scores, lse, first, kl);
-    }
-    st = launch_status();
-    if (st != POLESTAR_OK) return st;
-    hipLaunchKernelGGL(head_mean_kernel, dim3(ceil_div(BK, 256)), dim3(256), 0, stream, kl, BK, n_heads, drift);
-    return launch_status();
+    return run_qkl(bf16, batch, seq, n_clusters, n_heads, n_kv_heads, head_dim, ws + L.q,
+                   static_cast<const char*>(k_cache), scale, scores, lse, first,
+                   reinterpret_cast<float*>(ws + L.part), drift, stream);
+}
+
+extern "C" size_t polestar_attention_drift_workspace_size(int batch, int seq, int n_rows, int n_heads) {
+    using namespace ps;
+    if (batch <= 0 || seq <= 0 || n_rows <= 0 || n_heads <= 0) return 0;
+    return qkl_plan(batch, seq, n_rows, n_heads).part_bytes;
+}
+
+// Drift of the attention distributions of given query rows (the commit drift
+// of Alg. 1 for the block's queries of the last layer).
+extern "C" polestar_status polestar_attention_drift(polestar_dtype dtype, int batch, int seq, int n_rows,
+                                                    int n_heads, int n_kv_heads, int head_dim, const void* q,
+                                                    const void* k_cache, float scale, float* scores, float* lse,
+                                                    int first, float* drift, void* workspace,
+                                                    size_t workspace_bytes, hipStream_t stream) {
+    using namespace ps;
+    if (!dtype_ok(dtype) || batch <= 0 || seq <= 0 || n_rows <= 0 || n_heads <= 0 || n_kv_heads <= 0 ||
+        head_dim <= 0 || n_heads % n_kv_heads != 0 || !q || !k_cache || !scores || !lse || !drift)
+        return POLESTAR_ERR_INVALID_ARGUMENT;
+    if ((head_dim != 64 && head_dim != 128) || n_rows > kQkMaxRows || !aligned16(q) || !aligned16(k_cache) ||
+        batch > 65535 || n_heads > 65535)
+        return POLESTAR_ERR_UNSUPPORTED;
+    const QklPlan p = qkl_plan(batch, seq, n_rows, n_heads);
+    if (workspace_bytes < p.part_bytes || !workspace) return POLESTAR_ERR_WORKSPACE;
+    return run_qkl(dtype == POLESTAR_BF16, batch, seq, n_rows, n_heads, n_kv_heads, head_dim,
+                   static_cast<const char*>(q), static_cast<const char*>(k_cache), scale, scores, lse, first,
+                   static_cast<float*>(workspace), drift, stream);
 }
 
 extern "C" polestar_status polestar_cluster_select(int batch, int seq, const int32_t* labels, int n_clusters,

@@ -99,6 +99,10 @@ def lib() -> ctypes.CDLL:
     L.polestar_commit.argtypes = [I, I, I, I, P, P, P, I, I, P, P, I, I, F, F, I, P, P, P, P, Z, P]
     L.polestar_suffix_commit.restype = S
     L.polestar_suffix_commit.argtypes = [I, I, I, I, P, P, P, I, F, P, P, P, P, Z, P]
+    L.polestar_attention_drift_workspace_size.restype = Z
+    L.polestar_attention_drift_workspace_size.argtypes = [I, I, I, I]
+    L.polestar_attention_drift.restype = S
+    L.polestar_attention_drift.argtypes = [I, I, I, I, I, I, I, P, P, F, P, P, I, P, P, Z, P]
     Lg = ctypes.c_long
     L.polestar_embed.restype = S
     L.polestar_embed.argtypes = [I, I, I, I, P, I, I, P, I, P, P, P]
@@ -457,6 +461,29 @@ def proxy_drift(sums: torch.Tensor, counts: torch.Tensor, w_q: torch.Tensor, k_c
         _ptr(w_q, k_cache.dtype), _ptr(k_cache), float(scale), _ptr(scores, torch.float32),
         _ptr(lse, torch.float32), int(bool(first)), _ptr(drift_out, torch.float32), _ptr(ws), nbytes,
         _stream(stream)))
+    return drift_out
+
+
+def attention_drift_workspace_size(batch: int, seq: int, n_rows: int, n_heads: int) -> int:
+    return lib().polestar_attention_drift_workspace_size(batch, seq, n_rows, n_heads)
+
+
+def attention_drift(q: torch.Tensor, k_cache: torch.Tensor, scores: torch.Tensor, lse: torch.Tensor, first: bool,
+                    drift_out: torch.Tensor | None = None, scale: float = 0.0,
+                    workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """KL of each query row's attention distribution against the previous
+    step's, averaged over heads -> [batch][n_rows]; scores [b][R][H][seq] and
+    lse [b][R][H] are the previous step's on entry and this step's on return."""
+    b, R, H, hd = q.shape
+    _, seq, kvh, _ = k_cache.shape
+    if drift_out is None:
+        drift_out = torch.empty((b, R), dtype=torch.float32, device=q.device)
+    ws = _workspace(attention_drift_workspace_size(b, seq, R, H), q.device, workspace)
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check("polestar_attention_drift", lib().polestar_attention_drift(
+        _dtype_code(q), b, seq, R, H, kvh, hd, _ptr(q), _ptr(k_cache, q.dtype), float(scale),
+        _ptr(scores, torch.float32), _ptr(lse, torch.float32), int(bool(first)), _ptr(drift_out, torch.float32),
+        _ptr(ws), nbytes, _stream(stream)))
     return drift_out
 
 

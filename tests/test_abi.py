@@ -29,7 +29,7 @@ def _header_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = _header_functions()
-    assert len(names) == 27, names
+    assert len(names) == 29, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -184,6 +184,25 @@ def test_model_entry_validation(L):
     assert L.polestar_copy_rows(1, 2, 96, 256, FAKE, FAKE, None, None, 4, 0, 32, None) == INVALID
     assert L.polestar_copy_rows(1, 2, 96, 4, FAKE, FAKE, None, None, 0, 0, 32, None) == UNSUPPORTED
     assert L.polestar_copy_rows(1, 2, 96, 256, FAKE, FAKE, None, None, 0, 80, 32, None) == INVALID
+
+
+def test_attention_drift_validation(L):
+    f = L.polestar_attention_drift
+    ws = ps.attention_drift_workspace_size(1, 768, 32, 32)
+    assert ws > 0
+    args = [1, 1, 768, 32, 32, 32, 128, FAKE, FAKE, 0.0, FAKE, FAKE, 0, FAKE, FAKE, ws, None]
+    a = list(args); a[12 + 1] = None
+    assert f(*a) == INVALID                                   # drift output required
+    a = list(args); a[5] = 5
+    assert f(*a) == INVALID                                   # heads not a multiple of kv heads
+    a = list(args); a[3] = 65
+    assert f(*a) == UNSUPPORTED                               # more than 64 query rows
+    a = list(args); a[6] = 96
+    assert f(*a) == UNSUPPORTED
+    a = list(args); a[7] = MISALIGNED
+    assert f(*a) == UNSUPPORTED
+    a = list(args); a[15] = ws - 1
+    assert f(*a) == WORKSPACE
 
 
 def test_step_validation_and_workspace(L):

@@ -273,3 +273,38 @@ def test_proxy_pipeline_end_to_end(P):
     k_want = ref.round_to((h_cur @ dec["w_k"].T).reshape(shape), "bf16")
     for r in rows:
         assert np.abs(kr[0, r] - k_want[0, r]).max() <= 2 ** -7 * np.abs(k_want[0, r]).max() + 1e-6
+
+
+@pytest.mark.parametrize("dtype,b,seq,R,H,Hkv,hd", [
+    ("bf16", 1, 768, 32, 32, 32, 128),     # the block's queries of the LLaDA-8B-shaped layer
+    ("bf16", 4, 2048, 64, 28, 4, 128),     # Dream-7B GQA block of 64, long cache
+    ("fp32", 2, 100, 5, 4, 2, 64),         # ragged key tile, few rows
+])
+def test_attention_drift_matches_oracle(P, dtype, b, seq, R, H, Hkv, hd):
+    torch = _torch()
+    g = np.random.default_rng(17)
+    st = lambda a: inputs.store(a.astype(np.float32), dtype)
+    q = st(g.standard_normal((b, R, H, hd)) * 0.5)
+    k0 = st(g.standard_normal((b, seq, Hkv, hd)) * 0.5)
+    k1f = ref.decode(k0, dtype).copy()
+    rows = g.choice(seq, size=seq // 10, replace=False)
+    k1f[:, rows] += g.standard_normal((b, len(rows), Hkv, hd)) * 0.3    # a refresh changed some keys
+    k1 = st(k1f)
+    qd, k0d, k1d = ref.decode(q, dtype), ref.decode(k0, dtype), ref.decode(k1, dtype)
+    scores = torch.empty((b, R, H, seq), dtype=torch.float32, device="cuda")
+    lse = torch.empty((b, R, H), dtype=torch.float32, device="cuda")
+    qt = to_dev(q, dtype)
+    d0 = P.attention_drift(qt, to_dev(k0, dtype), scores, lse, True)
+    s0 = pr.query_scores(qd, k0d)
+    assert np.all(from_dev(d0) == 0.0)
+    np.testing.assert_allclose(from_dev(scores), s0, rtol=1e-4, atol=1e-4 * np.abs(s0).max())
+    np.testing.assert_allclose(from_dev(lse), pr.log_sum_exp(s0), rtol=1e-4, atol=1e-5)
+    d1 = P.attention_drift(qt, to_dev(k1, dtype), scores, lse, False)
+    s1 = pr.query_scores(qd, k1d)
+    want = pr.attention_drift(s1, s0)
+    assert want.min() > 1e-5
+    np.testing.assert_allclose(from_dev(d1), want, rtol=2e-3, atol=1e-6)
+    np.testing.assert_allclose(from_dev(scores), s1, rtol=1e-4, atol=1e-4 * np.abs(s1).max())
+    # an unchanged cache gives (numerically) zero drift
+    d2 = P.attention_drift(qt, to_dev(k1, dtype), scores, lse, False)
+    assert np.abs(from_dev(d2)).max() < 1e-5
