@@ -186,9 +186,9 @@ def window(prompt_len: int, block_len: int, seq: int, b: int, prefix: int, suffi
     return max(0, s - prefix), min(seq, e + suffix)
 
 
-def window_top_k(lo: int, hi: int, block_len: int) -> int:
-    """M-9: ceil(|Omega| / 2), Omega = R minus the block."""
-    return int(math.ceil((hi - lo - block_len) / 2))
+def window_top_k(lo: int, hi: int, block_len: int, frac: float = 0.5) -> int:
+    """M-9: ceil(frac * |Omega|), Omega = R minus the block (frac 1/2 by default)."""
+    return int(math.ceil(frac * (hi - lo - block_len)))
 
 
 def refreshes(committed_since: int, tau_upd: int) -> bool:
@@ -214,6 +214,7 @@ class LoopParams:
     tau_s: float = 0.9
     force_one: bool = True
     suffix_commit: bool = True
+    window_frac: float = 0.5        # share of the window a refreshing step re-projects (window flow)
 
 
 @dataclass
@@ -261,7 +262,7 @@ def generate(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams) -> 
         while (y[:, bs:be] == mask).any():
             refresh = refreshes(int(since.max()), p.tau_upd)
             rlo, rhi = (lo, hi) if refresh else (bs, be)
-            kt = window_top_k(lo, hi, p.block_len) if refresh else 0
+            kt = window_top_k(lo, hi, p.block_len, p.window_frac) if refresh else 0
             x = embed(weights["tok_emb"], weights["pos_emb"], y, rlo, rhi)
             last = None
             for li in range(shape.n_layers):
@@ -288,6 +289,226 @@ def generate(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams) -> 
                 n_commit = n_commit + scm.sum(axis=1)
             tr.forwards.append(dict(kind="refresh" if refresh else "plain", block=blk, rows=(rlo, rhi),
                                     commit=cm, token=tok, suffix_commit=scm))
+            tr.committed += int(n_commit.sum())
+            since = n_commit if refresh else since + n_commit
+    return y, tr
+
+
+# ---------------------------------------------------------------------------
+# The paper's own flow (Alg. 1, per-layer loop; Sec. 4.1 "Measuring Drift and
+# Layer-wise KV Updates"): clustered proxy drift per layer and update packets
+# passed from layer to layer.  Readings (also listed in the design doc):
+#   F3-1  each layer caches its inputs X (the residual stream, kept exact
+#         here, fp32 on the GPU) besides K/V and H = RMSNorm(X); the local
+#         window's H is clustered per layer at block entry (proxy_ref), and
+#         the proxy scores of that entry are the first P;
+#   F3-2  on a refreshing step (the tau_upd schedule), layer l: (1) patches
+#         the rows of the packet U(l) it receives -- X and H of those rows,
+#         their K/V and the cluster sums; (2) forwards the block; (3) takes
+#         the proxy drift of its clusters against its last P and the members
+#         of the top-k clusters as S(l); (4) forwards the rows S(l) from their
+#         cached inputs, and their outputs are the packet U(l + 1);
+#   F3-3  the packet of layer 0 holds the window rows whose token a suffix
+#         commit changed since the last refreshing forward (new embeddings);
+#   F3-4  a plain step forwards the block only; the commit drift of the
+#         block is the attention drift of its queries at the last layer
+#         (proxy_ref.attention_drift), measured every forward after the entry
+#         set its baseline; the suffix commit reads the last layer's packet
+#         rows that lie in the suffix window.
+# ---------------------------------------------------------------------------
+
+from oracle import proxy_ref as pr
+
+
+@dataclass
+class PacketLayer:
+    st: LayerState                 # K, V, H (= rounded RMSNorm of X)
+    x: np.ndarray                  # [b][S][d] cached layer inputs
+    labels: np.ndarray             # [b][S] cluster of each window position, -1 elsewhere
+    sums: np.ndarray               # [b][K][d] sums of the members' H
+    counts: np.ndarray             # [b][K]
+    scores: np.ndarray             # [b][K][H][S] last proxy scores
+
+
+def patch(pl: PacketLayer, rows, x_new: np.ndarray, w: dict, shape: Shape) -> PacketLayer:
+    """F3-2 (1): rows[b] = list of positions, x_new[b][i] their new inputs."""
+    dt = shape.dtype
+    k, v, h = (np.array(a, copy=True) for a in (pl.st.k, pl.st.v, pl.st.h))
+    x = np.array(pl.x, copy=True)
+    sums = np.array(pl.sums, copy=True)
+    H, hd = shape.n_heads, shape.head_dim
+    for s in range(x.shape[0]):
+        for i, p in enumerate(rows[s]):
+            hn = ref.round_to(rmsnorm(x_new[s][i]), dt)
+            lab = int(pl.labels[s, p])
+            if lab >= 0:
+                sums[s, lab] += hn - h[s, p]                       # P-6
+            h[s, p] = hn
+            x[s, p] = x_new[s][i]
+            k[s, p] = ref.round_to(hn @ w["w_k"].T, dt).reshape(H, hd)
+            v[s, p] = ref.round_to(hn @ w["w_v"].T, dt).reshape(H, hd)
+    return PacketLayer(LayerState(k, v, h), x, pl.labels, sums, pl.counts, pl.scores)
+
+
+def sparse_forward(pl: PacketLayer, rows, w: dict, shape: Shape) -> list:
+    """F3-2 (4): the rows' outputs of this layer from their cached inputs,
+    attending over the current cache; returns x_out[b] = [n_b][d]."""
+    dt = shape.dtype
+    out = []
+    for s in range(pl.x.shape[0]):
+        r = np.asarray(rows[s], np.int64)
+        if r.size == 0:
+            out.append(np.zeros((0, shape.d)))
+            continue
+        xr = pl.x[s, r][None]
+        h = ref.round_to(rmsnorm(xr), dt)
+        q = ref.round_to(h @ w["w_q"].T, dt).reshape(1, r.size, shape.n_heads, shape.head_dim)
+        o, _ = ref.attend(q, pl.st.k[s:s + 1], pl.st.v[s:s + 1])
+        o = ref.round_to(o, dt).reshape(1, r.size, -1)
+        xx = xr + ref.round_to(o @ w["w_o"].T, dt)
+        g = ref.round_to(rmsnorm(xx), dt)
+        gu = ref.round_to(g @ w["w_gu"].T, dt)
+        a = ref.round_to(silu(gu[..., :shape.ffn]) * gu[..., shape.ffn:], dt)
+        out.append((xx + ref.round_to(a @ w["w_down"].T, dt))[0])
+    return out
+
+
+def proxy_select(pl: PacketLayer, w: dict, shape: Shape, k_top: int):
+    """F3-2 (3): drift per cluster against the last proxy scores, the top
+    k_top clusters and their member rows; returns (drift, rows, new scores)."""
+    tok = pr.proxy_tokens(pl.sums, pl.counts, shape.dtype)
+    sc = pr.proxy_scores(tok, w["w_q"], pl.st.k, shape.n_heads, shape.dtype)
+    drift = pr.proxy_kl(sc, pl.scores)
+    sel = pr.select_clusters(drift, k_top)
+    idx, cnt = pr.cluster_members(pl.labels, sel)
+    rows = [list(idx[s, :cnt[s]]) for s in range(idx.shape[0])]
+    return drift, rows, sc
+
+
+def _window_positions(lo: int, bs: int, be: int, hi: int) -> np.ndarray:
+    return np.concatenate([np.arange(lo, bs), np.arange(be, hi)]).astype(np.int64)
+
+
+def cluster_layer(h: np.ndarray, win: np.ndarray, n_clusters: int, iters: int):
+    """Spherical K-means of every sequence's window rows of H (F3-1):
+    (labels by position [b][S], sums [b][K][d], counts [b][K])."""
+    b, seq, d = h.shape
+    labels = np.full((b, seq), -1, np.int64)
+    sums = np.zeros((b, n_clusters, d))
+    counts = np.zeros((b, n_clusters), np.int64)
+    for s in range(b):
+        lab, _ = pr.spherical_kmeans(h[s, win], n_clusters, iters)
+        sums[s], counts[s] = pr.cluster_sums(h[s, win], lab, n_clusters)
+        labels[s] = pr.labels_by_position(win, lab, seq)
+    return labels, sums, counts
+
+
+def block_queries(h_block: np.ndarray, w_q: np.ndarray, shape: Shape) -> np.ndarray:
+    """The block's rounded queries [b][B][H][hd] from its rows of H."""
+    b, n, _ = h_block.shape
+    return ref.round_to(h_block @ w_q.T, shape.dtype).reshape(b, n, shape.n_heads, shape.head_dim)
+
+
+def generate_packets(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams, n_clusters: int = 8,
+                     k_top: int = 4, iters: int = 10) -> tuple[np.ndarray, Trace]:
+    """The loop of Alg. 1 with update packets and proxy drift (F3-1..F3-4)."""
+    b = prompt.shape[0]
+    seq = p.prompt_len + p.gen_len
+    assert seq == shape.seq
+    dt, mask, L = shape.dtype, shape.mask_id, shape.n_layers
+    y = np.full((b, seq), mask, np.int64)
+    y[:, :p.prompt_len] = prompt
+    hd, H = shape.head_dim, shape.n_heads
+    zeros = lambda *s: np.zeros(s)
+    layers = [PacketLayer(LayerState(zeros(b, seq, H, hd), zeros(b, seq, H, hd), zeros(b, seq, shape.d)),
+                          zeros(b, seq, shape.d), np.full((b, seq), -1, np.int64), zeros(b, n_clusters, shape.d),
+                          np.zeros((b, n_clusters), np.int64), zeros(b, n_clusters, H, seq))
+              for _ in range(L)]
+    tr = Trace()
+    hist = np.zeros((b, max(p.h, 1), p.block_len), np.float32)
+    for blk in range(p.gen_len // p.block_len):
+        bs, be = block_bounds(p.prompt_len, p.block_len, blk)
+        lo, hi = window(p.prompt_len, p.block_len, seq, blk, p.prefix, p.suffix)
+        win = _window_positions(lo, bs, be, hi)
+        elo, ehi = (0, seq) if blk % 2 == 0 else (lo, hi)
+        x = embed(weights["tok_emb"], weights["pos_emb"], y, elo, ehi)
+        for li in range(L):
+            w = weights["layers"][li]
+            r = layer_forward(x, elo, w, layers[li].st, mode="all", block=(bs, p.block_len), shape=shape)
+            xc = np.array(layers[li].x, copy=True)
+            xc[:, elo:ehi] = x
+            st = r["state"]
+            labels, sums, counts = cluster_layer(st.h, win, n_clusters, iters)
+            sc0 = pr.proxy_scores(pr.proxy_tokens(sums, counts, dt), w["w_q"], st.k, H, dt)
+            layers[li] = PacketLayer(st, xc, labels, sums, counts, sc0)
+            if li == L - 1:
+                att = pr.query_scores(block_queries(r["h"][:, bs - elo:be - elo], w["w_q"], shape), st.k)
+            x = r["x_out"]
+        lg = logits(x[:, bs - elo:be - elo], weights["w_lm"], dt)
+        tok, conf = ref.confidence(lg, mask)
+        masked = y[:, bs:be] == mask
+        cm = masked & (conf.astype(np.float32) > np.float32(p.tau_s))
+        y[:, bs:be] = np.where(cm, tok, y[:, bs:be])
+        tr.forwards.append(dict(kind="entry_full" if blk % 2 == 0 else "entry_window", block=blk,
+                                rows=(elo, ehi), commit=cm, token=tok))
+        tr.committed += int(cm.sum())
+        since = cm.sum(axis=1)
+        hist_len = np.zeros(b, np.int32)
+        dirty = [[] for _ in range(b)]
+        while (y[:, bs:be] == mask).any():
+            refresh = refreshes(int(since.max()), p.tau_upd)
+            x = embed(weights["tok_emb"], weights["pos_emb"], y, bs, be)
+            pkt_rows = dirty if refresh else [[] for _ in range(b)]
+            pkt_x = [weights["tok_emb"][y[s, pkt_rows[s]]] + weights["pos_emb"][pkt_rows[s]] for s in range(b)]
+            proxy = []                       # per layer: (drift per cluster, the proxy scores it measured)
+            for li in range(L):
+                w = weights["layers"][li]
+                pl = layers[li]
+                if refresh and any(len(rr) for rr in pkt_rows):
+                    pl = patch(pl, pkt_rows, pkt_x, w, shape)
+                # (X of the block rows is not kept: packets carry window rows only,
+                # and the next block entry rewrites X of this block)
+                r = layer_forward(x, bs, w, pl.st, mode="plain", block=(bs, p.block_len), shape=shape)
+                pl = PacketLayer(r["state"], pl.x, pl.labels, pl.sums, pl.counts, pl.scores)
+                if refresh:
+                    pdrift, rows, sc = proxy_select(pl, w, shape, k_top)
+                    proxy.append((pdrift, sc))
+                    pl = PacketLayer(pl.st, pl.x, pl.labels, pl.sums, pl.counts, sc)
+                    pkt_x = sparse_forward(pl, rows, w, shape)
+                    pkt_rows = rows
+                layers[li] = pl
+                if li == L - 1:
+                    att_new = pr.query_scores(block_queries(r["h"], w["w_q"], shape), pl.st.k)
+                    delta = pr.attention_drift(att_new, att).astype(np.float32)
+                    att = att_new
+                x = r["x_out"]
+            lg = logits(x, weights["w_lm"], dt)
+            tok, conf = ref.confidence(lg, mask)
+            masked = y[:, bs:be] == mask
+            cm, hist, hist_len = ref.commit_rule(conf.astype(np.float32), delta, masked, hist, hist_len, p.h,
+                                                 p.tau_s, p.alpha, p.force_one)
+            y[:, bs:be] = np.where(cm, tok, y[:, bs:be])
+            n_commit = cm.sum(axis=1)
+            scm = None
+            if p.suffix_commit and refresh and be < hi:
+                n_s = hi - be
+                el = np.zeros((b, n_s), bool)
+                slg = np.zeros((b, n_s, shape.vocab))
+                for s in range(b):
+                    for i, pos in enumerate(pkt_rows[s]):
+                        if be <= pos < hi:
+                            el[s, pos - be] = True
+                            slg[s, pos - be] = logits(pkt_x[s][i][None, None], weights["w_lm"], dt)[0, 0]
+                stok, sconf = ref.confidence(slg, mask)
+                smask = y[:, be:hi] == mask
+                scm = ref.suffix_commit_rule(sconf.astype(np.float32), smask, el, p.tau_s)
+                y[:, be:hi] = np.where(scm, stok, y[:, be:hi])
+                n_commit = n_commit + scm.sum(axis=1)
+            if refresh:      # F3-3: the rows this step's suffix commit changed go to the next layer-0 packet
+                dirty = [[] for _ in range(b)] if scm is None else \
+                    [[int(be + j) for j in np.flatnonzero(scm[s])] for s in range(b)]
+            tr.forwards.append(dict(kind="refresh" if refresh else "plain", block=blk, rows=(bs, be),
+                                    commit=cm, token=tok, suffix_commit=scm, proxy=proxy))
             tr.committed += int(n_commit.sum())
             since = n_commit if refresh else since + n_commit
     return y, tr

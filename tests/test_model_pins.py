@@ -10,6 +10,7 @@ import pytest
 
 from oracle import model_ref as mr
 from oracle import polestar_ref as ref
+from oracle import proxy_ref as pr
 
 
 def rand_weights(shape: mr.Shape, seed=0, std=0.3, lm_std=None):
@@ -178,3 +179,99 @@ def test_free_running_loop_invariants():
         # force_one: every within-block step commits at least one token per unfinished sequence
         assert f["commit"].any(axis=1).sum() >= 1
     assert len(tr.forwards) < 2 * 32                 # some steps commit several tokens
+
+
+# ---------------------------------------------------------------------------
+# the update-packet flow (Alg. 1 per-layer loop)
+# ---------------------------------------------------------------------------
+
+def _packet_layer_from_full(shape, seed, lo, bs, be, hi, K=2):
+    wts = rand_weights(shape, seed=seed)
+    g = np.random.default_rng(seed + 1)
+    x = g.standard_normal((1, shape.seq, shape.d))
+    full = mr.layer_forward(x, 0, wts["layers"][0], empty_state(1, shape), mode="all", block=(bs, be - bs),
+                            shape=shape)
+    win = mr._window_positions(lo, bs, be, hi)
+    labels, sums, counts = mr.cluster_layer(full["state"].h, win, K, 10)
+    pl = mr.PacketLayer(full["state"], x.copy(), labels, sums, counts,
+                        np.zeros((1, K, shape.n_heads, shape.seq)))
+    return wts["layers"][0], x, full, pl
+
+
+def test_packet_rows_forward_against_a_consistent_cache_reproduces_the_full_forward():
+    shape = mr.Shape(n_layers=1, d=16, n_heads=2, head_dim=8, ffn=12, vocab=16, seq=20)
+    w, x, full, pl = _packet_layer_from_full(shape, 21, 2, 8, 12, 16)
+    rows = [[3, 9, 14, 17]]
+    out = mr.sparse_forward(pl, rows, w, shape)
+    np.testing.assert_array_equal(out[0], full["x_out"][0, rows[0]])
+
+
+def test_patch_with_unchanged_inputs_changes_nothing_and_sums_track_the_window():
+    shape = mr.Shape(n_layers=1, d=16, n_heads=2, head_dim=8, ffn=12, vocab=16, seq=20)
+    w, x, full, pl = _packet_layer_from_full(shape, 23, 2, 8, 12, 16)
+    same = mr.patch(pl, [[3, 13]], [x[0, [3, 13]]], w, shape)
+    for a, b in ((same.st.k, pl.st.k), (same.st.v, pl.st.v), (same.st.h, pl.st.h), (same.x, pl.x), (same.sums, pl.sums)):
+        np.testing.assert_array_equal(a, b)
+    g = np.random.default_rng(5)
+    new = x[0, [3, 13]] + g.standard_normal((2, shape.d))
+    pt = mr.patch(pl, [[3, 13]], [new], w, shape)
+    win = mr._window_positions(2, 8, 12, 16)
+    lab_w = pl.labels[0, win]
+    want, _ = pr.cluster_sums(pt.st.h[0, win], lab_w, 2)
+    np.testing.assert_allclose(pt.sums[0], want, atol=1e-12)
+    hn = ref.round_to(mr.rmsnorm(new), shape.dtype)
+    np.testing.assert_array_equal(pt.st.h[0, [3, 13]], hn)
+    np.testing.assert_array_equal(pt.st.k[0, 3].reshape(-1), ref.round_to(hn[0] @ w["w_k"].T, shape.dtype))
+
+
+def test_proxy_select_with_unchanged_scores_picks_the_lowest_clusters():
+    shape = mr.Shape(n_layers=1, d=16, n_heads=2, head_dim=8, ffn=12, vocab=16, seq=20)
+    w, x, full, pl = _packet_layer_from_full(shape, 25, 2, 8, 12, 16, K=3)
+    tok = pr.proxy_tokens(pl.sums, pl.counts, shape.dtype)
+    pl.scores[:] = pr.proxy_scores(tok, w["w_q"], pl.st.k, shape.n_heads, shape.dtype)
+    drift, rows, sc = mr.proxy_select(pl, w, shape, 2)
+    assert np.all(drift == 0.0)
+    members = sorted(int(p) for p in np.flatnonzero((pl.labels[0] == 0) | (pl.labels[0] == 1)))
+    assert rows[0] == members
+
+
+def test_packet_flow_selecting_every_cluster_equals_the_window_flow():
+    # with every window row in every packet, a refreshing step of the packet
+    # flow computes what the window flow's full-window forward does; drift
+    # commits are off (their deltas are measured differently), so both loops
+    # must decode the same tokens through the same forwards
+    shape = mr.Shape(n_layers=2, d=32, n_heads=2, head_dim=16, ffn=48, vocab=48, seq=40)
+    wts = rand_weights(shape, seed=31, lm_std=0.6)
+    prompt = np.random.default_rng(32).integers(0, shape.vocab - 1, size=(2, 8))
+    common = dict(prompt_len=8, gen_len=32, block_len=8, prefix=16, suffix=8, tau_upd=1, h=2, alpha=1e9)
+    y1, t1 = mr.generate(wts, prompt, shape, mr.LoopParams(window_frac=1.0, **common))
+    y2, t2 = mr.generate_packets(wts, prompt, shape, mr.LoopParams(**common), n_clusters=3, k_top=3)
+    assert [f["kind"] for f in t1.forwards] == [f["kind"] for f in t2.forwards]
+    assert np.array_equal(y1, y2)
+    assert any(f["kind"] == "refresh" for f in t2.forwards)
+    assert any(f.get("suffix_commit") is not None and f["suffix_commit"].any() for f in t2.forwards)
+
+
+def test_packet_flow_loop_invariants():
+    shape = mr.Shape(n_layers=2, d=32, n_heads=2, head_dim=16, ffn=48, vocab=48, seq=40)
+    wts = rand_weights(shape, seed=11, lm_std=0.6)
+    prompt = np.random.default_rng(12).integers(0, shape.vocab - 1, size=(2, 8))
+    p = mr.LoopParams(prompt_len=8, gen_len=32, block_len=8, prefix=16, suffix=8, tau_upd=1, h=2)
+    y, tr = mr.generate_packets(wts, prompt, shape, p, n_clusters=4, k_top=2)
+    assert not (y == shape.mask_id).any() and np.array_equal(y[:, :8], prompt)
+    assert tr.committed == 2 * 32
+    assert [f["kind"] for f in tr.forwards if f["kind"].startswith("entry")] == ["entry_full", "entry_window"] * 2
+    # D = KL(P(t) || P(t-1)): every refreshing step's drift is taken against the
+    # proxy scores of the previous refreshing step of the same block
+    prev = None
+    n_checked = 0
+    for f in tr.forwards:
+        if f["kind"].startswith("entry"):
+            prev = None
+        elif f["kind"] == "refresh":
+            if prev is not None:
+                for li, (d, sc) in enumerate(f["proxy"]):
+                    np.testing.assert_allclose(d, pr.proxy_kl(sc, prev[li][1]), rtol=1e-12, atol=1e-15)
+                    n_checked += 1
+            prev = f["proxy"]
+    assert n_checked > 0
