@@ -68,6 +68,8 @@ def parse():
     p.add_argument("--stack", type=int, default=None,
                    help="run the denoising loop of a whole layer stack (4: LLaDA-8B-shaped, 32 layers, batch 16) "
                         "once and print its tokens/s and tokens per forward instead of the layer-step benchmark")
+    p.add_argument("--flow", default="window", choices=("window", "packet"),
+                   help="--stack: window forwards with per-token drift, or the update-packet flow with proxy drift")
     return p.parse_args()
 
 
@@ -308,7 +310,7 @@ def cpu_baseline(cfg, x, k, budget_s):
                       f"attention, commit) of the benchmarked workload, {t_total:.1f} s"}
 
 
-def stack_bench(index, P, torch):
+def stack_bench(index, P, torch, flow="window"):
     """The loop of Alg. 1 on a whole stack with random weights: weights are
     drawn on the host (one thread per matrix) and uploaded as they complete,
     then one full generation is timed (wall clock around the loop, GPU time
@@ -342,7 +344,7 @@ def stack_bench(index, P, torch):
             if done % 24 == 0:
                 print(f"weights {done}/{len(jobs)} ({time.perf_counter() - t0:.0f} s)", file=sys.stderr, flush=True)
     shape = model.ModelShape(cfg.n_layers, cfg.d, cfg.n_heads, cfg.head_dim, cfg.ffn, cfg.vocab, cfg.seq)
-    lc = model.LoopConfig(prompt_len=cfg.prompt_len, gen_len=cfg.gen_len, block_len=cfg.block_len)
+    lc = model.LoopConfig(prompt_len=cfg.prompt_len, gen_len=cfg.gen_len, block_len=cfg.block_len, flow=flow)
     den = model.Denoiser(w, shape, cfg.batch, lc)
     print(f"weights ready ({time.perf_counter() - t0:.0f} s); generating", file=sys.stderr, flush=True)
     y, st = den.generate(inputs.stack_prompt(cfg), progress=lambda blk, f: print(
@@ -356,6 +358,7 @@ def stack_bench(index, P, torch):
            "config": {"workload": f"{cfg.name}: {cfg.n_layers} layers, d {cfg.d}, {cfg.n_heads}x{cfg.head_dim} MHA, "
                                   f"SwiGLU {cfg.ffn}, vocab {cfg.vocab}, batch {cfg.batch}, prompt {cfg.prompt_len}, "
                                   f"{cfg.gen_len} generated in blocks of {cfg.block_len}, random N(0, 0.02) weights",
+                      "flow": flow,
                       "global_batch": cfg.batch, "seq_len": cfg.seq},
            "tpf": round(st["tpf"], 3), "forwards": st["forwards"], "committed": st["committed"],
            "suffix_committed": st["suffix_committed"], "seconds": round(st["seconds"], 3),
@@ -389,7 +392,7 @@ def main():
         build.build(verbose=False)
     P.lib()
     if args.stack is not None:
-        return stack_bench(args.stack, P, torch)
+        return stack_bench(args.stack, P, torch, args.flow)
 
     cfg = inputs.CONFIGS[args.config]
     x = inputs.layer_inputs(cfg, args.subrun)

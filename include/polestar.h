@@ -461,6 +461,25 @@ polestar_status polestar_copy_rows(polestar_dtype dtype, int batch, int seq, int
                                    int k_max, int block_start, int block_len, hipStream_t stream);
 
 /*
+ * polestar_gather_rows / polestar_scatter_rows -- move the rows an update
+ * packet carries (Alg. 1: the sparse forward of the selected rows and the
+ * next layer's patch) between a [batch][seq] array and a compact
+ * [batch][k_max] one; rows are row_bytes bytes (any element type).
+ *   gather : dst[b][r] = src[b][idx[b][r]] for r < count[b]; zero rows for
+ *            r in [count[b], k_max) and for entries outside [0, seq)
+ *   scatter: dst[b][idx[b][r]] = src[b][r] for r < count[b]; entries
+ *            outside [0, seq) are skipped (distinct entries expected)
+ *   idx : [batch][k_max] int32, count : [batch] int32 (clamped to [0, k_max])
+ * UNSUPPORTED unless row_bytes % 16 == 0 and src, dst are 16-byte aligned.
+ */
+polestar_status polestar_gather_rows(int batch, int seq, int row_bytes, const void* src,
+                                     const int32_t* idx, const int32_t* count, int k_max, void* dst,
+                                     hipStream_t stream);
+polestar_status polestar_scatter_rows(int batch, int seq, int row_bytes, const void* src,
+                                      const int32_t* idx, const int32_t* count, int k_max, void* dst,
+                                      hipStream_t stream);
+
+/*
  * polestar_step -- one whole layer step: polestar_drift, polestar_select,
  * polestar_refresh_kv, polestar_project_q, polestar_attend (queries from q)
  * and polestar_commit (with the drift branch on), with exactly their

@@ -137,6 +137,36 @@ __global__ __launch_bounds__(kRowBlock) void copy_rows_kernel(const char* __rest
         st16(dst + off + c, ld16(src + off + c));
 }
 
+// dst[b][r] = src[b][idx[b][r]] for r < count[b] (entries outside [0, seq)
+// give zero rows), zero rows for r in [count[b], k_max); grid (k_max, batch)
+__global__ __launch_bounds__(kRowBlock) void gather_rows_kernel(const char* __restrict__ src, char* __restrict__ dst,
+                                                                int seq, int row_bytes, const int32_t* __restrict__ idx,
+                                                                const int32_t* __restrict__ count, int k_max) {
+    const int r = blockIdx.x, b = blockIdx.y;
+    const int cnt = min(max(count[b], 0), k_max);
+    const int p = r < cnt ? idx[static_cast<size_t>(b) * k_max + r] : -1;
+    const bool ok = p >= 0 && p < seq;
+    const char* s = src + (static_cast<size_t>(b) * seq + (ok ? p : 0)) * row_bytes;
+    char* d = dst + (static_cast<size_t>(b) * k_max + r) * row_bytes;
+    for (int c = 16 * threadIdx.x; c < row_bytes; c += 16 * kRowBlock)
+        st16(d + c, ok ? ld16(s + c) : make_uint4(0u, 0u, 0u, 0u));
+}
+
+// dst[b][idx[b][r]] = src[b][r] for r < count[b] (entries outside [0, seq)
+// skipped); grid (k_max, batch)
+__global__ __launch_bounds__(kRowBlock) void scatter_rows_kernel(const char* __restrict__ src, char* __restrict__ dst,
+                                                                 int seq, int row_bytes, const int32_t* __restrict__ idx,
+                                                                 const int32_t* __restrict__ count, int k_max) {
+    const int r = blockIdx.x, b = blockIdx.y;
+    const int cnt = min(max(count[b], 0), k_max);
+    if (r >= cnt) return;
+    const int p = idx[static_cast<size_t>(b) * k_max + r];
+    if (p < 0 || p >= seq) return;
+    const char* s = src + (static_cast<size_t>(b) * k_max + r) * row_bytes;
+    char* d = dst + (static_cast<size_t>(b) * seq + p) * row_bytes;
+    for (int c = 16 * threadIdx.x; c < row_bytes; c += 16 * kRowBlock) st16(d + c, ld16(s + c));
+}
+
 int grid_for(long n4) {
     const long g = (n4 + kRowBlock - 1) / kRowBlock;
     return static_cast<int>(g < 8192 ? (g > 0 ? g : 1) : 8192);
@@ -276,4 +306,30 @@ extern "C" polestar_status polestar_linear(polestar_dtype dtype, int batch, int 
     g.ws = static_cast<float*>(workspace);
     g.m_max = batch * n_rows;
     return gemm_run(bf16, plan, g, stream);
+}
+
+extern "C" polestar_status polestar_gather_rows(int batch, int seq, int row_bytes, const void* src,
+                                                const int32_t* idx, const int32_t* count, int k_max, void* dst,
+                                                hipStream_t stream) {
+    using namespace ps;
+    if (batch <= 0 || seq <= 0 || row_bytes <= 0 || k_max < 0 || (k_max > 0 && (!src || !idx || !count || !dst)))
+        return POLESTAR_ERR_INVALID_ARGUMENT;
+    if (row_bytes % 16 != 0 || !aligned16(src) || !aligned16(dst) || batch > 65535) return POLESTAR_ERR_UNSUPPORTED;
+    if (k_max == 0) return POLESTAR_OK;
+    hipLaunchKernelGGL(gather_rows_kernel, dim3(k_max, batch), dim3(kRowBlock), 0, stream,
+                       static_cast<const char*>(src), static_cast<char*>(dst), seq, row_bytes, idx, count, k_max);
+    return launch_status();
+}
+
+extern "C" polestar_status polestar_scatter_rows(int batch, int seq, int row_bytes, const void* src,
+                                                 const int32_t* idx, const int32_t* count, int k_max, void* dst,
+                                                 hipStream_t stream) {
+    using namespace ps;
+    if (batch <= 0 || seq <= 0 || row_bytes <= 0 || k_max < 0 || (k_max > 0 && (!src || !idx || !count || !dst)))
+        return POLESTAR_ERR_INVALID_ARGUMENT;
+    if (row_bytes % 16 != 0 || !aligned16(src) || !aligned16(dst) || batch > 65535) return POLESTAR_ERR_UNSUPPORTED;
+    if (k_max == 0) return POLESTAR_OK;
+    hipLaunchKernelGGL(scatter_rows_kernel, dim3(k_max, batch), dim3(kRowBlock), 0, stream,
+                       static_cast<const char*>(src), static_cast<char*>(dst), seq, row_bytes, idx, count, k_max);
+    return launch_status();
 }

@@ -284,6 +284,9 @@ STACKS = {
     # LM head makes the confidences spread so that the commit rule decides
     40: StackConfig(40, "tiny-stack-b2", "bf16", batch=2, n_layers=2, d=256, n_heads=4, head_dim=64, ffn=768,
                     vocab=512, prompt_len=64, gen_len=64, embed_std=1.0, lm_std=0.25),
+    # the packet flow at replay size (the window K-means needs d % 512 == 0 in bf16)
+    42: StackConfig(42, "tiny-packet-stack-b2", "bf16", batch=2, n_layers=2, d=512, n_heads=8, head_dim=64,
+                    ffn=1024, vocab=512, prompt_len=64, gen_len=64, embed_std=1.0, lm_std=0.2),
 }
 
 STACK_MATRICES = ("w_q", "w_k", "w_v", "w_o", "w_gu", "w_down")

@@ -7,7 +7,7 @@ and FFN projections, SwiGLU, the residual add, the LM head, the commit
 kernels); torch only provides device buffers and copies bookkeeping values
 between host and device (the per-step commit flags, the masks).
 
-Loop (Alg. 1 with per-token drift; Sec. 4.1 "Update Schedule", Sec. 4.2):
+Window flow (Alg. 1 with per-token drift; Sec. 4.1 "Update Schedule", Sec. 4.2):
   block entry -- a full forward on even blocks, a forward of the local window
                  R = [start - prefix, end + suffix) against the cache on odd
                  ones; then the confidence-only commit of the block;
@@ -22,6 +22,17 @@ Loop (Alg. 1 with per-token drift; Sec. 4.1 "Update Schedule", Sec. 4.2):
                  the last layer refreshed.
 A layer's hidden state H (drifted, projected to K/V, cached) is the
 normalised attention input RMSNorm(x); the residual stream x is fp32.
+
+Packet flow (Alg. 1's own per-layer loop; Sec. 4.1 "Measuring Drift and
+Layer-wise KV Updates"): every layer also caches its inputs X (fp32); at
+block entry each layer's window is clustered (spherical K-means of H) and its
+proxy scores taken; on a refreshing step layer l patches the rows of the
+packet it receives (X, H, K/V, cluster sums), forwards the block, selects the
+members of its top-k clusters by proxy drift and forwards those rows from
+their cached inputs -- their outputs are the next layer's packet.  The
+commit drift is the attention drift of the block's queries at the last layer;
+the suffix commit reads the last packet; the rows it commits are the next
+refreshing step's layer-0 packet.
 """
 
 from __future__ import annotations
@@ -64,6 +75,11 @@ class LoopConfig:
     tau_s: float = P.DEFAULT_TAU_S
     force_one: bool = True
     suffix_commit: bool = True
+    window_frac: float = 0.5     # window flow: share of the window a refreshing step re-projects
+    flow: str = "window"         # "window" or "packet" (update packets between layers, proxy drift)
+    n_clusters: int = 8          # packet flow: K-means clusters per layer and window
+    k_top: int = 4               # packet flow: clusters refreshed per layer and step
+    kmeans_iters: int = 10
 
 
 def _view(buf: torch.Tensor, *shape) -> torch.Tensor:
@@ -117,7 +133,37 @@ class Denoiser:
         self.conf = z(b * nl, t=torch.float32)
         self.commit = z(b * nl, t=torch.uint8)
         self.y = z(b, S, t=torch.int32)
+        self.packet = cfg.flow == "packet"
+        if cfg.flow not in ("window", "packet"):
+            raise ValueError(f"unknown flow {cfg.flow}")
+        if self.packet:
+            K = cfg.n_clusters
+            self.kpk = max(hi - lo - B for lo, hi in self._windows())      # rows a packet can hold
+            L = sh.n_layers
+            self.X = [z(b, S, d, t=torch.float32) for _ in range(L)]      # cached layer inputs
+            self.labels = [z(b, S, t=torch.int32) for _ in range(L)]
+            self.sums = [z(b, K, d, t=torch.float32) for _ in range(L)]
+            self.counts = [z(b, K, t=torch.int32) for _ in range(L)]
+            self.pscores = [z(b, K, H, S, t=torch.float32) for _ in range(L)]
+            self.plse = [z(b, K, H, t=torch.float32) for _ in range(L)]
+            self.pdrift = z(b, K, t=torch.float32)
+            self.ascores = z(b, B, H, S, t=torch.float32)                  # last layer's block attention
+            self.alse = z(b, B, H, t=torch.float32)
+            self.delta = z(b, B, t=torch.float32)
+            self.pk_idx = [z(b, self.kpk, t=torch.int32) for _ in range(2)]
+            self.pk_cnt = [z(b, t=torch.int32) for _ in range(2)]
+            self.pk_x = [z(b, self.kpk, d, t=torch.float32) for _ in range(2)]
+            self.hnew = z(b, S, d)
+            self.hs = z(b * max(self.kpk, cfg.suffix) * d)
+            self.xsuf = z(b * cfg.suffix * d, t=torch.float32)
+            self.qJ = z(b, B, H, hd)
         self.ws = torch.empty(self._workspace_bytes(), dtype=torch.uint8, device=dev)
+
+    def _windows(self):
+        cfg, S, B = self.cfg, self.shape.seq, self.cfg.block_len
+        for blk in range(cfg.gen_len // B):
+            bs = cfg.prompt_len + blk * B
+            yield max(0, bs - cfg.prefix), min(S, bs + B + cfg.suffix)
 
     def _workspace_bytes(self) -> int:
         """The largest workspace of any call the loop makes (a GEMM plan's
@@ -125,14 +171,16 @@ class Denoiser:
         sh, cfg, b, c = self.shape, self.cfg, self.b, self.code
         S, d, H, hd, F, V, B = sh.seq, sh.d, sh.n_heads, sh.head_dim, sh.ffn, sh.vocab, cfg.block_len
         row_counts, tops, heads = {S, B}, {0}, {B}
-        for blk in range(cfg.gen_len // B):
-            bs = cfg.prompt_len + blk * B
-            lo, hi = max(0, bs - cfg.prefix), min(S, bs + B + cfg.suffix)
+        for lo, hi in self._windows():
             row_counts.add(hi - lo)
-            tops.add(int(math.ceil((hi - lo - B) / 2)))
-            if hi > bs + B:
-                heads.add(hi - bs - B)
+            tops.add(int(math.ceil(cfg.window_frac * (hi - lo - B))))
+            tops.add(hi - lo - B)                 # packet rows
+            row_counts.add(hi - lo - B)
+            heads.add(max(1, cfg.suffix))
         sizes = [256]
+        if self.packet:
+            sizes += [P.proxy_drift_workspace_size(c, b, S, d, H, hd, cfg.n_clusters),
+                      P.attention_drift_workspace_size(b, S, B, H)]
         for m in row_counts:
             sizes += [P.refresh_kv_workspace_size(c, b, d, H, hd, 0, m), P.project_q_workspace_size(c, b, d, H, hd, m),
                       P.attend_workspace_size(c, b, S, d, H, H, hd, m),
@@ -140,6 +188,8 @@ class Denoiser:
                       P.linear_workspace_size(c, b, m, d, F)]
         for k in tops:
             sizes.append(P.refresh_kv_workspace_size(c, b, d, H, hd, k, B))
+            sizes.append(P.refresh_kv_workspace_size(c, b, d, H, hd, k, 0))      # a packet's patch
+        heads |= set(range(1, cfg.suffix + 1))                                  # suffix rows of a packet
         for n in heads:
             sizes += [P.linear_workspace_size(c, b, n, V, d), P.commit_workspace_size(c, b, n, V)]
         return max(sizes)
@@ -156,46 +206,244 @@ class Denoiser:
         bs, bl = block
         x = _view(self.x, b, m, d)
         P.embed(self.y, lo, m, w["tok_emb"], w["pos_emb"], x)
+        if self.packet and mode == "all":
+            self._rng_idx, self._rng_cnt = self._range(lo, m)
+        for li in range(sh.n_layers):
+            self._layer(li, x, lo, m, mode, block, k_top, trace, fwd)
+
+    def _range(self, lo: int, m: int):
+        """Positions [lo, lo + m) of every sequence as an index list."""
+        idx = torch.from_numpy(np.tile(np.arange(lo, lo + m, dtype=np.int32), (self.b, 1))).to(self.dev)
+        return idx, torch.full((self.b,), m, dtype=torch.int32, device=self.dev)
+
+    def _layer(self, li: int, x: torch.Tensor, lo: int, m: int, mode: str, block: tuple[int, int], k_top: int,
+               trace, fwd: int) -> None:
+        """Layer li over the rows [lo, lo + m) whose inputs x [b][m][d] hold; x
+        receives the outputs."""
+        sh, b, w = self.shape, self.b, self.w
+        d, H, hd, F = sh.d, sh.n_heads, sh.head_dim, sh.ffn
+        bs, bl = block
         q, o = _view(self.q, b, m, H, hd), _view(self.o, b, m, H, hd)
         t, g = _view(self.t, b, m, d), _view(self.g, b, m, d)
         gu, a = _view(self.gu, b, m, 2 * F), _view(self.a, b, m, F)
-        for li in range(sh.n_layers):
-            lw = w["layers"][li]
-            before = None
+        lw = w["layers"][li]
+        before = None
+        if trace is not None:
+            before = dict(x=x.clone(), k=self.k[li].clone(), v=self.v[li].clone(), h=self.hc[li].clone())
+        if self.packet and mode == "all":
+            P.scatter_rows(x, self._rng_idx, self._rng_cnt, self.X[li])      # cache the layer inputs
+        P.rmsnorm(x, 0, m, self.h_cur, lo)
+        if mode == "refresh" or (li == sh.n_layers - 1 and not self.packet):
+            P.drift(self.h_cur, self.hc[li], self.drift)
+        if mode == "all":
+            idx = cnt = None
+            rb, rl = lo, m
+        elif mode == "refresh":
+            idx, cnt = _view(self.stale_idx, b, k_top), self.stale_count
+            P.select(self.drift, k_top, bs, bl, self.eligible, idx, cnt)
+            rb, rl = bs, bl
+        else:
+            idx = cnt = None
+            rb, rl = bs, bl
+        P.refresh_kv(self.h_cur, idx, cnt, rb, rl, lw["w_k"], lw["w_v"], self.k[li], self.v[li],
+                     workspace=self.ws)
+        P.copy_rows(self.h_cur, self.hc[li], idx, cnt, rb, rl)
+        P.project_q(self.h_cur, lw["w_q"], lo, m, H, out=q, workspace=self.ws)
+        P.attend(None, None, self.k[li], self.v[li], lo, m, H, q_buf=q, out=o, workspace=self.ws)
+        P.linear(o.view(b, m, H * hd), 0, m, lw["w_o"], t, workspace=self.ws)
+        P.residual_add(x, t)
+        P.rmsnorm(x, 0, m, g, 0)
+        P.linear(g, 0, m, lw["w_gu"], gu, workspace=self.ws)
+        P.swiglu(gu, a)
+        P.linear(a, 0, m, lw["w_down"], t, workspace=self.ws)
+        P.residual_add(x, t)
+        if trace is not None:
+            trace(dict(event="layer", forward=fwd, layer=li, mode=mode, lo=lo, hi=lo + m, block=block,
+                       k_top=k_top, before=before,
+                       after=dict(x=x.clone(), k=self.k[li].clone(), v=self.v[li].clone(),
+                                  h=self.hc[li].clone(), h_cur=self.h_cur.clone(), drift=self.drift.clone(),
+                                  stale_idx=None if idx is None else idx.clone(),
+                                  stale_count=None if cnt is None else cnt.clone())))
+
+    # -- packet flow ---------------------------------------------------------------------
+
+    def _entry_packet(self, lo: int, bs: int, be: int, hi: int, trace, fwd: int) -> None:
+        """After a block entry forward: each layer's window clustered and its
+        proxy scores taken; the last layer's block attention scores (the
+        commit drift's first baseline)."""
+        sh, cfg, b = self.shape, self.cfg, self.b
+        H, L, B = sh.n_heads, sh.n_layers, cfg.block_len
+        win = np.array(list(range(lo, bs)) + list(range(be, hi)), np.int32)
+        self.win_idx = torch.from_numpy(np.tile(win, (b, 1))).to(self.dev)
+        for li in range(L):
+            lw = self.w["layers"][li]
+            lab, sums, cnts, cents = P.cluster(self.hc[li], self.win_idx, cfg.n_clusters, cfg.kmeans_iters)
+            self.labels[li], self.sums[li], self.counts[li] = lab, sums, cnts
+            P.proxy_drift(sums, cnts, lw["w_q"], self.k[li], H, self.pscores[li], self.plse[li], True, self.pdrift,
+                          workspace=self.ws)
             if trace is not None:
-                before = dict(x=x.clone(), k=self.k[li].clone(), v=self.v[li].clone(), h=self.hc[li].clone())
-            P.rmsnorm(x, 0, m, self.h_cur, lo)
-            if mode == "refresh" or li == sh.n_layers - 1:
-                P.drift(self.h_cur, self.hc[li], self.drift)
-            if mode == "all":
-                idx = cnt = None
-                rb, rl = lo, m
-            elif mode == "refresh":
-                idx, cnt = _view(self.stale_idx, b, k_top), self.stale_count
-                P.select(self.drift, k_top, bs, bl, self.eligible, idx, cnt)
-                rb, rl = bs, bl
-            else:
-                idx = cnt = None
-                rb, rl = bs, bl
-            P.refresh_kv(self.h_cur, idx, cnt, rb, rl, lw["w_k"], lw["w_v"], self.k[li], self.v[li],
-                         workspace=self.ws)
-            P.copy_rows(self.h_cur, self.hc[li], idx, cnt, rb, rl)
-            P.project_q(self.h_cur, lw["w_q"], lo, m, H, out=q, workspace=self.ws)
-            P.attend(None, None, self.k[li], self.v[li], lo, m, H, q_buf=q, out=o, workspace=self.ws)
-            P.linear(o.view(b, m, H * hd), 0, m, lw["w_o"], t, workspace=self.ws)
-            P.residual_add(x, t)
-            P.rmsnorm(x, 0, m, g, 0)
-            P.linear(g, 0, m, lw["w_gu"], gu, workspace=self.ws)
-            P.swiglu(gu, a)
-            P.linear(a, 0, m, lw["w_down"], t, workspace=self.ws)
-            P.residual_add(x, t)
+                trace(dict(event="cluster", forward=fwd, layer=li, win=win, h=self.hc[li].clone(), k=self.k[li].clone(),
+                           labels=lab.clone(), sums=sums.clone(), counts=cnts.clone(), centroids=cents.clone(),
+                           pscores=self.pscores[li].clone(), plse=self.plse[li].clone()))
+        lw = self.w["layers"][L - 1]
+        P.project_q(self.hc[L - 1], lw["w_q"], bs, B, H, out=self.qJ, workspace=self.ws)
+        P.attention_drift(self.qJ, self.k[L - 1], self.ascores, self.alse, True, self.delta, workspace=self.ws)
+
+    def _patch(self, li: int, idx: torch.Tensor, cnt: torch.Tensor, xin: torch.Tensor) -> None:
+        """The rows of a packet: their inputs, normalised rows, K/V and the
+        cluster sums of layer li."""
+        sh, b = self.shape, self.b
+        lw = self.w["layers"][li]
+        k = idx.shape[1]
+        P.scatter_rows(xin, idx, cnt, self.X[li])
+        hs = _view(self.hs, b, k, sh.d)
+        P.rmsnorm(xin, 0, k, hs, 0)
+        P.scatter_rows(hs, idx, cnt, self.hnew)
+        P.cluster_update(self.hnew, self.hc[li], self.labels[li], idx, cnt, self.sums[li])
+        P.copy_rows(self.hnew, self.hc[li], idx, cnt, 0, 0)
+        P.refresh_kv(self.hnew, idx, cnt, 0, 0, lw["w_k"], lw["w_v"], self.k[li], self.v[li], workspace=self.ws)
+
+    def _packet_rows(self, li: int, idx: torch.Tensor, cnt: torch.Tensor, xs: torch.Tensor) -> None:
+        """Forward the rows idx of layer li from their cached inputs; xs
+        [b][k][d] receives their outputs (rows past the count: zeros in)."""
+        sh, b = self.shape, self.b
+        d, H, hd, F = sh.d, sh.n_heads, sh.head_dim, sh.ffn
+        lw = self.w["layers"][li]
+        k = idx.shape[1]
+        P.gather_rows(self.X[li], idx, cnt, xs)
+        hs = _view(self.hs, b, k, d)
+        P.rmsnorm(xs, 0, k, hs, 0)
+        q, o = _view(self.q, b, k, H, hd), _view(self.o, b, k, H, hd)
+        t, g = _view(self.t, b, k, d), _view(self.g, b, k, d)
+        gu, a = _view(self.gu, b, k, 2 * F), _view(self.a, b, k, F)
+        P.project_q(hs, lw["w_q"], 0, k, H, out=q, workspace=self.ws)
+        P.attend(None, None, self.k[li], self.v[li], 0, k, H, q_buf=q, out=o, workspace=self.ws)
+        P.linear(o.view(b, k, H * hd), 0, k, lw["w_o"], t, workspace=self.ws)
+        P.residual_add(xs, t)
+        P.rmsnorm(xs, 0, k, g, 0)
+        P.linear(g, 0, k, lw["w_gu"], gu, workspace=self.ws)
+        P.swiglu(gu, a)
+        P.linear(a, 0, k, lw["w_down"], t, workspace=self.ws)
+        P.residual_add(xs, t)
+
+    def _packet_step(self, bs: int, refresh: bool, have_pin: bool, trace, fwd: int):
+        """One step of the packet flow (the layer-0 packet, if any, is in
+        packet buffer 0).  Returns the index of the buffer holding the last
+        layer's packet on refreshing steps, else None."""
+        sh, cfg, b = self.shape, self.cfg, self.b
+        d, H, hd, L, B = sh.d, sh.n_heads, sh.head_dim, sh.n_layers, cfg.block_len
+        x = _view(self.x, b, B, d)
+        P.embed(self.y, bs, B, self.w["tok_emb"], self.w["pos_emb"], x)
+        cur = 0
+        for li in range(L):
+            lw = self.w["layers"][li]
+            ev = None
             if trace is not None:
-                trace(dict(event="layer", forward=fwd, layer=li, mode=mode, lo=lo, hi=hi, block=block,
-                           k_top=k_top, before=before,
-                           after=dict(x=x.clone(), k=self.k[li].clone(), v=self.v[li].clone(),
-                                      h=self.hc[li].clone(), h_cur=self.h_cur.clone(), drift=self.drift.clone(),
-                                      stale_idx=None if idx is None else idx.clone(),
-                                      stale_count=None if cnt is None else cnt.clone())))
+                ev = dict(event="packet_layer", forward=fwd, layer=li, refresh=refresh)
+                ev["before"] = dict(X=self.X[li].clone(), k=self.k[li].clone(), v=self.v[li].clone(),
+                                    h=self.hc[li].clone(), sums=self.sums[li].clone(),
+                                    pscores=self.pscores[li].clone(), plse=self.plse[li].clone(),
+                                    labels=self.labels[li].clone(), counts=self.counts[li].clone())
+                ev["pin"] = (self.pk_idx[cur].clone(), self.pk_cnt[cur].clone(), self.pk_x[cur].clone()) \
+                    if (refresh and have_pin) else None
+            if refresh and have_pin:
+                self._patch(li, self.pk_idx[cur], self.pk_cnt[cur], self.pk_x[cur])
+                if ev is not None:
+                    ev["patched"] = dict(X=self.X[li].clone(), k=self.k[li].clone(), v=self.v[li].clone(),
+                                         h=self.hc[li].clone(), sums=self.sums[li].clone())
+            self._layer(li, x, bs, B, "plain", (bs, B), 0, trace, fwd)
+            if li == L - 1:
+                qb = _view(self.q, b, B, H, hd)
+                if ev is not None:
+                    ev["att"] = dict(q=qb.clone(), k=self.k[li].clone(), scores_in=self.ascores.clone(),
+                                     lse_in=self.alse.clone())
+                P.attention_drift(qb, self.k[li], self.ascores, self.alse, False, self.delta, workspace=self.ws)
+                if ev is not None:
+                    ev["att"].update(delta=self.delta.clone(), scores_out=self.ascores.clone())
+            if refresh:
+                P.proxy_drift(self.sums[li], self.counts[li], lw["w_q"], self.k[li], H, self.pscores[li],
+                              self.plse[li], False, self.pdrift, workspace=self.ws)
+                nxt = 1 - cur
+                P.cluster_select(self.labels[li], self.pdrift, cfg.k_top, self.kpk, self.pk_idx[nxt],
+                                 self.pk_cnt[nxt])
+                self._packet_rows(li, self.pk_idx[nxt], self.pk_cnt[nxt], self.pk_x[nxt])
+                if ev is not None:
+                    ev["proxy"] = dict(k=self.k[li].clone(), v=self.v[li].clone(), X=self.X[li].clone(),
+                                       pdrift=self.pdrift.clone(),
+                                       pscores=self.pscores[li].clone(), sums=self.sums[li].clone())
+                    ev["pout"] = (self.pk_idx[nxt].clone(), self.pk_cnt[nxt].clone(), self.pk_x[nxt].clone())
+                cur = nxt
+                have_pin = True
+            if ev is not None:
+                trace(ev)
+        return cur if refresh else None
+
+    def _layer0_packet(self, dirty: list, be: int, hi: int) -> bool:
+        """The rows whose token a suffix commit changed, with their new
+        embeddings, into packet buffer 0; False when there are none."""
+        b, d = self.b, self.shape.d
+        if not any(dirty):
+            return False
+        n = hi - be
+        xe = _view(self.xsuf, b, n, d)
+        P.embed(self.y, be, n, self.w["tok_emb"], self.w["pos_emb"], xe)
+        loc = np.zeros((b, self.kpk), np.int32)
+        pos = np.zeros((b, self.kpk), np.int32)
+        cnt = np.zeros(b, np.int32)
+        for s in range(b):
+            rows = sorted(dirty[s])
+            cnt[s] = len(rows)
+            loc[s, :len(rows)] = [p - be for p in rows]
+            pos[s, :len(rows)] = rows
+        li = torch.from_numpy(loc).to(self.dev)
+        c = torch.from_numpy(cnt).to(self.dev)
+        P.gather_rows(xe, li, c, self.pk_x[0])
+        self.pk_idx[0].copy_(torch.from_numpy(pos))
+        self.pk_cnt[0].copy_(c)
+        return True
+
+    def _suffix_packet(self, y, cur: int, be: int, hi: int, trace, fwd: int, full: bool):
+        """Suffix commit of the last layer's packet rows in [be, hi); returns
+        (committed per sequence, the committed positions per sequence)."""
+        sh, cfg, b, mask = self.shape, self.cfg, self.b, self.shape.mask_id
+        idx = self.pk_idx[cur].cpu().numpy()
+        cnt = self.pk_cnt[cur].cpu().numpy()
+        rows = [[(r, int(p)) for r, p in enumerate(idx[s, :cnt[s]]) if be <= p < hi] for s in range(b)]
+        n = max(len(r) for r in rows)
+        none = [[] for _ in range(b)]
+        if n == 0:
+            return np.zeros(b, np.int64), none
+        loc = np.zeros((b, n), np.int32)
+        el = np.zeros((b, n), np.uint8)
+        msk = np.zeros((b, n), np.uint8)
+        for s in range(b):
+            for j, (r, p) in enumerate(rows[s]):
+                loc[s, j], el[s, j], msk[s, j] = r, 1, y[s, p] == mask
+        c = torch.from_numpy(el.sum(axis=1).astype(np.int32)).to(self.dev)
+        xs = _view(self.xsuf, b, n, sh.d)
+        P.gather_rows(self.pk_x[cur], torch.from_numpy(loc).to(self.dev), c, xs)
+        hf = _view(self.hf, b, n, sh.d)
+        P.rmsnorm(xs, 0, n, hf, 0)
+        lg = _view(self.logits, b, n, sh.vocab)
+        P.linear(hf, 0, n, self.w["w_lm"], lg, workspace=self.ws)
+        masked = torch.from_numpy(msk).to(self.dev)
+        elig = torch.from_numpy(el).to(self.dev)
+        tok, conf, cm = P.suffix_commit(lg, masked, elig, mask, cfg.tau_s, _view(self.token, b, n),
+                                        _view(self.conf, b, n), _view(self.commit, b, n), workspace=self.ws)
+        t = tok.cpu().numpy()
+        cmh = cm.cpu().numpy().astype(bool)
+        committed = [[] for _ in range(b)]
+        for s in range(b):
+            for j, (r, p) in enumerate(rows[s]):
+                if cmh[s, j]:
+                    y[s, p] = t[s, j]
+                    committed[s].append(p)
+        self.y.copy_(torch.from_numpy(y))
+        if trace is not None:
+            trace(dict(event="packet_suffix", forward=fwd, be=be, hi=hi, positions=[[p for _, p in r] for r in rows],
+                       logits=lg.clone() if full else None, conf=conf.clone(), token=tok.clone(), commit=cm.clone(),
+                       masked=masked.clone(), eligible=elig.clone(), x=xs.clone()))
+        return cmh.sum(axis=1), committed
 
     def head(self, lo: int, r0: int, n: int) -> torch.Tensor:
         """Logits of rows [r0, r0 + n) of the last forward over [lo, ...)."""
@@ -259,17 +507,46 @@ class Denoiser:
                                      workspace=self.ws)
             n = self._apply(y, bs, tok, cm, trace, fwd, "entry", lg if full(fwd) else None, conf, masked)
             gpu_ms["all"] += ev0.elapsed_time(ev1)
+            if self.packet:
+                self._entry_packet(lo, bs, be, hi, trace if full(fwd) else None, fwd)
             stats["committed"] += int(n.sum())
             fwd += 1
             since = n                       # per sequence; a batch refreshes when any sequence would
             self.hist_len.zero_()
+            dirty = [[] for _ in range(b)]
             while (y[:, bs:be] == mask).any():
                 refresh = int(since.max()) > cfg.tau_upd
+                mode = "refresh" if refresh else "plain"
+                if self.packet:
+                    ev0.record()
+                    have_pin = refresh and self._layer0_packet(dirty, be, hi)
+                    cur = self._packet_step(bs, refresh, have_pin, trace if full(fwd, mode) else None, fwd)
+                    ev1.record()
+                    stats["refreshing_steps" if refresh else "plain_steps"] += 1
+                    self.rows = B
+                    lg = self.head(bs, bs, B)
+                    masked = torch.from_numpy((y[:, bs:be] == mask).astype(np.uint8)).to(self.dev)
+                    hist_in = (self.hist.clone(), self.hist_len.clone()) if trace is not None else None
+                    tok, conf, cm = P.commit(lg, masked, self.delta, 0, self.hist, self.hist_len, mask, cfg.tau_s,
+                                             cfg.alpha, cfg.force_one, _view(self.token, b, B),
+                                             _view(self.conf, b, B), _view(self.commit, b, B), workspace=self.ws)
+                    n = self._apply(y, bs, tok, cm, trace, fwd, "step", lg if full(fwd) else None, conf, masked,
+                                    hist_in, self.delta)
+                    gpu_ms[mode] += ev0.elapsed_time(ev1)
+                    if refresh:
+                        dirty = [[] for _ in range(b)]
+                    if cfg.suffix_commit and refresh and be < hi:
+                        n_s, dirty = self._suffix_packet(y, cur, be, hi, trace, fwd, full(fwd))
+                        stats["suffix_committed"] += int(n_s.sum())
+                        n = n + n_s
+                    stats["committed"] += int(n.sum())
+                    fwd += 1
+                    since = n if refresh else since + n
+                    continue
                 rlo, rhi = (lo, hi) if refresh else (bs, be)
-                k_top = int(math.ceil((hi - lo - B) / 2)) if refresh else 0
+                k_top = int(math.ceil(cfg.window_frac * (hi - lo - B))) if refresh else 0
                 self.rows = rhi - rlo
                 ev0.record()
-                mode = "refresh" if refresh else "plain"
                 self.forward(rlo, rhi, mode, (bs, B), k_top, trace=trace if full(fwd, mode) else None, fwd=fwd)
                 ev1.record()
                 stats["refreshing_steps" if refresh else "plain_steps"] += 1
@@ -297,7 +574,7 @@ class Denoiser:
         stats["forward_gpu_ms"] = {k: round(v, 3) for k, v in gpu_ms.items()}
         return y, stats
 
-    def _apply(self, y, r0, tok, cm, trace, fwd, kind, lg, conf, masked, hist_in=None) -> int:
+    def _apply(self, y, r0, tok, cm, trace, fwd, kind, lg, conf, masked, hist_in=None, drift=None) -> int:
         """Copy the commit flags and tokens to the host, write committed
         tokens into y (host and device); returns the number committed per
         sequence."""
@@ -309,7 +586,8 @@ class Denoiser:
         if trace is not None:
             trace(dict(event="commit", forward=fwd, kind=kind, r0=r0, logits=None if lg is None else lg.clone(),
                        conf=conf.clone(),
-                       token=tok.clone(), commit=cm.clone(), masked=masked.clone(), drift=self.drift.clone(),
+                       token=tok.clone(), commit=cm.clone(), masked=masked.clone(),
+                       drift=(self.drift if drift is None else drift).clone(),
                        hist_in=hist_in, hist_out=(self.hist.clone(), self.hist_len.clone())))
         return c.sum(axis=1)
 

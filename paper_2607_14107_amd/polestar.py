@@ -103,6 +103,10 @@ def lib() -> ctypes.CDLL:
     L.polestar_attention_drift_workspace_size.argtypes = [I, I, I, I]
     L.polestar_attention_drift.restype = S
     L.polestar_attention_drift.argtypes = [I, I, I, I, I, I, I, P, P, F, P, P, I, P, P, Z, P]
+    L.polestar_gather_rows.restype = S
+    L.polestar_gather_rows.argtypes = [I, I, I, P, P, P, I, P, P]
+    L.polestar_scatter_rows.restype = S
+    L.polestar_scatter_rows.argtypes = [I, I, I, P, P, P, I, P, P]
     Lg = ctypes.c_long
     L.polestar_embed.restype = S
     L.polestar_embed.argtypes = [I, I, I, I, P, I, I, P, I, P, P, P]
@@ -405,6 +409,33 @@ def copy_rows(src: torch.Tensor, dst: torch.Tensor, stale_idx: torch.Tensor | No
         _dtype_code(src), b, seq, d, _ptr(src), _ptr(dst, src.dtype),
         _ptr(stale_idx, torch.int32) if k_max > 0 else None,
         _ptr(stale_count, torch.int32) if k_max > 0 else None, k_max, block_start, block_len, _stream(stream)))
+
+
+def gather_rows(src: torch.Tensor, idx: torch.Tensor, count: torch.Tensor, dst: torch.Tensor, stream=None):
+    """dst[b][r] = src[b][idx[b][r]] for r < count[b], zero rows after;
+    src [batch][seq][...], dst [batch][k_max][...] of the same row shape and dtype."""
+    b, seq = src.shape[0], src.shape[1]
+    k_max = idx.shape[1]
+    rb = src[0, 0].numel() * src.element_size()
+    if dst.shape[0] != b or dst.shape[1] != k_max or dst[0, 0].numel() * dst.element_size() != rb:
+        raise ValueError("gather_rows: shapes do not match")
+    _check("polestar_gather_rows", lib().polestar_gather_rows(
+        b, seq, rb, _ptr(src), _ptr(idx, torch.int32), _ptr(count, torch.int32), k_max, _ptr(dst, src.dtype),
+        _stream(stream)))
+    return dst
+
+
+def scatter_rows(src: torch.Tensor, idx: torch.Tensor, count: torch.Tensor, dst: torch.Tensor, stream=None):
+    """dst[b][idx[b][r]] = src[b][r] for r < count[b]; src [batch][k_max][...], dst [batch][seq][...]."""
+    b, seq = dst.shape[0], dst.shape[1]
+    k_max = idx.shape[1]
+    rb = dst[0, 0].numel() * dst.element_size()
+    if src.shape[0] != b or src.shape[1] != k_max or src[0, 0].numel() * src.element_size() != rb:
+        raise ValueError("scatter_rows: shapes do not match")
+    _check("polestar_scatter_rows", lib().polestar_scatter_rows(
+        b, seq, rb, _ptr(src, dst.dtype), _ptr(idx, torch.int32), _ptr(count, torch.int32), k_max, _ptr(dst),
+        _stream(stream)))
+    return dst
 
 
 # ---------------------------------------------------------------------------

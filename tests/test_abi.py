@@ -29,7 +29,7 @@ def _header_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = _header_functions()
-    assert len(names) == 29, names
+    assert len(names) == 31, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -184,6 +184,11 @@ def test_model_entry_validation(L):
     assert L.polestar_copy_rows(1, 2, 96, 256, FAKE, FAKE, None, None, 4, 0, 32, None) == INVALID
     assert L.polestar_copy_rows(1, 2, 96, 4, FAKE, FAKE, None, None, 0, 0, 32, None) == UNSUPPORTED
     assert L.polestar_copy_rows(1, 2, 96, 256, FAKE, FAKE, None, None, 0, 80, 32, None) == INVALID
+    for f in (L.polestar_gather_rows, L.polestar_scatter_rows):
+        assert f(2, 96, 512, FAKE, None, FAKE, 8, FAKE, None) == INVALID     # rows need indices
+        assert f(2, 96, 500, FAKE, FAKE, FAKE, 8, FAKE, None) == UNSUPPORTED
+        assert f(2, 96, 512, FAKE, FAKE, FAKE, 8, MISALIGNED, None) == UNSUPPORTED
+        assert f(2, 96, 512, None, None, None, 0, None, None) == 0          # nothing to move
 
 
 def test_attention_drift_validation(L):

@@ -128,12 +128,12 @@ def stack_weights(cfg, oracle_embeddings=True):
     return devw, ow
 
 
-def run_stack(P, index, trace=True, capture=None):
+def run_stack(P, index, trace=True, capture=None, **loop):
     from paper_2607_14107_amd import model
     cfg = inputs.STACKS[index]
     devw, ow = stack_weights(cfg, oracle_embeddings=cfg.d <= 1024)
     shape = model.ModelShape(cfg.n_layers, cfg.d, cfg.n_heads, cfg.head_dim, cfg.ffn, cfg.vocab, cfg.seq)
-    lc = model.LoopConfig(prompt_len=cfg.prompt_len, gen_len=cfg.gen_len, block_len=cfg.block_len)
+    lc = model.LoopConfig(prompt_len=cfg.prompt_len, gen_len=cfg.gen_len, block_len=cfg.block_len, **loop)
     den = model.Denoiser(devw, shape, cfg.batch, lc)
     events = []
     y, stats = den.generate(inputs.stack_prompt(cfg), trace=events.append if trace else None, capture=capture)
@@ -161,7 +161,7 @@ def replay(events, cfg, lc, ow, seqs=None):
             h_gpu = dec(af["h_cur"])[sq][:, lo:hi]
             assert_rows_close(h_gpu, ref.round_to(mr.rmsnorm(x_in), "bf16"), 2e-2, f"h rows, layer {li}")
             stale = None
-            if mode == "refresh" or li == cfg.n_layers - 1:
+            if mode == "refresh" or (li == cfg.n_layers - 1 and lc.flow != "packet"):
                 gd = from_dev(af["drift"])[sq][:, lo:hi]
                 assert_drift_close(gd, ref.drift(h_gpu, st.h[:, lo:hi]))
             if mode == "refresh":
@@ -208,7 +208,12 @@ def replay(events, cfg, lc, ow, seqs=None):
                 np.testing.assert_allclose(gconf[sq], conf, rtol=1e-4)
             masked = from_dev(ev["masked"]).astype(bool)
             gcm = from_dev(ev["commit"]).astype(bool)
-            if ev["kind"] == "entry":
+            if ev["kind"] == "step" and lc.flow == "packet":
+                hist, hl = (from_dev(t) for t in ev["hist_in"])
+                delta = from_dev(ev["drift"])                     # the attention drift of the block rows
+                wm, wh, wl = ref.commit_rule(gconf, delta, masked, hist, hl, lc.h, lc.tau_s, lc.alpha, lc.force_one)
+                assert np.array_equal(gcm, wm)
+            elif ev["kind"] == "entry":
                 assert np.array_equal(gcm, masked & (gconf > np.float32(lc.tau_s)))
             elif ev["kind"] == "step":
                 hist, hl = (from_dev(t) for t in ev["hist_in"])
@@ -290,3 +295,132 @@ def test_tiny_stack_loop_schedule_and_determinism(P):
         since = f["n"] if f["mode"] == "refresh" else since + f["n"]
     assert n_blocks == cfg.gen_len // lc.block_len
     assert stats["tpf"] == pytest.approx(stats["committed"] / (stats["forwards"] * cfg.batch))
+
+
+# ---------------------------------------------------------------------------
+# the packet flow (update packets between layers, proxy drift per layer)
+# ---------------------------------------------------------------------------
+
+def _centroid_check(h, win, labels, sums, counts, cents, K):
+    """GPU clustering of one sequence: labels are a nearest final centroid,
+    counts and sums match the members."""
+    hw = h[win]
+    u = hw / np.linalg.norm(hw, axis=1, keepdims=True)
+    cos = u @ cents.T
+    lab = labels[win]
+    assert np.all(cos[np.arange(len(win)), lab] >= cos.max(axis=1) - 1e-5)
+    for k in range(K):
+        m = hw[lab == k]
+        assert counts[k] == len(m)
+        np.testing.assert_allclose(sums[k], m.sum(axis=0), rtol=1e-5, atol=1e-5 * max(1.0, np.abs(m).max(initial=0)))
+    assert np.all(labels[np.setdiff1d(np.arange(len(labels)), win)] == -1)
+
+
+def replay_packets(events, cfg, lc, ow):
+    """The packet flow's own events against the oracle: clustering at block
+    entry, the patch, proxy drift and selection, the packet rows, the commit
+    drift and the suffix commit.  Returns the number of layer steps checked."""
+    from oracle import proxy_ref as pr
+    shape = mr.Shape(cfg.n_layers, cfg.d, cfg.n_heads, cfg.head_dim, cfg.ffn, cfg.vocab, cfg.seq, cfg.dtype)
+    K, H = lc.n_clusters, cfg.n_heads
+    n = 0
+    last_pout = {}
+    for ev in events:
+        if ev["event"] == "cluster":
+            h = dec(ev["h"])
+            lab, sums, cnts, cents = (from_dev(ev[k]) for k in ("labels", "sums", "counts", "centroids"))
+            for s in range(cfg.batch):
+                _centroid_check(h[s], ev["win"], lab[s], sums[s], cnts[s], cents[s], K)
+            want = pr.proxy_scores(pr.proxy_tokens(sums, cnts, "bf16"), ow["layers"][ev["layer"]]["w_q"],
+                                   dec(ev["k"]), H, "bf16")
+            assert_rows_close(from_dev(ev["pscores"]), want, 4e-3, "entry proxy scores")   # bf16 queries
+        elif ev["event"] == "packet_layer":
+            li = ev["layer"]
+            w = ow["layers"][li]
+            bf = ev["before"]
+            labels = from_dev(bf["labels"]).astype(np.int64)
+            counts = from_dev(bf["counts"]).astype(np.int64)
+            pl = mr.PacketLayer(mr.LayerState(dec(bf["k"]), dec(bf["v"]), dec(bf["h"])),
+                                from_dev(bf["X"]).astype(np.float64), labels,
+                                from_dev(bf["sums"]).astype(np.float64), counts, from_dev(bf["pscores"]))
+            if ev["pin"] is not None:
+                idx, cnt, xin = (from_dev(t) for t in ev["pin"])
+                rows = [list(idx[s, :cnt[s]]) for s in range(cfg.batch)]
+                xs = [xin[s, :cnt[s]].astype(np.float64) for s in range(cfg.batch)]
+                want = mr.patch(pl, rows, xs, w, shape)
+                got = ev["patched"]
+                np.testing.assert_array_equal(from_dev(got["X"]), want.x.astype(np.float32))
+                for nm, a in (("k", want.st.k), ("v", want.st.v), ("h", want.st.h)):
+                    assert_rows_close(dec(got[nm]), a, 2e-2, f"patched {nm}")
+                # the sums move by the GPU's own new rows (whose bf16 rounding may
+                # differ from the oracle's by an ulp; the rows are checked above)
+                gh = dec(got["h"])
+                wsums = from_dev(bf["sums"]).astype(np.float64)
+                for s in range(cfg.batch):
+                    for p in rows[s]:
+                        if labels[s, p] >= 0:
+                            wsums[s, labels[s, p]] += gh[s, p] - pl.st.h[s, p]
+                np.testing.assert_allclose(from_dev(got["sums"]), wsums, rtol=1e-5, atol=1e-5 * np.abs(wsums).max())
+            if ev["refresh"]:
+                pr_ = ev["proxy"]
+                sums = from_dev(pr_["sums"]).astype(np.float64)
+                sc = pr.proxy_scores(pr.proxy_tokens(sums, counts, "bf16"), w["w_q"], dec(pr_["k"]), H, "bf16")
+                # the proxy queries are rounded to bf16 on both sides from fp32 / fp64
+                # arithmetic: an element can differ by an ulp, so the scores are
+                # compared per (cluster, head) row at a bf16-derived tolerance, and
+                # the drift is the KL of the GPU's own current and previous scores
+                gsc = from_dev(pr_["pscores"])
+                assert_rows_close(gsc, sc, 4e-3, "proxy scores")
+                gd = from_dev(pr_["pdrift"])
+                np.testing.assert_allclose(gd, pr.proxy_kl(gsc, from_dev(bf["pscores"])), rtol=2e-3, atol=1e-6)
+                sel = pr.select_clusters(gd, lc.k_top)
+                widx, wcnt = pr.cluster_members(labels, sel)
+                oidx, ocnt, ox = (from_dev(t) for t in ev["pout"])
+                assert np.array_equal(ocnt, wcnt)
+                for s in range(cfg.batch):
+                    assert np.array_equal(oidx[s, :ocnt[s]], widx[s, :wcnt[s]])
+                rows = [list(oidx[s, :ocnt[s]]) for s in range(cfg.batch)]
+                cur = mr.PacketLayer(mr.LayerState(dec(pr_["k"]), dec(pr_["v"]), pl.st.h),
+                                     from_dev(pr_["X"]).astype(np.float64), labels, sums, counts, sc)
+                out = mr.sparse_forward(cur, rows, w, shape)
+                for s in range(cfg.batch):
+                    assert_rows_close(ox[s, :ocnt[s]], out[s], 2e-2, "packet rows")
+                last_pout[ev["forward"]] = (oidx, ocnt, ox)
+            if "att" in ev:                   # the commit drift of the block's queries, last layer
+                at = ev["att"]
+                s1 = pr.query_scores(dec(at["q"]), dec(at["k"]))
+                np.testing.assert_allclose(from_dev(at["scores_out"]), s1, rtol=1e-4, atol=1e-4 * np.abs(s1).max())
+                np.testing.assert_allclose(from_dev(at["delta"]), pr.attention_drift(s1, from_dev(at["scores_in"])),
+                                           rtol=2e-3, atol=1e-6)
+            n += 1
+        elif ev["event"] == "packet_suffix":
+            gconf = from_dev(ev["conf"])
+            el = from_dev(ev["eligible"]).astype(bool)
+            masked = from_dev(ev["masked"]).astype(bool)
+            oidx, ocnt, _ = last_pout[ev["forward"]]
+            for s in range(cfg.batch):     # the last packet's rows in the suffix window, in order
+                assert ev["positions"][s] == [int(p) for p in oidx[s, :ocnt[s]] if ev["be"] <= p < ev["hi"]]
+                assert el[s].sum() == len(ev["positions"][s])
+            if ev["logits"] is not None:
+                xs = from_dev(ev["x"]).astype(np.float64)
+                lg = ref.decode(from_dev(ev["logits"]), "bf16")
+                for s in range(cfg.batch):
+                    m = int(el[s].sum())
+                    if m:
+                        assert_rows_close(lg[s, :m], mr.logits(xs[s:s + 1, :m], ow["w_lm"], "bf16")[0], 2e-2, "suffix")
+                tok, conf = ref.confidence(lg, cfg.vocab - 1)
+                np.testing.assert_allclose(gconf[el], conf[el], rtol=1e-4)
+            assert np.array_equal(from_dev(ev["commit"]).astype(bool), ref.suffix_commit_rule(gconf, masked, el, lc.tau_s))
+    return n
+
+
+def test_tiny_packet_stack_replay(P):
+    cfg, lc, ow, y, stats, events = run_stack(P, 42, flow="packet")
+    assert not (y == cfg.vocab - 1).any()
+    assert np.array_equal(y[:, :cfg.prompt_len], inputs.stack_prompt(cfg))
+    assert stats["committed"] == cfg.batch * cfg.gen_len
+    assert stats["refreshing_steps"] > 0
+    n = replay_packets(events, cfg, lc, ow)
+    assert n == cfg.n_layers * (stats["refreshing_steps"] + stats["plain_steps"])
+    # the block forwards and the decisions through the common replay
+    assert replay(events, cfg, lc, ow) > 0
