@@ -461,6 +461,50 @@ polestar_status polestar_copy_rows(polestar_dtype dtype, int batch, int seq, int
                                    int k_max, int block_start, int block_len, hipStream_t stream);
 
 /*
+ * Cached hidden-state residual codec (Sec. 4.1 "Cluster and Quantize Hidden
+ * States"; App. C quantization format; App. D format ablation): a window
+ * row is kept as its residual to its cluster's mean, quantized along the
+ * channels in an OCP microscaling format -- blocks of 32 channels share one
+ * E8M0 scale 2^e (byte e + 127, e = floor(log2 amax) - emax, clamped to
+ * [-127, 127]); values v / 2^e rounded to nearest even and saturated:
+ *   POLESTAR_MXFP4: FP4 E2M1 (emax 2, |v| <= 6), two per byte, lower
+ *                   channel in the low nibble, sign in bit 3;
+ *   POLESTAR_MXFP8: FP8 E4M3 (emax 8, |v| <= 448), one per byte, sign in bit 7.
+ * The residual is x - mean formed in fp32; rows whose label is -1 use a zero
+ * mean.  Codes [batch][seq][polestar_codec_row_bytes(fmt, d)] and scales
+ * [batch][seq][d / 32] are laid out by position (rows not encoded are left
+ * as they are).  UNSUPPORTED unless d % 32 == 0 and the float arrays and
+ * codes are 16-byte aligned.
+ *
+ * polestar_cluster_means -- means[b][k] = mean over the window positions
+ *   win_idx[b][0..n_win) with labels[b][p] == k of x[b][p] (fp32, summed in
+ *   window order; zeros for an empty cluster).  K <= 16, d % 4 == 0.
+ * polestar_codec_encode -- codes/scales of the rows idx[b][0..count[b]) of x
+ *   against means[b][labels[b][p]].
+ * polestar_codec_gather -- for r < count[b], p = idx[b][r]:
+ *   x_out[b][r] = means[b][labels[b][p]] + decoded residual (fp32), and if
+ *   h_out != NULL, h_out[b][r] = RMSNorm(x_out[b][r]) (unit gain, eps) in
+ *   dtype -- the dequantisation fused into the gather that starts a packet's
+ *   forward (the paper fuses it with the update-packet computation);
+ *   rows r >= count[b]: zeros.  x_out [batch][k_max][d], h_out
+ *   [batch][k_max][d]; d <= 16384.
+ */
+typedef enum { POLESTAR_MXFP4 = 0, POLESTAR_MXFP8 = 1 } polestar_codec;
+
+size_t polestar_codec_row_bytes(int fmt, int d);
+polestar_status polestar_cluster_means(int batch, int seq, int d, const float* x, const int32_t* win_idx,
+                                       int n_win, const int32_t* labels, int n_clusters, float* means,
+                                       hipStream_t stream);
+polestar_status polestar_codec_encode(int fmt, int batch, int seq, int d, const float* x, const int32_t* idx,
+                                      const int32_t* count, int k_max, const int32_t* labels, int n_clusters,
+                                      const float* means, uint8_t* codes, uint8_t* scales, hipStream_t stream);
+polestar_status polestar_codec_gather(int fmt, polestar_dtype dtype, int batch, int seq, int d,
+                                      const uint8_t* codes, const uint8_t* scales, const int32_t* idx,
+                                      const int32_t* count, int k_max, const int32_t* labels, int n_clusters,
+                                      const float* means, float eps, float* x_out, void* h_out,
+                                      hipStream_t stream);
+
+/*
  * polestar_gather_rows / polestar_scatter_rows -- move the rows an update
  * packet carries (Alg. 1: the sparse forward of the selected rows and the
  * next layer's patch) between a [batch][seq] array and a compact

@@ -22,7 +22,7 @@ LIB = os.path.join(PKG, "libpolestar.so")
 ARCH = "gfx950"
 
 SOURCES = ["api.hip", "drift.hip", "select.hip", "gemm.hip", "attend.hip", "commit.hip", "step.hip",
-           "proxy.hip", "model.hip"]
+           "proxy.hip", "model.hip", "codec.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

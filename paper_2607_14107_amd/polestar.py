@@ -23,6 +23,8 @@ LIB_PATH = os.path.join(PKG, "libpolestar.so")
 OK = 0
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "launch failed", 4: "workspace too small"}
 FP32, BF16 = 0, 1
+MXFP4, MXFP8 = 0, 1
+CODECS = {"mxfp4": MXFP4, "mxfp8": MXFP8}
 
 # hyperparameter defaults (table of default hyperparameters, App. D)
 DEFAULT_TAU_S = 0.9
@@ -107,6 +109,14 @@ def lib() -> ctypes.CDLL:
     L.polestar_gather_rows.argtypes = [I, I, I, P, P, P, I, P, P]
     L.polestar_scatter_rows.restype = S
     L.polestar_scatter_rows.argtypes = [I, I, I, P, P, P, I, P, P]
+    L.polestar_codec_row_bytes.restype = Z
+    L.polestar_codec_row_bytes.argtypes = [I, I]
+    L.polestar_cluster_means.restype = S
+    L.polestar_cluster_means.argtypes = [I, I, I, P, P, I, P, I, P, P]
+    L.polestar_codec_encode.restype = S
+    L.polestar_codec_encode.argtypes = [I, I, I, I, P, P, P, I, P, I, P, P, P, P]
+    L.polestar_codec_gather.restype = S
+    L.polestar_codec_gather.argtypes = [I, I, I, I, I, P, P, P, P, I, P, I, P, F, P, P, P]
     Lg = ctypes.c_long
     L.polestar_embed.restype = S
     L.polestar_embed.argtypes = [I, I, I, I, P, I, I, P, I, P, P, P]
@@ -436,6 +446,46 @@ def scatter_rows(src: torch.Tensor, idx: torch.Tensor, count: torch.Tensor, dst:
         b, seq, rb, _ptr(src, dst.dtype), _ptr(idx, torch.int32), _ptr(count, torch.int32), k_max, _ptr(dst),
         _stream(stream)))
     return dst
+
+
+def codec_row_bytes(fmt: int, d: int) -> int:
+    return lib().polestar_codec_row_bytes(fmt, d)
+
+
+def cluster_means(x: torch.Tensor, win_idx: torch.Tensor, labels: torch.Tensor, n_clusters: int,
+                  means: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Per cluster the mean of its window members' rows of x [b][seq][d] (float32) -> [b][K][d]."""
+    b, seq, d = x.shape
+    if means is None:
+        means = torch.empty((b, n_clusters, d), dtype=torch.float32, device=x.device)
+    _check("polestar_cluster_means", lib().polestar_cluster_means(
+        b, seq, d, _ptr(x, torch.float32), _ptr(win_idx, torch.int32), win_idx.shape[1], _ptr(labels, torch.int32),
+        n_clusters, _ptr(means, torch.float32), _stream(stream)))
+    return means
+
+
+def codec_encode(fmt: int, x: torch.Tensor, idx: torch.Tensor, count: torch.Tensor, labels: torch.Tensor,
+                 means: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor, stream=None) -> None:
+    """Codes and scales of the rows idx (residuals of x to their cluster mean), by position."""
+    b, seq, d = x.shape
+    _check("polestar_codec_encode", lib().polestar_codec_encode(
+        fmt, b, seq, d, _ptr(x, torch.float32), _ptr(idx, torch.int32), _ptr(count, torch.int32), idx.shape[1],
+        _ptr(labels, torch.int32), means.shape[1], _ptr(means, torch.float32), _ptr(codes, torch.uint8),
+        _ptr(scales, torch.uint8), _stream(stream)))
+
+
+def codec_gather(fmt: int, codes: torch.Tensor, scales: torch.Tensor, idx: torch.Tensor, count: torch.Tensor,
+                 labels: torch.Tensor, means: torch.Tensor, x_out: torch.Tensor, h_out: torch.Tensor | None = None,
+                 eps: float = 1e-5, stream=None) -> None:
+    """x_out[b][r] = mean + decoded residual of row idx[b][r]; h_out = its RMSNorm (fused)."""
+    b, seq = labels.shape
+    k_max = idx.shape[1]
+    d = x_out.shape[2]
+    dt = _dtype_code(h_out) if h_out is not None else BF16
+    _check("polestar_codec_gather", lib().polestar_codec_gather(
+        fmt, dt, b, seq, d, _ptr(codes, torch.uint8), _ptr(scales, torch.uint8), _ptr(idx, torch.int32),
+        _ptr(count, torch.int32), k_max, _ptr(labels, torch.int32), means.shape[1], _ptr(means, torch.float32),
+        float(eps), _ptr(x_out, torch.float32), _ptr(h_out), _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

@@ -29,7 +29,7 @@ def _header_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = _header_functions()
-    assert len(names) == 31, names
+    assert len(names) == 35, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -189,6 +189,18 @@ def test_model_entry_validation(L):
         assert f(2, 96, 500, FAKE, FAKE, FAKE, 8, FAKE, None) == UNSUPPORTED
         assert f(2, 96, 512, FAKE, FAKE, FAKE, 8, MISALIGNED, None) == UNSUPPORTED
         assert f(2, 96, 512, None, None, None, 0, None, None) == 0          # nothing to move
+    # codec
+    assert L.polestar_codec_row_bytes(0, 4096) == 2048 and L.polestar_codec_row_bytes(1, 4096) == 4096
+    assert L.polestar_codec_row_bytes(2, 4096) == 0 and L.polestar_codec_row_bytes(0, 4010) == 0
+    assert L.polestar_cluster_means(2, 96, 512, FAKE, FAKE, 32, FAKE, 17, FAKE, None) == UNSUPPORTED
+    assert L.polestar_cluster_means(2, 96, 512, None, FAKE, 32, FAKE, 8, FAKE, None) == INVALID
+    enc = L.polestar_codec_encode
+    assert enc(2, 2, 96, 512, FAKE, FAKE, FAKE, 8, FAKE, 8, FAKE, FAKE, FAKE, None) == INVALID     # format
+    assert enc(0, 2, 96, 500, FAKE, FAKE, FAKE, 8, FAKE, 8, FAKE, FAKE, FAKE, None) == UNSUPPORTED
+    assert enc(0, 2, 96, 512, FAKE, None, FAKE, 8, FAKE, 8, FAKE, FAKE, FAKE, None) == INVALID
+    gat = L.polestar_codec_gather
+    assert gat(0, 1, 2, 96, 512, FAKE, FAKE, FAKE, FAKE, 8, FAKE, 8, FAKE, -1.0, FAKE, None, None) == INVALID
+    assert gat(0, 1, 2, 96, 512, FAKE, FAKE, FAKE, FAKE, 8, FAKE, 8, FAKE, 1e-5, MISALIGNED, None, None) == UNSUPPORTED
 
 
 def test_attention_drift_validation(L):
