@@ -310,6 +310,10 @@ def generate(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams) -> 
 #         cached inputs, and their outputs are the packet U(l + 1);
 #   F3-3  the packet of layer 0 holds the window rows whose token a suffix
 #         commit changed since the last refreshing forward (new embeddings);
+#   F3-5  with a codec (codec_ref, MXFP4 / MXFP8), the window rows' cached
+#         inputs are kept as residuals to their cluster's mean input (taken
+#         at block entry and fixed for the block); patched rows are
+#         re-encoded, and a packet's forward starts from the decoded inputs;
 #   F3-4  a plain step forwards the block only; the commit drift of the
 #         block is the attention drift of its queries at the last layer
 #         (proxy_ref.attention_drift), measured every forward after the entry
@@ -317,6 +321,7 @@ def generate(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams) -> 
 #         rows that lie in the suffix window.
 # ---------------------------------------------------------------------------
 
+from oracle import codec_ref as cr
 from oracle import proxy_ref as pr
 
 
@@ -328,6 +333,33 @@ class PacketLayer:
     sums: np.ndarray               # [b][K][d] sums of the members' H
     counts: np.ndarray             # [b][K]
     scores: np.ndarray             # [b][K][H][S] last proxy scores
+    codec: dict | None = None      # F3-5: fmt, codes [b][S][d], exps [b][S][d/32], means [b][K][d]
+
+
+def _mean_rows(codec: dict, labels: np.ndarray, s: int, rows) -> np.ndarray:
+    """Each row's cluster mean (zeros outside every cluster)."""
+    d = codec["means"].shape[2]
+    return np.stack([codec["means"][s, labels[s, p]] if labels[s, p] >= 0 else np.zeros(d) for p in rows])
+
+
+def encode_rows(codec: dict, x: np.ndarray, labels: np.ndarray, rows) -> dict:
+    """F3-5: codes of the listed rows [b][...] of x against their cluster means."""
+    out = dict(codec, codes=np.array(codec["codes"], copy=True), exps=np.array(codec["exps"], copy=True))
+    for s in range(x.shape[0]):
+        r = list(rows[s])
+        if r:
+            c, e = cr.encode(x[s, r], _mean_rows(codec, labels, s, r), codec["fmt"])
+            out["codes"][s, r], out["exps"][s, r] = c, e
+    return out
+
+
+def decoded_rows(pl: "PacketLayer", s: int, rows) -> np.ndarray:
+    """The cached inputs of rows of sequence s, decoded when a codec is on."""
+    r = np.asarray(rows, np.int64)
+    if pl.codec is None:
+        return pl.x[s, r]
+    c = pl.codec
+    return cr.decode(c["codes"][s, r], c["exps"][s, r], _mean_rows(c, pl.labels, s, r), c["fmt"])
 
 
 def patch(pl: PacketLayer, rows, x_new: np.ndarray, w: dict, shape: Shape) -> PacketLayer:
@@ -347,7 +379,8 @@ def patch(pl: PacketLayer, rows, x_new: np.ndarray, w: dict, shape: Shape) -> Pa
             x[s, p] = x_new[s][i]
             k[s, p] = ref.round_to(hn @ w["w_k"].T, dt).reshape(H, hd)
             v[s, p] = ref.round_to(hn @ w["w_v"].T, dt).reshape(H, hd)
-    return PacketLayer(LayerState(k, v, h), x, pl.labels, sums, pl.counts, pl.scores)
+    codec = None if pl.codec is None else encode_rows(pl.codec, x, pl.labels, rows)
+    return PacketLayer(LayerState(k, v, h), x, pl.labels, sums, pl.counts, pl.scores, codec)
 
 
 def sparse_forward(pl: PacketLayer, rows, w: dict, shape: Shape) -> list:
@@ -360,7 +393,7 @@ def sparse_forward(pl: PacketLayer, rows, w: dict, shape: Shape) -> list:
         if r.size == 0:
             out.append(np.zeros((0, shape.d)))
             continue
-        xr = pl.x[s, r][None]
+        xr = decoded_rows(pl, s, r)[None]
         h = ref.round_to(rmsnorm(xr), dt)
         q = ref.round_to(h @ w["w_q"].T, dt).reshape(1, r.size, shape.n_heads, shape.head_dim)
         o, _ = ref.attend(q, pl.st.k[s:s + 1], pl.st.v[s:s + 1])
@@ -410,8 +443,8 @@ def block_queries(h_block: np.ndarray, w_q: np.ndarray, shape: Shape) -> np.ndar
 
 
 def generate_packets(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams, n_clusters: int = 8,
-                     k_top: int = 4, iters: int = 10) -> tuple[np.ndarray, Trace]:
-    """The loop of Alg. 1 with update packets and proxy drift (F3-1..F3-4)."""
+                     k_top: int = 4, iters: int = 10, codec: str | None = None) -> tuple[np.ndarray, Trace]:
+    """The loop of Alg. 1 with update packets and proxy drift (F3-1..F3-5)."""
     b = prompt.shape[0]
     seq = p.prompt_len + p.gen_len
     assert seq == shape.seq
@@ -440,7 +473,13 @@ def generate_packets(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopPar
             st = r["state"]
             labels, sums, counts = cluster_layer(st.h, win, n_clusters, iters)
             sc0 = pr.proxy_scores(pr.proxy_tokens(sums, counts, dt), w["w_q"], st.k, H, dt)
-            layers[li] = PacketLayer(st, xc, labels, sums, counts, sc0)
+            cd = None
+            if codec is not None:
+                means = np.stack([cr.cluster_means(xc[s], labels[s], n_clusters) for s in range(b)])
+                cd = dict(fmt=codec, codes=np.zeros((b, seq, shape.d), np.int64),
+                          exps=np.zeros((b, seq, shape.d // cr.BLOCK), np.int64), means=means)
+                cd = encode_rows(cd, xc, labels, [win] * b)
+            layers[li] = PacketLayer(st, xc, labels, sums, counts, sc0, cd)
             if li == L - 1:
                 att = pr.query_scores(block_queries(r["h"][:, bs - elo:be - elo], w["w_q"], shape), st.k)
             x = r["x_out"]
@@ -469,11 +508,11 @@ def generate_packets(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopPar
                 # (X of the block rows is not kept: packets carry window rows only,
                 # and the next block entry rewrites X of this block)
                 r = layer_forward(x, bs, w, pl.st, mode="plain", block=(bs, p.block_len), shape=shape)
-                pl = PacketLayer(r["state"], pl.x, pl.labels, pl.sums, pl.counts, pl.scores)
+                pl = PacketLayer(r["state"], pl.x, pl.labels, pl.sums, pl.counts, pl.scores, pl.codec)
                 if refresh:
                     pdrift, rows, sc = proxy_select(pl, w, shape, k_top)
                     proxy.append((pdrift, sc))
-                    pl = PacketLayer(pl.st, pl.x, pl.labels, pl.sums, pl.counts, sc)
+                    pl = PacketLayer(pl.st, pl.x, pl.labels, pl.sums, pl.counts, sc, pl.codec)
                     pkt_x = sparse_forward(pl, rows, w, shape)
                     pkt_rows = rows
                 layers[li] = pl

@@ -275,3 +275,37 @@ def test_packet_flow_loop_invariants():
                     n_checked += 1
             prev = f["proxy"]
     assert n_checked > 0
+
+
+def test_codec_packet_rows_start_from_the_decoded_inputs():
+    # with the codec on, a packet's forward equals the codec-free forward of
+    # the decoded inputs; a patch re-encodes exactly the patched rows
+    from oracle import codec_ref as cr
+    shape = mr.Shape(n_layers=1, d=64, n_heads=2, head_dim=32, ffn=64, vocab=16, seq=20)
+    w, x, full, pl = _packet_layer_from_full(shape, 41, 2, 8, 12, 16)
+    win = mr._window_positions(2, 8, 12, 16)
+    means = cr.cluster_means(pl.x[0], pl.labels[0], 2)[None]
+    cd = dict(fmt="mxfp4", codes=np.zeros((1, 20, 64), np.int64), exps=np.zeros((1, 20, 2), np.int64), means=means)
+    pc = mr.PacketLayer(pl.st, pl.x, pl.labels, pl.sums, pl.counts, pl.scores, mr.encode_rows(cd, pl.x, pl.labels, [win]))
+    rows = [[3, 13, 15]]
+    dec = mr.decoded_rows(pc, 0, rows[0])
+    assert np.abs(dec - pl.x[0, rows[0]]).max() > 0                     # lossy
+    plain = mr.PacketLayer(pl.st, pl.x.copy(), pl.labels, pl.sums, pl.counts, pl.scores)
+    plain.x[0, rows[0]] = dec
+    np.testing.assert_array_equal(mr.sparse_forward(pc, rows, w, shape)[0], mr.sparse_forward(plain, rows, w, shape)[0])
+    new = x[0, [13]] + 0.5
+    pt = mr.patch(pc, [[13]], [new], w, shape)
+    c, e = cr.encode(new, means[0, [pc.labels[0, 13]]], "mxfp4")
+    assert np.array_equal(pt.codec["codes"][0, 13], c[0]) and np.array_equal(pt.codec["exps"][0, 13], e[0])
+    untouched = [p for p in win if p != 13]
+    assert np.array_equal(pt.codec["codes"][0, untouched], pc.codec["codes"][0, untouched])
+
+
+def test_packet_flow_with_codec_runs_to_completion():
+    shape = mr.Shape(n_layers=2, d=64, n_heads=2, head_dim=32, ffn=64, vocab=48, seq=40)
+    wts = rand_weights(shape, seed=13, lm_std=0.6)
+    prompt = np.random.default_rng(14).integers(0, shape.vocab - 1, size=(1, 8))
+    p = mr.LoopParams(prompt_len=8, gen_len=32, block_len=8, prefix=16, suffix=8, tau_upd=1, h=2)
+    for fmt in ("mxfp4", "mxfp8"):
+        y, tr = mr.generate_packets(wts, prompt, shape, p, n_clusters=3, k_top=2, codec=fmt)
+        assert not (y == shape.mask_id).any() and tr.committed == 32
