@@ -160,3 +160,16 @@ def pack(codes: np.ndarray, exps: np.ndarray, fmt: str) -> tuple[np.ndarray, np.
     else:
         b = c & 0xFF
     return b.astype(np.uint8), (np.asarray(exps, np.int64) + 127).astype(np.uint8)
+
+
+def unpack(b: np.ndarray, e8: np.ndarray, fmt: str) -> tuple[np.ndarray, np.ndarray]:
+    """Inverse of pack: bytes [n][d/2 or d] and E8M0 bytes [n][d/32] ->
+    (codes [n][d], exponents [n][d/32])."""
+    b = np.asarray(b, np.int64)
+    if fmt == "mxfp4":
+        c = np.empty(b.shape[:-1] + (2 * b.shape[-1],), np.int64)
+        c[..., 0::2] = b & 0xF
+        c[..., 1::2] = (b >> 4) & 0xF
+    else:
+        c = b
+    return c, np.asarray(e8, np.int64) - 127

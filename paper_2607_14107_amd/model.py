@@ -80,6 +80,7 @@ class LoopConfig:
     n_clusters: int = 8          # packet flow: K-means clusters per layer and window
     k_top: int = 4               # packet flow: clusters refreshed per layer and step
     kmeans_iters: int = 10
+    codec: str | None = None     # packet flow: "mxfp4" / "mxfp8" window inputs kept as quantized residuals
 
 
 def _view(buf: torch.Tensor, *shape) -> torch.Tensor:
@@ -157,6 +158,14 @@ class Denoiser:
             self.hs = z(b * max(self.kpk, cfg.suffix) * d)
             self.xsuf = z(b * cfg.suffix * d, t=torch.float32)
             self.qJ = z(b, B, H, hd)
+            self.codec = None if cfg.codec is None else P.CODECS[cfg.codec]
+            if self.codec is not None:
+                rb = P.codec_row_bytes(self.codec, d)
+                self.codes = [z(b, S, rb, t=torch.uint8) for _ in range(L)]
+                self.scales = [z(b, S, d // 32, t=torch.uint8) for _ in range(L)]
+                self.means = [z(b, K, d, t=torch.float32) for _ in range(L)]
+        elif cfg.codec is not None:
+            raise ValueError("the codec applies to the packet flow")
         self.ws = torch.empty(self._workspace_bytes(), dtype=torch.uint8, device=dev)
 
     def _windows(self):
@@ -275,16 +284,25 @@ class Denoiser:
         H, L, B = sh.n_heads, sh.n_layers, cfg.block_len
         win = np.array(list(range(lo, bs)) + list(range(be, hi)), np.int32)
         self.win_idx = torch.from_numpy(np.tile(win, (b, 1))).to(self.dev)
+        wcnt = torch.full((b,), len(win), dtype=torch.int32, device=self.dev)
         for li in range(L):
             lw = self.w["layers"][li]
             lab, sums, cnts, cents = P.cluster(self.hc[li], self.win_idx, cfg.n_clusters, cfg.kmeans_iters)
             self.labels[li], self.sums[li], self.counts[li] = lab, sums, cnts
+            if self.codec is not None:
+                P.cluster_means(self.X[li], self.win_idx, lab, cfg.n_clusters, self.means[li])
+                P.codec_encode(self.codec, self.X[li], self.win_idx, wcnt, lab, self.means[li], self.codes[li],
+                               self.scales[li])
             P.proxy_drift(sums, cnts, lw["w_q"], self.k[li], H, self.pscores[li], self.plse[li], True, self.pdrift,
                           workspace=self.ws)
             if trace is not None:
-                trace(dict(event="cluster", forward=fwd, layer=li, win=win, h=self.hc[li].clone(), k=self.k[li].clone(),
-                           labels=lab.clone(), sums=sums.clone(), counts=cnts.clone(), centroids=cents.clone(),
-                           pscores=self.pscores[li].clone(), plse=self.plse[li].clone()))
+                ev = dict(event="cluster", forward=fwd, layer=li, win=win, h=self.hc[li].clone(), k=self.k[li].clone(),
+                          labels=lab.clone(), sums=sums.clone(), counts=cnts.clone(), centroids=cents.clone(),
+                          pscores=self.pscores[li].clone(), plse=self.plse[li].clone())
+                if self.codec is not None:
+                    ev.update(X=self.X[li].clone(), means=self.means[li].clone(), codes=self.codes[li].clone(),
+                              scales=self.scales[li].clone())
+                trace(ev)
         lw = self.w["layers"][L - 1]
         P.project_q(self.hc[L - 1], lw["w_q"], bs, B, H, out=self.qJ, workspace=self.ws)
         P.attention_drift(self.qJ, self.k[L - 1], self.ascores, self.alse, True, self.delta, workspace=self.ws)
@@ -296,6 +314,9 @@ class Denoiser:
         lw = self.w["layers"][li]
         k = idx.shape[1]
         P.scatter_rows(xin, idx, cnt, self.X[li])
+        if self.codec is not None:
+            P.codec_encode(self.codec, self.X[li], idx, cnt, self.labels[li], self.means[li], self.codes[li],
+                           self.scales[li])
         hs = _view(self.hs, b, k, sh.d)
         P.rmsnorm(xin, 0, k, hs, 0)
         P.scatter_rows(hs, idx, cnt, self.hnew)
@@ -310,9 +331,13 @@ class Denoiser:
         d, H, hd, F = sh.d, sh.n_heads, sh.head_dim, sh.ffn
         lw = self.w["layers"][li]
         k = idx.shape[1]
-        P.gather_rows(self.X[li], idx, cnt, xs)
         hs = _view(self.hs, b, k, d)
-        P.rmsnorm(xs, 0, k, hs, 0)
+        if self.codec is not None:           # dequantisation fused into the gather (and the RMSNorm)
+            P.codec_gather(self.codec, self.codes[li], self.scales[li], idx, cnt, self.labels[li], self.means[li],
+                           xs, hs)
+        else:
+            P.gather_rows(self.X[li], idx, cnt, xs)
+            P.rmsnorm(xs, 0, k, hs, 0)
         q, o = _view(self.q, b, k, H, hd), _view(self.o, b, k, H, hd)
         t, g = _view(self.t, b, k, d), _view(self.g, b, k, d)
         gu, a = _view(self.gu, b, k, 2 * F), _view(self.a, b, k, F)
@@ -351,6 +376,9 @@ class Denoiser:
                 if ev is not None:
                     ev["patched"] = dict(X=self.X[li].clone(), k=self.k[li].clone(), v=self.v[li].clone(),
                                          h=self.hc[li].clone(), sums=self.sums[li].clone())
+                    if self.codec is not None:
+                        ev["patched"].update(codes=self.codes[li].clone(), scales=self.scales[li].clone(),
+                                             means=self.means[li].clone())
             self._layer(li, x, bs, B, "plain", (bs, B), 0, trace, fwd)
             if li == L - 1:
                 qb = _view(self.q, b, B, H, hd)
@@ -369,6 +397,9 @@ class Denoiser:
                 self._packet_rows(li, self.pk_idx[nxt], self.pk_cnt[nxt], self.pk_x[nxt])
                 if ev is not None:
                     ev["proxy"] = dict(k=self.k[li].clone(), v=self.v[li].clone(), X=self.X[li].clone(),
+                                       codes=None if self.codec is None else self.codes[li].clone(),
+                                       scales=None if self.codec is None else self.scales[li].clone(),
+                                       means=None if self.codec is None else self.means[li].clone(),
                                        pdrift=self.pdrift.clone(),
                                        pscores=self.pscores[li].clone(), sums=self.sums[li].clone())
                     ev["pout"] = (self.pk_idx[nxt].clone(), self.pk_cnt[nxt].clone(), self.pk_x[nxt].clone())

@@ -107,3 +107,13 @@ def test_pack_layout_and_cluster_means():
     x = np.array([[1.0, 2.0], [3.0, 4.0], [10.0, 0.0], [7.0, 7.0]])
     m = cr.cluster_means(x, np.array([0, 0, 2, -1]), 3)
     assert m.tolist() == [[2.0, 3.0], [0.0, 0.0], [10.0, 0.0]]
+
+
+@pytest.mark.parametrize("fmt", ["mxfp4", "mxfp8"])
+def test_unpack_inverts_pack(fmt):
+    g = np.random.default_rng(5)
+    r = (g.standard_normal((3, 64)) * 0.1).astype(np.float32)
+    c, e = cr.encode(r, np.zeros_like(r), fmt)
+    b, e8 = cr.pack(c, e, fmt)
+    c2, e2 = cr.unpack(b, e8, fmt)
+    assert np.array_equal(c2, c) and np.array_equal(e2, e)

@@ -12,6 +12,7 @@ relative on the rows the GPU normalised, decisions exactly."""
 import numpy as np
 import pytest
 
+from oracle import codec_ref as cr
 from oracle import model_ref as mr
 from oracle import polestar_ref as ref
 from paper_2607_14107_amd import inputs
@@ -316,6 +317,18 @@ def _centroid_check(h, win, labels, sums, counts, cents, K):
     assert np.all(labels[np.setdiff1d(np.arange(len(labels)), win)] == -1)
 
 
+def _check_codes(fmt, X, means, labels, rows, gcodes, gscales):
+    """Codes and scales of the listed rows of one sequence, bit-exact."""
+    rows = [int(p) for p in rows]
+    if not rows:
+        return
+    d = X.shape[1]
+    mrows = np.stack([means[labels[p]] if labels[p] >= 0 else np.zeros(d, np.float32) for p in rows])
+    c, e = cr.encode(X[rows], mrows, fmt)
+    pc, pe = cr.pack(c, e, fmt)
+    assert np.array_equal(gcodes[rows], pc) and np.array_equal(gscales[rows], pe), "codes differ"
+
+
 def replay_packets(events, cfg, lc, ow):
     """The packet flow's own events against the oracle: clustering at block
     entry, the patch, proxy drift and selection, the packet rows, the commit
@@ -331,6 +344,13 @@ def replay_packets(events, cfg, lc, ow):
             lab, sums, cnts, cents = (from_dev(ev[k]) for k in ("labels", "sums", "counts", "centroids"))
             for s in range(cfg.batch):
                 _centroid_check(h[s], ev["win"], lab[s], sums[s], cnts[s], cents[s], K)
+            if "codes" in ev:                 # the window's inputs encoded against the cluster means
+                X, gm = from_dev(ev["X"]), from_dev(ev["means"])
+                gcodes, gscales = from_dev(ev["codes"]), from_dev(ev["scales"])
+                for s in range(cfg.batch):
+                    np.testing.assert_allclose(gm[s], cr.cluster_means(X[s].astype(np.float64), lab[s], K),
+                                               rtol=1e-5, atol=1e-6)
+                    _check_codes(lc.codec, X[s], gm[s], lab[s], ev["win"], gcodes[s], gscales[s])
             want = pr.proxy_scores(pr.proxy_tokens(sums, cnts, "bf16"), ow["layers"][ev["layer"]]["w_q"],
                                    dec(ev["k"]), H, "bf16")
             assert_rows_close(from_dev(ev["pscores"]), want, 4e-3, "entry proxy scores")   # bf16 queries
@@ -361,6 +381,11 @@ def replay_packets(events, cfg, lc, ow):
                         if labels[s, p] >= 0:
                             wsums[s, labels[s, p]] += gh[s, p] - pl.st.h[s, p]
                 np.testing.assert_allclose(from_dev(got["sums"]), wsums, rtol=1e-5, atol=1e-5 * np.abs(wsums).max())
+                if "codes" in got:             # patched rows re-encoded against the block's means
+                    X, gm = from_dev(got["X"]), from_dev(got["means"])
+                    for s in range(cfg.batch):
+                        _check_codes(lc.codec, X[s], gm[s], labels[s], rows[s], from_dev(got["codes"])[s],
+                                     from_dev(got["scales"])[s])
             if ev["refresh"]:
                 pr_ = ev["proxy"]
                 sums = from_dev(pr_["sums"]).astype(np.float64)
@@ -380,8 +405,12 @@ def replay_packets(events, cfg, lc, ow):
                 for s in range(cfg.batch):
                     assert np.array_equal(oidx[s, :ocnt[s]], widx[s, :wcnt[s]])
                 rows = [list(oidx[s, :ocnt[s]]) for s in range(cfg.batch)]
+                codec = None
+                if pr_["codes"] is not None:   # the packet rows start from the GPU's codes, decoded
+                    c, e = cr.unpack(from_dev(pr_["codes"]), from_dev(pr_["scales"]), lc.codec)
+                    codec = dict(fmt=lc.codec, codes=c, exps=e, means=from_dev(pr_["means"]).astype(np.float64))
                 cur = mr.PacketLayer(mr.LayerState(dec(pr_["k"]), dec(pr_["v"]), pl.st.h),
-                                     from_dev(pr_["X"]).astype(np.float64), labels, sums, counts, sc)
+                                     from_dev(pr_["X"]).astype(np.float64), labels, sums, counts, sc, codec)
                 out = mr.sparse_forward(cur, rows, w, shape)
                 for s in range(cfg.batch):
                     assert_rows_close(ox[s, :ocnt[s]], out[s], 2e-2, "packet rows")
@@ -423,4 +452,14 @@ def test_tiny_packet_stack_replay(P):
     n = replay_packets(events, cfg, lc, ow)
     assert n == cfg.n_layers * (stats["refreshing_steps"] + stats["plain_steps"])
     # the block forwards and the decisions through the common replay
+    assert replay(events, cfg, lc, ow) > 0
+
+
+@pytest.mark.parametrize("codec", ["mxfp4", "mxfp8"])
+def test_tiny_packet_stack_with_codec_replay(P, codec):
+    cfg, lc, ow, y, stats, events = run_stack(P, 42, flow="packet", codec=codec)
+    assert not (y == cfg.vocab - 1).any()
+    assert stats["committed"] == cfg.batch * cfg.gen_len
+    n = replay_packets(events, cfg, lc, ow)
+    assert n == cfg.n_layers * (stats["refreshing_steps"] + stats["plain_steps"])
     assert replay(events, cfg, lc, ow) > 0
