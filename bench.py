@@ -70,6 +70,8 @@ def parse():
                         "once and print its tokens/s and tokens per forward instead of the layer-step benchmark")
     p.add_argument("--flow", default="window", choices=("window", "packet"),
                    help="--stack: window forwards with per-token drift, or the update-packet flow with proxy drift")
+    p.add_argument("--codec", default=None, choices=("mxfp4", "mxfp8"),
+                   help="--stack --flow packet: keep the window's cached inputs as quantized residuals")
     return p.parse_args()
 
 
@@ -310,7 +312,7 @@ def cpu_baseline(cfg, x, k, budget_s):
                       f"attention, commit) of the benchmarked workload, {t_total:.1f} s"}
 
 
-def stack_bench(index, P, torch, flow="window"):
+def stack_bench(index, P, torch, flow="window", codec=None):
     """The loop of Alg. 1 on a whole stack with random weights: weights are
     drawn on the host (one thread per matrix) and uploaded as they complete,
     then one full generation is timed (wall clock around the loop, GPU time
@@ -344,7 +346,8 @@ def stack_bench(index, P, torch, flow="window"):
             if done % 24 == 0:
                 print(f"weights {done}/{len(jobs)} ({time.perf_counter() - t0:.0f} s)", file=sys.stderr, flush=True)
     shape = model.ModelShape(cfg.n_layers, cfg.d, cfg.n_heads, cfg.head_dim, cfg.ffn, cfg.vocab, cfg.seq)
-    lc = model.LoopConfig(prompt_len=cfg.prompt_len, gen_len=cfg.gen_len, block_len=cfg.block_len, flow=flow)
+    lc = model.LoopConfig(prompt_len=cfg.prompt_len, gen_len=cfg.gen_len, block_len=cfg.block_len, flow=flow,
+                          codec=codec)
     den = model.Denoiser(w, shape, cfg.batch, lc)
     print(f"weights ready ({time.perf_counter() - t0:.0f} s); generating", file=sys.stderr, flush=True)
     y, st = den.generate(inputs.stack_prompt(cfg), progress=lambda blk, f: print(
@@ -358,7 +361,7 @@ def stack_bench(index, P, torch, flow="window"):
            "config": {"workload": f"{cfg.name}: {cfg.n_layers} layers, d {cfg.d}, {cfg.n_heads}x{cfg.head_dim} MHA, "
                                   f"SwiGLU {cfg.ffn}, vocab {cfg.vocab}, batch {cfg.batch}, prompt {cfg.prompt_len}, "
                                   f"{cfg.gen_len} generated in blocks of {cfg.block_len}, random N(0, 0.02) weights",
-                      "flow": flow,
+                      "flow": flow, "codec": codec,
                       "global_batch": cfg.batch, "seq_len": cfg.seq},
            "tpf": round(st["tpf"], 3), "forwards": st["forwards"], "committed": st["committed"],
            "suffix_committed": st["suffix_committed"], "seconds": round(st["seconds"], 3),
@@ -392,7 +395,7 @@ def main():
         build.build(verbose=False)
     P.lib()
     if args.stack is not None:
-        return stack_bench(args.stack, P, torch, args.flow)
+        return stack_bench(args.stack, P, torch, args.flow, args.codec)
 
     cfg = inputs.CONFIGS[args.config]
     x = inputs.layer_inputs(cfg, args.subrun)
