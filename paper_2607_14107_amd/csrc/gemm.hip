@@ -17,6 +17,9 @@
 //   - each wave streams its weight rows from HBM straight into registers,
 //     128 contiguous bytes per lane, two super-steps ahead (triple buffer,
 //     loop unrolled three times so the buffers rotate without copies).
+//   A row's (sequence, position) is one load away (fixed stride of
+//   k_max + block_len rows per sequence), so the first input rows follow
+//   the weight prefetch closely.
 //   When rows x columns do not fill the chip, K is split over workgroups;
 //   each writes its fp32 partial tile as one contiguous block of the
 //   workspace ([split][column tile][row][128]: long DRAM bursts, not 512-byte
@@ -27,7 +30,8 @@
 // gemm_small_kernel (at most 64 rows, e.g. the Q projection): a workgroup
 //   owns all rows and 16 columns; its 4 waves take interleaved super-steps
 //   of the full K with both operands loaded straight into registers and are
-//   summed in LDS, so no partials leave the chip.
+//   summed in LDS, so no partials leave the chip.  A load instruction covers
+//   64 contiguous bytes of each of 16 rows.
 //
 // In both, A and B use the same lane -> k assignment, so k may be visited in
 // any order.  All loads are unconditional (rows or columns past the end read
@@ -57,8 +61,6 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_rows_kernel(GemmArgs g) {
     constexpr int ES = T::kBytes;
     __shared__ __align__(16) char sa[2][BM * kLda];
     __shared__ int rowb[BM], rowp[BM];
-    __shared__ int scan_tmp[17];
-    extern __shared__ int pre[];           // batch + 1 (refresh mode)
 
     const int tile = blockIdx.x / g.ksplit;
     const int split = blockIdx.x - tile * g.ksplit;
@@ -91,23 +93,17 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_rows_kernel(GemmArgs g) {
     load_b(s0, b0);
     load_b(min(s0 + 1, slast), b1);
 
-    const int total = g.mode == kGemmRefresh ? build_prefix(g, pre, scan_tmp)
-                                             : g.batch * g.block_len;
-    // Split K: the first workgroup of each row tile publishes its rows'
-    // (sequence, position) for the reduce kernel (-1: row maps to nothing).
-    if (g.ksplit > 1 && split == 0 && col_tile == 0 && t < BM && m0 + t < g.m_max) {
-        int b, pos;
-        map_row(g, pre, total, m0 + t, b, pos);
-        *reinterpret_cast<int2*>(g.rowmap + 2 * (m0 + t)) = make_int2(b, pos);
-    }
-    if (m0 >= total) return;               // uniform over the workgroup
+    // Row bookkeeping: one load per row.  The first workgroup of each row
+    // tile also publishes the map for the split-K reduction.
+    int rb_ = -1, rp_ = 0;
+    if (t < BM) map_row(g, m0 + t, rb_, rp_);
     if (t < BM) {
-        int b, pos;
-        map_row(g, pre, total, m0 + t, b, pos);
-        rowb[t] = b;
-        rowp[t] = pos;
+        rowb[t] = rb_;
+        rowp[t] = rp_;
+        if (g.ksplit > 1 && split == 0 && col_tile == 0 && m0 + t < g.m_max)
+            *reinterpret_cast<int2*>(g.rowmap + 2 * (m0 + t)) = make_int2(rb_, rp_);
     }
-    __syncthreads();
+    if (!__syncthreads_or(rb_ >= 0)) return;   // no row of this tile maps anywhere (uniform)
 
     // Rows that map to nothing read row 0 instead: their accumulators are
     // never stored, and every load stays unconditional (static wait counts).
@@ -268,33 +264,33 @@ __global__ __launch_bounds__(kSmallBlock) void gemm_small_kernel(GemmArgs g) {
 }
 
 template <bool BF16, int MT>
-void launch_rows(const GemmPlan& p, const GemmArgs& g, size_t dyn, hipStream_t s) {
-    hipLaunchKernelGGL((gemm_rows_kernel<BF16, MT>), dim3(p.grid), dim3(kGemmBlock), dyn, s, g);
+void launch_rows(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
+    hipLaunchKernelGGL((gemm_rows_kernel<BF16, MT>), dim3(p.grid), dim3(kGemmBlock), 0, s, g);
 }
 
 template <bool BF16>
-bool dispatch_rows(const GemmPlan& p, const GemmArgs& g, size_t dyn, hipStream_t s) {
+bool dispatch_rows(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
     switch (p.mt) {   // 32-row tiles per workgroup
-        case 1: launch_rows<BF16, 1>(p, g, dyn, s); return true;
-        case 2: launch_rows<BF16, 2>(p, g, dyn, s); return true;
-        case 3: launch_rows<BF16, 3>(p, g, dyn, s); return true;
-        case 4: launch_rows<BF16, 4>(p, g, dyn, s); return true;
-        case 5: launch_rows<BF16, 5>(p, g, dyn, s); return true;
-        case 6: launch_rows<BF16, 6>(p, g, dyn, s); return true;
-        case 7: launch_rows<BF16, 7>(p, g, dyn, s); return true;
-        case 8: launch_rows<BF16, 8>(p, g, dyn, s); return true;
+        case 1: launch_rows<BF16, 1>(p, g, s); return true;
+        case 2: launch_rows<BF16, 2>(p, g, s); return true;
+        case 3: launch_rows<BF16, 3>(p, g, s); return true;
+        case 4: launch_rows<BF16, 4>(p, g, s); return true;
+        case 5: launch_rows<BF16, 5>(p, g, s); return true;
+        case 6: launch_rows<BF16, 6>(p, g, s); return true;
+        case 7: launch_rows<BF16, 7>(p, g, s); return true;
+        case 8: launch_rows<BF16, 8>(p, g, s); return true;
         default: return false;
     }
 }
 
 template <bool BF16>
-bool dispatch_small(const GemmPlan& p, const GemmArgs& g, size_t dyn, hipStream_t s) {
+bool dispatch_small(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
     dim3 grid(p.col_tiles, p.row_tiles);
     switch (p.mt) {
-        case 1: hipLaunchKernelGGL((gemm_small_kernel<BF16, 1>), grid, dim3(kSmallBlock), dyn, s, g); return true;
-        case 2: hipLaunchKernelGGL((gemm_small_kernel<BF16, 2>), grid, dim3(kSmallBlock), dyn, s, g); return true;
-        case 3: hipLaunchKernelGGL((gemm_small_kernel<BF16, 3>), grid, dim3(kSmallBlock), dyn, s, g); return true;
-        case 4: hipLaunchKernelGGL((gemm_small_kernel<BF16, 4>), grid, dim3(kSmallBlock), dyn, s, g); return true;
+        case 1: hipLaunchKernelGGL((gemm_small_kernel<BF16, 1>), grid, dim3(kSmallBlock), 0, s, g); return true;
+        case 2: hipLaunchKernelGGL((gemm_small_kernel<BF16, 2>), grid, dim3(kSmallBlock), 0, s, g); return true;
+        case 3: hipLaunchKernelGGL((gemm_small_kernel<BF16, 3>), grid, dim3(kSmallBlock), 0, s, g); return true;
+        case 4: hipLaunchKernelGGL((gemm_small_kernel<BF16, 4>), grid, dim3(kSmallBlock), 0, s, g); return true;
         default: return false;
     }
 }
@@ -345,10 +341,9 @@ polestar_status gemm_run(bool bf16, const GemmPlan& p, GemmArgs g, hipStream_t s
     g.steps_per_split = p.steps_per_split;
     g.row_tiles = p.row_tiles;
     g.col_tiles = p.col_tiles;
-    const size_t dyn = g.mode == kGemmRefresh ? (static_cast<size_t>(g.batch) + 1) * sizeof(int) : 0;
     bool ok;
-    if (p.small) ok = bf16 ? dispatch_small<true>(p, g, dyn, stream) : dispatch_small<false>(p, g, dyn, stream);
-    else ok = bf16 ? dispatch_rows<true>(p, g, dyn, stream) : dispatch_rows<false>(p, g, dyn, stream);
+    if (p.small) ok = bf16 ? dispatch_small<true>(p, g, stream) : dispatch_small<false>(p, g, stream);
+    else ok = bf16 ? dispatch_rows<true>(p, g, stream) : dispatch_rows<false>(p, g, stream);
     if (!ok) return POLESTAR_ERR_UNSUPPORTED;
     polestar_status st = launch_status();
     if (st != POLESTAR_OK || p.small || p.ksplit == 1) return st;

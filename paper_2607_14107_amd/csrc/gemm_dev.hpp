@@ -14,54 +14,40 @@ constexpr int kSmallWaves = 4;    // gemm_small_kernel: waves per workgroup
 constexpr int kSmallBlock = kSmallWaves * 64;
 
 // Row bookkeeping --------------------------------------------------------------
-// Refresh mode: sequence b contributes count_b stale rows followed by its
-// block_len active-block rows; rows of all sequences are numbered
-// consecutively.  pre[b] is the first row of sequence b, pre[batch] the total.
-__device__ int build_prefix(const GemmArgs& g, int* pre, int* scan_tmp) {
-    int carry = 0;
-    for (int base = 0; base < g.batch; base += blockDim.x) {
-        const int b = base + threadIdx.x;
-        int v = 0;
-        if (b < g.batch) {
-            int c = g.stale_count ? g.stale_count[b] : 0;
-            c = c < 0 ? 0 : (c > g.k_max ? g.k_max : c);
-            v = c + g.block_len;
-        }
-        int tot;
-        const int ex = block_excl_scan(v, scan_tmp, &tot);
-        if (b < g.batch) pre[b] = carry + ex;
-        carry += tot;
-    }
-    if (threadIdx.x == 0) pre[g.batch] = carry;
-    __syncthreads();
-    return carry;
+// Refresh mode: sequence b owns rows [b*R, (b+1)*R), R = k_max + block_len:
+// its first count_b rows are its stale positions, the last block_len rows
+// its active block; rows in between (count_b < k_max) map to nothing.  A
+// fixed stride costs no prefix over the counts, so a row's position is one
+// load away.  Block-rows mode: row m is position block_start + m % block_len
+// of sequence m / block_len.
+__device__ __forceinline__ int gemm_rows_total(const GemmArgs& g) {
+    return g.batch * (g.mode == kGemmRefresh ? g.k_max + g.block_len : g.block_len);
 }
 
 // Row m -> (sequence, position); b = -1 when the row maps to nothing.
-__device__ void map_row(const GemmArgs& g, const int* pre, int total, int m, int& b, int& pos) {
+__device__ __forceinline__ void map_row(const GemmArgs& g, int m, int& b, int& pos) {
     b = -1;
     pos = 0;
-    if (m < 0 || m >= total) return;
+    if (m < 0 || m >= gemm_rows_total(g)) return;
     if (g.mode == kGemmBlockRows) {
         b = m / g.block_len;
         pos = g.block_start + (m - b * g.block_len);
         return;
     }
-    int lo = 0, hi = g.batch - 1;       // last b with pre[b] <= m
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (pre[mid] <= m) lo = mid; else hi = mid - 1;
+    const int R = g.k_max + g.block_len;
+    const int sb = m / R;
+    const int local = m - sb * R;
+    if (local >= g.k_max) {
+        b = sb;
+        pos = g.block_start + (local - g.k_max);
+        return;
     }
-    const int local = m - pre[lo];
-    const int cnt = pre[lo + 1] - pre[lo] - g.block_len;
-    if (local < cnt) {
-        const int p = g.stale_idx[static_cast<size_t>(lo) * g.k_max + local];
-        if (p < 0 || p >= g.seq) return;          // out-of-range entries refresh nothing
-        pos = p;
-    } else {
-        pos = g.block_start + (local - cnt);
-    }
-    b = lo;
+    int c = g.stale_count[sb];
+    const int p = g.stale_idx[static_cast<size_t>(sb) * g.k_max + local];
+    c = c < 0 ? 0 : (c > g.k_max ? g.k_max : c);
+    if (local >= c || p < 0 || p >= g.seq) return;   // unused slot or out-of-range entry: refresh nothing
+    b = sb;
+    pos = p;
 }
 
 template <bool BF16>
@@ -114,16 +100,14 @@ __device__ __forceinline__ void small_body(const GemmArgs& g, int bx, int by) {
     constexpr int ES = T::kBytes;
     constexpr int BM = MT * 16;
     __shared__ int rowb[BM], rowp[BM];
-    __shared__ int scan_tmp[17];
     __shared__ float red[kSmallWaves][BM][17];
-    extern __shared__ int pre[];
 
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int w = t >> 6;
     const int col0 = bx * 16;
     const int m0 = by * BM;
-    const int kcol = (lane >> 4) * 64;
+    const int kcol = (lane >> 4) * 16;   // lane group g reads bytes 16g + 64s: 64 contiguous bytes of a row per load
     const int nsteps = g.K / (256 / ES);
     // wave w: super-steps w, w+W, ...; the last one it owns is slast
     // (prefetches past it re-read slast and are ignored).
@@ -137,18 +121,16 @@ __device__ __forceinline__ void small_body(const GemmArgs& g, int bx, int by) {
     if (!brow) brow = g.w0;
     auto load_b = [&](int step, uint4 (&rb)[4]) {
 #pragma unroll
-        for (int s = 0; s < 4; ++s) rb[s] = ld16(brow + step * 256 + kcol + 16 * s);
+        for (int s = 0; s < 4; ++s) rb[s] = ld16(brow + step * 256 + 64 * s + kcol);
     };
     uint4 q0[4], q1[4], q2[4];
     load_b(min(w, slast), q0);
     load_b(min(w + W, slast), q1);
 
-    const int total = g.mode == kGemmRefresh ? build_prefix(g, pre, scan_tmp)
-                                             : g.batch * g.block_len;
-    if (m0 >= total) return;
+    if (m0 >= gemm_rows_total(g)) return;
     if (t < BM) {
         int b, pos;
-        map_row(g, pre, total, m0 + t, b, pos);
+        map_row(g, m0 + t, b, pos);
         rowb[t] = b;
         rowp[t] = pos;
     }
@@ -166,7 +148,7 @@ __device__ __forceinline__ void small_body(const GemmArgs& g, int bx, int by) {
 #pragma unroll
         for (int s = 0; s < 4; ++s)
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) ra[mt][s] = ld16(arow[mt] + step * 256 + kcol + 16 * s);
+            for (int mt = 0; mt < MT; ++mt) ra[mt][s] = ld16(arow[mt] + step * 256 + 64 * s + kcol);
     };
     floatx4 acc[MT];
 #pragma unroll

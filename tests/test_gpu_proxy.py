@@ -17,7 +17,7 @@ import pytest
 from oracle import polestar_ref as ref
 from oracle import proxy_ref as pr
 from paper_2607_14107_amd import inputs
-from tests._util import ensure_built, from_dev, to_dev
+from tests._util import assert_rows_close, ensure_built, from_dev, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -149,14 +149,28 @@ def test_proxy_drift_matches_oracle(P, dtype):
                        first=True)
     torch.cuda.synchronize()
     assert np.all(from_dev(d0) == 0.0)
-    np.testing.assert_allclose(from_dev(scores), s0, rtol=1e-4, atol=1e-4 * np.abs(s0).max())
-    np.testing.assert_allclose(from_dev(lse), pr.log_sum_exp(s0), rtol=1e-4, atol=1e-5)
+    g0 = from_dev(scores)
+    if dtype == "fp32":
+        np.testing.assert_allclose(g0, s0, rtol=1e-4, atol=1e-4 * np.abs(s0).max())
+        np.testing.assert_allclose(from_dev(lse), pr.log_sum_exp(s0), rtol=1e-4, atol=1e-5)
+    else:
+        # bf16 queries: an element on a rounding boundary may round the other
+        # way under a different fp32 summation order, moving a score by
+        # 2^-8 |q_j k_j| per such element
+        assert_rows_close(g0, s0, 4e-3, "proxy scores")
+        np.testing.assert_allclose(from_dev(lse), pr.log_sum_exp(g0), rtol=1e-5, atol=1e-5)
     d1 = P.proxy_drift(sums, counts, wq, to_dev(_bits(k1, cfg.dtype), cfg.dtype), cfg.n_heads, scores, lse,
                        first=False)
     torch.cuda.synchronize()
-    np.testing.assert_allclose(from_dev(d1), want, rtol=2e-3, atol=1e-6)
+    g1 = from_dev(scores)
     assert want.max() > 1e-4                  # the changed rows do move the proxies
-    np.testing.assert_allclose(from_dev(scores), s1, rtol=1e-4, atol=1e-4 * np.abs(s1).max())
+    if dtype == "fp32":
+        np.testing.assert_allclose(from_dev(d1), want, rtol=2e-3, atol=1e-6)
+        np.testing.assert_allclose(g1, s1, rtol=1e-4, atol=1e-4 * np.abs(s1).max())
+    else:
+        assert_rows_close(g1, s1, 4e-3, "proxy scores")
+        np.testing.assert_allclose(from_dev(d1), pr.proxy_kl(g1, g0), rtol=2e-3, atol=1e-6)
+        np.testing.assert_allclose(from_dev(d1), want, rtol=0.1, atol=1e-5)
     # an unchanged cache gives zero drift
     d2 = P.proxy_drift(sums, counts, wq, to_dev(_bits(k1, cfg.dtype), cfg.dtype), cfg.n_heads, scores, lse,
                        first=False)
