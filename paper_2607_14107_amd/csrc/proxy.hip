@@ -276,7 +276,337 @@ __global__ __launch_bounds__(kKmBlock) void kmeans_kernel(const char* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// polestar_proxy_drift kernels
+// polestar_cluster for windows of at most kGramMaxWin positions: the same
+// K-means, run on the window's Gram matrix.  Every centroid is a combination
+// z_k = sum_j C[k][j] u_j of the window's directions u_j = h_j / |h_j| (a
+// start point, or the normalised sum of a cluster's members), hence
+//   cos(u_i, z_k) = sum_j C[k][j] (u_i . u_j),
+//   |sum_{j in M} u_j|^2 = sum_{j, l in M} u_j . u_l.
+// kmeans_gram_kernel, one workgroup per sequence:
+//   1. G = (h_i . h_j) with MFMAs, the window rows staged in LDS 256 bytes of
+//      each row at a time (upper-triangle tiles, mirrored);
+//   2. the rounds on G_ij / (|h_i| |h_j|) and C, all in LDS: the cosines are
+//      G C^T and a new centroid's squared norm is the sum of G over its
+//      member pairs, both as small fp32 MFMA products (fixed order:
+//      deterministic);
+//   3. labels and counts.
+// Then, over many workgroups (channel ranges), kmeans_centroid_kernel writes
+// the unit centroids sum_j C[k][j] u_j and kmeans_sum_kernel the raw sums
+// (points in order, as the direct kernel).  The rows are read three times
+// instead of twice per round.
+// ---------------------------------------------------------------------------
+
+constexpr int kGramBlock = 512;                 // 8 waves
+constexpr int kGramWaves = kGramBlock / kWave;
+constexpr int kGramMaxWin = 176;                // 11 row tiles: G fits in LDS
+constexpr int kGramTiles = kGramMaxWin / 16;
+constexpr int kGramPairs = kGramTiles * (kGramTiles + 1) / 2;
+constexpr int kGramPairsPerWave = (kGramPairs + kGramWaves - 1) / kGramWaves;
+constexpr int kGramLda = 272;                   // staged row pitch (bytes): conflict-free fragments
+constexpr int kGramPitch = kGramMaxWin + 4;     // G row pitch (floats; 16-byte rows)
+constexpr int kGramRowsPerThread = (kGramMaxWin * 16 + kGramBlock - 1) / kGramBlock;
+constexpr int kGramStageBytes = 2 * kGramMaxWin * kGramLda;
+constexpr int kGramBytes = kGramMaxWin * kGramPitch * 4;
+constexpr int kGramUnionBytes = kGramStageBytes > kGramBytes ? kGramStageBytes : kGramBytes;
+
+template <bool BF16>
+__global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __restrict__ h, int seq, int d,
+                                                                 const int32_t* __restrict__ win_idx, int n,
+                                                                 int K, int iters, int32_t* __restrict__ labels_out,
+                                                                 float* __restrict__ sums,
+                                                                 int32_t* __restrict__ counts,
+                                                                 float* __restrict__ centroids) {
+    __shared__ __align__(16) char un[kGramUnionBytes];   // staging (phase 1), then G
+    __shared__ __align__(16) float cf[kMaxClusters][kGramMaxWin];   // C
+    __shared__ float cosv[kGramMaxWin][kMaxClusters + 1];
+    __shared__ float invn[kGramMaxWin];
+    __shared__ float tsum[kGramMaxWin];
+    __shared__ __align__(16) int lab[kGramMaxWin];
+    __shared__ int posw[kGramMaxWin];
+    __shared__ float nrm[kMaxClusters];
+    __shared__ int cnt_s[kMaxClusters];
+    using T = Elem<BF16>;
+    constexpr int ES = T::kBytes;
+    const int b = blockIdx.x;
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const char* hb = h + static_cast<size_t>(b) * seq * d * ES;
+    const int32_t* wi = win_idx + static_cast<size_t>(b) * n;
+    float* G = reinterpret_cast<float*>(un);
+    const int nt = (n + 15) / 16;
+    const int npairs = nt * (nt + 1) / 2;
+
+    // window entries are clamped into [0, seq): a bad index cannot leave the rows
+    for (int i = t; i < n; i += kGramBlock) posw[i] = min(max(wi[i], 0), seq - 1);
+    __syncthreads();
+
+    // 1. Gram matrix.  Wave w owns the upper-triangle tile pairs w, w + 8, ...
+    int pti[kGramPairsPerWave], ptj[kGramPairsPerWave];
+#pragma unroll
+    for (int r = 0; r < kGramPairsPerWave; ++r) {
+        int q = w + kGramWaves * r, ti = 0;
+        if (q >= npairs) q = 0;                          // idle slot: computes pair 0, never stored
+        while (q >= nt - ti) { q -= nt - ti; ++ti; }
+        pti[r] = ti;
+        ptj[r] = ti + q;
+    }
+    floatx4 acc[kGramPairsPerWave];
+#pragma unroll
+    for (int r = 0; r < kGramPairsPerWave; ++r) acc[r] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // staging thread t moves 16-byte chunk t%16 of rows t/16 + 32r; rows past
+    // the window read the first window row and are stored as zeros
+    const char* srow[kGramRowsPerThread];
+#pragma unroll
+    for (int r = 0; r < kGramRowsPerThread; ++r) {
+        const int row = (t >> 4) + 32 * r;
+        srow[r] = hb + static_cast<size_t>(posw[row < n ? row : 0]) * d * ES + (t & 15) * 16;
+    }
+    const int nstages = d * ES / 256;
+    auto load_stage = [&](int st, uint4 (&ra)[kGramRowsPerThread]) {
+#pragma unroll
+        for (int r = 0; r < kGramRowsPerThread; ++r) ra[r] = ld16(srow[r] + min(st, nstages - 1) * 256);
+    };
+    auto store_stage = [&](int buf, const uint4 (&ra)[kGramRowsPerThread]) {
+#pragma unroll
+        for (int r = 0; r < kGramRowsPerThread; ++r) {
+            const int row = (t >> 4) + 32 * r;
+            if (row < nt * 16) st16(un + buf * (kGramMaxWin * kGramLda) + row * kGramLda + (t & 15) * 16,
+                                    row < n ? ra[r] : zero16());
+        }
+    };
+    const int frag = (lane & 15) * kGramLda + (lane >> 4) * 16;
+    auto compute = [&](int buf) {
+        const char* sb = un + buf * (kGramMaxWin * kGramLda) + frag;
+#pragma unroll
+        for (int r = 0; r < kGramPairsPerWave; ++r) {
+            if (w + kGramWaves * r < npairs) {
+#pragma unroll
+                for (int p = 0; p < 4; ++p) {
+                    const uint4 a = *reinterpret_cast<const uint4*>(sb + pti[r] * 16 * kGramLda + 64 * p);
+                    const uint4 bb = *reinterpret_cast<const uint4*>(sb + ptj[r] * 16 * kGramLda + 64 * p);
+                    acc[r] = Mma<BF16>::step(a, bb, acc[r]);
+                }
+            }
+        }
+    };
+    // two stages in flight (register ring of three): stage st+1 is stored
+    // into LDS at the end of stage st while stage st+2 is still loading
+    uint4 q0[kGramRowsPerThread], q1[kGramRowsPerThread], q2[kGramRowsPerThread];
+    load_stage(0, q0);
+    load_stage(1, q1);
+    load_stage(2, q2);
+    store_stage(0, q0);
+    __syncthreads();
+#define PS_GRAM_STEP(ST, Q_STORE, Q_LOAD)                                   \
+    {                                                                       \
+        const int st_ = (ST);                                               \
+        compute(st_ & 1);                                                   \
+        if (st_ + 1 < nstages) store_stage((st_ + 1) & 1, Q_STORE);         \
+        __syncthreads();                                                    \
+        load_stage(st_ + 3, Q_LOAD);                                        \
+    }
+    int sc = 0;
+    for (; sc + 3 <= nstages; sc += 3) {   // stage st sits in q(st % 3)
+        PS_GRAM_STEP(sc, q1, q0)
+        PS_GRAM_STEP(sc + 1, q2, q1)
+        PS_GRAM_STEP(sc + 2, q0, q2)
+    }
+    if (sc < nstages) PS_GRAM_STEP(sc, q1, q0)
+    if (sc + 1 < nstages) PS_GRAM_STEP(sc + 1, q2, q1)
+#undef PS_GRAM_STEP
+    // lane l holds G[16 ti + 4 (l/16) + i][16 tj + l%16], i = 0..3 (and its mirror)
+#pragma unroll
+    for (int r = 0; r < kGramPairsPerWave; ++r) {
+        if (w + kGramWaves * r < npairs) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int gi = pti[r] * 16 + 4 * (lane >> 4) + i, gj = ptj[r] * 16 + (lane & 15);
+                G[gi * kGramPitch + gj] = acc[r][i];
+                if (pti[r] != ptj[r]) G[gj * kGramPitch + gi] = acc[r][i];   // a diagonal tile holds both halves
+            }
+        }
+    }
+    __syncthreads();
+
+    // 2. rounds on the cosine Gram matrix
+    for (int i = t; i < n; i += kGramBlock) {
+        const float g = G[i * kGramPitch + i];
+        invn[i] = g > 0.f ? 1.0f / sqrtf(g) : 0.f;
+    }
+    __syncthreads();
+    for (int e = t; e < n * n; e += kGramBlock) {
+        const int i = e / n, j = e - i * n;
+        G[i * kGramPitch + j] = G[i * kGramPitch + j] * invn[i] * invn[j];
+    }
+    // centroid k starts at the point of window rank floor(k n / K); C (all 16
+    // rows) and the labels are padded with zeros / -1 to n4 = n rounded up to 4
+    const int n4 = (n + 3) & ~3;
+    for (int e = t; e < kMaxClusters * n4; e += kGramBlock) {
+        const int k = e / n4, j = e - k * n4;
+        cf[k][j] = k < K && j == static_cast<int>((static_cast<long>(k) * n) / K) ? 1.f : 0.f;
+    }
+    for (int j = n + t; j < n4; j += kGramBlock) lab[j] = -1;
+    __syncthreads();
+    // Products of G with 16 columns (one per cluster), v_mfma_f32_16x16x4f32
+    // over j in order: wave w takes the 16-point tiles w, w + 8.  Lane l
+    // feeds G[i0 + l%16][j0 + l/16] and column l%16 at j0 + l/16, and holds
+    // the result of points i0 + 4 (l/16) + r, column l%16.
+    //   mode 0: column k = C[k][.]            -> cosines of the points
+    //   mode 1: column k = (label == k)        -> sum of G over the point's cluster
+    auto gram_product = [&](int mode) {
+        for (int tile = w; tile < nt; tile += kGramWaves) {
+            const int i0 = tile * 16;
+            const float* gi = G + (i0 + (lane & 15)) * kGramPitch + (lane >> 4);
+            const int col = lane & 15;
+            auto bval = [&](int j0) {
+                const int j = j0 + (lane >> 4);
+                return mode == 0 ? cf[col][j] : (lab[j] == col ? 1.f : 0.f);
+            };
+            // two interleaved chains (j0 = 0, 8, 16, ... and 4, 12, ...), then summed
+            floatx4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+            int j0 = 0;
+            for (; j0 + 8 <= n4; j0 += 8) {
+                const float a0 = gi[j0], b0 = bval(j0), a1 = gi[j0 + 4], b1 = bval(j0 + 4);
+                c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0, c0, 0, 0, 0);
+                c1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1, c1, 0, 0, 0);
+            }
+            if (j0 < n4) c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(gi[j0], bval(j0), c0, 0, 0, 0);
+            const floatx4 c = c0 + c1;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int i = i0 + 4 * (lane >> 4) + r;
+                if (i >= n || col >= K) continue;
+                if (mode == 0) cosv[i][col] = c[r];
+                else if (lab[i] == col) tsum[i] = c[r];
+            }
+        }
+    };
+    for (int it = 0; it <= iters; ++it) {
+        // assignment: cos(point i, centroid k) = sum_j C[k][j] G[i][j]
+        gram_product(0);
+        __syncthreads();
+        for (int i = t; i < n; i += kGramBlock) {
+            int best = 0;
+            float bv = -INFINITY;
+            for (int k = 0; k < K; ++k)
+                if (cosv[i][k] > bv) { bv = cosv[i][k]; best = k; }   // strict: lowest cluster on ties
+            lab[i] = best;
+        }
+        if (t < kMaxClusters) cnt_s[t] = 0;
+        __syncthreads();
+        if (it == iters) break;                          // the last round only assigns
+        // update: |sum of the members' directions|^2 = sum over member pairs of G
+        for (int i = t; i < n; i += kGramBlock) atomicAdd(&cnt_s[lab[i]], 1);
+        gram_product(1);
+        __syncthreads();
+        for (int k = w; k < K; k += kGramWaves) {
+            float s2 = 0.f;
+            for (int j = lane; j < n; j += kWave) s2 += lab[j] == k ? tsum[j] : 0.f;
+            s2 = wave_sum(s2);
+            if (lane == 0) nrm[k] = s2;
+        }
+        __syncthreads();
+        // clusters with no member keep their centroid
+        for (int e = t; e < K * n4; e += kGramBlock) {
+            const int k = e / n4, j = e - k * n4;
+            if (cnt_s[k] > 0 && nrm[k] > 0.f) cf[k][j] = lab[j] == k ? 1.0f / sqrtf(nrm[k]) : 0.f;
+        }
+        __syncthreads();
+    }
+
+    // 3. outputs: labels by position, counts, raw sums, unit centroids
+    for (int i = t; i < n; i += kGramBlock) atomicAdd(&cnt_s[lab[i]], 1);
+    for (int p = t; p < seq; p += kGramBlock) labels_out[static_cast<size_t>(b) * seq + p] = -1;
+    __syncthreads();
+    for (int i = t; i < n; i += kGramBlock) labels_out[static_cast<size_t>(b) * seq + posw[i]] = lab[i];
+    if (t < K) counts[static_cast<size_t>(b) * K + t] = cnt_s[t];
+    // the final C and 1/|h_i| go to the caller's sums array (K*n + n <= K*d
+    // floats) for kmeans_centroid_kernel, which kmeans_sum_kernel then
+    // overwrites with the raw sums
+    float* stash = sums + static_cast<size_t>(b) * K * d;
+    for (int e = t; e < K * n; e += kGramBlock) {
+        const int k = e / n, j = e - k * n;
+        stash[e] = cf[k][j];
+    }
+    for (int i = t; i < n; i += kGramBlock) stash[K * n + i] = invn[i];
+}
+
+constexpr int kKmOutBlock = 256;               // output kernels: thread per 4 channels
+
+// Unit centroids z_k = sum_i C[k][i] h_i / |h_i| (points in order) from the
+// stash kmeans_gram_kernel leaves in the sums array.
+template <bool BF16>
+__global__ __launch_bounds__(kKmOutBlock) void kmeans_centroid_kernel(const char* __restrict__ h, int seq, int d,
+                                                                      const int32_t* __restrict__ win_idx, int n,
+                                                                      int K, const float* __restrict__ stash_all,
+                                                                      float* __restrict__ centroids) {
+    __shared__ float w_s[kMaxClusters][kGramMaxWin];   // C[k][i] / |h_i|
+    __shared__ int pos_s[kGramMaxWin];
+    constexpr int ES = Elem<BF16>::kBytes;
+    const int b = blockIdx.y;
+    const int t = threadIdx.x;
+    const float* stash = stash_all + static_cast<size_t>(b) * K * d;
+    for (int e = t; e < K * n; e += kKmOutBlock) {
+        const int k = e / n, i = e - k * n;
+        w_s[k][i] = stash[e] * stash[K * n + i];
+    }
+    for (int i = t; i < n; i += kKmOutBlock)
+        pos_s[i] = min(max(win_idx[static_cast<size_t>(b) * n + i], 0), seq - 1);
+    __syncthreads();
+    const int c = (blockIdx.x * kKmOutBlock + t) * 4;
+    if (c >= d) return;
+    const char* hb = h + static_cast<size_t>(b) * seq * d * ES;
+    float4 acc[kMaxClusters];
+#pragma unroll
+    for (int k = 0; k < kMaxClusters; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i0 = 0; i0 < n; i0 += 16) {     // loads of 16 points issued before any is used
+        float4 v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = load4<BF16>(hb + static_cast<size_t>(pos_s[min(i0 + u, n - 1)]) * d * ES, c);
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const int i = i0 + u;
+            if (i >= n) break;
+#pragma unroll
+            for (int k = 0; k < kMaxClusters; ++k) {
+                if (k < K) {
+                    const float wk = w_s[k][i];
+                    acc[k].x = fmaf(v[u].x, wk, acc[k].x);
+                    acc[k].y = fmaf(v[u].y, wk, acc[k].y);
+                    acc[k].z = fmaf(v[u].z, wk, acc[k].z);
+                    acc[k].w = fmaf(v[u].w, wk, acc[k].w);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < kMaxClusters; ++k)
+        if (k < K) *reinterpret_cast<float4*>(centroids + (static_cast<size_t>(b) * K + k) * d + c) = acc[k];
+}
+
+// Raw sums of the final clusters (points in order, as the direct kernel).
+template <bool BF16>
+__global__ __launch_bounds__(kKmOutBlock) void kmeans_sum_kernel(const char* __restrict__ h, int seq, int d,
+                                                                 const int32_t* __restrict__ win_idx, int n, int K,
+                                                                 const int32_t* __restrict__ labels,
+                                                                 float* __restrict__ sums) {
+    __shared__ int lab_s[kMaxWin];
+    __shared__ float inv_unused[1];
+    const int b = blockIdx.y;
+    const int t = threadIdx.x;
+    const int32_t* wi = win_idx + static_cast<size_t>(b) * n;
+    for (int i = t; i < n; i += kKmOutBlock)
+        lab_s[i] = labels[static_cast<size_t>(b) * seq + min(max(wi[i], 0), seq - 1)];
+    __syncthreads();
+    const int c = (blockIdx.x * kKmOutBlock + t) * 4;
+    if (c >= d) return;
+    float4 acc[kMaxClusters];
+    quad_sums<BF16, false>(h + static_cast<size_t>(b) * seq * d * Elem<BF16>::kBytes, wi, seq, n, d, c,
+                           inv_unused, lab_s, acc);
+#pragma unroll
+    for (int k = 0; k < kMaxClusters; ++k)
+        if (k < K) *reinterpret_cast<float4*>(sums + (static_cast<size_t>(b) * K + k) * d + c) = acc[k];
+}
+
 // ---------------------------------------------------------------------------
 // polestar_proxy_drift kernels
 // ---------------------------------------------------------------------------
@@ -673,6 +1003,27 @@ extern "C" polestar_status polestar_cluster(polestar_dtype dtype, int batch, int
         d % (dtype == POLESTAR_BF16 ? 512 : 256) != 0 || !aligned16(h) || !aligned16(sums) ||
         !aligned16(centroids))
         return POLESTAR_ERR_UNSUPPORTED;
+    // the Gram path stashes (K + 1) * n_win floats in each sequence's K * d sums
+    if (n_win <= kGramMaxWin && static_cast<long>(n_clusters) * d >= static_cast<long>(n_clusters + 1) * n_win) {
+        const char* hc = static_cast<const char*>(h);
+        const dim3 out_grid(ceil_div(d, 4 * kKmOutBlock), batch);
+        if (dtype == POLESTAR_BF16) {
+            hipLaunchKernelGGL((kmeans_gram_kernel<true>), dim3(batch), dim3(kGramBlock), 0, stream, hc, seq, d,
+                               win_idx, n_win, n_clusters, iters, labels, sums, counts, centroids);
+            hipLaunchKernelGGL((kmeans_centroid_kernel<true>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq,
+                               d, win_idx, n_win, n_clusters, sums, centroids);
+            hipLaunchKernelGGL((kmeans_sum_kernel<true>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq, d,
+                               win_idx, n_win, n_clusters, labels, sums);
+        } else {
+            hipLaunchKernelGGL((kmeans_gram_kernel<false>), dim3(batch), dim3(kGramBlock), 0, stream, hc, seq, d,
+                               win_idx, n_win, n_clusters, iters, labels, sums, counts, centroids);
+            hipLaunchKernelGGL((kmeans_centroid_kernel<false>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq,
+                               d, win_idx, n_win, n_clusters, sums, centroids);
+            hipLaunchKernelGGL((kmeans_sum_kernel<false>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq, d,
+                               win_idx, n_win, n_clusters, labels, sums);
+        }
+        return launch_status();
+    }
     const size_t lds = static_cast<size_t>(n_clusters) * d * sizeof(float);
     if (dtype == POLESTAR_BF16)
         hipLaunchKernelGGL((kmeans_kernel<true>), dim3(batch), dim3(kKmBlock), lds, stream,
