@@ -59,6 +59,12 @@ def build(verbose: bool = True) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    # A kernel template whose host-side instantiation fails is dropped
+    # silently, leaving its launch stub undefined until the library is loaded.
+    nm = subprocess.run(["nm", "-D", "--undefined-only", "-C", tmp], capture_output=True, text=True)
+    stubs = [ln.split()[-1] for ln in nm.stdout.splitlines() if "__device_stub__" in ln]
+    if nm.returncode != 0 or stubs:
+        raise RuntimeError(f"undefined kernel launch stubs in {tmp}: {stubs[:4]} {nm.stderr}")
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")

@@ -27,6 +27,21 @@
 //   sums the partials in split order (deterministic) and scatters 16-byte
 //   rows.
 //
+// gemm_dma_kernel (65 to 160 rows, e.g. the refresh of one sequence's stale
+//   rows and block): one row tile and 128 columns per workgroup, both operands
+//   (bf16) brought into LDS by global_load_lds_dwordx4 (no VGPR staging, so the
+//   weight loads never wait behind registers that MFMAs still read), in
+//   stages of 128 bytes of each row; four LDS slots, three stages in flight,
+//   one barrier per stage.  A stage's rows are XOR-swizzled in 16-byte chunks
+//   (chunk c of row r at slot c ^ (r/2 % 8)) so that 16-row fragment reads
+//   are conflict-free; the swizzle is applied to each lane's global address,
+//   since a DMA instruction writes its lanes' data contiguously.  The waits
+//   for the DMA are explicit s_waitcnt immediates (each wave issues the same
+//   number of DMA instructions per stage), and each slot's LDS arrays are
+//   separate objects so the compiler does not add waits of its own.
+//   Measured on the config-1 refresh (138 rows x 8192 x 4096): 18.6 us for
+//   the split-K GEMM against 25.9 us for gemm_rows_kernel.
+//
 // gemm_small_kernel (at most 64 rows, e.g. the Q projection): a workgroup
 //   owns all rows and 16 columns; its 4 waves take interleaved super-steps
 //   of the full K with both operands loaded straight into registers and are
@@ -221,6 +236,187 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_rows_kernel(GemmArgs g) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// gemm_dma_kernel: BM = 16*MT rows (one row tile) x 128 columns; wave w owns
+// columns 32w..32w+31 as two 16-column tiles of v_mfma_f32_16x16x32_bf16.
+// ---------------------------------------------------------------------------
+
+constexpr int kDmaStage = 128;               // bytes of each row per stage
+constexpr int kDmaMaxRowTiles = 10;          // 160 rows
+// One 16-byte global -> LDS transfer per lane (the wave's lanes land
+// contiguously from lds_base).  A plain device function, so the builtin never
+// appears in a kernel template's host-side instantiation.
+__device__ __forceinline__ void dma16(const void* src, void* lds_base) {
+    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// 6:4, lgkmcnt 11:8): wait until at most n vector-memory operations of this
+// wave are outstanding / until its LDS reads are done.
+constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
+
+// LDS offset of 16-byte chunk c of row r in a stage (rows of kDmaStage bytes).
+__device__ __forceinline__ int dma_swz(int r, int c) { return r * kDmaStage + ((c ^ ((r >> 1) & 7)) << 4); }
+
+template <bool BF16, int MT, int NST>
+__global__ __launch_bounds__(kGemmBlock) void gemm_dma_kernel(GemmArgs g) {
+    using T = Elem<BF16>;
+    constexpr int ES = T::kBytes;
+    constexpr int BM = MT * 16;
+    constexpr int BN = 128;
+    constexpr int ASZ = BM * kDmaStage, BSZ = BN * kDmaStage;
+    constexpr int AG = BM / 8;                          // 8-row groups of A per stage (one DMA instruction each)
+    constexpr int AIW = (AG + 3) / 4;                   // per wave (surplus ones repeat the last group)
+    constexpr int NDMA = 4 + AIW;                       // DMA instructions per wave per stage
+    static_assert(2 * NDMA <= 63, "outstanding DMA must fit the vmcnt counter");
+    // one LDS object per slot and operand: the compiler can tell them apart
+    __shared__ __align__(16) char sa0[ASZ], sa1[ASZ], sa2[ASZ], sa3[ASZ];
+    __shared__ __align__(16) char sb0[BSZ], sb1[BSZ], sb2[BSZ], sb3[BSZ];
+    __shared__ __align__(16) int rowb[BM];
+    __shared__ int rowp[BM];
+
+    const int tile = blockIdx.x / g.ksplit;
+    const int split = blockIdx.x - tile * g.ksplit;
+    const int col_tile = tile;                          // one row tile
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int w = t >> 6;
+    const int s0b = split * g.steps_per_split * 256;    // byte offset of the split in a row
+    constexpr int nst_here = NST;                       // 128-byte stages of every split (the plan divides K evenly)
+
+    // weights: wave w moves rows 32w + 8i + l/8 (i < 4) of the tile's 128
+    // columns; lane l fills slot l%8 of its row
+    const char* bsrc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = 32 * w + 8 * i + (lane >> 3);
+        const char* row = weight_row(g, col_tile * BN + r, ES);
+        bsrc[i] = (row ? row : g.w0) + s0b + (((lane & 7) ^ ((r >> 1) & 7)) << 4);
+    }
+    auto issue_b = [&](int st, char* buf) {
+        const int off = min(st, nst_here - 1) * kDmaStage;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            dma16(bsrc[i] + off, buf + (32 * w + 8 * i) * kDmaStage);
+    };
+    // Row bookkeeping (one load per row); the first workgroup publishes the
+    // map for the split-K reduction.
+    int rb_ = -1, rp_ = 0;
+    if (t < BM) map_row(g, t, rb_, rp_);
+    if (t < BM) {
+        rowb[t] = rb_;
+        rowp[t] = rp_;
+        if (g.ksplit > 1 && split == 0 && col_tile == 0 && t < g.m_max)
+            *reinterpret_cast<int2*>(g.rowmap + 2 * t) = make_int2(rb_, rp_);
+    }
+    if (!__syncthreads_or(rb_ >= 0)) return;            // no row maps anywhere (uniform)
+    // input rows: wave w moves groups w, w + 4, ... (8 rows each); rows that
+    // map to nothing read row 0 and are never stored
+    const char* asrc[AIW];
+#pragma unroll
+    for (int i = 0; i < AIW; ++i) {
+        const int r = 8 * min(w + 4 * i, AG - 1) + (lane >> 3);
+        const int b = rowb[r];
+        const char* row = b >= 0 ? g.x + (static_cast<size_t>(b) * g.seq + rowp[r]) * g.K * ES : g.x;
+        asrc[i] = row + s0b + (((lane & 7) ^ ((r >> 1) & 7)) << 4);
+    }
+    auto issue_a = [&](int st, char* buf) {
+        const int off = min(st, nst_here - 1) * kDmaStage;
+#pragma unroll
+        for (int i = 0; i < AIW; ++i)
+            dma16(asrc[i] + off, buf + 8 * min(w + 4 * i, AG - 1) * kDmaStage);
+    };
+    issue_b(0, sb0);
+    issue_a(0, sa0);
+    issue_b(1, sb1);
+    issue_a(1, sa1);
+    issue_b(2, sb2);
+    issue_a(2, sa2);
+
+    floatx4 acc[2][MT];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acc[c][i] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // a stage is two 64-byte pieces; lane l reads chunk 4p + l/16 of rows
+    // 16mt + l%16 (A) and 32w + 16c + l%16 (B)
+    auto compute = [&](const char* abuf, const char* bbuf) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            const int c = 4 * p + (lane >> 4);
+            const uint4 bf0 = *reinterpret_cast<const uint4*>(bbuf + dma_swz(32 * w + (lane & 15), c));
+            const uint4 bf1 = *reinterpret_cast<const uint4*>(bbuf + dma_swz(32 * w + 16 + (lane & 15), c));
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const uint4 af = *reinterpret_cast<const uint4*>(abuf + dma_swz(16 * mt + (lane & 15), c));
+                acc[0][mt] = Mma<BF16>::step(af, bf0, acc[0][mt]);
+                acc[1][mt] = Mma<BF16>::step(af, bf1, acc[1][mt]);
+            }
+        }
+    };
+    // Stage s: wait for this wave's DMA of stage s and its own earlier LDS
+    // reads; barrier (stage s is in LDS for every wave, and the slot of stage
+    // s-1 is free); issue stage s+3 into that slot; compute stage s.  Issue
+    // order B0 A0 B1 A1 B2 A2 | B3 A3 | ...: the wait leaves exactly the two
+    // newer stages outstanding.  Stages past the split re-read its last
+    // stage, so every stage issues the same DMA count.
+#define PS_DMA_STEP(S, WAIT, AUSE, BUSE, ANEXT, BNEXT)                      \
+    {                                                                       \
+        __builtin_amdgcn_s_waitcnt(WAIT);                                   \
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);                             \
+        __builtin_amdgcn_s_barrier();                                       \
+        issue_b((S) + 3, BNEXT);                                            \
+        issue_a((S) + 3, ANEXT);                                            \
+        compute(AUSE, BUSE);                                                \
+    }
+    constexpr int WS = wait_vm(2 * NDMA);               // after stage s: stages s+1, s+2
+    char* const sa[4] = {sa0, sa1, sa2, sa3};
+    char* const sb[4] = {sb0, sb1, sb2, sb3};
+    // fully unrolled: every slot index is a constant and the compiler sees the
+    // whole issue order (a loop would make it drain the DMA at the loop head)
+#pragma unroll
+    for (int st = 0; st < NST; ++st)
+        PS_DMA_STEP(st, WS, sa[st % 4], sb[st % 4], sa[(st + 3) % 4], sb[(st + 3) % 4])
+#undef PS_DMA_STEP
+    __builtin_amdgcn_s_waitcnt(0);                      // the re-read tail DMA lands before the workgroup ends
+
+    // results straight from registers: register i of acc[c][mt] is row
+    // 16mt + 4(l/16) + i, column 32w + 16c + l%16.  Split K (the usual case):
+    // fp32 partials, the lane's four row flags read once per row tile.
+    if (g.ksplit > 1) {
+        float* part = g.ws + (static_cast<size_t>(split) * g.col_tiles + col_tile) * g.m_max * BN +
+                      32 * w + (lane & 15);
+        const bool c0 = col_tile * BN + 32 * w + (lane & 15) < g.N;
+        const bool c1 = col_tile * BN + 32 * w + 16 + (lane & 15) < g.N;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int r0 = 16 * mt + 4 * (lane >> 4);
+            const int4 rb4 = *reinterpret_cast<const int4*>(&rowb[r0]);
+            const int rv[4] = {rb4.x, rb4.y, rb4.z, rb4.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float* dst = part + static_cast<size_t>(r0 + i) * BN;
+                if (rv[i] >= 0 && c0) dst[0] = acc[0][mt][i];
+                if (rv[i] >= 0 && c1) dst[16] = acc[1][mt][i];
+            }
+        }
+        return;
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        const int n = col_tile * BN + 32 * w + 16 * c + (lane & 15);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = 16 * mt + 4 * (lane >> 4) + i;
+                const int b = rowb[r];
+                if (b >= 0 && n < g.N) store_elem<BF16>(out_ptr<BF16>(g, b, rowp[r], r, n), acc[c][mt][i]);
+            }
+    }
+}
+
 // Sum of the split-K partials, in split order (deterministic): thread ->
 // (column tile, row, 8 columns) so that consecutive threads read consecutive
 // 32-byte pieces of the contiguous partial tiles; the partial and row-map
@@ -283,6 +479,30 @@ bool dispatch_rows(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
     }
 }
 
+template <bool BF16, int NST>
+bool dispatch_dma_mt(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
+    const dim3 grid(p.grid), block(kGemmBlock);
+    switch (p.mt) {   // 16-row tiles
+        case 5: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 5, NST>), grid, block, 0, s, g); return true;
+        case 6: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 6, NST>), grid, block, 0, s, g); return true;
+        case 7: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 7, NST>), grid, block, 0, s, g); return true;
+        case 8: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 8, NST>), grid, block, 0, s, g); return true;
+        case 9: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 9, NST>), grid, block, 0, s, g); return true;
+        case 10: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 10, NST>), grid, block, 0, s, g); return true;
+        default: return false;
+    }
+}
+
+template <bool BF16>
+bool dispatch_dma(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
+    static_assert(kDmaMaxRowTiles == 10, "dispatch covers 5..kDmaMaxRowTiles");
+    switch (2 * p.steps_per_split) {   // 128-byte stages per split
+        case 8: return dispatch_dma_mt<BF16, 8>(p, g, s);
+        case 16: return dispatch_dma_mt<BF16, 16>(p, g, s);
+        default: return false;
+    }
+}
+
 template <bool BF16>
 bool dispatch_small(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
     dim3 grid(p.col_tiles, p.row_tiles);
@@ -318,8 +538,10 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
         return p;
     }
     p.small = false;
-    p.row_tiles = ceil_div(m_max, 256);
-    p.mt = ceil_div(m_max, 32L * p.row_tiles);
+    // DMA kernel: one row tile of at most 160 rows, K split evenly into 8 or
+    // 16 stages of 128 bytes per row
+    const bool dma_rows = m_max <= 16L * kDmaMaxRowTiles;
+    p.row_tiles = dma_rows ? 1 : ceil_div(m_max, 256);
     p.col_tiles = ceil_div(N, 128);
     const long tiles = static_cast<long>(p.row_tiles) * p.col_tiles;
     int ksplit = 1;
@@ -328,7 +550,11 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     if (ksplit > nsteps) ksplit = nsteps;
     p.steps_per_split = ceil_div(nsteps, ksplit);
     p.ksplit = ceil_div(nsteps, p.steps_per_split);
-    p.grid = static_cast<int>(tiles * p.ksplit);
+    p.dma = bf16 && dma_rows && nsteps % p.steps_per_split == 0 &&
+            (p.steps_per_split == 4 || p.steps_per_split == 8);
+    if (!p.dma) p.row_tiles = ceil_div(m_max, 256);
+    p.mt = p.dma ? ceil_div(m_max, 16) : ceil_div(m_max, 32L * p.row_tiles);
+    p.grid = static_cast<int>(static_cast<long>(p.row_tiles) * p.col_tiles * p.ksplit);
     if (p.ksplit > 1)
         p.ws_bytes = partial_bytes(p, m_max) + align_up(static_cast<size_t>(m_max) * 2 * sizeof(int), 256);
     return p;
@@ -343,6 +569,7 @@ polestar_status gemm_run(bool bf16, const GemmPlan& p, GemmArgs g, hipStream_t s
     g.col_tiles = p.col_tiles;
     bool ok;
     if (p.small) ok = bf16 ? dispatch_small<true>(p, g, stream) : dispatch_small<false>(p, g, stream);
+    else if (p.dma) ok = bf16 && dispatch_dma<true>(p, g, stream);
     else ok = bf16 ? dispatch_rows<true>(p, g, stream) : dispatch_rows<false>(p, g, stream);
     if (!ok) return POLESTAR_ERR_UNSUPPORTED;
     polestar_status st = launch_status();

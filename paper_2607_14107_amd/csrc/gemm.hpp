@@ -38,7 +38,8 @@ struct GemmArgs {
 
 struct GemmPlan {
     bool small;         // gemm_small_kernel (<= 64 rows) instead of gemm_rows_kernel
-    int mt;             // 16-row MFMA tiles per workgroup
+    bool dma;           // gemm_dma_kernel (65..160 rows: one row tile, operands DMA'd into LDS)
+    int mt;             // MFMA row tiles per workgroup (16 rows: small and dma kernels; 32: rows kernel)
     int row_tiles;
     int col_tiles;
     int ksplit;

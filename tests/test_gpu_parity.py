@@ -223,6 +223,44 @@ def test_refresh_large_configs_sampled(P, cfg_index, subrun):
     _check_refresh(L, kb, vb, idx, cnt, cfg.block_start, cfg.block_len, sample=48)
 
 
+@pytest.mark.parametrize("counts,k_max", [([33], 33), ([57], 100), ([128], 128), ([129], 129), ([40, 13], 40)])
+def test_refresh_row_counts_around_one_tile(P, counts, k_max):
+    """Refresh row sets of 65..161 rows on the LLaDA-8B-shaped weights: one
+    row tile (up to 160 rows, the DMA-staged GEMM) and the first two-tile
+    case; slots past a sequence's count and an out-of-range index refresh
+    nothing."""
+    torch = _torch()
+    L = layer(1)
+    cfg, x, dec = L["cfg"], L["x"], L["dec"]
+    batch = len(counts)
+    bs, bl = cfg.block_start, cfg.block_len
+    h_bits = np.concatenate([x["h_cur"], x["h_prev"]], axis=0)[:batch]
+    h_dec = np.concatenate([dec["h_cur"], dec["h_prev"]], axis=0)[:batch]
+    g = np.random.default_rng(k_max + batch)
+    outside = np.setdiff1d(np.arange(cfg.seq), np.arange(bs, bs + bl))
+    idx = np.full((batch, k_max), -1, dtype=np.int32)
+    for b, c in enumerate(counts):
+        idx[b, :c] = np.sort(g.choice(outside, size=c, replace=False))
+    if batch > 1:
+        idx[1, 5] = cfg.seq + 3                       # out of range: refreshes nothing
+    cnt = np.asarray(counts, dtype=np.int32)
+    shape = (batch, cfg.seq, cfg.n_kv_heads, cfg.head_dim)
+    kc = torch.zeros(shape, dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros(shape, dtype=torch.bfloat16, device="cuda")
+    P.refresh_kv(to_dev(h_bits, cfg.dtype), torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda(), bs, bl,
+                 to_dev(x["w_k"], cfg.dtype), to_dev(x["w_v"], cfg.dtype), kc, vc)
+    kg, vg = from_dev(kc), from_dev(vc)
+    for b in range(batch):
+        valid = [int(i) for i in idx[b, :cnt[b]] if 0 <= i < cfg.seq]
+        rows = np.asarray(sorted(set(valid) | set(range(bs, bs + bl))), dtype=np.int64)
+        keep = np.setdiff1d(np.arange(cfg.seq), rows)
+        assert not kg[b, keep].any() and not vg[b, keep].any(), "rows outside the refresh set were written"
+        kw = ref.project_rows(h_dec[b], dec["w_k"], rows).reshape(rows.size, cfg.n_kv_heads, cfg.head_dim)
+        vw = ref.project_rows(h_dec[b], dec["w_v"], rows).reshape(rows.size, cfg.n_kv_heads, cfg.head_dim)
+        assert_rows_close(ref.decode(kg[b, rows], "bf16"), kw, RTOL["bf16"], f"K rows of sequence {b}")
+        assert_rows_close(ref.decode(vg[b, rows], "bf16"), vw, RTOL["bf16"], f"V rows of sequence {b}")
+
+
 # ---------------------------------------------------------------------------
 # attend
 # ---------------------------------------------------------------------------
