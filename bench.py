@@ -97,7 +97,7 @@ def algorithmic_cost(cfg, k, es):
 
 # Kernels launched by each call, and the sources they are built from.
 CALL_KERNELS = {
-    "refresh_kv": ("gemm_rows_kernel", "gemm_reduce_kernel", "gemm_small_kernel"),
+    "refresh_kv": ("gemm_dma_kernel", "gemm_reduce_kernel", "gemm_rows_kernel", "gemm_small_kernel"),
     "project_q": ("gemm_small_kernel", "gemm_rows_kernel", "gemm_reduce_kernel"),
     "attend": ("attend_kernel", "attend_merge_kernel"),
     "drift": ("drift_kernel",),

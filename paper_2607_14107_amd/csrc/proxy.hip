@@ -530,7 +530,7 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
     for (int i = t; i < n; i += kGramBlock) stash[K * n + i] = invn[i];
 }
 
-constexpr int kKmOutBlock = 256;               // output kernels: thread per 4 channels
+constexpr int kKmOutBlock = 64;                // output kernels: one wave, thread per 4 channels (many workgroups)
 
 // Unit centroids z_k = sum_i C[k][i] h_i / |h_i| (points in order) from the
 // stash kmeans_gram_kernel leaves in the sums array.
@@ -589,18 +589,21 @@ __global__ __launch_bounds__(kKmOutBlock) void kmeans_sum_kernel(const char* __r
                                                                  const int32_t* __restrict__ win_idx, int n, int K,
                                                                  const int32_t* __restrict__ labels,
                                                                  float* __restrict__ sums) {
-    __shared__ int lab_s[kMaxWin];
+    __shared__ int lab_s[kGramMaxWin];
+    __shared__ int32_t pos_s[kGramMaxWin];
     __shared__ float inv_unused[1];
     const int b = blockIdx.y;
     const int t = threadIdx.x;
     const int32_t* wi = win_idx + static_cast<size_t>(b) * n;
-    for (int i = t; i < n; i += kKmOutBlock)
-        lab_s[i] = labels[static_cast<size_t>(b) * seq + min(max(wi[i], 0), seq - 1)];
+    for (int i = t; i < n; i += kKmOutBlock) {
+        pos_s[i] = min(max(wi[i], 0), seq - 1);
+        lab_s[i] = labels[static_cast<size_t>(b) * seq + pos_s[i]];
+    }
     __syncthreads();
     const int c = (blockIdx.x * kKmOutBlock + t) * 4;
     if (c >= d) return;
     float4 acc[kMaxClusters];
-    quad_sums<BF16, false>(h + static_cast<size_t>(b) * seq * d * Elem<BF16>::kBytes, wi, seq, n, d, c,
+    quad_sums<BF16, false>(h + static_cast<size_t>(b) * seq * d * Elem<BF16>::kBytes, pos_s, seq, n, d, c,
                            inv_unused, lab_s, acc);
 #pragma unroll
     for (int k = 0; k < kMaxClusters; ++k)
