@@ -32,18 +32,19 @@ struct GemmArgs {
     int* rowmap;        // split-K: [m_max][2] (sequence, position) of row m, -1: none
     int m_max;
     int ksplit;
-    int steps_per_split;
+    int steps_per_split;   // 256-byte super-steps per split (tile kernel: 64-byte stages)
     int row_tiles, col_tiles;
 };
 
 struct GemmPlan {
     bool small;         // gemm_small_kernel (<= 64 rows) instead of gemm_rows_kernel
     bool dma;           // gemm_dma_kernel (65..160 rows: one row tile, operands DMA'd into LDS)
+    bool tile;          // gemm_tile_kernel (bf16, more than 160 rows: 256 x 256 tiles)
     int mt;             // MFMA row tiles per workgroup (16 rows: small and dma kernels; 32: rows kernel)
     int row_tiles;
     int col_tiles;
     int ksplit;
-    int steps_per_split;
+    int steps_per_split;   // 256-byte super-steps per split (tile kernel: 64-byte stages)
     int grid;           // workgroups of gemm_rows_kernel
     size_t ws_bytes;    // fp32 partials + row map, 0 when ksplit == 1
 };

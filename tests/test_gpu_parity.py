@@ -223,12 +223,13 @@ def test_refresh_large_configs_sampled(P, cfg_index, subrun):
     _check_refresh(L, kb, vb, idx, cnt, cfg.block_start, cfg.block_len, sample=48)
 
 
-@pytest.mark.parametrize("counts,k_max", [([33], 33), ([57], 100), ([128], 128), ([129], 129), ([40, 13], 40)])
+@pytest.mark.parametrize("counts,k_max", [([33], 33), ([57], 100), ([128], 128), ([129], 129), ([40, 13], 40),
+                                          ([300], 320), ([600, 250], 600), ([700], 735)])
 def test_refresh_row_counts_around_one_tile(P, counts, k_max):
-    """Refresh row sets of 65..161 rows on the LLaDA-8B-shaped weights: one
-    row tile (up to 160 rows, the DMA-staged GEMM) and the first two-tile
-    case; slots past a sequence's count and an out-of-range index refresh
-    nothing."""
+    """Refresh row sets on the LLaDA-8B-shaped weights: 65..160 rows (one row
+    tile, the DMA-staged GEMM), the first two-tile case, and 352..1264 rows
+    (256 x 256 tiles with a ragged last row tile, K split in 2 or 4); slots
+    past a sequence's count and an out-of-range index refresh nothing."""
     torch = _torch()
     L = layer(1)
     cfg, x, dec = L["cfg"], L["x"], L["dec"]
