@@ -52,7 +52,7 @@ __device__ __forceinline__ void scan_body(const char* __restrict__ logits, int v
                                           ScanPart* __restrict__ parts, int split, int j, int b) {
     using T = Elem<BF16>;
     constexpr int ES = T::kBytes;
-    constexpr int G = 4;   // 16-byte chunks per lane kept in flight
+    constexpr int G = 8;   // 16-byte chunks per lane kept in flight
     __shared__ float sm[4], ss[4], sb[4];
     __shared__ int si[4];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -64,9 +64,13 @@ __device__ __forceinline__ void scan_body(const char* __restrict__ logits, int v
     float m = -INFINITY, s = 0.f, bv = -INFINITY;
     int bi = 0x7fffffff;
     // Elements [v0, v1) in 16-byte chunks; chunk c starts at element v0 + c*E.
-    // Straight-line code: chunks past the slice re-read chunk 0 and count as
+    // Straight-line loads: chunks past the slice re-read chunk 0 and count as
     // -inf (no exp contribution, never the argmax); the mask id takes part in
-    // the softmax but not in the argmax.
+    // the softmax but not in the argmax.  A thread visits its elements in
+    // increasing id order, so once it holds a candidate an element can only
+    // replace it by being strictly larger: each chunk's maximum is compared
+    // with the running best, and only a chunk that beats it (or any chunk
+    // before the first candidate) is searched element by element.
     const int nchunks = (v1 - v0) / T::E;
     for (int c0 = 0; c0 < nchunks; c0 += kScanBlock * G) {
         uint4 r[G];
@@ -79,16 +83,25 @@ __device__ __forceinline__ void scan_body(const char* __restrict__ logits, int v
         }
         __builtin_amdgcn_sched_barrier(0);   // all G loads in flight before any use
         float lm = -INFINITY;
+        float cmx[G];
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq) {
+            float f[T::E];
+            T::unpack(r[gq], f);
+            float cm = f[0];
+#pragma unroll
+            for (int e = 1; e < T::E; ++e) cm = fmaxf(cm, f[e]);
+            cmx[gq] = ok[gq] ? cm : -INFINITY;
+            lm = fmaxf(lm, cmx[gq]);
+        }
 #pragma unroll
         for (int gq = 0; gq < G; ++gq) {
             const int vb = v0 + (c0 + gq * kScanBlock + threadIdx.x) * T::E;
-            float f[T::E];
-            T::unpack(r[gq], f);
+            if (ok[gq] && (cmx[gq] > bv || bi == 0x7fffffff)) {
+                float f[T::E];
+                T::unpack(r[gq], f);
 #pragma unroll
-            for (int e = 0; e < T::E; ++e) {
-                const float x = ok[gq] ? f[e] : -INFINITY;
-                lm = fmaxf(lm, x);
-                better(bv, bi, x, vb + e, ok[gq] & (vb + e != mask_id));
+                for (int e = 0; e < T::E; ++e) better(bv, bi, f[e], vb + e, vb + e != mask_id);
             }
         }
         const float mn = fmaxf(m, lm);
@@ -99,11 +112,10 @@ __device__ __forceinline__ void scan_body(const char* __restrict__ logits, int v
         for (int gq = 0; gq < G; ++gq) {
             float f[T::E];
             T::unpack(r[gq], f);
+            float cs = 0.f;
 #pragma unroll
-            for (int e = 0; e < T::E; ++e) {
-                const float x = ok[gq] ? f[e] : -INFINITY;
-                ls += fast_exp2(fmaf(x, kLog2e, -mnl));
-            }
+            for (int e = 0; e < T::E; ++e) cs += fast_exp2(fmaf(f[e], kLog2e, -mnl));
+            ls += ok[gq] ? cs : 0.f;
         }
         s = s * fast_exp2((m - mref) * kLog2e) + ls;
         m = mn;
@@ -240,7 +252,7 @@ inline CommitPlan commit_plan(bool bf16, int batch, int nq, int vocab) {
     CommitPlan p{};
     const int e = bf16 ? 8 : 4;
     const long toks = static_cast<long>(batch) * nq;
-    int splits = static_cast<int>((512 + toks - 1) / toks);
+    int splits = static_cast<int>((2048 + toks - 1) / toks);   // ~2048 workgroups: several resident per CU
     const int max_splits = ceil_div(vocab, 2048);
     if (splits > max_splits) splits = max_splits;
     if (splits > kMaxSplits) splits = kMaxSplits;

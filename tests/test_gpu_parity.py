@@ -478,6 +478,41 @@ def test_commit_plain_config_logits(P, cfg_index):
     assert np.array_equal(gm, (conf > cfg.tau_s) & x["masked"].astype(bool))
 
 
+@pytest.mark.parametrize("cfg_index", [0, 1])
+def test_commit_argmax_edges(P, cfg_index):
+    """Argmax corner cases of the vocabulary scan against the oracle: ties
+    (the lowest id wins, within one vocabulary slice and across slices), the
+    [MASK] id holding the strict maximum, long -inf runs (so that a lane's
+    and a slice's first elements are -inf), a row that is -inf except for its
+    last element, and -inf rows with a tie among their few finite entries."""
+    L = layer(cfg_index)
+    cfg, x = L["cfg"], L["x"]
+    lg = x["logits"].copy()
+    V = lg.shape[-1]
+    mask_id = 5
+    bf16 = cfg.dtype == "bf16"
+
+    def val(v):
+        return np.uint16(np.float32(v).view(np.uint32) >> 16) if bf16 else np.float32(v)
+
+    lg[0, 0, 3] = lg[0, 0, V - 1] = val(60.0)                                    # tie: first and last id
+    lg[0, 1, V // 3] = lg[0, 1, V // 3 + 1] = lg[0, 1, 2 * V // 3] = val(60.0)   # ties in two slices
+    lg[0, 2, mask_id] = val(70.0)                                               # [MASK] is the maximum
+    lg[0, 2, V // 2] = val(65.0)
+    lg[0, 3, : V // 2] = val(-np.inf)                                           # -inf first half
+    lg[0, 3, V - 7] = val(50.0)
+    lg[0, 4, :] = val(-np.inf)                                                  # only the last id finite
+    lg[0, 4, V - 1] = val(0.5)
+    lg[0, 5, :] = val(-np.inf)                                                  # tie among three finite ids
+    for pos in (V // 7, V // 2, V - 3):
+        lg[0, 5, pos] = val(1.0)
+    token, conf = ref.confidence(ref.decode(lg, cfg.dtype), mask_id)
+    assert token[0, :6].tolist() == [3, V // 3, V // 2, V - 7, V - 1, V // 7]
+    gt, gc, _, _, _ = _run_commit(P, cfg, lg, None, None, None, x["masked"], False, mask_id)
+    assert np.array_equal(gt, token)
+    np.testing.assert_allclose(gc, conf, rtol=1e-4)
+
+
 @pytest.mark.parametrize("cfg_index", [0, 1, 2, 3])
 def test_suffix_commit(P, cfg_index):
     """Suffix-block commit: the coverage logits stand for the final-layer packet
