@@ -48,7 +48,7 @@ __device__ __forceinline__ int vslot(int kk) {
 }
 
 template <bool BF16, int HD>
-__global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
+__global__ __launch_bounds__(kAttBlock, 2) void attend_kernel(AttArgs a) {
     using T = Elem<BF16>;
     constexpr int ES = T::kBytes;
     constexpr int NC = HD * ES / 64;        // 16-byte chunks of one lane's d-range
@@ -56,9 +56,13 @@ __global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
     constexpr int DT = HD / 16;             // 16-row d tiles of O^T
     // V^T rows: bf16 32 keys (64 B) + 16 B pad; fp32 32 keys (128 B) + 16 B pad
     constexpr int VP = BF16 ? 80 : 144;
-    __shared__ __align__(16) char vt[4][HD * VP];
+    // The V^T staging of the loop and the wave merge after it share one LDS
+    // array (two workgroups fit per CU instead of one).
+    constexpr int kVtBytes = 4 * HD * VP;
+    constexpr int kWoBytes = 4 * kQG * (HD + 4) * 4;
+    __shared__ __align__(16) char smem[kVtBytes > kWoBytes ? kVtBytes : kWoBytes];
     __shared__ float wm[4][kQG], wl[4][kQG];
-    __shared__ __align__(16) float wo[4][kQG][HD + 4];
+    auto wo = reinterpret_cast<float (*)[kQG][HD + 4]>(smem);
 
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
@@ -98,7 +102,7 @@ __global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
     const int t_end = min(ntiles, t_begin + a.tiles_per_split);
     // Each wave stages and reads only its own V^T region, so no workgroup
     // barrier is needed until the waves are merged.
-    char* myvt = vt[w];
+    char* myvt = smem + w * HD * VP;
     const int wu = __builtin_amdgcn_readfirstlane(w);   // wave-uniform tile choice
 
     for (int base = t_begin; base < t_end; base += 4) {
@@ -255,6 +259,9 @@ __global__ __launch_bounds__(kAttBlock) void attend_kernel(AttArgs a) {
     }
 
     // Merge the four waves.  Lane holds O^T[d = 16 dt + 4 g + i][q = 16 u + (lane & 15)].
+    // The merge buffer overlays the V^T staging: every wave must be done with
+    // its tiles first (all waves run the same number of loop trips).
+    __syncthreads();
     if (lane < 16) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
