@@ -27,8 +27,9 @@
 //   sums the partials in split order (deterministic) and scatters 16-byte
 //   rows.
 //
-// gemm_dma_kernel (65 to 160 rows, e.g. the refresh of one sequence's stale
-//   rows and block): one row tile and 128 columns per workgroup, both operands
+// gemm_dma_kernel (65 to 320 rows, e.g. the refresh of one sequence's stale
+//   rows and block, or the Q projection of a batch's blocks): one of at most
+//   two row tiles of up to 160 rows and 128 columns per workgroup, both operands
 //   (bf16) brought into LDS by global_load_lds_dwordx4 (no VGPR staging, so the
 //   weight loads never wait behind registers that MFMAs still read), in
 //   stages of 128 bytes of each row; four LDS slots, three stages in flight,
@@ -278,7 +279,8 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_dma_kernel(GemmArgs g) {
 
     const int tile = blockIdx.x / g.ksplit;
     const int split = blockIdx.x - tile * g.ksplit;
-    const int col_tile = tile;                          // one row tile
+    const int col_tile = tile % g.col_tiles;
+    const int m0 = (tile / g.col_tiles) * BM;           // one or two row tiles
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int w = t >> 6;
@@ -303,14 +305,14 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_dma_kernel(GemmArgs g) {
     // Row bookkeeping (one load per row); the first workgroup publishes the
     // map for the split-K reduction.
     int rb_ = -1, rp_ = 0;
-    if (t < BM) map_row(g, t, rb_, rp_);
+    if (t < BM) map_row(g, m0 + t, rb_, rp_);
     if (t < BM) {
         rowb[t] = rb_;
         rowp[t] = rp_;
-        if (g.ksplit > 1 && split == 0 && col_tile == 0 && t < g.m_max)
-            *reinterpret_cast<int2*>(g.rowmap + 2 * t) = make_int2(rb_, rp_);
+        if (g.ksplit > 1 && split == 0 && col_tile == 0 && m0 + t < g.m_max)
+            *reinterpret_cast<int2*>(g.rowmap + 2 * (m0 + t)) = make_int2(rb_, rp_);
     }
-    if (!__syncthreads_or(rb_ >= 0)) return;            // no row maps anywhere (uniform)
+    if (!__syncthreads_or(rb_ >= 0)) return;            // no row of this tile maps anywhere (uniform)
     // input rows: wave w moves groups w, w + 4, ... (8 rows each); rows that
     // map to nothing read row 0 and are never stored
     const char* asrc[AIW];
@@ -396,7 +398,7 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_dma_kernel(GemmArgs g) {
             const int rv[4] = {rb4.x, rb4.y, rb4.z, rb4.w};
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                float* dst = part + static_cast<size_t>(r0 + i) * BN;
+                float* dst = part + static_cast<size_t>(m0 + r0 + i) * BN;
                 if (rv[i] >= 0 && c0) dst[0] = acc[0][mt][i];
                 if (rv[i] >= 0 && c1) dst[16] = acc[1][mt][i];
             }
@@ -412,7 +414,7 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_dma_kernel(GemmArgs g) {
             for (int i = 0; i < 4; ++i) {
                 const int r = 16 * mt + 4 * (lane >> 4) + i;
                 const int b = rowb[r];
-                if (b >= 0 && n < g.N) store_elem<BF16>(out_ptr<BF16>(g, b, rowp[r], r, n), acc[c][mt][i]);
+                if (b >= 0 && n < g.N) store_elem<BF16>(out_ptr<BF16>(g, b, rowp[r], m0 + r, n), acc[c][mt][i]);
             }
     }
 }
@@ -772,30 +774,34 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     }
     p.small = false;
     p.col_tiles = ceil_div(N, 128);                     // split-K partials: 128-column tiles
-    // Tile kernel: more rows than one DMA tile; 256 x 256 tiles, K split in
-    // halves while the tiles alone leave compute units idle and each split
-    // keeps at least 16 stages of 32 bf16.  Measured against the row kernel
-    // it wins when at most four splits fill the chip or each split still
-    // runs 48 stages or more; short eight-way splits (e.g. 256 or 512 rows
-    // of a 4096 x 4096 projection) stay on the row kernel.
+    // Tile kernel: more rows than one DMA tile; 256 x 256 tiles, K split
+    // while the tiles alone leave compute units idle.  Measured against the
+    // other kernels it wins when it launches at least 128 workgroups and at
+    // most four splits fill the chip, each split still runs 48 stages or
+    // more, or there are four row tiles or more (the Dream-7B refresh: 1052
+    // rows x 1024 x 3584 in seven splits, 33 us against 44 us); short splits
+    // of one or two row tiles (256 or 512 rows of a 4096 x 4096 projection)
+    // stay on the DMA or row kernel.
     if (bf16 && m_max > 16L * kDmaMaxRowTiles && K % kTileStage == 0) {
-        const int nstage = K / (kTileStage / 2);
-        const long tiles = static_cast<long>(ceil_div(m_max, kTileDim)) * ceil_div(N, kTileDim);
-        int ksplit = 1;
-        while (tiles * ksplit < kTargetWgs && 2 * ksplit <= kMaxSplit && nstage % (8 * ksplit) == 0 &&
-               nstage / (2 * ksplit) >= 16)
-            ksplit *= 2;
-        p.tile = ksplit <= 4 || nstage / ksplit >= 48;
-    }
-    if (p.tile) {
         const int nstage = K / (kTileStage / 2);
         p.row_tiles = ceil_div(m_max, kTileDim);
         const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, kTileDim);
+        // the smallest split that fills the chip, else the largest; every
+        // split runs a whole number of 4-stage loop trips and at least 16 stages
         int ksplit = 1;
-        while (tiles * ksplit < kTargetWgs && 2 * ksplit <= kMaxSplit && nstage % (8 * ksplit) == 0 &&
-               nstage / (2 * ksplit) >= 16)
-            ksplit *= 2;
+        for (int k = 1; k <= kMaxSplit; ++k) {
+            if (nstage % (4 * k) != 0 || nstage / k < 16) continue;
+            ksplit = k;
+            if (tiles * k >= kTargetWgs) break;
+        }
+        p.tile = tiles * ksplit >= kTargetWgs / 2 &&
+                 (ksplit <= 4 || nstage / ksplit >= 48 || p.row_tiles >= 4);
         p.ksplit = ksplit;
+    }
+    if (p.tile) {
+        const int nstage = K / (kTileStage / 2);
+        const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, kTileDim);
+        const int ksplit = p.ksplit;
         p.steps_per_split = nstage / ksplit;
         p.mt = kTileDim / 32;
         p.grid = static_cast<int>(tiles * ksplit);
@@ -803,10 +809,11 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
             p.ws_bytes = partial_bytes(p, m_max) + align_up(static_cast<size_t>(m_max) * 2 * sizeof(int), 256);
         return p;
     }
-    // DMA kernel: one row tile of at most 160 rows, K split evenly into 8 or
-    // 16 stages of 128 bytes per row
-    const bool dma_rows = m_max <= 16L * kDmaMaxRowTiles;
-    p.row_tiles = dma_rows ? 1 : ceil_div(m_max, 256);
+    // DMA kernel: one or two row tiles of at most 160 rows, K split evenly
+    // into 8 or 16 stages of 128 bytes per row (the smallest such split at
+    // or above the one that fills the chip)
+    const bool dma_rows = bf16 && m_max <= 2L * 16 * kDmaMaxRowTiles;
+    p.row_tiles = dma_rows ? ceil_div(m_max, 16L * kDmaMaxRowTiles) : ceil_div(m_max, 256);
     const long tiles = static_cast<long>(p.row_tiles) * p.col_tiles;
     int ksplit = 1;
     if (tiles < kTargetWgs) ksplit = ceil_div(kTargetWgs, tiles);
@@ -814,10 +821,16 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     if (ksplit > nsteps) ksplit = nsteps;
     p.steps_per_split = ceil_div(nsteps, ksplit);
     p.ksplit = ceil_div(nsteps, p.steps_per_split);
-    p.dma = bf16 && dma_rows && nsteps % p.steps_per_split == 0 &&
-            (p.steps_per_split == 4 || p.steps_per_split == 8);
+    p.dma = false;
+    for (int ks = p.ksplit; dma_rows && !p.dma && ks <= kMaxSplit; ++ks) {
+        if (nsteps % ks == 0 && (nsteps / ks == 4 || nsteps / ks == 8)) {
+            p.dma = true;
+            p.ksplit = ks;
+            p.steps_per_split = nsteps / ks;
+        }
+    }
     if (!p.dma) p.row_tiles = ceil_div(m_max, 256);
-    p.mt = p.dma ? ceil_div(m_max, 16) : ceil_div(m_max, 32L * p.row_tiles);
+    p.mt = p.dma ? ceil_div(ceil_div(m_max, p.row_tiles), 16) : ceil_div(m_max, 32L * p.row_tiles);
     p.grid = static_cast<int>(static_cast<long>(p.row_tiles) * p.col_tiles * p.ksplit);
     if (p.ksplit > 1)
         p.ws_bytes = partial_bytes(p, m_max) + align_up(static_cast<size_t>(m_max) * 2 * sizeof(int), 256);
