@@ -401,7 +401,9 @@ inline AttPlan att_plan(int batch, int seq, int H, int nq, int hd) {
     AttPlan p{};
     const int ntiles = ceil_div(seq, kKT);
     const long base = static_cast<long>(batch) * H * ceil_div(nq, kQG);
-    int splits = static_cast<int>((512 + base - 1) / base);
+    // about 512 workgroups, rounded down: two fit per CU, so a grid of at most
+    // 512 runs in one round without a partial second one
+    int splits = static_cast<int>(512 / base);
     const int max_splits = ceil_div(ntiles, 4);      // at least one tile per wave
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
