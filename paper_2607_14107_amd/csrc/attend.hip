@@ -71,10 +71,11 @@ extern "C" polestar_status polestar_project_q(polestar_dtype dtype, int batch, i
 
 namespace ps {
 namespace {
-AttendLayout attend_layout(bool bf16, int batch, int seq, int d, int H, int hd, int nq, bool project) {
+AttendLayout attend_layout(bool bf16, int batch, int seq, int d, int H, int Hkv, int hd, int nq,
+                           bool project) {
     AttendLayout L{};
     if (project) L.qp = gemm_plan(bf16, static_cast<long>(batch) * nq, H * hd, d);
-    L.ap = att_plan(batch, seq, H, nq, hd);
+    L.ap = att_plan(bf16, batch, seq, H, Hkv, nq, hd);
     L.q_ws = align_up(L.qp.ws_bytes, 256);
     L.total = L.q_ws + L.ap.part_bytes;
     return L;
@@ -90,7 +91,8 @@ extern "C" size_t polestar_attend_workspace_size(polestar_dtype dtype, int batch
     if (!dtype_ok(dtype) || batch <= 0 || seq <= 0 || d <= 0 || n_heads <= 0 || n_kv_heads <= 0 ||
         head_dim <= 0 || block_len <= 0)
         return 0;
-    return attend_layout(dtype == POLESTAR_BF16, batch, seq, d, n_heads, head_dim, block_len, true).total;
+    return attend_layout(dtype == POLESTAR_BF16, batch, seq, d, n_heads, n_kv_heads, head_dim, block_len, true)
+        .total;
 }
 
 extern "C" polestar_status polestar_attend(polestar_dtype dtype, int batch, int seq, int d,
@@ -114,7 +116,8 @@ extern "C" polestar_status polestar_attend(polestar_dtype dtype, int batch, int 
     if (batch > 65535 || static_cast<long>(n_heads) * ceil_div(block_len, kQG) > 65535)
         return POLESTAR_ERR_UNSUPPORTED;
     const bool bf16 = dtype == POLESTAR_BF16;
-    const AttendLayout L = attend_layout(bf16, batch, seq, d, n_heads, head_dim, block_len, w_q != nullptr);
+    const AttendLayout L =
+        attend_layout(bf16, batch, seq, d, n_heads, n_kv_heads, head_dim, block_len, w_q != nullptr);
     if (workspace_bytes < L.total || (L.total > 0 && !workspace)) return POLESTAR_ERR_WORKSPACE;
     char* ws = static_cast<char*>(workspace);
 

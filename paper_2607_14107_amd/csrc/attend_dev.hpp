@@ -1,4 +1,5 @@
 // Device side of polestar_attend, shared by attend.hip and the fused step.
+// (Grouped KV heads take attend_group_kernel, described at its definition.)
 //
 // Bidirectional attention of the active block over the whole
 // cache (Sec. 2, eq. 3: queries of J_b attend to the cached K/V of I and the
@@ -391,15 +392,279 @@ __device__ __forceinline__ void merge_body(const AttArgs& a, int blk) {
     if (a.lse && lane == 0) a.lse[(static_cast<size_t>(b) * a.H + h) * a.nq + q] = (M + __log2f(L)) * kLn2;
 }
 
+// Grouped-query attention (bf16).  The H / Hkv query heads of a KV group all
+// read that group's K/V, so the workgroup is (sequence b, KV head, row block,
+// key split): its NW waves each own one (query head, 32-query group) pair of
+// the group and walk the same keys, which the whole workgroup stages once in
+// LDS -- K as [key][d] rows, V^T as attend_kernel lays it out, per 32 keys --
+// 64 keys per step, double-buffered with one barrier per step (the next
+// step's loads are in flight while the current one is computed).  A step
+// computes the scores of both 32-key halves before the softmax, so a wave has
+// eight independent MFMA chains in flight instead of four, and the online
+// softmax rescales once per 64 keys.  There is no wave merge: each wave
+// writes its own output (one split) or its (m, l, O) partial in the layout
+// the merge kernel reads.  Waves past the group's last pair help stage and
+// skip the arithmetic.
+constexpr int kGKT = 64;   // keys per step of the grouped kernel
+
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW) void attend_group_kernel(AttArgs a) {
+    constexpr int NT = 64 * NW;
+    constexpr int NC = HD * 2 / 64;          // 16-byte chunks of one lane's d-range
+    constexpr int DPL = HD / 4;              // d values per lane group
+    constexpr int DT = HD / 16;              // 16-row d tiles of O^T
+    constexpr int VP = 80;                   // V^T row: 32 keys x 2 B + 16 B pad
+    constexpr int KP = HD * 2 + 16;          // K row + 16 B pad: the 16 rows of a fragment read use distinct banks
+    constexpr int KCH = kGKT * HD * 2 / 16;  // 16-byte chunks of a step's K
+    constexpr int KI = (KCH + NT - 1) / NT;
+    constexpr int VU = 16 * HD / 2;          // V staging units: 4 keys x 2 d
+    constexpr int VI = (VU + NT - 1) / NT;
+    __shared__ __align__(16) char ks[2][kGKT * KP];
+    __shared__ __align__(16) char vs[2][2][HD * VP];   // [buffer][32-key half]
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = tid >> 6;
+    const int g = lane >> 4;
+    const int split = blockIdx.x;
+    const int G = a.H / a.Hkv;
+    const int qgroups = (a.nq + kQG - 1) / kQG;
+    const int npairs = G * qgroups;
+    const int pair_raw = blockIdx.y * NW + w;
+    const bool active = pair_raw < npairs;   // wave-uniform
+    const int pair = min(pair_raw, npairs - 1);
+    const int hh = pair / qgroups;
+    const int qg = pair - hh * qgroups;
+    const int b = blockIdx.z / a.Hkv;
+    const int kvh = blockIdx.z - b * a.Hkv;
+    const int h = kvh * G + hh;
+
+    const size_t krow = static_cast<size_t>(a.Hkv) * HD * 2;   // bytes per cache row
+    const char* kbase = a.k + (static_cast<size_t>(b) * a.seq * a.Hkv + kvh) * HD * 2;
+    const char* vbase = a.v + (static_cast<size_t>(b) * a.seq * a.Hkv + kvh) * HD * 2;
+
+    // Q fragments (B operand of S^T), as in attend_kernel.
+    uint4 qf[2][NC];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int q = min(qg * kQG + 16 * u + (lane & 15), a.nq - 1);
+        const char* qp = a.q + ((static_cast<size_t>(b) * a.nq + q) * a.H + h) * HD * 2 + g * DPL * 2;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) qf[u][c] = ld16(qp + 16 * c);
+    }
+
+    floatx4 o[DT][2];
+#pragma unroll
+    for (int i = 0; i < DT; ++i) o[i][0] = o[i][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+    float mrun[2] = {-INFINITY, -INFINITY};
+    float lrun[2] = {0.f, 0.f};
+
+    const int nsteps = (a.seq + kGKT - 1) / kGKT;
+    const int s_begin = split * a.tiles_per_split;
+    const int s_end = min(nsteps, s_begin + a.tiles_per_split);
+
+    // Staging registers of one step: K chunks (16 B) and V units (4 keys x 2 d).
+    // Indices past the step are clamped on load and skipped on store; keys past
+    // seq read the last row (their scores are masked).
+    auto load_step = [&](int step, uint4 (&kr)[KI], uint32_t (&vr)[VI][4]) {
+        const int key0 = step * kGKT;
+#pragma unroll
+        for (int i = 0; i < KI; ++i) {
+            const int c = min(tid + i * NT, KCH - 1);
+            const int key = min(key0 + c / (HD / 8), a.seq - 1);
+            kr[i] = ld16(kbase + static_cast<size_t>(key) * krow + (c % (HD / 8)) * 16);
+        }
+#pragma unroll
+        for (int i = 0; i < VI; ++i) {
+            const int u = min(tid + i * NT, VU - 1);
+            const int dp = u % (HD / 2), kg = u / (HD / 2);   // kg: 4-key group 0..15
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int key = min(key0 + 4 * kg + j, a.seq - 1);
+                vr[i][j] = *reinterpret_cast<const uint32_t*>(vbase + static_cast<size_t>(key) * krow + dp * 4);
+            }
+        }
+    };
+    auto store_step = [&](int buf, const uint4 (&kr)[KI], const uint32_t (&vr)[VI][4]) {
+#pragma unroll
+        for (int i = 0; i < KI; ++i) {
+            const int c = tid + i * NT;
+            if (KCH % NT == 0 || c < KCH)
+                st16(ks[buf] + (c / (HD / 8)) * KP + (c % (HD / 8)) * 16, kr[i]);
+        }
+#pragma unroll
+        for (int i = 0; i < VI; ++i) {
+            const int u = tid + i * NT;
+            if (VU % NT == 0 || u < VU) {
+                const int dp = u % (HD / 2), kg = u / (HD / 2);
+                char* vt = vs[buf][kg >> 3];
+                const int slot = vslot(4 * (kg & 7));
+                const uint2 lo = make_uint2((vr[i][0] & 0xffffu) | (vr[i][1] << 16),
+                                            (vr[i][2] & 0xffffu) | (vr[i][3] << 16));
+                const uint2 hi = make_uint2((vr[i][0] >> 16) | (vr[i][1] & 0xffff0000u),
+                                            (vr[i][2] >> 16) | (vr[i][3] & 0xffff0000u));
+                *reinterpret_cast<uint2*>(vt + (2 * dp) * VP + slot * 2) = lo;
+                *reinterpret_cast<uint2*>(vt + (2 * dp + 1) * VP + slot * 2) = hi;
+            }
+        }
+    };
+    auto compute_step = [&](int buf, int step) {
+        const int key0 = step * kGKT;
+        const char* kb = ks[buf];
+        // S^T tiles st[t][u] = K_t Q_u^T for the four 16-key tiles t of the step.
+        floatx4 st[4][2];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            uint4 kf[NC];
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                kf[c] = *reinterpret_cast<const uint4*>(kb + (16 * t + (lane & 15)) * KP + g * DPL * 2 + 16 * c);
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                floatx4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int c = 0; c < NC; ++c) s = mfma_bf16(kf[c], qf[u][c], s);
+                st[t][u] = s;
+            }
+        }
+        float p[4][2][4];   // [t][u][i]
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int key = key0 + 16 * t + 4 * g + i;
+                    const float s = key < a.seq ? st[t][u][i] * a.scale_log2 : -INFINITY;
+                    p[t][u][i] = s;
+                    mx = fmaxf(mx, s);
+                }
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float mnew = fmaxf(mrun[u], mx);
+            const float mref = mnew == -INFINITY ? 0.f : mnew;
+            const float alpha = fast_exp2(mrun[u] - mref);
+            float sum = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float e = fast_exp2(p[t][u][i] - mref);
+                    p[t][u][i] = e;
+                    sum += e;
+                }
+            sum += __shfl_xor(sum, 16);
+            sum += __shfl_xor(sum, 32);
+            lrun[u] = lrun[u] * alpha + sum;
+            mrun[u] = mnew;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) o[dt][u] *= alpha;
+        }
+        // O^T += V^T P^T, one 32-key half at a time (tiles 2 hf and 2 hf + 1).
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+            const char* vb = vs[buf][hf];
+            uint4 pf[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                pf[u] = make_uint4(pack_bf16x2(p[2 * hf][u][0], p[2 * hf][u][1]),
+                                   pack_bf16x2(p[2 * hf][u][2], p[2 * hf][u][3]),
+                                   pack_bf16x2(p[2 * hf + 1][u][0], p[2 * hf + 1][u][1]),
+                                   pack_bf16x2(p[2 * hf + 1][u][2], p[2 * hf + 1][u][3]));
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const uint4 va = *reinterpret_cast<const uint4*>(vb + (dt * 16 + (lane & 15)) * VP + g * 16);
+#pragma unroll
+                for (int u = 0; u < 2; ++u) o[dt][u] = mfma_bf16(va, pf[u], o[dt][u]);
+            }
+        }
+    };
+
+    // Two register sets: step i is stored to LDS buffer i % 2 while step i + 1
+    // is being loaded.  Buffer i % 2 is rewritten two steps after it was read;
+    // the barrier of the step in between orders every wave's reads before the
+    // rewrite.  The loop is unrolled by two so that the sets are fixed per
+    // position.
+    uint4 kr[2][KI];
+    uint32_t vr[2][VI][4];
+    const int n = s_end - s_begin;
+    if (n > 0) load_step(s_begin, kr[0], vr[0]);
+    for (int base = 0; base < n; base += 2) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int i = base + j;
+            if (i < n) {
+                store_step(j, kr[j], vr[j]);
+                if (i + 1 < n) load_step(s_begin + i + 1, kr[j ^ 1], vr[j ^ 1]);
+                __syncthreads();
+                if (active) compute_step(j, s_begin + i);
+            }
+        }
+    }
+    if (!active) return;
+
+    // Lane holds O^T[d = 16 dt + 4 g + i][q = 16 u + (lane & 15)].
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int q = qg * kQG + 16 * u + (lane & 15);
+        if (q >= a.nq) continue;
+        const size_t row = (static_cast<size_t>(b) * a.nq + q) * a.H + h;   // [b][q][h]
+        if (a.splits == 1) {
+            const float inv = 1.f / lrun[u];
+            char* op = a.out + row * HD * 2;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+                *reinterpret_cast<uint2*>(op + (16 * dt + 4 * g) * 2) =
+                    make_uint2(pack_bf16x2(o[dt][u][0] * inv, o[dt][u][1] * inv),
+                               pack_bf16x2(o[dt][u][2] * inv, o[dt][u][3] * inv));
+            if (a.lse && g == 0)
+                a.lse[(static_cast<size_t>(b) * a.H + h) * a.nq + q] = (mrun[u] + __log2f(lrun[u])) * kLn2;
+        } else {
+            const size_t prow = ((static_cast<size_t>(b) * a.H + h) * a.nq + q) * a.splits + split;
+            float* po = a.part_o + prow * HD;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * g) = o[dt][u];
+            if (g == 0) {
+                a.part_ml[prow * 2] = mrun[u];
+                a.part_ml[prow * 2 + 1] = lrun[u];
+            }
+        }
+    }
+}
+
 struct AttPlan {
     int splits;
     int tiles_per_split;
     size_t part_bytes;   // partial O + (m, l)
+    int group_waves;     // 0: attend_kernel; 4 or 8: attend_group_kernel with that many waves
+                         // (its tiles_per_split then counts 64-key steps)
+    int row_blocks;      // grouped: workgroups per (sequence, KV head, split)
 };
 
-inline AttPlan att_plan(int batch, int seq, int H, int nq, int hd) {
+// Plan of the attention launch.  Grouped heads (bf16, at least four (query
+// head, 32-query group) pairs per KV head) take attend_group_kernel with about
+// one workgroup per CU; everything else attend_kernel.
+inline AttPlan att_plan(bool bf16, int batch, int seq, int H, int Hkv, int nq, int hd) {
     AttPlan p{};
     const int ntiles = ceil_div(seq, kKT);
+    const int npairs = (H / Hkv) * ceil_div(nq, kQG);
+    if (bf16 && npairs >= 4 && static_cast<long>(batch) * Hkv <= 65535) {
+        p.group_waves = npairs >= 8 ? 8 : 4;
+        p.row_blocks = ceil_div(npairs, p.group_waves);
+        const int nsteps = ceil_div(seq, kGKT);          // tiles_per_split counts 64-key steps
+        const long base = static_cast<long>(batch) * Hkv * p.row_blocks;
+        int splits = static_cast<int>(256 / base);
+        if (splits > nsteps) splits = nsteps;
+        if (splits < 1) splits = 1;
+        p.tiles_per_split = ceil_div(nsteps, splits);
+        p.splits = ceil_div(nsteps, p.tiles_per_split);
+        if (p.splits > 1) {
+            const size_t rows = static_cast<size_t>(batch) * H * nq * p.splits;
+            p.part_bytes = align_up(rows * hd * sizeof(float), 256) + align_up(rows * 2 * sizeof(float), 256);
+        }
+        return p;
+    }
     const long base = static_cast<long>(batch) * H * ceil_div(nq, kQG);
     // about 512 workgroups, rounded down: two fit per CU, so a grid of at most
     // 512 runs in one round without a partial second one
@@ -418,6 +683,16 @@ inline AttPlan att_plan(int batch, int seq, int H, int nq, int hd) {
 
 template <bool BF16, int HD>
 void launch_att(const AttPlan& p, const AttArgs& a, hipStream_t s) {
+    if constexpr (BF16) {
+        if (p.group_waves > 0) {
+            const dim3 grid(p.splits, p.row_blocks, a.batch * a.Hkv);
+            if (p.group_waves == 8)
+                hipLaunchKernelGGL((attend_group_kernel<HD, 8>), grid, dim3(512), 0, s, a);
+            else
+                hipLaunchKernelGGL((attend_group_kernel<HD, 4>), grid, dim3(256), 0, s, a);
+            return;
+        }
+    }
     dim3 grid(p.splits, a.H * ceil_div(a.nq, kQG), a.batch);
     hipLaunchKernelGGL((attend_kernel<BF16, HD>), grid, dim3(kAttBlock), 0, s, a);
 }

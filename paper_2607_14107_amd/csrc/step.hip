@@ -149,7 +149,7 @@ StepLayout step_layout(const polestar_step_args& a) {
     L.refresh_bytes = polestar_refresh_kv_workspace_size(a.dtype, a.batch, a.d, a.n_kv_heads, a.head_dim, a.k,
                                                          a.block_len);
     L.qp = gemm_plan(bf16, static_cast<long>(a.batch) * a.block_len, a.n_heads * a.head_dim, a.d);
-    L.ap = att_plan(a.batch, a.seq, a.n_heads, a.block_len, a.head_dim);
+    L.ap = att_plan(bf16, a.batch, a.seq, a.n_heads, a.n_kv_heads, a.block_len, a.head_dim);
     L.cp = commit_plan(bf16, a.batch, a.block_len, a.vocab);
     L.ipt = select_ipt(a.seq);
     L.fused = L.ipt >= 1 && L.ipt <= 8 && L.qp.small && a.block_len <= kStepBlock &&

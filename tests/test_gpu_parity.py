@@ -316,8 +316,15 @@ def test_project_q_ragged_shapes(P, dtype, batch, seq, bs, bl, d, H, hd):
 
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-@pytest.mark.parametrize("batch,seq,bs,bl,H,Hkv,hd", [(2, 50, 10, 20, 4, 2, 64), (1, 300, 0, 45, 3, 1, 128),
-                                                      (3, 129, 97, 32, 2, 2, 128), (1, 1, 0, 1, 2, 1, 64)])
+@pytest.mark.parametrize("batch,seq,bs,bl,H,Hkv,hd", [
+    (2, 50, 10, 20, 4, 2, 64), (1, 300, 0, 45, 3, 1, 128), (3, 129, 97, 32, 2, 2, 128), (1, 1, 0, 1, 2, 1, 64),
+    # bf16 with >= 4 (head, 32-query group) pairs per KV head: the grouped-head kernel
+    (2, 130, 5, 40, 8, 2, 128),      # 8 pairs, one 8-wave workgroup per KV head and split
+    (1, 77, 0, 64, 7, 1, 64),        # 14 pairs in two row blocks (two idle waves), ragged keys
+    (3, 33, 1, 32, 4, 1, 128),       # 4 pairs, 4-wave workgroups
+    (2, 2100, 0, 20, 6, 1, 128),     # 6 pairs (two idle waves), many key splits
+    (1, 1, 0, 1, 8, 2, 64),          # a single key
+])
 def test_attend_small_shapes_with_given_queries(P, dtype, batch, seq, bs, bl, H, Hkv, hd):
     """Ragged key tiles and query groups, GQA grouping, a single key."""
     g = np.random.default_rng(seq * 7 + bl)
