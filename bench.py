@@ -4,9 +4,10 @@
 
 A step is the whole hot path over one batch: drift -> select -> sparse K/V
 refresh -> Q projection of the active block -> bidirectional attention ->
-commit, one polestar_step call on one stream (five launch groups: the
-select, the Q projection and the vocabulary scan share one launch, the
-attention merge and the commit finalize another).  The default workload is the LLaDA-8B-shaped layer (bf16,
+commit, one polestar_step call on one stream (six launches: drift beside
+the vocabulary scan, select beside the Q projection, the refresh GEMM, the
+refresh's split-K reduction beside the Q projection's, attention, and the
+attention merge beside the commit finalize).  The default workload is the LLaDA-8B-shaped layer (bf16,
 batch 1, d=4096, 32 heads of 128, sequence 768 = prompt 512 + 256 generated,
 active block 32, vocabulary 126464) with 15% of the positions heavily
 perturbed.  Inputs are seeded synthetic data, resident in HBM before timing.
@@ -97,18 +98,22 @@ def algorithmic_cost(cfg, k, es):
 
 # Kernels launched by each call, and the sources they are built from.
 CALL_KERNELS = {
-    "refresh_kv": ("gemm_dma_kernel", "gemm_reduce_kernel", "gemm_rows_kernel", "gemm_small_kernel"),
-    "project_q": ("gemm_small_kernel", "gemm_rows_kernel", "gemm_reduce_kernel"),
+    # polestar_step's refresh: the GEMM, then reduce2_kernel (the split-K
+    # reduction, with the Q projection's beside it); the stand-alone call's
+    # reduction is gemm_reduce_kernel
+    "refresh_kv": ("gemm_dma_kernel", "gemm_reduce_kernel", "reduce2_kernel", "gemm_rows_kernel",
+                   "gemm_small_kernel"),
+    "project_q": ("gemm_dma_kernel", "gemm_small_kernel", "gemm_rows_kernel", "gemm_reduce_kernel"),
     "attend": ("attend_kernel", "attend_merge_kernel"),
     "drift": ("drift_kernel",),
     "select": ("select_kernel",),
     "commit": ("scan_kernel", "finalize_kernel"),
 }
 CALL_SOURCES = {
-    "refresh_kv": ("gemm.hip", "gemm.hpp"),
-    "project_q": ("attend.hip", "gemm.hip", "gemm.hpp"),
+    "refresh_kv": ("gemm.hip", "gemm.hpp", "gemm_dev.hpp", "step.hip"),
+    "project_q": ("attend.hip", "gemm.hip", "gemm.hpp", "gemm_dev.hpp"),
     "attend": ("attend.hip",),
-    "drift": ("drift.hip",),
+    "drift": ("drift.hip", "drift_dev.hpp"),
     "select": ("select.hip",),
     "commit": ("commit.hip",),
 }

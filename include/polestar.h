@@ -530,8 +530,9 @@ polestar_status polestar_scatter_rows(int batch, int seq, int row_bytes, const v
  * definitions and results, on one stream.
  *
  * Work that does not depend on the previous launch shares launches: the
- * per-sequence select runs beside the Q projection and the vocabulary scan,
- * and the attention's split merge beside the commit's finalize step, so the
+ * drift beside the vocabulary scan, the per-sequence select beside the Q
+ * projection, the refresh's split-K reduction beside the Q projection's, and
+ * the attention's split merge beside the commit's finalize step, so the
  * latency-bound pieces overlap bandwidth-bound ones.  Shapes outside the
  * fused kernels (seq > 2048, batch * block_len > 64, block_len > 256) run
  * the six calls one after another instead, with the same results.
@@ -543,7 +544,9 @@ polestar_status polestar_scatter_rows(int batch, int seq, int row_bytes, const v
  *   workspace : >= polestar_step_workspace_size(args) bytes, no initialisation
  *   refresh_begin, refresh_end : optional events (NULL: none) recorded on the
  *       stream right before and right after the refresh launches, so that a
- *       caller can time the K/V refresh inside the step.
+ *       caller can time the K/V refresh inside the step (on the fused path
+ *       the second of them, the split-K reduction, also reduces the Q
+ *       projection's partials when its plan splits K).
  * Returns the first non-OK status of the pieces; as with the stand-alone
  * calls, argument errors are found on the host before anything is enqueued
  * (for the fused path: every check of every piece).

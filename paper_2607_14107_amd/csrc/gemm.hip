@@ -60,7 +60,6 @@ namespace {
 
 constexpr int kLda = 272;         // LDS row pitch (bytes) of the staged input rows
 constexpr int kTargetWgs = 256;   // one workgroup per compute unit on MI355X
-constexpr int kMaxSplit = 8;
 
 // ---------------------------------------------------------------------------
 // gemm_rows_kernel: BM = 32*MT rows x 128 columns per workgroup; wave w owns
@@ -238,185 +237,12 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_rows_kernel(GemmArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// gemm_dma_kernel: BM = 16*MT rows (one row tile) x 128 columns; wave w owns
-// columns 32w..32w+31 as two 16-column tiles of v_mfma_f32_16x16x32_bf16.
+// gemm_dma_kernel: the DMA-staged body of gemm_dev.hpp (dma_body).
 // ---------------------------------------------------------------------------
-
-constexpr int kDmaStage = 128;               // bytes of each row per stage
-constexpr int kDmaMaxRowTiles = 10;          // 160 rows
-// One 16-byte global -> LDS transfer per lane (the wave's lanes land
-// contiguously from lds_base).  A plain device function, so the builtin never
-// appears in a kernel template's host-side instantiation.
-__device__ __forceinline__ void dma16(const void* src, void* lds_base) {
-    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
-}
-
-// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
-// 6:4, lgkmcnt 11:8): wait until at most n vector-memory operations of this
-// wave are outstanding / until its LDS reads are done.
-constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
-constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
-
-// LDS offset of 16-byte chunk c of row r in a stage (rows of kDmaStage bytes).
-__device__ __forceinline__ int dma_swz(int r, int c) { return r * kDmaStage + ((c ^ ((r >> 1) & 7)) << 4); }
 
 template <bool BF16, int MT, int NST>
 __global__ __launch_bounds__(kGemmBlock) void gemm_dma_kernel(GemmArgs g) {
-    using T = Elem<BF16>;
-    constexpr int ES = T::kBytes;
-    constexpr int BM = MT * 16;
-    constexpr int BN = 128;
-    constexpr int ASZ = BM * kDmaStage, BSZ = BN * kDmaStage;
-    constexpr int AG = BM / 8;                          // 8-row groups of A per stage (one DMA instruction each)
-    constexpr int AIW = (AG + 3) / 4;                   // per wave (surplus ones repeat the last group)
-    constexpr int NDMA = 4 + AIW;                       // DMA instructions per wave per stage
-    static_assert(2 * NDMA <= 63, "outstanding DMA must fit the vmcnt counter");
-    // one LDS object per slot and operand: the compiler can tell them apart
-    __shared__ __align__(16) char sa0[ASZ], sa1[ASZ], sa2[ASZ], sa3[ASZ];
-    __shared__ __align__(16) char sb0[BSZ], sb1[BSZ], sb2[BSZ], sb3[BSZ];
-    __shared__ __align__(16) int rowb[BM];
-    __shared__ int rowp[BM];
-
-    const int tile = blockIdx.x / g.ksplit;
-    const int split = blockIdx.x - tile * g.ksplit;
-    const int col_tile = tile % g.col_tiles;
-    const int m0 = (tile / g.col_tiles) * BM;           // one or two row tiles
-    const int t = threadIdx.x;
-    const int lane = t & 63;
-    const int w = t >> 6;
-    const int s0b = split * g.steps_per_split * 256;    // byte offset of the split in a row
-    constexpr int nst_here = NST;                       // 128-byte stages of every split (the plan divides K evenly)
-
-    // weights: wave w moves rows 32w + 8i + l/8 (i < 4) of the tile's 128
-    // columns; lane l fills slot l%8 of its row
-    const char* bsrc[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int r = 32 * w + 8 * i + (lane >> 3);
-        const char* row = weight_row(g, col_tile * BN + r, ES);
-        bsrc[i] = (row ? row : g.w0) + s0b + (((lane & 7) ^ ((r >> 1) & 7)) << 4);
-    }
-    auto issue_b = [&](int st, char* buf) {
-        const int off = min(st, nst_here - 1) * kDmaStage;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            dma16(bsrc[i] + off, buf + (32 * w + 8 * i) * kDmaStage);
-    };
-    // Row bookkeeping (one load per row); the first workgroup publishes the
-    // map for the split-K reduction.
-    int rb_ = -1, rp_ = 0;
-    if (t < BM) map_row(g, m0 + t, rb_, rp_);
-    if (t < BM) {
-        rowb[t] = rb_;
-        rowp[t] = rp_;
-        if (g.ksplit > 1 && split == 0 && col_tile == 0 && m0 + t < g.m_max)
-            *reinterpret_cast<int2*>(g.rowmap + 2 * (m0 + t)) = make_int2(rb_, rp_);
-    }
-    if (!__syncthreads_or(rb_ >= 0)) return;            // no row of this tile maps anywhere (uniform)
-    // input rows: wave w moves groups w, w + 4, ... (8 rows each); rows that
-    // map to nothing read row 0 and are never stored
-    const char* asrc[AIW];
-#pragma unroll
-    for (int i = 0; i < AIW; ++i) {
-        const int r = 8 * min(w + 4 * i, AG - 1) + (lane >> 3);
-        const int b = rowb[r];
-        const char* row = b >= 0 ? g.x + (static_cast<size_t>(b) * g.seq + rowp[r]) * g.K * ES : g.x;
-        asrc[i] = row + s0b + (((lane & 7) ^ ((r >> 1) & 7)) << 4);
-    }
-    auto issue_a = [&](int st, char* buf) {
-        const int off = min(st, nst_here - 1) * kDmaStage;
-#pragma unroll
-        for (int i = 0; i < AIW; ++i)
-            dma16(asrc[i] + off, buf + 8 * min(w + 4 * i, AG - 1) * kDmaStage);
-    };
-    issue_b(0, sb0);
-    issue_a(0, sa0);
-    issue_b(1, sb1);
-    issue_a(1, sa1);
-    issue_b(2, sb2);
-    issue_a(2, sa2);
-
-    floatx4 acc[2][MT];
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int i = 0; i < MT; ++i) acc[c][i] = floatx4{0.f, 0.f, 0.f, 0.f};
-    // a stage is two 64-byte pieces; lane l reads chunk 4p + l/16 of rows
-    // 16mt + l%16 (A) and 32w + 16c + l%16 (B)
-    auto compute = [&](const char* abuf, const char* bbuf) {
-#pragma unroll
-        for (int p = 0; p < 2; ++p) {
-            const int c = 4 * p + (lane >> 4);
-            const uint4 bf0 = *reinterpret_cast<const uint4*>(bbuf + dma_swz(32 * w + (lane & 15), c));
-            const uint4 bf1 = *reinterpret_cast<const uint4*>(bbuf + dma_swz(32 * w + 16 + (lane & 15), c));
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                const uint4 af = *reinterpret_cast<const uint4*>(abuf + dma_swz(16 * mt + (lane & 15), c));
-                acc[0][mt] = Mma<BF16>::step(af, bf0, acc[0][mt]);
-                acc[1][mt] = Mma<BF16>::step(af, bf1, acc[1][mt]);
-            }
-        }
-    };
-    // Stage s: wait for this wave's DMA of stage s and its own earlier LDS
-    // reads; barrier (stage s is in LDS for every wave, and the slot of stage
-    // s-1 is free); issue stage s+3 into that slot; compute stage s.  Issue
-    // order B0 A0 B1 A1 B2 A2 | B3 A3 | ...: the wait leaves exactly the two
-    // newer stages outstanding.  Stages past the split re-read its last
-    // stage, so every stage issues the same DMA count.
-#define PS_DMA_STEP(S, WAIT, AUSE, BUSE, ANEXT, BNEXT)                      \
-    {                                                                       \
-        __builtin_amdgcn_s_waitcnt(WAIT);                                   \
-        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);                             \
-        __builtin_amdgcn_s_barrier();                                       \
-        issue_b((S) + 3, BNEXT);                                            \
-        issue_a((S) + 3, ANEXT);                                            \
-        compute(AUSE, BUSE);                                                \
-    }
-    constexpr int WS = wait_vm(2 * NDMA);               // after stage s: stages s+1, s+2
-    char* const sa[4] = {sa0, sa1, sa2, sa3};
-    char* const sb[4] = {sb0, sb1, sb2, sb3};
-    // fully unrolled: every slot index is a constant and the compiler sees the
-    // whole issue order (a loop would make it drain the DMA at the loop head)
-#pragma unroll
-    for (int st = 0; st < NST; ++st)
-        PS_DMA_STEP(st, WS, sa[st % 4], sb[st % 4], sa[(st + 3) % 4], sb[(st + 3) % 4])
-#undef PS_DMA_STEP
-    __builtin_amdgcn_s_waitcnt(0);                      // the re-read tail DMA lands before the workgroup ends
-
-    // results straight from registers: register i of acc[c][mt] is row
-    // 16mt + 4(l/16) + i, column 32w + 16c + l%16.  Split K (the usual case):
-    // fp32 partials, the lane's four row flags read once per row tile.
-    if (g.ksplit > 1) {
-        float* part = g.ws + (static_cast<size_t>(split) * g.col_tiles + col_tile) * g.m_max * BN +
-                      32 * w + (lane & 15);
-        const bool c0 = col_tile * BN + 32 * w + (lane & 15) < g.N;
-        const bool c1 = col_tile * BN + 32 * w + 16 + (lane & 15) < g.N;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const int r0 = 16 * mt + 4 * (lane >> 4);
-            const int4 rb4 = *reinterpret_cast<const int4*>(&rowb[r0]);
-            const int rv[4] = {rb4.x, rb4.y, rb4.z, rb4.w};
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                float* dst = part + static_cast<size_t>(m0 + r0 + i) * BN;
-                if (rv[i] >= 0 && c0) dst[0] = acc[0][mt][i];
-                if (rv[i] >= 0 && c1) dst[16] = acc[1][mt][i];
-            }
-        }
-        return;
-    }
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-        const int n = col_tile * BN + 32 * w + 16 * c + (lane & 15);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = 16 * mt + 4 * (lane >> 4) + i;
-                const int b = rowb[r];
-                if (b >= 0 && n < g.N) store_elem<BF16>(out_ptr<BF16>(g, b, rowp[r], m0 + r, n), acc[c][mt][i]);
-            }
-    }
+    dma_body<BF16, MT, NST>(g, blockIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -658,35 +484,7 @@ __global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmArgs g) {
 // loads are independent, then one rounded 16-byte store.
 template <bool BF16>
 __global__ __launch_bounds__(kGemmBlock) void gemm_reduce_kernel(GemmArgs g) {
-    const long id = static_cast<long>(blockIdx.x) * kGemmBlock + threadIdx.x;
-    const long per_tile = static_cast<long>(g.m_max) * 16;
-    const int ct = static_cast<int>(id / per_tile);
-    if (ct >= g.col_tiles) return;
-    const int rem = static_cast<int>(id - ct * per_tile);
-    const int m = rem >> 4;
-    const int c = (rem & 15) * 8;
-    const size_t stride = static_cast<size_t>(g.col_tiles) * g.m_max * 128;   // one split
-    const float* src = g.ws + (static_cast<size_t>(ct) * g.m_max + m) * 128 + c;
-    float4 x[2 * kMaxSplit];
-#pragma unroll
-    for (int s = 0; s < kMaxSplit; ++s) {
-        if (s < g.ksplit) {
-            x[2 * s] = *reinterpret_cast<const float4*>(src + s * stride);
-            x[2 * s + 1] = *reinterpret_cast<const float4*>(src + s * stride + 4);
-        }
-    }
-    const int2 mp = *reinterpret_cast<const int2*>(g.rowmap + 2 * m);
-    const int n = ct * 128 + c;
-    if (mp.x < 0 || n >= g.N) return;
-    float v[8] = {x[0].x, x[0].y, x[0].z, x[0].w, x[1].x, x[1].y, x[1].z, x[1].w};
-#pragma unroll
-    for (int s = 1; s < kMaxSplit; ++s) {
-        if (s < g.ksplit) {
-            v[0] += x[2 * s].x; v[1] += x[2 * s].y; v[2] += x[2 * s].z; v[3] += x[2 * s].w;
-            v[4] += x[2 * s + 1].x; v[5] += x[2 * s + 1].y; v[6] += x[2 * s + 1].z; v[7] += x[2 * s + 1].w;
-        }
-    }
-    store8<BF16>(out_ptr<BF16>(g, mp.x, mp.y, m, n), v);
+    reduce_body<BF16>(g, blockIdx.x);
 }
 
 template <bool BF16, int MT>
@@ -718,6 +516,9 @@ template <bool BF16, int NST>
 bool dispatch_dma_mt(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
     const dim3 grid(p.grid), block(kGemmBlock);
     switch (p.mt) {   // 16-row tiles
+        case 2: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 2, NST>), grid, block, 0, s, g); return true;
+        case 3: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 3, NST>), grid, block, 0, s, g); return true;
+        case 4: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 4, NST>), grid, block, 0, s, g); return true;
         case 5: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 5, NST>), grid, block, 0, s, g); return true;
         case 6: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 6, NST>), grid, block, 0, s, g); return true;
         case 7: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 7, NST>), grid, block, 0, s, g); return true;
@@ -730,7 +531,7 @@ bool dispatch_dma_mt(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
 
 template <bool BF16>
 bool dispatch_dma(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
-    static_assert(kDmaMaxRowTiles == 10, "dispatch covers 5..kDmaMaxRowTiles");
+    static_assert(kDmaMaxRowTiles == 10, "dispatch covers 2..kDmaMaxRowTiles");
     switch (2 * p.steps_per_split) {   // 128-byte stages per split
         case 8: return dispatch_dma_mt<BF16, 8>(p, g, s);
         case 16: return dispatch_dma_mt<BF16, 16>(p, g, s);
@@ -762,6 +563,29 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     const int ks = bf16 ? 128 : 64;
     const int nsteps = ceil_div(K, ks);
     if (m_max <= 0) m_max = 1;
+    // 17..64 rows (bf16): the DMA kernel with split-K partials streams each
+    // weight once with its A rows shared through LDS, where the small kernel
+    // re-reads the rows once per 16 columns (the 32-row LLaDA-8B block
+    // projection: 12.4 against 13.7 us with the reduce, 64 rows 13.6 against
+    // 21.0); other shapes, or when K does not split into 8 or 16 stages, the
+    // small kernel
+    if (m_max <= 64 && bf16 && m_max > 16) {
+        const int col_tiles = ceil_div(N, 128);
+        for (int ks = ceil_div(kTargetWgs, col_tiles); ks <= kMaxSplit; ++ks) {
+            if (nsteps % ks == 0 && (nsteps / ks == 4 || nsteps / ks == 8)) {
+                p.dma = true;
+                p.row_tiles = 1;
+                p.col_tiles = col_tiles;
+                p.ksplit = ks;
+                p.steps_per_split = nsteps / ks;
+                p.mt = ceil_div(m_max, 16);
+                p.grid = col_tiles * ks;
+                if (ks > 1)
+                    p.ws_bytes = partial_bytes(p, m_max) + align_up(static_cast<size_t>(m_max) * 2 * sizeof(int), 256);
+                return p;
+            }
+        }
+    }
     if (m_max <= 64) {
         p.small = true;
         p.mt = ceil_div(m_max, 16);
@@ -837,13 +661,47 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     return p;
 }
 
-polestar_status gemm_run(bool bf16, const GemmPlan& p, GemmArgs g, hipStream_t stream) {
+GemmArgs refresh_gemm_args(int batch, int seq, int d, int kvd, const void* h_cur, const int32_t* stale_idx,
+                           const int32_t* stale_count, int k_max, int block_start, int block_len,
+                           const void* w_k, const void* w_v, void* k_cache, void* v_cache, void* workspace) {
+    GemmArgs g{};
+    g.x = static_cast<const char*>(h_cur);
+    g.w0 = static_cast<const char*>(w_k);
+    g.w1 = static_cast<const char*>(w_v);
+    g.n0 = kvd;
+    g.N = 2 * kvd;
+    g.K = d;
+    g.mode = kGemmRefresh;
+    g.batch = batch;
+    g.seq = seq;
+    g.stale_idx = k_max > 0 ? stale_idx : nullptr;
+    g.stale_count = k_max > 0 ? stale_count : nullptr;
+    g.k_max = k_max;
+    g.block_start = block_start;
+    g.block_len = block_len;
+    g.out0 = static_cast<char*>(k_cache);
+    g.out1 = static_cast<char*>(v_cache);
+    g.ws = static_cast<float*>(workspace);
+    g.m_max = batch * (k_max + block_len);
+    return g;
+}
+
+void gemm_finalize_args(const GemmPlan& p, GemmArgs& g) {
     g.rowmap = p.ksplit > 1 ? reinterpret_cast<int*>(reinterpret_cast<char*>(g.ws) + partial_bytes(p, g.m_max))
                             : nullptr;
     g.ksplit = p.ksplit;
     g.steps_per_split = p.steps_per_split;
     g.row_tiles = p.row_tiles;
     g.col_tiles = p.col_tiles;
+}
+
+int gemm_reduce_blocks(const GemmPlan& p, const GemmArgs& g) {
+    if (p.small || p.ksplit == 1) return 0;
+    return ceil_div(static_cast<long>(p.col_tiles) * g.m_max * 16, kGemmBlock);
+}
+
+polestar_status gemm_run(bool bf16, const GemmPlan& p, GemmArgs g, hipStream_t stream, GemmArgs* deferred) {
+    gemm_finalize_args(p, g);
     bool ok;
     if (p.small) ok = bf16 ? dispatch_small<true>(p, g, stream) : dispatch_small<false>(p, g, stream);
     else if (p.tile) {
@@ -854,8 +712,11 @@ polestar_status gemm_run(bool bf16, const GemmPlan& p, GemmArgs g, hipStream_t s
     if (!ok) return POLESTAR_ERR_UNSUPPORTED;
     polestar_status st = launch_status();
     if (st != POLESTAR_OK || p.small || p.ksplit == 1) return st;
-    const long threads = static_cast<long>(g.col_tiles) * g.m_max * 16;
-    const int blocks = ceil_div(threads, kGemmBlock);
+    if (deferred) {   // the caller launches the reduction (fused with other work)
+        *deferred = g;
+        return POLESTAR_OK;
+    }
+    const int blocks = gemm_reduce_blocks(p, g);
     if (bf16)
         hipLaunchKernelGGL((gemm_reduce_kernel<true>), dim3(blocks), dim3(kGemmBlock), 0, stream, g);
     else
@@ -903,24 +764,7 @@ extern "C" polestar_status polestar_refresh_kv(polestar_dtype dtype, int batch, 
     const int kvd = n_kv_heads * head_dim;
     const GemmPlan p = gemm_plan(bf16, m_max, 2 * kvd, d);
     if (workspace_bytes < p.ws_bytes || (p.ws_bytes > 0 && !workspace)) return POLESTAR_ERR_WORKSPACE;
-    GemmArgs g{};
-    g.x = static_cast<const char*>(h_cur);
-    g.w0 = static_cast<const char*>(w_k);
-    g.w1 = static_cast<const char*>(w_v);
-    g.n0 = kvd;
-    g.N = 2 * kvd;
-    g.K = d;
-    g.mode = kGemmRefresh;
-    g.batch = batch;
-    g.seq = seq;
-    g.stale_idx = k_max > 0 ? stale_idx : nullptr;
-    g.stale_count = k_max > 0 ? stale_count : nullptr;
-    g.k_max = k_max;
-    g.block_start = block_start;
-    g.block_len = block_len;
-    g.out0 = static_cast<char*>(k_cache);
-    g.out1 = static_cast<char*>(v_cache);
-    g.ws = static_cast<float*>(workspace);
-    g.m_max = static_cast<int>(m_max);
+    const GemmArgs g = refresh_gemm_args(batch, seq, d, kvd, h_cur, stale_idx, stale_count, k_max, block_start,
+                                         block_len, w_k, w_v, k_cache, v_cache, workspace);
     return gemm_run(bf16, p, g, stream);
 }

@@ -38,7 +38,7 @@ struct GemmArgs {
 
 struct GemmPlan {
     bool small;         // gemm_small_kernel (<= 64 rows) instead of gemm_rows_kernel
-    bool dma;           // gemm_dma_kernel (65..320 rows: one or two row tiles, operands DMA'd into LDS)
+    bool dma;           // gemm_dma_kernel (17..64 or 65..320 rows: one or two row tiles, operands DMA'd into LDS)
     bool tile;          // gemm_tile_kernel (bf16, more than 160 rows: 256 x 256 tiles)
     int mt;             // MFMA row tiles per workgroup (16 rows: small and dma kernels; 32: rows kernel)
     int row_tiles;
@@ -55,7 +55,24 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K);
 inline bool gemm_k_ok(bool bf16, int K) { return K > 0 && K % (bf16 ? 128 : 64) == 0; }
 
 // Enqueue the GEMM (and the split-K reduction when the plan splits K).
-// `g.ws` must hold plan.ws_bytes.  Returns POLESTAR_OK or a launch error.
-polestar_status gemm_run(bool bf16, const GemmPlan& plan, GemmArgs g, hipStream_t stream);
+// `g.ws` must hold plan.ws_bytes.  With `deferred`, a plan that needs the
+// reduction leaves it to the caller: *deferred receives the arguments of
+// the reduction (reduce_body, gemm_reduce_blocks workgroups).  Returns
+// POLESTAR_OK or a launch error.
+polestar_status gemm_run(bool bf16, const GemmPlan& plan, GemmArgs g, hipStream_t stream,
+                         GemmArgs* deferred = nullptr);
+
+// Arguments of the K/V refresh GEMM (polestar_refresh_kv's, after its checks):
+// rows = the stale positions and the active block of every sequence, output
+// columns [0, kvd) to k_cache and [kvd, 2 kvd) to v_cache.
+GemmArgs refresh_gemm_args(int batch, int seq, int d, int kvd, const void* h_cur, const int32_t* stale_idx,
+                           const int32_t* stale_count, int k_max, int block_start, int block_len,
+                           const void* w_k, const void* w_v, void* k_cache, void* v_cache, void* workspace);
+
+// The plan's fields of the arguments (split, tiles, row map in the workspace).
+void gemm_finalize_args(const GemmPlan& plan, GemmArgs& g);
+
+// Workgroups of the split-K reduction of a plan (0: none).
+int gemm_reduce_blocks(const GemmPlan& plan, const GemmArgs& g);
 
 }  // namespace ps

@@ -205,5 +205,231 @@ __device__ __forceinline__ void small_body(const GemmArgs& g, int bx, int by) {
     }
 }
 
+constexpr int kMaxSplit = 8;      // largest split-K factor of a plan
+
+// ---------------------------------------------------------------------------
+// dma_body (gemm_dma_kernel, and the fused step's Q projection): BM = 16*MT rows (one row tile) x 128 columns; wave w owns
+// columns 32w..32w+31 as two 16-column tiles of v_mfma_f32_16x16x32_bf16.
+// ---------------------------------------------------------------------------
+
+constexpr int kDmaStage = 128;               // bytes of each row per stage
+constexpr int kDmaMaxRowTiles = 10;          // 160 rows
+// One 16-byte global -> LDS transfer per lane (the wave's lanes land
+// contiguously from lds_base).  A plain device function, so the builtin never
+// appears in a kernel template's host-side instantiation.
+__device__ __forceinline__ void dma16(const void* src, void* lds_base) {
+    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+
+// s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
+// 6:4, lgkmcnt 11:8): wait until at most n vector-memory operations of this
+// wave are outstanding / until its LDS reads are done.
+constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
+
+// LDS offset of 16-byte chunk c of row r in a stage (rows of kDmaStage bytes).
+__device__ __forceinline__ int dma_swz(int r, int c) { return r * kDmaStage + ((c ^ ((r >> 1) & 7)) << 4); }
+
+// NS: LDS slots per operand (4: three stages in flight; 3: two, for a
+// workgroup that must share its compute unit).
+template <bool BF16, int MT, int NST, int NS = 4>
+__device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
+    static_assert(NS == 3 || NS == 4, "three or four LDS slots");
+    using T = Elem<BF16>;
+    constexpr int ES = T::kBytes;
+    constexpr int BM = MT * 16;
+    constexpr int BN = 128;
+    constexpr int ASZ = BM * kDmaStage, BSZ = BN * kDmaStage;
+    constexpr int AG = BM / 8;                          // 8-row groups of A per stage (one DMA instruction each)
+    constexpr int AIW = (AG + 3) / 4;                   // per wave (surplus ones repeat the last group)
+    constexpr int NDMA = 4 + AIW;                       // DMA instructions per wave per stage
+    static_assert(2 * NDMA <= 63, "outstanding DMA must fit the vmcnt counter");
+    // one LDS object per slot and operand: the compiler can tell them apart
+    __shared__ __align__(16) char sa0[ASZ], sa1[ASZ], sa2[ASZ], sa3[NS == 4 ? ASZ : 16];
+    __shared__ __align__(16) char sb0[BSZ], sb1[BSZ], sb2[BSZ], sb3[NS == 4 ? BSZ : 16];
+    __shared__ __align__(16) int rowb[BM];
+    __shared__ int rowp[BM];
+
+    const int tile = blk / g.ksplit;
+    const int split = blk - tile * g.ksplit;
+    const int col_tile = tile % g.col_tiles;
+    const int m0 = (tile / g.col_tiles) * BM;           // one or two row tiles
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int w = t >> 6;
+    const int s0b = split * g.steps_per_split * 256;    // byte offset of the split in a row
+    constexpr int nst_here = NST;                       // 128-byte stages of every split (the plan divides K evenly)
+
+    // weights: wave w moves rows 32w + 8i + l/8 (i < 4) of the tile's 128
+    // columns; lane l fills slot l%8 of its row
+    const char* bsrc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = 32 * w + 8 * i + (lane >> 3);
+        const char* row = weight_row(g, col_tile * BN + r, ES);
+        bsrc[i] = (row ? row : g.w0) + s0b + (((lane & 7) ^ ((r >> 1) & 7)) << 4);
+    }
+    auto issue_b = [&](int st, char* buf) {
+        const int off = min(st, nst_here - 1) * kDmaStage;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            dma16(bsrc[i] + off, buf + (32 * w + 8 * i) * kDmaStage);
+    };
+    // Row bookkeeping (one load per row); the first workgroup publishes the
+    // map for the split-K reduction.
+    int rb_ = -1, rp_ = 0;
+    if (t < BM) map_row(g, m0 + t, rb_, rp_);
+    if (t < BM) {
+        rowb[t] = rb_;
+        rowp[t] = rp_;
+        if (g.ksplit > 1 && split == 0 && col_tile == 0 && m0 + t < g.m_max)
+            *reinterpret_cast<int2*>(g.rowmap + 2 * (m0 + t)) = make_int2(rb_, rp_);
+    }
+    if (!__syncthreads_or(rb_ >= 0)) return;            // no row of this tile maps anywhere (uniform)
+    // input rows: wave w moves groups w, w + 4, ... (8 rows each); rows that
+    // map to nothing read row 0 and are never stored
+    const char* asrc[AIW];
+#pragma unroll
+    for (int i = 0; i < AIW; ++i) {
+        const int r = 8 * min(w + 4 * i, AG - 1) + (lane >> 3);
+        const int b = rowb[r];
+        const char* row = b >= 0 ? g.x + (static_cast<size_t>(b) * g.seq + rowp[r]) * g.K * ES : g.x;
+        asrc[i] = row + s0b + (((lane & 7) ^ ((r >> 1) & 7)) << 4);
+    }
+    auto issue_a = [&](int st, char* buf) {
+        const int off = min(st, nst_here - 1) * kDmaStage;
+#pragma unroll
+        for (int i = 0; i < AIW; ++i)
+            dma16(asrc[i] + off, buf + 8 * min(w + 4 * i, AG - 1) * kDmaStage);
+    };
+    issue_b(0, sb0);
+    issue_a(0, sa0);
+    issue_b(1, sb1);
+    issue_a(1, sa1);
+    if constexpr (NS == 4) {
+        issue_b(2, sb2);
+        issue_a(2, sa2);
+    }
+
+    floatx4 acc[2][MT];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acc[c][i] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // a stage is two 64-byte pieces; lane l reads chunk 4p + l/16 of rows
+    // 16mt + l%16 (A) and 32w + 16c + l%16 (B)
+    auto compute = [&](const char* abuf, const char* bbuf) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            const int c = 4 * p + (lane >> 4);
+            const uint4 bf0 = *reinterpret_cast<const uint4*>(bbuf + dma_swz(32 * w + (lane & 15), c));
+            const uint4 bf1 = *reinterpret_cast<const uint4*>(bbuf + dma_swz(32 * w + 16 + (lane & 15), c));
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const uint4 af = *reinterpret_cast<const uint4*>(abuf + dma_swz(16 * mt + (lane & 15), c));
+                acc[0][mt] = Mma<BF16>::step(af, bf0, acc[0][mt]);
+                acc[1][mt] = Mma<BF16>::step(af, bf1, acc[1][mt]);
+            }
+        }
+    };
+    // Stage s: wait for this wave's DMA of stage s and its own earlier LDS
+    // reads; barrier (stage s is in LDS for every wave, and the slot of stage
+    // s-1 is free); issue stage s+NS-1 into that slot; compute stage s.
+    // Issue order (NS = 4) B0 A0 B1 A1 B2 A2 | B3 A3 | ...: the wait leaves
+    // exactly the NS-2 newer stages outstanding.  Stages past the split
+    // re-read its last stage, so every stage issues the same DMA count.
+#define PS_DMA_STEP(S, WAIT, AUSE, BUSE, ANEXT, BNEXT)                      \
+    {                                                                       \
+        __builtin_amdgcn_s_waitcnt(WAIT);                                   \
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);                             \
+        __builtin_amdgcn_s_barrier();                                       \
+        issue_b((S) + NS - 1, BNEXT);                                       \
+        issue_a((S) + NS - 1, ANEXT);                                       \
+        compute(AUSE, BUSE);                                                \
+    }
+    constexpr int WS = wait_vm((NS - 2) * NDMA);        // after stage s: stages s+1 .. s+NS-2
+    char* const sa[4] = {sa0, sa1, sa2, sa3};
+    char* const sb[4] = {sb0, sb1, sb2, sb3};
+    // fully unrolled: every slot index is a constant and the compiler sees the
+    // whole issue order (a loop would make it drain the DMA at the loop head)
+#pragma unroll
+    for (int st = 0; st < NST; ++st)
+        PS_DMA_STEP(st, WS, sa[st % NS], sb[st % NS], sa[(st + NS - 1) % NS], sb[(st + NS - 1) % NS])
+#undef PS_DMA_STEP
+    __builtin_amdgcn_s_waitcnt(0);                      // the re-read tail DMA lands before the workgroup ends
+
+    // results straight from registers: register i of acc[c][mt] is row
+    // 16mt + 4(l/16) + i, column 32w + 16c + l%16.  Split K (the usual case):
+    // fp32 partials, the lane's four row flags read once per row tile.
+    if (g.ksplit > 1) {
+        float* part = g.ws + (static_cast<size_t>(split) * g.col_tiles + col_tile) * g.m_max * BN +
+                      32 * w + (lane & 15);
+        const bool c0 = col_tile * BN + 32 * w + (lane & 15) < g.N;
+        const bool c1 = col_tile * BN + 32 * w + 16 + (lane & 15) < g.N;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int r0 = 16 * mt + 4 * (lane >> 4);
+            const int4 rb4 = *reinterpret_cast<const int4*>(&rowb[r0]);
+            const int rv[4] = {rb4.x, rb4.y, rb4.z, rb4.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float* dst = part + static_cast<size_t>(m0 + r0 + i) * BN;
+                if (rv[i] >= 0 && c0) dst[0] = acc[0][mt][i];
+                if (rv[i] >= 0 && c1) dst[16] = acc[1][mt][i];
+            }
+        }
+        return;
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        const int n = col_tile * BN + 32 * w + 16 * c + (lane & 15);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = 16 * mt + 4 * (lane >> 4) + i;
+                const int b = rowb[r];
+                if (b >= 0 && n < g.N) store_elem<BF16>(out_ptr<BF16>(g, b, rowp[r], m0 + r, n), acc[c][mt][i]);
+            }
+    }
+}
+
+
+// Split-K reduction: thread = (column tile, row, 8 columns); sums the splits
+// in order and stores the row through the published row map.  One
+// kGemmBlock workgroup per 16 rows of a column tile.
+template <bool BF16>
+__device__ __forceinline__ void reduce_body(const GemmArgs& g, int blk) {
+    const long id = static_cast<long>(blk) * kGemmBlock + threadIdx.x;
+    const long per_tile = static_cast<long>(g.m_max) * 16;
+    const int ct = static_cast<int>(id / per_tile);
+    if (ct >= g.col_tiles) return;
+    const int rem = static_cast<int>(id - ct * per_tile);
+    const int m = rem >> 4;
+    const int c = (rem & 15) * 8;
+    const size_t stride = static_cast<size_t>(g.col_tiles) * g.m_max * 128;   // one split
+    const float* src = g.ws + (static_cast<size_t>(ct) * g.m_max + m) * 128 + c;
+    float4 x[2 * kMaxSplit];
+#pragma unroll
+    for (int s = 0; s < kMaxSplit; ++s) {
+        if (s < g.ksplit) {
+            x[2 * s] = *reinterpret_cast<const float4*>(src + s * stride);
+            x[2 * s + 1] = *reinterpret_cast<const float4*>(src + s * stride + 4);
+        }
+    }
+    const int2 mp = *reinterpret_cast<const int2*>(g.rowmap + 2 * m);
+    const int n = ct * 128 + c;
+    if (mp.x < 0 || n >= g.N) return;
+    float v[8] = {x[0].x, x[0].y, x[0].z, x[0].w, x[1].x, x[1].y, x[1].z, x[1].w};
+#pragma unroll
+    for (int s = 1; s < kMaxSplit; ++s) {
+        if (s < g.ksplit) {
+            v[0] += x[2 * s].x; v[1] += x[2 * s].y; v[2] += x[2 * s].z; v[3] += x[2 * s].w;
+            v[4] += x[2 * s + 1].x; v[5] += x[2 * s + 1].y; v[6] += x[2 * s + 1].z; v[7] += x[2 * s + 1].w;
+        }
+    }
+    store8<BF16>(out_ptr<BF16>(g, mp.x, mp.y, m, n), v);
+}
+
 }  // namespace
 }  // namespace ps

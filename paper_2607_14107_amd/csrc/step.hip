@@ -2,16 +2,17 @@
 // projection -> attention -> commit) on one stream, with the work that does
 // not depend on the previous launch fused into shared launches:
 //
-//   1. drift                          (every position)
-//   2. front: select | Q projection | vocabulary scan
+//   1. lead: drift | vocabulary scan   (both read only the step's inputs)
+//   2. front: select | Q projection
 //      The select of a sequence is one latency-bound workgroup; the Q
-//      projection and the logit scan read only the step's inputs, so they
-//      fill the GPU while it runs.
-//   3. refresh: gather -> GEMM -> split-K reduce -> scatter (needs 2)
-//   4. attention over the refreshed cache (needs 2, 3)
-//   5. back: attention merge | commit finalize (needs 4, and 1-2)
+//      projection (split-K partials when the plan splits K) reads only the
+//      inputs, so it fills the GPU while select runs.
+//   3. refresh GEMM: gather -> MFMA -> split-K partials (needs 2)
+//   4. reduce: refresh split-K reduce + scatter | Q split-K reduce
+//   5. attention over the refreshed cache (needs 2, 3, 4)
+//   6. back: attention merge | commit finalize (needs 5, and 1-2)
 //
-// Five launch groups instead of nine kernels on their own.  Workgroups of a
+// Six launches instead of eleven kernels on their own.  Workgroups of a
 // fused launch take their role from their block index; each role is the
 // device body the stand-alone kernel runs, so results are bit-identical to
 // calling the six entry points in order.  Shapes outside the fused kernels'
@@ -19,6 +20,7 @@
 // longer than 256) run exactly that sequence of entry points instead.
 #include "attend_dev.hpp"
 #include "commit_dev.hpp"
+#include "drift_dev.hpp"
 #include "gemm_dev.hpp"
 #include "host_common.hpp"
 #include "select_dev.hpp"
@@ -28,8 +30,35 @@ namespace {
 
 constexpr int kStepBlock = 256;
 static_assert(kSelBlock == kStepBlock && kSmallBlock == kStepBlock && kScanBlock == kStepBlock &&
-                  kAttBlock == kStepBlock,
+                  kAttBlock == kStepBlock && kDriftBlock == kStepBlock && kGemmBlock == kStepBlock,
               "fused roles share one workgroup size");
+
+struct LeadArgs {
+    // drift
+    const char* hc;
+    const char* hp;
+    float* drift;
+    int rows, d;
+    // vocabulary scan
+    const char* logits;
+    int vocab, nq, chunk, splits, mask_id;
+    ScanPart* parts;
+    int n_drift;   // workgroups of the drift role, first in launch order
+};
+
+template <bool BF16, int TPR, int NCH>
+__global__ __launch_bounds__(kStepBlock) void lead_kernel(LeadArgs l) {
+    const int vb = blockIdx.x;
+    if (vb < l.n_drift) {
+        drift_body<BF16, TPR, NCH>(l.hc, l.hp, l.drift, l.rows, l.d, vb);
+        return;
+    }
+    const int r = vb - l.n_drift;
+    const int split = r % l.splits;
+    const int tok = r / l.splits;
+    scan_body<BF16>(l.logits, l.vocab, l.nq, l.chunk, l.splits, l.mask_id, l.parts, split, tok % l.nq,
+                    tok / l.nq);
+}
 
 struct FrontArgs {
     // select
@@ -40,31 +69,47 @@ struct FrontArgs {
     int32_t* cnt;
     // Q projection (block rows, at most 64 of them)
     GemmArgs q;
-    // vocabulary scan
-    const char* logits;
-    int vocab, nq, chunk, splits, mask_id;
-    ScanPart* parts;
-    // workgroups per role, in launch order
-    int n_sel, n_q;
+    int n_sel;     // workgroups of the select role, first in launch order
 };
 
+// select | Q projection on the small-M kernel (no partials)
 template <bool BF16, int IPT, int MT>
 __global__ __launch_bounds__(kStepBlock) void front_kernel(FrontArgs f) {
-    int vb = blockIdx.x;
+    const int vb = blockIdx.x;
     if (vb < f.n_sel) {
         select_body<IPT>(f.drift, f.elig, f.seq, f.bs, f.bl, f.k, f.idx, f.cnt, vb);
         return;
     }
-    vb -= f.n_sel;
-    if (vb < f.n_q) {
-        small_body<BF16, MT>(f.q, vb, 0);
+    small_body<BF16, MT>(f.q, vb - f.n_sel, 0);
+}
+
+// select | Q projection on the DMA-staged kernel (bf16; split-K partials
+// reduced in launch 4).  With three LDS slots two workgroups fit per
+// compute unit, so the select workgroups do not push the Q projection's
+// one-per-CU grid into a second round.
+template <int IPT, int MT, int NST>
+__global__ __launch_bounds__(kStepBlock) void front_dma_kernel(FrontArgs f) {
+    const int vb = blockIdx.x;
+    if (vb < f.n_sel) {
+        select_body<IPT>(f.drift, f.elig, f.seq, f.bs, f.bl, f.k, f.idx, f.cnt, vb);
         return;
     }
-    vb -= f.n_q;
-    const int split = vb % f.splits;
-    const int tok = vb / f.splits;
-    scan_body<BF16>(f.logits, f.vocab, f.nq, f.chunk, f.splits, f.mask_id, f.parts, split, tok % f.nq,
-                    tok / f.nq);
+    dma_body<true, MT, NST, 3>(f.q, vb - f.n_sel);   // three slots: the select workgroup shares a CU
+}
+
+struct ReduceArgs {
+    GemmArgs r;    // refresh (n_r workgroups, first)
+    GemmArgs q;    // Q projection
+    int n_r;
+};
+
+template <bool BF16>
+__global__ __launch_bounds__(kStepBlock) void reduce2_kernel(ReduceArgs k) {
+    if (static_cast<int>(blockIdx.x) < k.n_r) {
+        reduce_body<BF16>(k.r, blockIdx.x);
+        return;
+    }
+    reduce_body<BF16>(k.q, blockIdx.x - k.n_r);
 }
 
 struct BackArgs {
@@ -96,6 +141,24 @@ __global__ __launch_bounds__(kStepBlock) void back_kernel(BackArgs k) {
                   blockIdx.x - k.n_merge);
 }
 
+template <bool BF16, int TPR, int NCH>
+void launch_lead1(dim3 grid, const LeadArgs& l, hipStream_t s) {
+    hipLaunchKernelGGL((lead_kernel<BF16, TPR, NCH>), grid, dim3(kStepBlock), 0, s, l);
+}
+
+template <bool BF16>
+bool launch_lead(int tpr, int nch, dim3 grid, const LeadArgs& l, hipStream_t s) {
+    switch (tpr * 16 + nch) {
+        case 64 * 16 + 1: launch_lead1<BF16, 64, 1>(grid, l, s); return true;
+        case 64 * 16 + 2: launch_lead1<BF16, 64, 2>(grid, l, s); return true;
+        case 128 * 16 + 2: launch_lead1<BF16, 128, 2>(grid, l, s); return true;
+        case 256 * 16 + 2: launch_lead1<BF16, 256, 2>(grid, l, s); return true;
+        case 256 * 16 + 4: launch_lead1<BF16, 256, 4>(grid, l, s); return true;
+        case 256 * 16 + 8: launch_lead1<BF16, 256, 8>(grid, l, s); return true;
+        default: return false;
+    }
+}
+
 template <bool BF16, int IPT>
 bool launch_front_mt(int mt, dim3 grid, const FrontArgs& f, hipStream_t s) {
     switch (mt) {
@@ -107,8 +170,38 @@ bool launch_front_mt(int mt, dim3 grid, const FrontArgs& f, hipStream_t s) {
     }
 }
 
+template <int IPT, int NST>
+bool launch_front_dma_mt(int mt, dim3 grid, const FrontArgs& f, hipStream_t s) {
+    switch (mt) {
+        case 2: hipLaunchKernelGGL((front_dma_kernel<IPT, 2, NST>), grid, dim3(kStepBlock), 0, s, f); return true;
+        case 3: hipLaunchKernelGGL((front_dma_kernel<IPT, 3, NST>), grid, dim3(kStepBlock), 0, s, f); return true;
+        case 4: hipLaunchKernelGGL((front_dma_kernel<IPT, 4, NST>), grid, dim3(kStepBlock), 0, s, f); return true;
+        default: return false;
+    }
+}
+
+template <int IPT>
+bool launch_front_dma_nst(int nst, int mt, dim3 grid, const FrontArgs& f, hipStream_t s) {
+    if (nst == 8) return launch_front_dma_mt<IPT, 8>(mt, grid, f, s);
+    if (nst == 16) return launch_front_dma_mt<IPT, 16>(mt, grid, f, s);
+    return false;
+}
+
+// dma: the Q plan takes the DMA kernel (bf16), nst its 128-byte stages per split
 template <bool BF16>
-bool launch_front(int ipt, int mt, dim3 grid, const FrontArgs& f, hipStream_t s) {
+bool launch_front(int ipt, bool dma, int nst, int mt, dim3 grid, const FrontArgs& f, hipStream_t s) {
+    if (dma) {
+        if constexpr (!BF16) return false;
+        switch (ipt) {
+            case 1: return launch_front_dma_nst<1>(nst, mt, grid, f, s);
+            case 2: return launch_front_dma_nst<2>(nst, mt, grid, f, s);
+            case 3: return launch_front_dma_nst<3>(nst, mt, grid, f, s);
+            case 4: return launch_front_dma_nst<4>(nst, mt, grid, f, s);
+            case 6: return launch_front_dma_nst<6>(nst, mt, grid, f, s);
+            case 8: return launch_front_dma_nst<8>(nst, mt, grid, f, s);
+            default: return false;
+        }
+    }
     switch (ipt) {
         case 1: return launch_front_mt<BF16, 1>(mt, grid, f, s);
         case 2: return launch_front_mt<BF16, 2>(mt, grid, f, s);
@@ -132,15 +225,17 @@ void launch_attention(int hd, const AttPlan& p, const AttArgs& a, hipStream_t s)
     else launch_att<BF16, 64>(p, a, s);
 }
 
-// Workspace of the fused path: refresh partials, attention partials, scan
-// partials, each 256-byte aligned.
+// Workspace of the step: refresh partials, attention partials, scan
+// partials, Q-projection partials, each 256-byte aligned.
 struct StepLayout {
-    GemmPlan qp;        // Q projection plan (small path when fused)
+    GemmPlan qp;        // Q projection plan
+    GemmPlan rp;        // refresh plan
     AttPlan ap;
     CommitPlan cp;
-    size_t refresh_bytes, att_off, scan_off, total;
+    size_t refresh_bytes, att_off, scan_off, q_off, total;
     bool fused;
     int ipt;
+    int drift_tpr, drift_nch;
 };
 
 StepLayout step_layout(const polestar_step_args& a) {
@@ -149,15 +244,19 @@ StepLayout step_layout(const polestar_step_args& a) {
     L.refresh_bytes = polestar_refresh_kv_workspace_size(a.dtype, a.batch, a.d, a.n_kv_heads, a.head_dim, a.k,
                                                          a.block_len);
     L.qp = gemm_plan(bf16, static_cast<long>(a.batch) * a.block_len, a.n_heads * a.head_dim, a.d);
+    L.rp = gemm_plan(bf16, static_cast<long>(a.batch) * (a.k + a.block_len), 2 * a.n_kv_heads * a.head_dim, a.d);
     L.ap = att_plan(bf16, a.batch, a.seq, a.n_heads, a.n_kv_heads, a.block_len, a.head_dim);
     L.cp = commit_plan(bf16, a.batch, a.block_len, a.vocab);
     L.ipt = select_ipt(a.seq);
-    L.fused = L.ipt >= 1 && L.ipt <= 8 && L.qp.small && a.block_len <= kStepBlock &&
+    const bool q_dma = bf16 && L.qp.dma && L.qp.row_tiles == 1 && L.qp.mt >= 2 && L.qp.mt <= 4 &&
+                       (2 * L.qp.steps_per_split == 8 || 2 * L.qp.steps_per_split == 16);
+    const bool drift_ok = drift_config(a.d / (bf16 ? 8 : 4), L.drift_tpr, L.drift_nch);
+    L.fused = L.ipt >= 1 && L.ipt <= 8 && (L.qp.small || q_dma) && drift_ok && a.block_len <= kStepBlock &&
               (a.head_dim == 64 || a.head_dim == 128);
     L.att_off = align_up(L.refresh_bytes, 256);
     L.scan_off = L.att_off + align_up(L.ap.part_bytes, 256);
-    const size_t q_ws = align_up(L.qp.ws_bytes, 256);   // unfused path: stand-alone Q projection
-    L.total = L.scan_off + align_up(L.cp.ws_bytes, 256) + (L.fused ? 0 : q_ws);
+    L.q_off = L.scan_off + align_up(L.cp.ws_bytes, 256);   // Q projection partials (when its plan splits K)
+    L.total = L.q_off + align_up(L.qp.ws_bytes, 256);
     return L;
 }
 
@@ -175,9 +274,8 @@ polestar_status run_unfused(const polestar_step_args& a, const StepLayout& L, ch
                              a.v_cache, ws, L.refresh_bytes, s);
     if (st != POLESTAR_OK) return st;
     if (ev1 && hipEventRecord(ev1, s) != hipSuccess) return POLESTAR_ERR_LAUNCH;
-    const size_t q_off = L.scan_off + align_up(L.cp.ws_bytes, 256);
     st = polestar_project_q(a.dtype, a.batch, a.seq, a.d, a.n_heads, a.head_dim, a.block_start, a.block_len,
-                            a.h_cur, a.w_q, a.q, L.qp.ws_bytes ? ws + q_off : nullptr, L.qp.ws_bytes, s);
+                            a.h_cur, a.w_q, a.q, L.qp.ws_bytes ? ws + L.q_off : nullptr, L.qp.ws_bytes, s);
     if (st != POLESTAR_OK) return st;
     st = polestar_attend(a.dtype, a.batch, a.seq, a.d, a.n_heads, a.n_kv_heads, a.head_dim, a.block_start,
                          a.block_len, nullptr, nullptr, a.q, a.k_cache, a.v_cache, a.scale, a.out, a.lse,
@@ -226,11 +324,30 @@ extern "C" polestar_status polestar_step(const polestar_step_args* a, void* work
         a->batch > 65535 || static_cast<long>(a->n_heads) * ceil_div(a->block_len, kQG) > 65535)
         return POLESTAR_ERR_UNSUPPORTED;
 
-    // 1. drift
-    polestar_status st = polestar_drift(a->dtype, a->batch, a->seq, a->d, a->h_cur, a->h_prev, a->drift, stream);
+    // 1. drift | vocabulary scan
+    LeadArgs l{};
+    l.hc = static_cast<const char*>(a->h_cur);
+    l.hp = static_cast<const char*>(a->h_prev);
+    l.drift = a->drift;
+    l.rows = a->batch * a->seq;
+    l.d = a->d;
+    l.logits = static_cast<const char*>(a->logits);
+    l.vocab = a->vocab;
+    l.nq = a->block_len;
+    l.chunk = L.cp.chunk;
+    l.splits = L.cp.splits;
+    l.mask_id = a->mask_token_id;
+    l.parts = reinterpret_cast<ScanPart*>(ws + L.scan_off);
+    l.n_drift = ceil_div(l.rows, kDriftBlock / L.drift_tpr);
+    const long n_lead = static_cast<long>(l.n_drift) + static_cast<long>(L.cp.splits) * a->block_len * a->batch;
+    if (n_lead > 0x7fffffffL) return POLESTAR_ERR_UNSUPPORTED;
+    const bool lok = bf16 ? launch_lead<true>(L.drift_tpr, L.drift_nch, dim3(n_lead), l, stream)
+                          : launch_lead<false>(L.drift_tpr, L.drift_nch, dim3(n_lead), l, stream);
+    if (!lok) return POLESTAR_ERR_UNSUPPORTED;
+    polestar_status st = launch_status();
     if (st != POLESTAR_OK) return st;
 
-    // 2. select | Q projection | vocabulary scan
+    // 2. select | Q projection
     FrontArgs f{};
     f.drift = a->drift;
     f.elig = a->eligible;
@@ -252,33 +369,37 @@ extern "C" polestar_status polestar_step(const polestar_step_args* a, void* work
     f.q.block_len = a->block_len;
     f.q.out0 = static_cast<char*>(a->q);
     f.q.m_max = a->batch * a->block_len;
-    f.q.ksplit = 1;
-    f.q.steps_per_split = L.qp.steps_per_split;
-    f.q.row_tiles = 1;
-    f.q.col_tiles = L.qp.col_tiles;
-    f.logits = static_cast<const char*>(a->logits);
-    f.vocab = a->vocab;
-    f.nq = a->block_len;
-    f.chunk = L.cp.chunk;
-    f.splits = L.cp.splits;
-    f.mask_id = a->mask_token_id;
-    f.parts = reinterpret_cast<ScanPart*>(ws + L.scan_off);
+    f.q.ws = reinterpret_cast<float*>(ws + L.q_off);
+    gemm_finalize_args(L.qp, f.q);
     f.n_sel = a->batch;
-    f.n_q = L.qp.col_tiles;
-    const long n_front = static_cast<long>(f.n_sel) + f.n_q + static_cast<long>(L.cp.splits) * a->block_len * a->batch;
-    if (n_front > 0x7fffffffL) return POLESTAR_ERR_UNSUPPORTED;
-    const bool ok = bf16 ? launch_front<true>(L.ipt, L.qp.mt, dim3(n_front), f, stream)
-                         : launch_front<false>(L.ipt, L.qp.mt, dim3(n_front), f, stream);
+    const int n_q = L.qp.small ? L.qp.col_tiles : L.qp.grid;
+    const bool ok = bf16 ? launch_front<true>(L.ipt, !L.qp.small, 2 * L.qp.steps_per_split, L.qp.mt,
+                                              dim3(f.n_sel + n_q), f, stream)
+                         : launch_front<false>(L.ipt, !L.qp.small, 2 * L.qp.steps_per_split, L.qp.mt,
+                                               dim3(f.n_sel + n_q), f, stream);
     if (!ok) return POLESTAR_ERR_UNSUPPORTED;
     st = launch_status();
     if (st != POLESTAR_OK) return st;
 
-    // 3. refresh (the caller's events bracket exactly this launch group)
+    // 3. refresh GEMM, 4. refresh reduce | Q reduce (the caller's events
+    // bracket exactly these two launches)
     if (refresh_begin && hipEventRecord(refresh_begin, stream) != hipSuccess) return POLESTAR_ERR_LAUNCH;
-    st = polestar_refresh_kv(a->dtype, a->batch, a->seq, a->d, a->n_kv_heads, a->head_dim, a->h_cur,
-                             a->stale_idx, a->stale_count, a->k, a->block_start, a->block_len, a->w_k, a->w_v,
-                             a->k_cache, a->v_cache, ws, L.refresh_bytes, stream);
+    ReduceArgs rk{};
+    GemmArgs rg = refresh_gemm_args(a->batch, a->seq, a->d, a->n_kv_heads * a->head_dim, a->h_cur, a->stale_idx,
+                                    a->stale_count, a->k, a->block_start, a->block_len, a->w_k, a->w_v,
+                                    a->k_cache, a->v_cache, ws);
+    st = gemm_run(bf16, L.rp, rg, stream, &rk.r);
     if (st != POLESTAR_OK) return st;
+    gemm_finalize_args(L.rp, rg);
+    rk.n_r = gemm_reduce_blocks(L.rp, rg);
+    rk.q = f.q;
+    const int n_red = rk.n_r + gemm_reduce_blocks(L.qp, f.q);
+    if (n_red > 0) {
+        if (bf16) hipLaunchKernelGGL(reduce2_kernel<true>, dim3(n_red), dim3(kStepBlock), 0, stream, rk);
+        else hipLaunchKernelGGL(reduce2_kernel<false>, dim3(n_red), dim3(kStepBlock), 0, stream, rk);
+        st = launch_status();
+        if (st != POLESTAR_OK) return st;
+    }
     if (refresh_end && hipEventRecord(refresh_end, stream) != hipSuccess) return POLESTAR_ERR_LAUNCH;
 
     // 4. attention
@@ -294,7 +415,7 @@ extern "C" polestar_status polestar_step(const polestar_step_args* a, void* work
     BackArgs k{};
     k.att = att;
     k.n_merge = L.ap.splits > 1 ? static_cast<int>(ceil_div(static_cast<long>(a->batch) * a->n_heads * a->block_len, 4)) : 0;
-    k.parts = f.parts;
+    k.parts = l.parts;
     k.splits = L.cp.splits;
     k.nq = a->block_len;
     k.masked = a->masked;

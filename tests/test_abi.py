@@ -104,7 +104,9 @@ def test_attend_validation_and_workspace(L):
 
 def test_project_q_validation_and_workspace(L):
     f = L.polestar_project_q
-    assert ps.project_q_workspace_size(ps.BF16, 1, 4096, 32, 128, 32) == 0      # 32 rows: no partials
+    assert ps.project_q_workspace_size(ps.BF16, 1, 4096, 32, 128, 16) == 0      # 16 rows: small kernel, no partials
+    assert ps.project_q_workspace_size(ps.FP32, 1, 4096, 32, 128, 32) == 0      # fp32: small kernel
+    assert ps.project_q_workspace_size(ps.BF16, 1, 4096, 32, 128, 32) > 0       # 32 bf16 rows: DMA kernel, split-K
     ws = ps.project_q_workspace_size(ps.BF16, 8, 4096, 32, 128, 32)
     assert ws > 0                                                                # 256 rows: split-K
     args = [1, 8, 1536, 4096, 32, 128, 1024, 32, FAKE, FAKE, FAKE, FAKE, ws, None]
