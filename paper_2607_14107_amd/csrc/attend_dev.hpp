@@ -48,6 +48,14 @@ __device__ __forceinline__ int vslot(int kk) {
     return kk < 16 ? 8 * (kk >> 2) + (kk & 3) : 8 * ((kk - 16) >> 2) + 4 + (kk & 3);
 }
 
+// Physical LDS row of V^T row r (d index) in attend_kernel's bf16 path.  A
+// transposing store instruction writes rows 8 dc + e (dc = 16-byte chunk of
+// d, one per lane, e fixed), which with the 80-byte pitch fall on only two
+// bank offsets; XOR-ing the low three bits of the row with bits 4..6 spreads
+// them over 16, while the fragment reads (16 consecutive rows) stay a
+// permutation of 16 rows.
+__device__ __forceinline__ int vrow(int r) { return r ^ ((r >> 4) & 7); }
+
 template <bool BF16, int HD>
 __global__ __launch_bounds__(kAttBlock, 2) void attend_kernel(AttArgs a) {
     using T = Elem<BF16>;
@@ -106,41 +114,74 @@ __global__ __launch_bounds__(kAttBlock, 2) void attend_kernel(AttArgs a) {
     char* myvt = smem + w * HD * VP;
     const int wu = __builtin_amdgcn_readfirstlane(w);   // wave-uniform tile choice
 
-    for (int base = t_begin; base < t_end; base += 4) {
-        const int tile = base + wu;
-        if (tile < t_end) {
+    // K fragments (A operand of S^T: key key0 + 16 t + (lane & 15)) and the V
+    // tile (item pr = lane + 64 it: 4 keys x one 16-byte chunk of d) of one
+    // tile, loaded into registers.  In bf16 the next tile's loads are issued
+    // as soon as this tile's registers are consumed -- V transposed into LDS,
+    // the score MFMAs issued -- so they are in flight during the softmax and
+    // PV work instead of after it.
+    constexpr int DCV = BF16 ? HD / 8 : HD / 4;   // 16-byte chunks of a V row
+    constexpr int ITV = DCV * 8 / 64;
+    uint4 kf[2][NC];
+    uint4 vv[ITV][4];
+    // V item `it` of this lane: 16-byte chunk dc of d for the 4 keys of group
+    // kg.  bf16: the 4 key groups a store instruction covers are it, it + IT,
+    // it + 2 IT, ... so that they use both 8-byte halves of a 16-byte slot
+    // group (with vrow, a 2-way bank conflict, the minimum for a 512-byte
+    // store); the loads stay 256 contiguous bytes per 16 lanes.
+    auto vitem = [&](int it, int& dc, int& kg) {
+        if constexpr (BF16) {
+            dc = lane % DCV;
+            kg = it + ITV * (lane / DCV);
+        } else {
+            const int pr = lane + 64 * it;
+            dc = pr % DCV;
+            kg = pr / DCV;
+        }
+    };
+    auto load_tile = [&](int tile) {
+        const int key0 = tile * kKT;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const int key = min(key0 + 16 * t + (lane & 15), a.seq - 1);
+            const char* kp = kbase + static_cast<size_t>(key) * krow + g * DPL * ES;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) kf[t][c] = ld16(kp + 16 * c);
+        }
+#pragma unroll
+        for (int it = 0; it < ITV; ++it) {
+            int dc, kg;
+            vitem(it, dc, kg);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int key = min(key0 + 4 * kg + j, a.seq - 1);
+                vv[it][j] = ld16(vbase + static_cast<size_t>(key) * krow + dc * 16);
+            }
+        }
+    };
+
+    // Wave w takes tiles t_begin + w, t_begin + w + 4, ... (no barrier inside
+    // the loop, so the waves' trip counts may differ).
+    int tile = t_begin + wu;
+    if constexpr (BF16) {
+        if (tile < t_end) load_tile(tile);
+    }
+    for (; tile < t_end; tile += 4) {
+        {
+            // fp32 tiles are twice as wide: there the registers do not hold
+            // the next tile across the softmax and PV work, so it loads here
+            if constexpr (!BF16) load_tile(tile);
             const int key0 = tile * kKT;
             floatx4 st[2][2];
-            // K fragments (A operand): key key0 + 16 t + (lane & 15).
-            uint4 kf[2][NC];
-#pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                const int key = min(key0 + 16 * t + (lane & 15), a.seq - 1);
-                const char* kp = kbase + static_cast<size_t>(key) * krow + g * DPL * ES;
-#pragma unroll
-                for (int c = 0; c < NC; ++c) kf[t][c] = ld16(kp + 16 * c);
-            }
-            // V tile -> LDS, transposed to [d][key slot].  Every V load of
-            // the tile is issued before any packing (compile-time trip count).
+            // V tile (loaded into vv) -> LDS, transposed to [d][key slot].
             if constexpr (BF16) {
                 // 8 groups of 4 keys x HD/8 chunks of 8 d; item pr = lane + 64 it
                 constexpr int DC = HD / 8;
                 constexpr int IT = DC * 8 / 64;
-                uint4 vv[IT][4];
 #pragma unroll
                 for (int it = 0; it < IT; ++it) {
-                    const int pr = lane + 64 * it;
-                    const int dc = pr % DC, kg = pr / DC;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int key = min(key0 + 4 * kg + j, a.seq - 1);
-                        vv[it][j] = ld16(vbase + static_cast<size_t>(key) * krow + dc * 16);
-                    }
-                }
-#pragma unroll
-                for (int it = 0; it < IT; ++it) {
-                    const int pr = lane + 64 * it;
-                    const int dc = pr % DC, kg = pr / DC;
+                    int dc, kg;
+                    vitem(it, dc, kg);
                     const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vv[it][0]);
                     const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vv[it][1]);
                     const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vv[it][2]);
@@ -154,27 +195,16 @@ __global__ __launch_bounds__(kAttBlock, 2) void attend_kernel(AttArgs a) {
                         const uint32_t k2 = (x2[e >> 1] >> sh) & 0xffffu;
                         const uint32_t k3 = (x3[e >> 1] >> sh) & 0xffffu;
                         uint2 pk = make_uint2(k0 | (k1 << 16), k2 | (k3 << 16));
-                        *reinterpret_cast<uint2*>(myvt + (dc * 8 + e) * VP + slot * 2) = pk;
+                        *reinterpret_cast<uint2*>(myvt + vrow(dc * 8 + e) * VP + slot * 2) = pk;
                     }
                 }
             } else {
                 constexpr int DC = HD / 4;
                 constexpr int IT = DC * 8 / 64;
-                uint4 vv[IT][4];
 #pragma unroll
                 for (int it = 0; it < IT; ++it) {
-                    const int pr = lane + 64 * it;
-                    const int dc = pr % DC, kg = pr / DC;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int key = min(key0 + 4 * kg + j, a.seq - 1);
-                        vv[it][j] = ld16(vbase + static_cast<size_t>(key) * krow + dc * 16);
-                    }
-                }
-#pragma unroll
-                for (int it = 0; it < IT; ++it) {
-                    const int pr = lane + 64 * it;
-                    const int dc = pr % DC, kg = pr / DC;
+                    int dc, kg;
+                    vitem(it, dc, kg);
                     const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vv[it][0]);
                     const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vv[it][1]);
                     const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vv[it][2]);
@@ -195,6 +225,9 @@ __global__ __launch_bounds__(kAttBlock, 2) void attend_kernel(AttArgs a) {
                     for (int c = 0; c < NC; ++c) s = Mma<BF16>::step(kf[t][c], qf[u][c], s);
                     st[t][u] = s;
                 }
+            if constexpr (BF16) {
+                if (tile + 4 < t_end) load_tile(tile + 4);
+            }
             float p[2][2][4];   // [t][u][i]
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
@@ -238,7 +271,7 @@ __global__ __launch_bounds__(kAttBlock, 2) void attend_kernel(AttArgs a) {
                                        pack_bf16x2(p[1][u][0], p[1][u][1]), pack_bf16x2(p[1][u][2], p[1][u][3]));
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) {
-                    const uint4 va = *reinterpret_cast<const uint4*>(myvt + (dt * 16 + (lane & 15)) * VP + g * 16);
+                    const uint4 va = *reinterpret_cast<const uint4*>(myvt + vrow(dt * 16 + (lane & 15)) * VP + g * 16);
 #pragma unroll
                     for (int u = 0; u < 2; ++u) o[dt][u] = mfma_bf16(va, pf[u], o[dt][u]);
                 }
