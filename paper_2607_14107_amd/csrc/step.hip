@@ -15,9 +15,11 @@
 // Six launches instead of eleven kernels on their own.  Workgroups of a
 // fused launch take their role from their block index; each role is the
 // device body the stand-alone kernel runs, so results are bit-identical to
-// calling the six entry points in order.  Shapes outside the fused kernels'
-// instantiations (more than 2048 positions, more than 64 query rows, blocks
-// longer than 256) run exactly that sequence of entry points instead.
+// calling the six entry points in order.  With more than 64 query rows or
+// more than 2048 positions, select and the Q projection run as two launches
+// of their own (seven in all); shapes outside the other fused kernels
+// (blocks longer than 256, head_dim other than 64/128, rows above the
+// drift kernel's) run exactly the sequence of entry points instead.
 #include "attend_dev.hpp"
 #include "commit_dev.hpp"
 #include "drift_dev.hpp"
@@ -233,7 +235,8 @@ struct StepLayout {
     AttPlan ap;
     CommitPlan cp;
     size_t refresh_bytes, att_off, scan_off, q_off, total;
-    bool fused;
+    bool fused;         // all six launches fused (select | Q projection in one)
+    bool semi;          // the same launches with select and the Q projection as their own
     int ipt;
     int drift_tpr, drift_nch;
 };
@@ -251,8 +254,11 @@ StepLayout step_layout(const polestar_step_args& a) {
     const bool q_dma = bf16 && L.qp.dma && L.qp.row_tiles == 1 && L.qp.mt >= 2 && L.qp.mt <= 4 &&
                        (2 * L.qp.steps_per_split == 8 || 2 * L.qp.steps_per_split == 16);
     const bool drift_ok = drift_config(a.d / (bf16 ? 8 : 4), L.drift_tpr, L.drift_nch);
-    L.fused = L.ipt >= 1 && L.ipt <= 8 && (L.qp.small || q_dma) && drift_ok && a.block_len <= kStepBlock &&
-              (a.head_dim == 64 || a.head_dim == 128);
+    const bool common = drift_ok && a.block_len <= kStepBlock && (a.head_dim == 64 || a.head_dim == 128);
+    L.fused = common && L.ipt >= 1 && L.ipt <= 8 && (L.qp.small || q_dma);
+    // more query rows than the front kernel takes (or a longer sequence):
+    // select and the Q projection run as their own launches, the rest fused
+    L.semi = !L.fused && common && L.ipt >= 1;
     L.att_off = align_up(L.refresh_bytes, 256);
     L.scan_off = L.att_off + align_up(L.ap.part_bytes, 256);
     L.q_off = L.scan_off + align_up(L.cp.ws_bytes, 256);   // Q projection partials (when its plan splits K)
@@ -312,7 +318,7 @@ extern "C" polestar_status polestar_step(const polestar_step_args* a, void* work
     const StepLayout L = step_layout(*a);
     if (workspace_bytes < L.total || !workspace) return POLESTAR_ERR_WORKSPACE;
     char* ws = static_cast<char*>(workspace);
-    if (!L.fused) return run_unfused(*a, L, ws, refresh_begin, refresh_end, stream);
+    if (!L.fused && !L.semi) return run_unfused(*a, L, ws, refresh_begin, refresh_end, stream);
 
     const bool bf16 = a->dtype == POLESTAR_BF16;
     // Every check of the fused launches' stand-alone entry points, before
@@ -372,13 +378,23 @@ extern "C" polestar_status polestar_step(const polestar_step_args* a, void* work
     f.q.ws = reinterpret_cast<float*>(ws + L.q_off);
     gemm_finalize_args(L.qp, f.q);
     f.n_sel = a->batch;
-    const int n_q = L.qp.small ? L.qp.col_tiles : L.qp.grid;
-    const bool ok = bf16 ? launch_front<true>(L.ipt, !L.qp.small, 2 * L.qp.steps_per_split, L.qp.mt,
-                                              dim3(f.n_sel + n_q), f, stream)
-                         : launch_front<false>(L.ipt, !L.qp.small, 2 * L.qp.steps_per_split, L.qp.mt,
-                                               dim3(f.n_sel + n_q), f, stream);
-    if (!ok) return POLESTAR_ERR_UNSUPPORTED;
-    st = launch_status();
+    if (L.fused) {
+        const int n_q = L.qp.small ? L.qp.col_tiles : L.qp.grid;
+        const bool ok = bf16 ? launch_front<true>(L.ipt, !L.qp.small, 2 * L.qp.steps_per_split, L.qp.mt,
+                                                  dim3(f.n_sel + n_q), f, stream)
+                             : launch_front<false>(L.ipt, !L.qp.small, 2 * L.qp.steps_per_split, L.qp.mt,
+                                                   dim3(f.n_sel + n_q), f, stream);
+        if (!ok) return POLESTAR_ERR_UNSUPPORTED;
+        st = launch_status();
+    } else {
+        // the same two pieces as separate launches; the Q projection's split-K
+        // reduction still joins the refresh's in launch 4
+        st = polestar_select(a->batch, a->seq, a->drift, a->eligible, a->block_start, a->block_len, a->k,
+                             a->stale_idx, a->stale_count, stream);
+        if (st != POLESTAR_OK) return st;
+        GemmArgs qdef{};
+        st = gemm_run(bf16, L.qp, f.q, stream, &qdef);
+    }
     if (st != POLESTAR_OK) return st;
 
     // 3. refresh GEMM, 4. refresh reduce | Q reduce (the caller's events

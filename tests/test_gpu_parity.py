@@ -652,8 +652,9 @@ def _assert_same(a, b):
 
 @pytest.mark.parametrize("cfg_index,subrun", [(0, 0), (1, 1), (2, 0), (3, 0)])
 def test_step_fused_equals_calls_on_configs(P, cfg_index, subrun):
-    """Configs 0-1 take the fused launches, 2-3 (more than 64 query rows) the
-    six-call fallback; either way the results equal the six calls bit for bit."""
+    """Configs 0-1 take the six fused launches, 2-3 (more than 64 query rows)
+    the seven with select and the Q projection on their own; either way the
+    results equal the six calls bit for bit."""
     L = layer(cfg_index, subrun)
     a, b = _run_both(P, L["cfg"], L["x"], L["kc"], L["vc"], int(L["x"]["k"]))
     _assert_same(a, b)
@@ -665,6 +666,9 @@ def test_step_fused_equals_calls_on_configs(P, cfg_index, subrun):
     (2, 700, 600, 32, 256, 4, 4, 64, 2048, 70),     # 3 keys per thread, 64 query rows (MT 4)
     (1, 1500, 1400, 20, 512, 2, 2, 128, 4096, 0),   # 6 keys per thread, no stale rows
     (3, 2048, 0, 16, 256, 1, 1, 128, 512, 200),     # 8 keys per thread, block at the start
+    # select and the Q projection as their own launches, the rest fused:
+    (2, 3000, 100, 40, 256, 2, 1, 64, 1000, 50),    # 3000 positions (12 keys per thread), 80 query rows
+    (1, 300, 10, 100, 256, 4, 2, 64, 512, 20),      # 100 query rows, grouped KV heads
 ])
 def test_step_fused_equals_calls_small_shapes(P, dtype, batch, seq, bs, bl, d, H, Hkv, hd, vocab, k):
     from types import SimpleNamespace
