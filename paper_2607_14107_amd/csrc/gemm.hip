@@ -610,13 +610,27 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
         const int nstage = K / (kTileStage / 2);
         p.row_tiles = ceil_div(m_max, kTileDim);
         const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, kTileDim);
-        // the smallest split that fills the chip, else the largest; every
-        // split runs a whole number of 4-stage loop trips and at least 16 stages
+        // The split with the least estimated time: ceil(tiles * k / 256)
+        // rounds of one workgroup per CU, each 1/k of a tile's work (a whole
+        // 256 x 256 x K tile at the ~1 PFLOP/s this kernel sustains: 3.9
+        // GFLOP/ms per CU), plus the fp32 partials of a split run written
+        // and read back (8 k M N bytes at ~5 TB/s).  Measured on the
+        // batch-8 LLaDA-8B refresh: 192 tiles (10% stale) unsplit in one
+        // round 130 us, in two splits (384 workgroups, a round and a half,
+        // 98 MB of partials) 159 us; 64 tiles (2%) best in four splits;
+        // 20 tiles (the Dream-7B refresh) in seven.  Every split runs a whole
+        // number of 4-stage loop trips and at least 16 stages.
+        const double tile_us = 256.0 * 256.0 * 2.0 * K / 3.9e6;
         int ksplit = 1;
+        double best = 1e30;
         for (int k = 1; k <= kMaxSplit; ++k) {
             if (nstage % (4 * k) != 0 || nstage / k < 16) continue;
-            ksplit = k;
-            if (tiles * k >= kTargetWgs) break;
+            const double rounds = static_cast<double>((tiles * k + kTargetWgs - 1) / kTargetWgs);
+            const double cost = rounds * tile_us / k + (k > 1 ? 8.0 * k * m_max * N / 5e6 : 0.0);
+            if (cost < best) {
+                best = cost;
+                ksplit = k;
+            }
         }
         p.tile = tiles * ksplit >= kTargetWgs / 2 &&
                  (ksplit <= 4 || nstage / ksplit >= 48 || p.row_tiles >= 4);

@@ -219,7 +219,7 @@ def test_refresh_nothing_leaves_cache_untouched(P):
     assert np.array_equal(kb, L["kc"]) and np.array_equal(vb, L["vc"])
 
 
-@pytest.mark.parametrize("cfg_index,subrun", [(2, 0), (2, 2), (3, 0)])
+@pytest.mark.parametrize("cfg_index,subrun", [(2, 0), (2, 1), (2, 2), (3, 0)])
 def test_refresh_large_configs_sampled(P, cfg_index, subrun):
     L = layer(cfg_index, subrun)
     cfg = L["cfg"]
