@@ -19,6 +19,7 @@ namespace ps {
 namespace {
 
 constexpr int kScanBlock = 256;
+constexpr int kScanInFlight = 8;   // 16-byte chunks per lane kept in flight by scan_body
 constexpr int kMaxSplits = 16;    // vocabulary slices per token
 constexpr int kMaxHist = 16;      // drift history depth h
 
@@ -52,7 +53,7 @@ __device__ __forceinline__ void scan_body(const char* __restrict__ logits, int v
                                           ScanPart* __restrict__ parts, int split, int j, int b) {
     using T = Elem<BF16>;
     constexpr int ES = T::kBytes;
-    constexpr int G = 8;   // 16-byte chunks per lane kept in flight
+    constexpr int G = kScanInFlight;
     __shared__ float sm[4], ss[4], sb[4];
     __shared__ int si[4];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -253,6 +254,11 @@ inline CommitPlan commit_plan(bool bf16, int batch, int nq, int vocab) {
     const int e = bf16 ? 8 : 4;
     const long toks = static_cast<long>(batch) * nq;
     int splits = static_cast<int>((2048 + toks - 1) / toks);   // ~2048 workgroups: several resident per CU
+    // and no slice longer than one round of loads (kScanInFlight chunks per
+    // thread): a vocabulary of 152064 in 8 slices took a second, mostly
+    // empty, round per workgroup (25.4 us for 78 MB)
+    const int one_round = kScanBlock * kScanInFlight * e;
+    if (splits < ceil_div(vocab, one_round)) splits = ceil_div(vocab, one_round);
     const int max_splits = ceil_div(vocab, 2048);
     if (splits > max_splits) splits = max_splits;
     if (splits > kMaxSplits) splits = kMaxSplits;
