@@ -534,6 +534,9 @@ bool dispatch_dma(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
     static_assert(kDmaMaxRowTiles == 10, "dispatch covers 2..kDmaMaxRowTiles");
     switch (2 * p.steps_per_split) {   // 128-byte stages per split
         case 8: return dispatch_dma_mt<BF16, 8>(p, g, s);
+        case 10: return dispatch_dma_mt<BF16, 10>(p, g, s);
+        case 12: return dispatch_dma_mt<BF16, 12>(p, g, s);
+        case 14: return dispatch_dma_mt<BF16, 14>(p, g, s);
         case 16: return dispatch_dma_mt<BF16, 16>(p, g, s);
         default: return false;
     }
@@ -648,8 +651,10 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
         return p;
     }
     // DMA kernel: one or two row tiles of at most 160 rows, K split evenly
-    // into 8 or 16 stages of 128 bytes per row (the smallest such split at
-    // or above the one that fills the chip)
+    // into 8 to 16 stages of 128 bytes per row; the split with the fewest
+    // rounds of one workgroup per CU times stages per split, the smaller
+    // split on ties (the Dream-7B Q projection, 56 tiles of K = 3584: four
+    // splits of 14 stages in one round rather than seven of 8 in two)
     const bool dma_rows = bf16 && m_max <= 2L * 16 * kDmaMaxRowTiles;
     p.row_tiles = dma_rows ? ceil_div(m_max, 16L * kDmaMaxRowTiles) : ceil_div(m_max, 256);
     const long tiles = static_cast<long>(p.row_tiles) * p.col_tiles;
@@ -660,8 +665,12 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     p.steps_per_split = ceil_div(nsteps, ksplit);
     p.ksplit = ceil_div(nsteps, p.steps_per_split);
     p.dma = false;
-    for (int ks = p.ksplit; dma_rows && !p.dma && ks <= kMaxSplit; ++ks) {
-        if (nsteps % ks == 0 && (nsteps / ks == 4 || nsteps / ks == 8)) {
+    long best = -1;
+    for (int ks = 1; dma_rows && ks <= kMaxSplit; ++ks) {
+        if (nsteps % ks != 0 || nsteps / ks < 4 || nsteps / ks > 8) continue;
+        const long cost = (tiles * ks + kTargetWgs - 1) / kTargetWgs * (nsteps / ks);
+        if (best < 0 || cost < best) {
+            best = cost;
             p.dma = true;
             p.ksplit = ks;
             p.steps_per_split = nsteps / ks;

@@ -306,7 +306,9 @@ def test_project_q_matches_oracle_and_attend(P, cfg_index):
 
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 @pytest.mark.parametrize("batch,seq,bs,bl,d,H,hd", [(1, 40, 7, 33, 256, 2, 64), (3, 70, 60, 10, 512, 1, 128),
-                                                    (5, 20, 0, 20, 1024, 4, 64)])
+                                                    (5, 20, 0, 20, 1024, 4, 64),
+                                                    (2, 70, 5, 48, 1280, 8, 128),     # bf16: splits of 10 stages
+                                                    (1, 200, 50, 100, 1792, 4, 128)])  # bf16: splits of 14 stages
 def test_project_q_ragged_shapes(P, dtype, batch, seq, bs, bl, d, H, hd):
     """Row tiles with a ragged tail, more than 64 rows (split-K path), and a
     block at the start of the sequence."""
