@@ -225,17 +225,18 @@ def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, cal
         "source_digest": source_digest(call),
         "commands": [
             "cd /tmp && export TMPDIR=/tmp",
-            "rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/pmc_fetch -o c -- "
+            "rocprofv3 --pmc FETCH_SIZE -f csv -d $OUT/pmc_fetch -o c -- "
             "python3 $R/bench.py --no-cpu-baseline --steps 20 --warmup 2",
-            "rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/pmc_write -o c -- "
+            "rocprofv3 --pmc WRITE_SIZE -f csv -d $OUT/pmc_write -o c -- "
             "python3 $R/bench.py --no-cpu-baseline --steps 20 --warmup 2",
-            "rocprofv3 --pmc FETCH_SIZE -f csv -d $R/gpurun_out/pmc_cfetch -o c -- python3 $R/bench.py --copy-calibration",
-            "rocprofv3 --pmc WRITE_SIZE -f csv -d $R/gpurun_out/pmc_cwrite -o c -- python3 $R/bench.py --copy-calibration",
-            f"python3 $R/bench.py --summarize-counters gpurun_out/pmc_fetch gpurun_out/pmc_write "
-            f"gpurun_out/pmc_cfetch gpurun_out/pmc_cwrite --call {call}",
+            "rocprofv3 --pmc FETCH_SIZE -f csv -d $OUT/pmc_cfetch -o c -- python3 $R/bench.py --copy-calibration",
+            "rocprofv3 --pmc WRITE_SIZE -f csv -d $OUT/pmc_cwrite -o c -- python3 $R/bench.py --copy-calibration",
+            f"python3 $R/bench.py --summarize-counters $OUT/pmc_fetch $OUT/pmc_write "
+            f"$OUT/pmc_cfetch $OUT/pmc_cwrite --call {call}",
         ],
         "note": "counter KiB per launch summed over the call's kernels (median over launches); "
-                "bytes = KiB * 1024 * (copy bytes / copy counter bytes) for FETCH and WRITE",
+                "bytes = KiB * 1024 * (copy bytes / copy counter bytes) for FETCH and WRITE; "
+                "$R is the repository, $OUT any output directory",
     }
     with open(traffic_path(call, workload), "w") as f:
         json.dump(t, f, indent=1)
@@ -385,7 +386,7 @@ def main():
         return copy_calibration()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the layer step shards over the batch with no exchange, see DESIGN.md)", file=sys.stderr)
+              "(the layer step shards over the batch with no exchange between GPUs)", file=sys.stderr)
         return 2
 
     import torch

@@ -17,7 +17,7 @@ OCP microscaling formats that MI355X supports natively:
   MXFP8: the same blocks and scales, values in FP8 E4M3 (bias 7, no
          infinities, largest magnitude 448, subnormal step 2^-9).
 
-Readings (also listed in the design doc):
+Readings:
   Q-1  The block scale follows the OCP rule: e = floor(log2(amax)) - emax of
        the element format (2 for E2M1, 8 for E4M3), amax the block's largest
        magnitude, clamped to the E8M0 range [-127, 127]; a block of zeros

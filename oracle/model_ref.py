@@ -8,7 +8,7 @@ on purpose (replay).  float64 NumPy; the per-layer hot path is composed from
 `polestar_ref` (drift, select, refresh_kv, attend, confidence, commit_rule).
 
 The model (a masked-diffusion LM of the shape the paper evaluates, Sec. 5.1;
-readings where the paper gives no detail, also listed in the design doc):
+readings where the paper gives no detail):
   M-1  Pre-norm layers: x += W_o Attn(h), h = RMSNorm(x); then
        x += W_down (silu(W_gate g) * W_up g), g = RMSNorm(x).  Attention is
        bidirectional over every cache slot (eq. 3).
@@ -297,7 +297,7 @@ def generate(weights: dict, prompt: np.ndarray, shape: Shape, p: LoopParams) -> 
 # ---------------------------------------------------------------------------
 # The paper's own flow (Alg. 1, per-layer loop; Sec. 4.1 "Measuring Drift and
 # Layer-wise KV Updates"): clustered proxy drift per layer and update packets
-# passed from layer to layer.  Readings (also listed in the design doc):
+# passed from layer to layer.  Readings:
 #   F3-1  each layer caches its inputs X (the residual stream, kept exact
 #         here, fp32 on the GPU) besides K/V and H = RMSNorm(X); the local
 #         window's H is clustered per layer at block entry (proxy_ref), and

@@ -22,7 +22,7 @@ per-layer loop):
     6. after the refresh, the cluster sums move by the refreshed rows'
        change (labels stay fixed until the next block entry).
 
-Readings where the paper leaves the detail open (also listed in the design doc):
+Readings where the paper leaves the detail open:
   P-1  Spherical K-means clusters the directions h/|h| (cosine similarity).
   P-2  Initialisation is deterministic: centroid j starts at the window point
        of rank floor(j*n/K).  A fixed number of iterations (default 10):

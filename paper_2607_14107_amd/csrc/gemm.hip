@@ -40,7 +40,7 @@
 //   for the DMA are explicit s_waitcnt immediates (each wave issues the same
 //   number of DMA instructions per stage), and each slot's LDS arrays are
 //   separate objects so the compiler does not add waits of its own.
-//   Measured on the config-1 refresh (138 rows x 8192 x 4096): 18.6 us for
+//   Measured on the batch-1 LLaDA-8B refresh (138 rows x 8192 x 4096): 18.6 us for
 //   the split-K GEMM against 25.9 us for gemm_rows_kernel.
 //
 // gemm_small_kernel (at most 64 rows, e.g. the Q projection): a workgroup
