@@ -276,7 +276,7 @@ STACKS = {
     # batch 16, prompt 512, 256 generated tokens in blocks of 32
     4: StackConfig(4, "llada8b-stack-b16", "bf16", batch=16, n_layers=32, d=4096, n_heads=32, head_dim=128,
                    ffn=12288, vocab=126464, prompt_len=512, gen_len=256),
-    # config 4's width and sequence length with two layers and two blocks
+    # the 32-layer stack's width and sequence length with two layers and two blocks
     # (prompt 704 + 64 generated): the full-width parity case
     41: StackConfig(41, "llada8b-width-2layer-b16", "bf16", batch=16, n_layers=2, d=4096, n_heads=32,
                     head_dim=128, ffn=12288, vocab=126464, prompt_len=704, gen_len=64),

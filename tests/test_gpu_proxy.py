@@ -122,7 +122,7 @@ def test_cluster_labels_are_nearest_final_centroids_on_noisy_data(P):
 
 
 def _proxy_case(dtype, seed):
-    """Config-1-like layer (config 0 for fp32) with planted clusters in the
+    """The batch-1 LLaDA-8B layer (the tiny fp32 layer for fp32) with planted clusters in the
     window of h_prev: weights, the prior cache, and a second cache whose 20
     random rows are re-projected from perturbed states."""
     cfg = inputs.CONFIGS[1] if dtype == "bf16" else inputs.CONFIGS[0]
