@@ -245,6 +245,44 @@ def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, cal
     return 0
 
 
+def measure_gather_scatter(P, torch, cfg, sets, idx, cnt, es, reps=50):
+    """The row gather and scatter of an update packet on their own (untimed
+    for the headline): the stale rows of h_cur into a compact [batch][k][d]
+    buffer, and compact K rows back into the cache, rotating over the input
+    copies.  Algorithmic bytes: every moved row read once and written once
+    (the gather also writes the zero rows past a sequence's count).  Runs
+    after everything else: the scatter overwrites cache rows."""
+    if idx is None or idx.shape[1] == 0:
+        return None
+    b, k = idx.shape
+    kvd = cfg.n_kv_heads * cfg.head_dim
+    dev = idx.device
+    dt = sets[0]["h_cur"].dtype
+    rows = int(cnt.clamp(0, k).sum().item())
+    packet = torch.empty((b, k, cfg.d), dtype=dt, device=dev)
+    # one compact source per input copy, so that the scatter's reads come from HBM too
+    krows = [torch.zeros((b, k, kvd), dtype=dt, device=dev) for _ in sets]
+    out = {}
+    for name in ("gather", "scatter"):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        torch.cuda._sleep(20_000_000)
+        e0.record()
+        for i in range(reps):
+            c = sets[i % len(sets)]
+            if name == "gather":
+                P.gather_rows(c["h_cur"], idx, cnt, packet)
+            else:
+                P.scatter_rows(krows[i % len(sets)], idx, cnt, c["k_cache"].view(b, cfg.seq, kvd))
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        nbytes = (rows + b * k) * cfg.d * es if name == "gather" else 2 * rows * kvd * es
+        out[name] = {"us": round(us, 3), "rows": rows, "bytes": int(nbytes), "GB_s": round(nbytes / us / 1e3, 1),
+                     "hbm_frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4)}
+    return out
+
+
 def measure_proxy(P, torch, cfg, s, stream, es, n_clusters=8, k_top=4, reps=50):
     """The paper's clustered drift estimator on the same layer (untimed for
     the headline): block-entry K-means of the window (2B before the block, B
@@ -568,6 +606,7 @@ def main():
         "host_enqueue_us_per_step": round(enqueued / args.steps * 1e6, 2),
         "calls_us": calls,
     }
+    out["gather_scatter"] = measure_gather_scatter(P, torch, cfg, sets, step.stale_idx, step.stale_count, es)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, x, k, args.cpu_seconds)
     print(json.dumps(out))

@@ -533,9 +533,11 @@ polestar_status polestar_scatter_rows(int batch, int seq, int row_bytes, const v
  * drift beside the vocabulary scan, the per-sequence select beside the Q
  * projection, the refresh's split-K reduction beside the Q projection's, and
  * the attention's split merge beside the commit's finalize step, so the
- * latency-bound pieces overlap bandwidth-bound ones.  Shapes outside the
- * fused kernels (seq > 2048, batch * block_len > 64, block_len > 256) run
- * the six calls one after another instead, with the same results.
+ * latency-bound pieces overlap bandwidth-bound ones.  With seq > 2048 or
+ * batch * block_len > 64, select and the Q projection run as launches of
+ * their own and the rest stays fused; shapes outside the other fused
+ * kernels (block_len > 256, d above the drift kernel's rows) run the six
+ * calls one after another.  The results are the same on every path.
  *
  * All fields of polestar_step_args keep the meaning, layout and
  * requirements they have in the stand-alone calls above; eligible may be
