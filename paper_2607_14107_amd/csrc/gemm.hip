@@ -609,7 +609,13 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     // rows x 1024 x 3584 in seven splits, 33 us against 44 us); short splits
     // of one or two row tiles (256 or 512 rows of a 4096 x 4096 projection)
     // stay on the DMA or row kernel.
-    if (bf16 && m_max > 16L * kDmaMaxRowTiles && K % kTileStage == 0) {
+    // Narrow outputs (at most 1024 columns: four 256-wide tiles across) take
+    // the DMA kernel's 128-column tiles instead, up to eight row tiles: the
+    // Dream-7B refresh (1052 rows x 1024 x 3584) runs 56 tiles in four splits
+    // (224 workgroups, 17 MB of partials) in 27.7 us, where the tile kernel's
+    // 20 tiles needed seven splits (30 MB of partials) and 37.5 us.
+    const bool narrow_dma = bf16 && N <= 4 * kTileDim && m_max <= 8L * 16 * kDmaMaxRowTiles;
+    if (bf16 && m_max > 16L * kDmaMaxRowTiles && K % kTileStage == 0 && !narrow_dma) {
         const int nstage = K / (kTileStage / 2);
         p.row_tiles = ceil_div(m_max, kTileDim);
         const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, kTileDim);
@@ -655,7 +661,7 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     // rounds of one workgroup per CU times stages per split, the smaller
     // split on ties (the Dream-7B Q projection, 56 tiles of K = 3584: four
     // splits of 14 stages in one round rather than seven of 8 in two)
-    const bool dma_rows = bf16 && m_max <= 2L * 16 * kDmaMaxRowTiles;
+    const bool dma_rows = bf16 && (m_max <= 2L * 16 * kDmaMaxRowTiles || narrow_dma);
     p.row_tiles = dma_rows ? ceil_div(m_max, 16L * kDmaMaxRowTiles) : ceil_div(m_max, 256);
     const long tiles = static_cast<long>(p.row_tiles) * p.col_tiles;
     int ksplit = 1;
