@@ -67,10 +67,13 @@ const char* polestar_status_string(polestar_status s);
  * token (b, i) is the softmax of its layer-input hidden state over the d
  * channels, so, in nats,
  *     drift[b][i] = KL( softmax(h_cur[b][i][:]) || softmax(h_prev[b][i][:]) ).
- * It is evaluated in fp32 in the form
- *     sum_c p_c*dlt_c - log1p( sum_c q_c*expm1(dlt_c) ),  dlt = h_cur - h_prev,
- * which is exactly 0 for identical rows.  Tiny negative results of rounding
- * are returned as they are.
+ * It is evaluated in fp32 as
+ *     sum_c p_c*dl_c - log(Za / Zb),   dl = (h_cur - max h_cur) - (h_prev - max h_prev),
+ * with each row's exponentials taken against its own maximum (Za, Zb its
+ * softmax denominators) and Za - Zb summed term by term through expm1 where
+ * the rows are close, so rows that differ by any finite amount give a finite
+ * result and identical rows give exactly 0.  Tiny negative results of
+ * rounding are returned as they are.
  *
  *   h_cur, h_prev : [batch][seq][d] dtype   current / cached hidden states
  *   drift         : [batch][seq] float      output

@@ -5,15 +5,18 @@
 // A row is spread over 64-256 threads (4 waves at d = 4096, two 16-byte
 // chunks of each row per lane): the two rows of the token are loaded once
 // with coalesced 16-byte loads into registers (an HBM-bound stream of 2*d
-// elements), the common max is reduced (shuffles, then LDS across the
-// row's waves), then the thread accumulates in fp32
-//   Zb  = sum e_c,              e_c = exp(b_c - m)
-//   Sqe = sum e_c * expm1(dlt_c),   dlt = a - b
-//   Spd = sum e_c * (1 + expm1(dlt_c)) * dlt_c
-// so that sum exp(a_c - m) = Zb + Sqe and
-//   KL(softmax(a) || softmax(b)) = Spd / (Zb + Sqe) - log1p(Sqe / Zb).
-// Only one exponential per element is needed besides expm1, and identical
-// rows give exactly 0.
+// elements), both row maxima ma, mb are reduced (shuffles, then LDS across
+// the row's waves), then the thread accumulates in fp32, with reference
+// points ra = rb = max(ma, mb) when |ma - mb| <= 16, else ra = ma, rb = mb,
+// eb_c = exp(b_c - rb), ea_c = exp(a_c - ra) and dl_c = (a_c - b_c) - (ra - rb),
+//   Zb  = sum eb_c,   Za = sum ea_c,
+//   Sqe = sum (ea_c - eb_c)   (as eb_c * expm1(dl_c) when |dl_c| < 1/16),
+//   Spd = sum ea_c * dl_c
+// so that KL(softmax(a) || softmax(b)) = Spd / Za - log(Za / Zb), with
+// Za = Zb + Sqe and log(Za / Zb) = log1p(Sqe / Zb) while the two sums are
+// within a factor of two.  Every term lies in [0, 1] (no overflow or 0 * inf
+// for rows that differ by any amount), nearly equal rows keep their small
+// drift accurate, and identical rows give exactly 0.
 #include "drift_dev.hpp"
 
 namespace ps {

@@ -12,25 +12,18 @@ namespace ps {
 namespace {
 
 constexpr int kDriftBlock = 256;
-constexpr float kSmall = 0.0625f;              // |dlt| below this: series for expm1
+constexpr float kSmall = 0.0625f;              // |dl| below this: series for expm1
+constexpr float kNear = 16.0f;                 // row maxima closer than this: one reference
 
 // expm1 for |x| < 1/16 from its Taylor series; the first omitted term
 // x^6/720 is below 1.4e-9 relative there.
 __device__ __forceinline__ float expm1_small(float x) {
+#pragma clang fp contract(off)
     float p = fmaf(x, 1.0f / 120.0f, 1.0f / 24.0f);
     p = fmaf(x, p, 1.0f / 6.0f);
     p = fmaf(x, p, 0.5f);
     p = fmaf(x, p, 1.0f);
     return x * p;
-}
-
-// expm1 on either branch, chosen by a bitwise select so that the code stays
-// straight-line (no per-element exec-mask branches); both sides are cheap.
-__device__ __forceinline__ float expm1_any(float x) {
-    const float series = expm1_small(x);
-    const float direct = fast_exp2(x * kLog2e) - 1.0f;
-    const uint32_t pick = 0u - static_cast<uint32_t>(fabsf(x) < kSmall);
-    return __uint_as_float((__float_as_uint(series) & pick) | (__float_as_uint(direct) & ~pick));
 }
 
 // Reduce NV values at once over the TPR threads of a row: wave shuffles,
@@ -60,14 +53,30 @@ __device__ __forceinline__ void row_reduce(float (&v)[NV], float* red) {
     }
 }
 
+// The row's KL from its four sums (za and zb lie in [exp(-16), d]).  While
+// the two sums stay within a factor of two of each other, za is taken as
+// zb + sqe, consistent with log1p(sqe / zb), which keeps the small drift of
+// nearly equal rows accurate (and exactly 0 for equal rows); beyond that the
+// direct sum za and log(za / zb) carry no cancellation.
+__device__ __forceinline__ float drift_finish(float zb, float za, float sqe, float spd) {
+#pragma clang fp contract(off)
+    const float r = sqe / zb;
+    if (fabsf(r) <= 0.5f) return spd / (zb + sqe) - log1pf(r);
+    return spd / za - logf(za / zb);
+}
+
 // One row of d elements per TPR threads (TPR = 64, 128 or 256); each thread
 // keeps NCH 16-byte chunks of both rows in registers.  Rows of a workgroup:
 // kDriftBlock / TPR.
 template <bool BF16, int TPR, int NCH>
 __device__ __forceinline__ void drift_body(const char* __restrict__ hc, const char* __restrict__ hp,
                                            float* __restrict__ out, int rows, int d, int blk) {
+    // Every multiply-add below is an explicit fmaf: no other contraction, so
+    // the stand-alone kernel and the fused step's launch (different inline
+    // contexts) round identically.
+#pragma clang fp contract(off)
     using T = Elem<BF16>;
-    __shared__ float red[3 * (kDriftBlock / kWave)];
+    __shared__ float red[4 * (kDriftBlock / kWave)];
     const int tr = threadIdx.x % TPR;             // thread within the row
     const int row_raw = blk * (kDriftBlock / TPR) + threadIdx.x / TPR;
     const bool live = row_raw < rows;
@@ -89,25 +98,32 @@ __device__ __forceinline__ void drift_body(const char* __restrict__ hc, const ch
     }
     __builtin_amdgcn_sched_barrier(0);    // every load in flight before any use
 
-    // Pass 1: common maximum of the row.
-    float m = -INFINITY;
+    // Pass 1: the maximum of each row (ma of the current, mb of the previous).
+    float mx[2] = {-INFINITY, -INFINITY};
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         float a[T::E], b[T::E];
         T::unpack(ra[c], a);
         T::unpack(rb[c], b);
 #pragma unroll
-        for (int j = 0; j < T::E; ++j) m = fmaxf(m, ok[c] ? fmaxf(a[j], b[j]) : -INFINITY);
+        for (int j = 0; j < T::E; ++j) {
+            mx[0] = fmaxf(mx[0], ok[c] ? a[j] : -INFINITY);
+            mx[1] = fmaxf(mx[1], ok[c] ? b[j] : -INFINITY);
+        }
     }
-    {
-        float mx[1] = {m};
-        row_reduce<TPR, 1, true>(mx, red);
-        m = mx[0];
-    }
-    const float mlog = m * kLog2e;
+    row_reduce<TPR, 2, true>(mx, red);
+    // Reference points of the exponentials: the common maximum while the two
+    // maxima are within kNear of each other (the terms of the KL then cancel
+    // from their natural size), else each row's own maximum, the difference
+    // of the two moving into dl.  Either way each term lies in [0, 1] and
+    // both sums hold a term of at least exp(-kNear).
+    const bool near = fabsf(mx[0] - mx[1]) <= kNear;
+    const float m = fmaxf(mx[0], mx[1]);
+    const float shift = near ? 0.0f : mx[0] - mx[1];
+    const float mal = (near ? m : mx[0]) * kLog2e, mbl = (near ? m : mx[1]) * kLog2e;
 
-    // Pass 2: the three sums (masked chunks contribute nothing).
-    float zb = 0.0f, sqe = 0.0f, spd = 0.0f;
+    // Pass 2: the four sums (masked chunks contribute nothing).
+    float zb = 0.0f, za = 0.0f, sqe = 0.0f, spd = 0.0f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         float a[T::E], b[T::E];
@@ -116,22 +132,22 @@ __device__ __forceinline__ void drift_body(const char* __restrict__ hc, const ch
         const float keep = ok[c] ? 1.0f : 0.0f;
 #pragma unroll
         for (int j = 0; j < T::E; ++j) {
-            const float dl = a[j] - b[j];
-            const float e = keep * fast_exp2(fmaf(b[j], kLog2e, -mlog));
-            const float em = expm1_any(dl);
-            zb += e;
-            sqe = fmaf(e, em, sqe);
-            spd = fmaf(fmaf(e, em, e), dl, spd);
+            const float dl = (a[j] - b[j]) - shift;
+            const float eb = keep * fast_exp2(fmaf(b[j], kLog2e, -mbl));
+            const float ead = keep * fast_exp2(fmaf(a[j], kLog2e, -mal));
+            const float em = expm1_small(dl);
+            const bool small = fabsf(dl) < kSmall;
+            const float qe = small ? eb * em : ead - eb;
+            const float ea = small ? fmaf(eb, em, eb) : ead;
+            zb += eb;
+            za += ea;
+            sqe += qe;
+            spd = fmaf(ea, dl, spd);
         }
     }
-    {
-        float sums[3] = {zb, sqe, spd};
-        row_reduce<TPR, 3, false>(sums, red);
-        zb = sums[0];
-        sqe = sums[1];
-        spd = sums[2];
-    }
-    if (live && tr == 0) out[row] = spd / (zb + sqe) - log1pf(sqe / zb);
+    float sums[4] = {zb, za, sqe, spd};
+    row_reduce<TPR, 4, false>(sums, red);
+    if (live && tr == 0) out[row] = drift_finish(sums[0], sums[1], sums[2], sums[3]);
 }
 
 // chunks per row -> (threads per row, chunks per thread); false above 2048

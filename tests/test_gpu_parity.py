@@ -108,6 +108,29 @@ def test_drift_exact_zero_and_ragged_rows(P, dtype, d):
     assert_drift_close(got, ref.drift(ref.decode(h2, dtype), ref.decode(h, dtype)))
 
 
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("d", [256, 4096])
+def test_drift_outlier_channel(P, dtype, d):
+    """One channel of the current state moved by +-100 or +-1000 (a large
+    outlier between two steps), on an ordinary channel and on the row's
+    maximal channel: the drift must stay finite and match the oracle."""
+    g = np.random.default_rng(d + (1 if dtype == "bf16" else 0))
+    rows = 16
+    base = g.standard_normal((1, rows, d), dtype=np.float32)
+    h_prev = inputs.store(base, dtype)
+    prev = inputs.load_f32(h_prev, dtype)
+    cur = prev + 0.01 * g.standard_normal(prev.shape, dtype=np.float32)
+    moves = [100.0, -100.0, 1000.0, -1000.0]
+    for r in range(rows - 1):
+        c = 5 + 3 * r if r % 2 == 0 else int(np.argmax(prev[0, r]))
+        cur[0, r, c] += moves[r % 4]
+    h_cur = inputs.store(cur, dtype)        # the last row keeps only the light noise
+    got = from_dev(P.drift(to_dev(h_cur, dtype), to_dev(h_prev, dtype)))
+    assert np.all(np.isfinite(got))
+    want = ref.drift(ref.decode(h_cur, dtype), ref.decode(h_prev, dtype))
+    assert_drift_close(got, want)
+
+
 # ---------------------------------------------------------------------------
 # select
 # ---------------------------------------------------------------------------

@@ -85,6 +85,29 @@ def test_drift_pinsker_bound():
     assert np.all(l1 <= np.sqrt(2 * ref.drift(a, b)) + 1e-12)
 
 
+@pytest.mark.parametrize("delta", [100.0, -100.0, 1000.0, -1000.0, 1e-3])
+def test_drift_one_channel_moved_closed_form(delta):
+    """a = b + delta * e_c moves one channel.  With q = softmax(b), softmax(a)
+    is q with q_c scaled by e^delta and renormalised, so
+        KL(softmax(a) || q) = p_c * delta - log(1 - q_c + q_c e^delta),
+    p_c = q_c e^delta / (1 - q_c + q_c e^delta); evaluated here through
+    logaddexp so that e^1000 never forms.  Large moves of one channel (an
+    outlier in the hidden state) must give this finite value."""
+    g = np.random.default_rng(31)
+    b = g.standard_normal((1, 6, 96)) * 2.0
+    for c in (0, 17, int(np.argmax(b[0, 0]))):
+        a = b.copy()
+        a[..., c] += delta
+        qc = np.exp(b[..., c] - np.log(np.sum(np.exp(b), axis=-1)))
+        # log(1 - q_c + q_c e^delta) = logaddexp(log(1 - q_c), log(q_c) + delta)
+        lz = np.logaddexp(np.log1p(-qc), np.log(qc) + delta)
+        pc = np.exp(np.log(qc) + delta - lz)
+        want = pc * delta - lz
+        got = ref.drift(a, b)
+        assert np.all(np.isfinite(got))
+        np.testing.assert_allclose(got, want, rtol=1e-9, atol=1e-12)
+
+
 def test_drift_matches_pure_python_on_tiny_config():
     cfg, x, dec = _cfg0()
     got = ref.drift(dec["h_cur"], dec["h_prev"])
