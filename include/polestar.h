@@ -143,6 +143,33 @@ polestar_status polestar_refresh_kv(polestar_dtype dtype, int batch, int seq, in
                                     hipStream_t stream);
 
 /*
+ * polestar_refresh_kv_noalloc -- polestar_refresh_kv without a workspace
+ * argument, for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation).
+ *
+ * Same arguments (minus workspace), results and validation as
+ * polestar_refresh_kv; it runs the same kernels.  The scratch that
+ * polestar_refresh_kv takes from its workspace (split-K partials and the row
+ * map) lives instead in one array of polestar_refresh_kv_noalloc_max_bytes()
+ * bytes (64 MiB) of device memory per GPU, held by the library on each GPU it
+ * runs on until the process ends.  The call allocates nothing: no hipMalloc,
+ * hipFree or allocating library routine.  Shapes whose refresh needs more
+ * scratch than that (polestar_refresh_kv_workspace_size above the maximum)
+ * return POLESTAR_ERR_WORKSPACE with nothing enqueued.  Every call on one GPU
+ * shares that GPU's array: two calls whose execution overlaps on the same GPU
+ * (on different streams, or from different threads) race and give undefined
+ * results; calls ordered on one stream are safe.  The first call on a device
+ * looks up the array's device address (POLESTAR_ERR_LAUNCH if that fails).
+ */
+size_t polestar_refresh_kv_noalloc_max_bytes(void);
+polestar_status polestar_refresh_kv_noalloc(polestar_dtype dtype, int batch, int seq, int d,
+                                            int n_kv_heads, int head_dim, const void* h_cur,
+                                            const int32_t* stale_idx, const int32_t* stale_count,
+                                            int k_max, int block_start, int block_len,
+                                            const void* w_k, const void* w_v,
+                                            void* k_cache, void* v_cache, hipStream_t stream);
+
+/*
  * polestar_project_q -- query projection of the active block (Sec. 2, eq. 3:
  * the queries of the active positions J_b).
  *

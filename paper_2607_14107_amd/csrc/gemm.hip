@@ -52,6 +52,8 @@
 // In both, A and B use the same lane -> k assignment, so k may be visited in
 // any order.  All loads are unconditional (rows or columns past the end read
 // row 0 and are never stored) so the compiler's wait counts stay static.
+#include <mutex>
+
 #include "gemm_dev.hpp"
 #include "host_common.hpp"
 
@@ -795,5 +797,92 @@ extern "C" polestar_status polestar_refresh_kv(polestar_dtype dtype, int batch, 
     if (workspace_bytes < p.ws_bytes || (p.ws_bytes > 0 && !workspace)) return POLESTAR_ERR_WORKSPACE;
     const GemmArgs g = refresh_gemm_args(batch, seq, d, kvd, h_cur, stale_idx, stale_count, k_max, block_start,
                                          block_len, w_k, w_v, k_cache, v_cache, workspace);
+    return gemm_run(bf16, p, g, stream);
+}
+
+// ---------------------------------------------------------------------------
+// polestar_refresh_kv_noalloc: polestar_refresh_kv with its split-K partials
+// and row map in a file-scope device array instead of a caller workspace.
+// Each device holds its own copy of the array; its address on a device is
+// looked up once (hipGetSymbolAddress, with that device current) and kept,
+// since the array's name in host code is only a host-side stand-in.  The
+// kernels need no initialised scratch (every partial that the reduction
+// reads is written first in the same call), so nothing is cleared.
+// ---------------------------------------------------------------------------
+
+namespace ps {
+namespace {
+constexpr size_t kScratchBytes = size_t{64} << 20;
+constexpr int kMaxDevices = 64;
+}  // namespace
+}  // namespace ps
+
+static __device__ __align__(256) char scratch[ps::kScratchBytes];
+
+namespace ps {
+namespace {
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of the array, or nullptr if its address cannot
+// be obtained (status in *st).
+void* device_scratch(polestar_status* st) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        *st = dev >= kMaxDevices ? POLESTAR_ERR_UNSUPPORTED : POLESTAR_ERR_LAUNCH;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            *st = POLESTAR_ERR_LAUNCH;
+            return nullptr;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace
+}  // namespace ps
+
+extern "C" size_t polestar_refresh_kv_noalloc_max_bytes(void) { return ps::kScratchBytes; }
+
+extern "C" polestar_status polestar_refresh_kv_noalloc(polestar_dtype dtype, int batch, int seq, int d,
+                                                       int n_kv_heads, int head_dim, const void* h_cur,
+                                                       const int32_t* stale_idx,
+                                                       const int32_t* stale_count, int k_max,
+                                                       int block_start, int block_len, const void* w_k,
+                                                       const void* w_v, void* k_cache, void* v_cache,
+                                                       hipStream_t stream) {
+    using namespace ps;
+    // The same validation as polestar_refresh_kv, before the scratch lookup.
+    if (!dtype_ok(dtype) || batch <= 0 || seq <= 0 || d <= 0 || n_kv_heads <= 0 ||
+        head_dim <= 0 || k_max < 0 || k_max > seq || block_start < 0 || block_len < 0 ||
+        block_start > seq - block_len || !h_cur || !w_k || !w_v || !k_cache || !v_cache ||
+        (k_max > 0 && (!stale_idx || !stale_count)))
+        return POLESTAR_ERR_INVALID_ARGUMENT;
+    if ((head_dim != 64 && head_dim != 128) || !gemm_k_ok(dtype == POLESTAR_BF16, d) ||
+        !aligned16(h_cur) || !aligned16(w_k) || !aligned16(w_v) || !aligned16(k_cache) ||
+        !aligned16(v_cache))
+        return POLESTAR_ERR_UNSUPPORTED;
+    if (batch > 65536) return POLESTAR_ERR_UNSUPPORTED;
+    const long m_max = static_cast<long>(batch) * (k_max + block_len);
+    if (m_max == 0) return POLESTAR_OK;
+    if (m_max > 0x7fffffffL / 4) return POLESTAR_ERR_UNSUPPORTED;
+    const bool bf16 = dtype == POLESTAR_BF16;
+    const int kvd = n_kv_heads * head_dim;
+    const GemmPlan p = gemm_plan(bf16, m_max, 2 * kvd, d);
+    if (p.ws_bytes > kScratchBytes) return POLESTAR_ERR_WORKSPACE;
+    void* ws = nullptr;
+    if (p.ws_bytes > 0) {
+        polestar_status st = POLESTAR_OK;
+        ws = device_scratch(&st);
+        if (!ws) return st;
+    }
+    const GemmArgs g = refresh_gemm_args(batch, seq, d, kvd, h_cur, stale_idx, stale_count, k_max, block_start,
+                                         block_len, w_k, w_v, k_cache, v_cache, ws);
     return gemm_run(bf16, p, g, stream);
 }

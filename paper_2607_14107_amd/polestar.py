@@ -73,6 +73,10 @@ def lib() -> ctypes.CDLL:
     L.polestar_refresh_kv_workspace_size.argtypes = [I, I, I, I, I, I, I]
     L.polestar_refresh_kv.restype = S
     L.polestar_refresh_kv.argtypes = [I, I, I, I, I, I, P, P, P, I, I, I, P, P, P, P, P, Z, P]
+    L.polestar_refresh_kv_noalloc_max_bytes.argtypes = []
+    L.polestar_refresh_kv_noalloc_max_bytes.restype = Z
+    L.polestar_refresh_kv_noalloc.argtypes = [I, I, I, I, I, I, P, P, P, I, I, I, P, P, P, P, P]
+    L.polestar_refresh_kv_noalloc.restype = S
     L.polestar_project_q_workspace_size.restype = Z
     L.polestar_project_q_workspace_size.argtypes = [I, I, I, I, I, I]
     L.polestar_project_q.restype = S
@@ -230,6 +234,27 @@ def refresh_kv(h_cur: torch.Tensor, stale_idx: torch.Tensor | None, stale_count:
         _ptr(stale_count, torch.int32) if k_max > 0 else None, k_max, block_start, block_len,
         _ptr(w_k, h_cur.dtype), _ptr(w_v, h_cur.dtype), _ptr(k_cache, h_cur.dtype),
         _ptr(v_cache, h_cur.dtype), _ptr(ws), nbytes, _stream(stream)))
+
+
+def refresh_kv_noalloc(h_cur: torch.Tensor, stale_idx: torch.Tensor | None, stale_count: torch.Tensor | None,
+                       block_start: int, block_len: int, w_k: torch.Tensor, w_v: torch.Tensor,
+                       k_cache: torch.Tensor, v_cache: torch.Tensor, stream=None) -> None:
+    """refresh_kv with the library's own per-GPU scratch array instead of a
+    workspace (nothing is allocated; calls overlapping on one GPU race)."""
+    b, s, d = h_cur.shape
+    _, _, kvh, hd = k_cache.shape
+    dt = _dtype_code(h_cur)
+    k_max = 0 if stale_idx is None else stale_idx.shape[1]
+    _check("polestar_refresh_kv_noalloc", lib().polestar_refresh_kv_noalloc(
+        dt, b, s, d, kvh, hd, _ptr(h_cur),
+        _ptr(stale_idx, torch.int32) if k_max > 0 else None,
+        _ptr(stale_count, torch.int32) if k_max > 0 else None, k_max, block_start, block_len,
+        _ptr(w_k, h_cur.dtype), _ptr(w_v, h_cur.dtype), _ptr(k_cache, h_cur.dtype),
+        _ptr(v_cache, h_cur.dtype), _stream(stream)))
+
+
+def refresh_kv_noalloc_max_bytes() -> int:
+    return lib().polestar_refresh_kv_noalloc_max_bytes()
 
 
 def project_q_workspace_size(dtype: int, batch: int, d: int, n_heads: int, head_dim: int,

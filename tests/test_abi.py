@@ -29,7 +29,7 @@ def _header_functions():
 
 def test_every_declared_symbol_is_exported(L):
     names = _header_functions()
-    assert len(names) == 35, names
+    assert len(names) == 37, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -60,6 +60,29 @@ def test_select_validation(L):
     assert f(1, 10, FAKE, None, 0, 2, 3, None, FAKE, None) == INVALID        # k > 0 needs stale_idx
     assert f(1, 10, FAKE, None, -1, 2, 3, FAKE, FAKE, None) == INVALID
     assert f(1, 20000, FAKE, None, 0, 2, 3, FAKE, FAKE, None) == UNSUPPORTED
+
+
+def test_refresh_noalloc_validation_and_limit(L):
+    """The variant without a workspace validates like polestar_refresh_kv and
+    refuses, before any GPU call, shapes whose scratch exceeds its array."""
+    f = L.polestar_refresh_kv_noalloc
+    limit = ps.refresh_kv_noalloc_max_bytes()
+    assert limit == 64 << 20
+    args = [1, 1, 768, 4096, 32, 128, FAKE, FAKE, FAKE, 115, 512, 32, FAKE, FAKE, FAKE, FAKE, None]
+    a = list(args); a[6] = None
+    assert f(*a) == INVALID                                   # h_cur
+    a = list(args); a[10] = 760
+    assert f(*a) == INVALID                                   # block past the end
+    a = list(args); a[7] = None
+    assert f(*a) == INVALID                                   # k_max > 0 needs stale_idx
+    a = list(args); a[5] = 96
+    assert f(*a) == UNSUPPORTED                               # head_dim
+    a = list(args); a[15] = MISALIGNED
+    assert f(*a) == UNSUPPORTED
+    # 24 sequences x (60 stale + 32 block rows) at LLaDA-8B width: 138 MiB of partials
+    assert ps.refresh_kv_workspace_size(ps.BF16, 24, 4096, 32, 128, 60, 32) > limit
+    big = [1, 24, 768, 4096, 32, 128, FAKE, FAKE, FAKE, 60, 512, 32, FAKE, FAKE, FAKE, FAKE, None]
+    assert f(*big) == WORKSPACE
 
 
 def test_refresh_validation_and_workspace(L):

@@ -1,0 +1,82 @@
+"""polestar_refresh_kv_noalloc against polestar_refresh_kv on the GPU.
+
+The variant without a workspace keeps its split-K partials in the library's
+per-GPU scratch array.  Two calls in a row, the second on a smaller input
+(so the array still holds the first call's partials), each compared byte for
+byte with polestar_refresh_kv on the same inputs and its own workspace: both
+run the same kernels with the same plan and a deterministic split order.
+"""
+
+import numpy as np
+import pytest
+
+from paper_2607_14107_amd import inputs
+from tests._util import ensure_built, from_dev, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    ensure_built()
+    from paper_2607_14107_amd import polestar
+    return polestar
+
+
+def _case(seed, batch, seq, d, kvh, hd, block_start, block_len, k_max):
+    g = np.random.default_rng(seed)
+    h = inputs.store(g.standard_normal((batch, seq, d), dtype=np.float32), "bf16")
+    w_k = inputs.store(0.02 * g.standard_normal((kvh * hd, d), dtype=np.float32), "bf16")
+    w_v = inputs.store(0.02 * g.standard_normal((kvh * hd, d), dtype=np.float32), "bf16")
+    kc = inputs.store(g.standard_normal((batch, seq, kvh, hd), dtype=np.float32), "bf16")
+    vc = inputs.store(g.standard_normal((batch, seq, kvh, hd), dtype=np.float32), "bf16")
+    cached = np.array([i for i in range(seq) if not block_start <= i < block_start + block_len])
+    idx = np.full((batch, k_max), -1, dtype=np.int32)
+    cnt = np.zeros(batch, dtype=np.int32)
+    for b in range(batch):
+        n = int(g.integers(k_max // 2, k_max + 1))
+        idx[b, :n] = np.sort(g.choice(cached, size=n, replace=False))
+        cnt[b] = n
+    return dict(h=h, w_k=w_k, w_v=w_v, kc=kc, vc=vc, idx=idx, cnt=cnt, bs=block_start, bl=block_len)
+
+
+def _run_both(P, c):
+    import torch
+    h, w_k, w_v = (to_dev(c[k], "bf16") for k in ("h", "w_k", "w_v"))
+    idx = torch.from_numpy(c["idx"]).cuda()
+    cnt = torch.from_numpy(c["cnt"]).cuda()
+    k1, v1 = to_dev(c["kc"], "bf16"), to_dev(c["vc"], "bf16")
+    k2, v2 = k1.clone(), v1.clone()
+    P.refresh_kv(h, idx, cnt, c["bs"], c["bl"], w_k, w_v, k1, v1)
+    P.refresh_kv_noalloc(h, idx, cnt, c["bs"], c["bl"], w_k, w_v, k2, v2)
+    torch.cuda.synchronize()
+    return [from_dev(t) for t in (k1, v1, k2, v2)]
+
+
+def test_noalloc_matches_refresh_kv_twice(P):
+    big = _case(71, 8, 1536, 4096, 32, 128, 1024, 32, 30)      # batch-8 LLaDA-8B refresh, ~62 MiB scratch
+    small = _case(72, 1, 768, 4096, 32, 128, 512, 32, 106)     # batch-1 LLaDA-8B refresh, ~17 MiB scratch
+    for name, c in (("batch 8", big), ("batch 1", small)):
+        ws = P.refresh_kv_workspace_size(P.BF16, c["h"].shape[0], 4096, 32, 128, c["idx"].shape[1], 32)
+        assert 0 < ws <= P.refresh_kv_noalloc_max_bytes(), (name, ws)
+        k1, v1, k2, v2 = _run_both(P, c)
+        assert np.array_equal(k1, k2) and np.array_equal(v1, v2), name
+        # the refresh did write rows (the comparison is not of two untouched caches)
+        assert not np.array_equal(k1, c["kc"]) and not np.array_equal(v1, c["vc"]), name
+
+
+def test_noalloc_refuses_shapes_beyond_its_array(P):
+    c = _case(73, 24, 96, 4096, 32, 128, 64, 32, 60)
+    assert P.refresh_kv_workspace_size(P.BF16, 24, 4096, 32, 128, 60, 32) > P.refresh_kv_noalloc_max_bytes()
+    import torch
+    h, w_k, w_v = (to_dev(c[k], "bf16") for k in ("h", "w_k", "w_v"))
+    k2, v2 = to_dev(c["kc"], "bf16"), to_dev(c["vc"], "bf16")
+    with pytest.raises(P.PolestarError) as e:
+        P.refresh_kv_noalloc(h, torch.from_numpy(c["idx"]).cuda(), torch.from_numpy(c["cnt"]).cuda(),
+                             c["bs"], c["bl"], w_k, w_v, k2, v2)
+    assert e.value.status == 4       # POLESTAR_ERR_WORKSPACE, nothing enqueued
+    torch.cuda.synchronize()
+    assert np.array_equal(from_dev(k2), c["kc"])
