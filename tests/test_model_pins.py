@@ -74,6 +74,42 @@ def brute_layer_row(x_all, i, w, shape):
     return [x[c] + rnd(t) for c, t in enumerate(mat(w["w_down"], a))]
 
 
+def test_embed_places_token_and_position_rows():
+    """M-3: row r of sequence b is tok_emb[ids[b][lo + r]] + pos_emb[lo + r].
+    Token v is encoded as v in channel 0 and position p as p in channel 1, so
+    each output row reads back its (id, absolute position); a position table
+    indexed from 0 instead of lo, or ids taken from the wrong offset, fail."""
+    vocab, seq, d = 50, 12, 4
+    tok = np.zeros((vocab, d))
+    tok[:, 0] = np.arange(vocab)
+    pos = np.zeros((seq, d))
+    pos[:, 1] = np.arange(seq)
+    ids = np.array([[3, 9, 14, 7, 1, 0, 22, 31, 45, 2, 8, 11],
+                    [40, 41, 42, 43, 44, 45, 46, 47, 48, 49, 5, 6]])
+    x = mr.embed(tok, pos, ids, 5, 9)
+    assert x.shape == (2, 4, d)
+    for b in range(2):
+        for r in range(4):
+            assert x[b, r].tolist() == [ids[b, 5 + r], 5 + r, 0.0, 0.0]
+
+
+def test_logits_normalise_then_project():
+    """M-6: logits = W_lm RMSNorm(x).  For x = c e_j (c > 0), RMSNorm gives
+    e_j sqrt(d) / sqrt(1 + eps d / c^2), so the logits are that factor times
+    column j of W_lm: independent of c up to eps (a dropped RMSNorm scales
+    with c), and a column, not a row (a transposed W_lm reads row j)."""
+    g = np.random.default_rng(15)
+    d = 16
+    w_lm = g.standard_normal((d, d))
+    for c in (0.5, 3.0, 40.0):
+        x = np.zeros((1, 1, d))
+        x[0, 0, 9] = c
+        got = mr.logits(x, w_lm, "fp32")[0, 0]
+        scale = math.sqrt(d) / math.sqrt(1.0 + mr.EPS * d / (c * c))
+        np.testing.assert_allclose(got, scale * w_lm[:, 9], rtol=1e-6)
+    assert not np.allclose(got, scale * w_lm[9, :], rtol=1e-2)
+
+
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_layer_matches_brute_force(dtype):
     shape = mr.Shape(n_layers=1, d=8, n_heads=2, head_dim=4, ffn=6, vocab=16, seq=5, dtype=dtype)

@@ -189,6 +189,54 @@ def test_selection_agreement_with_paper_drift_and_staleness():
         assert set(idx[0, :cnt[0]].tolist()) == planted
 
 
+def _sigmoid(x):
+    return 1.0 / (1.0 + math.exp(-x))
+
+
+def _bernoulli_kl(p, q):
+    return p * math.log(p / q) + (1 - p) * math.log((1 - p) / (1 - q))
+
+
+def test_drift_attention_exact_two_key_hand_case():
+    """Two tokens, two heads of head_dim 2, W_q = W_k = I: head h of token i
+    sees logits l_ij = x_i[h] . x_j[h] / sqrt(2) over the two keys, so its
+    attention row is Bernoulli(sigmoid(l_i0 - l_i1)) and the drift of token i
+    is the mean over heads of KL(Bernoulli(cur) || Bernoulli(prev)) (eq.
+    drift, current || previous; heads averaged).  Worked by hand:
+      prev x0 = (1,0 | 0,0), x1 = (0,1 | 0,0);  cur x0 = (2,0 | 1,0), x1 = (0,1 | 0,1)
+      token 0: head 0 logits (4, 0)/sqrt2 vs (1, 0)/sqrt2, head 1 (1, 0)/sqrt2 vs (0, 0)
+      token 1: head 0 (0, 1)/sqrt2 both steps, head 1 (0, 1)/sqrt2 vs (0, 0).
+    A reversed KL, a missing 1/sqrt(d_h), or heads summed instead of averaged
+    each change these values."""
+    r2 = math.sqrt(2.0)
+    prev = np.array([[[1.0, 0, 0, 0], [0, 1.0, 0, 0]]])
+    cur = np.array([[[2.0, 0, 1.0, 0], [0, 1.0, 0, 1.0]]])
+    eye = np.eye(4)
+    got = ref.drift_attention_exact(cur, prev, eye, eye, 2, 2, 2)
+    t0 = 0.5 * (_bernoulli_kl(_sigmoid(4 / r2), _sigmoid(1 / r2)) + _bernoulli_kl(_sigmoid(1 / r2), 0.5))
+    t1 = 0.5 * (0.0 + _bernoulli_kl(_sigmoid(-1 / r2), 0.5))
+    np.testing.assert_allclose(got, [[t0, t1]], rtol=1e-12)
+    # the same hand case through the logits: l = x_i[h] . x_j[h] / sqrt(2)
+    lg = ref.attention_logits(cur, eye, eye, 2, 2, 2)
+    np.testing.assert_allclose(lg[0, 0], [[4 / r2, 0], [0, 1 / r2]], rtol=1e-14)
+    np.testing.assert_allclose(lg[0, 1], [[1 / r2, 0], [0, 1 / r2]], rtol=1e-14)
+
+
+def test_attention_logits_grouped_heads_share_their_kv_head():
+    """GQA: with one KV head, both query heads read it, which equals MHA with
+    that KV head's weights repeated; query head h uses rows h*d_h.. of W_q."""
+    g = np.random.default_rng(14)
+    h = g.standard_normal((1, 5, 6))
+    w_q = g.standard_normal((2 * 3, 6))
+    w_k = g.standard_normal((3, 6))
+    gqa = ref.attention_logits(h, w_q, w_k, 2, 1, 3)
+    mha = ref.attention_logits(h, w_q, np.vstack([w_k, w_k]), 2, 2, 3)
+    np.testing.assert_allclose(gqa, mha, rtol=1e-14)
+    q1 = h[0] @ w_q[3:6].T
+    k = h[0] @ w_k.T
+    np.testing.assert_allclose(gqa[0, 1], q1 @ k.T / math.sqrt(3), rtol=1e-12)
+
+
 # --------------------------------------------------------------------------
 # Step 3 -- sparse K/V refresh
 # --------------------------------------------------------------------------
@@ -215,6 +263,28 @@ def test_refresh_unit_vector_picks_weight_column():
     assert rows == [[2], []]
     np.testing.assert_array_equal(k_new[0, 2].reshape(-1), w_k[:, 7])
     np.testing.assert_array_equal(v_new[0, 2].reshape(-1), w_v[:, 7])
+
+
+def test_project_rows_is_w_times_h_on_a_square_weight():
+    """project_rows(h, W, r) = W h_r (App. B setup: k = W_K x).  The weight
+    is square, as W_K is on the LLaDA-8B layer (4096 x 4096), so a transposed
+    product keeps every shape: a unit hidden state e_j must give column j of
+    W, not row j; and the rows must agree with refresh_kv's."""
+    g = np.random.default_rng(12)
+    d = 8
+    w = g.standard_normal((d, d))
+    h = np.zeros((3, d))
+    h[1, 5] = 1.0
+    h[2] = g.standard_normal(d)
+    got = ref.project_rows(h, w, [1, 2])
+    np.testing.assert_array_equal(got[0], w[:, 5])
+    assert not np.allclose(got[0], w[5, :])
+    np.testing.assert_allclose(got[1], [sum(w[o, c] * h[2, c] for c in range(d)) for o in range(d)],
+                               rtol=1e-12)
+    kc = np.zeros((1, 3, 2, 4))
+    idx = np.array([[1, 2]], dtype=np.int32)
+    k_new, _, _ = ref.refresh_kv(h[None], w, w, kc, kc, idx, np.array([2], np.int32), 0, 0)
+    np.testing.assert_array_equal(k_new[0, 1:].reshape(2, d), got)
 
 
 def test_refresh_untouched_rows_and_empty_refresh():
