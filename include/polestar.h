@@ -119,9 +119,11 @@ polestar_status polestar_select(int batch, int seq, const float* drift,
  * twice with the same value).
  *
  *   h_cur          : [batch][seq][d] dtype
- *   stale_idx      : [batch][k_max] int32, entries 0 .. stale_count[b]-1 in
- *                    [0, seq) (values outside are undefined behaviour)
- *   stale_count    : [batch] int32, each in [0, k_max]
+ *   stale_idx      : [batch][k_max] int32; entries 0 .. stale_count[b]-1 are
+ *                    positions in [0, seq); an entry outside [0, seq) (e.g. the
+ *                    -1 padding) is skipped: no row is written for it
+ *   stale_count    : [batch] int32, clamped to [0, k_max] (a negative count
+ *                    refreshes only the active block)
  *   w_k, w_v       : [n_kv_heads*head_dim][d] dtype (output x input)
  *   k_cache, v_cache : [batch][seq][n_kv_heads][head_dim] dtype, in/out
  *   workspace      : >= polestar_refresh_kv_workspace_size(...) bytes

@@ -28,8 +28,9 @@
 //   rows.
 //
 // gemm_dma_kernel (65 to 320 rows, e.g. the refresh of one sequence's stale
-//   rows and block, or the Q projection of a batch's blocks): one of at most
-//   two row tiles of up to 160 rows and 128 columns per workgroup, both operands
+//   rows and block, or the Q projection of a batch's blocks; up to 1280 rows
+//   for outputs of at most 1024 columns): one of up to two row tiles (eight
+//   for narrow outputs) of up to 160 rows and 128 columns per workgroup, both operands
 //   (bf16) brought into LDS by global_load_lds_dwordx4 (no VGPR staging, so the
 //   weight loads never wait behind registers that MFMAs still read), in
 //   stages of 128 bytes of each row; four LDS slots, three stages in flight,
@@ -607,16 +608,19 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     // while the tiles alone leave compute units idle.  Measured against the
     // other kernels it wins when it launches at least 128 workgroups and at
     // most four splits fill the chip, each split still runs 48 stages or
-    // more, or there are four row tiles or more (the Dream-7B refresh: 1052
-    // rows x 1024 x 3584 in seven splits, 33 us against 44 us); short splits
-    // of one or two row tiles (256 or 512 rows of a 4096 x 4096 projection)
-    // stay on the DMA or row kernel.
+    // more, or there are four row tiles or more; short splits of one or two
+    // row tiles (256 or 512 rows of a 4096 x 4096 projection) stay on the DMA
+    // or row kernel.
     // Narrow outputs (at most 1024 columns: four 256-wide tiles across) take
     // the DMA kernel's 128-column tiles instead, up to eight row tiles: the
     // Dream-7B refresh (1052 rows x 1024 x 3584) runs 56 tiles in four splits
     // (224 workgroups, 17 MB of partials) in 27.7 us, where the tile kernel's
     // 20 tiles needed seven splits (30 MB of partials) and 37.5 us.
-    const bool narrow_dma = bf16 && N <= 4 * kTileDim && m_max <= 8L * 16 * kDmaMaxRowTiles;
+    // Only where the DMA kernel can take K: some split into 4 to 8 steps of
+    // 256 bytes (K = 2816, 22 steps, has none and stays on the tile kernel).
+    bool dma_k = false;
+    for (int ks = 1; ks <= kMaxSplit && !dma_k; ++ks) dma_k = nsteps % ks == 0 && nsteps / ks >= 4 && nsteps / ks <= 8;
+    const bool narrow_dma = bf16 && dma_k && N <= 4 * kTileDim && m_max <= 8L * 16 * kDmaMaxRowTiles;
     if (bf16 && m_max > 16L * kDmaMaxRowTiles && K % kTileStage == 0 && !narrow_dma) {
         const int nstage = K / (kTileStage / 2);
         p.row_tiles = ceil_div(m_max, kTileDim);
@@ -658,7 +662,8 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
             p.ws_bytes = partial_bytes(p, m_max) + align_up(static_cast<size_t>(m_max) * 2 * sizeof(int), 256);
         return p;
     }
-    // DMA kernel: one or two row tiles of at most 160 rows, K split evenly
+    // DMA kernel: up to two row tiles of at most 160 rows (eight for narrow
+    // outputs), K split evenly
     // into 8 to 16 stages of 128 bytes per row; the split with the fewest
     // rounds of one workgroup per CU times stages per split, the smaller
     // split on ties (the Dream-7B Q projection, 56 tiles of K = 3584: four

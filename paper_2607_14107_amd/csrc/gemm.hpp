@@ -38,7 +38,8 @@ struct GemmArgs {
 
 struct GemmPlan {
     bool small;         // gemm_small_kernel (<= 64 rows) instead of gemm_rows_kernel
-    bool dma;           // gemm_dma_kernel (17..64 or 65..320 rows: one or two row tiles, operands DMA'd into LDS)
+    bool dma;           // gemm_dma_kernel (17..320 rows in up to two row tiles, up to 1280 in eight for
+                        // outputs of <= 1024 columns; operands DMA'd into LDS)
     bool tile;          // gemm_tile_kernel (bf16, more than 160 rows: 256 x 256 tiles)
     int mt;             // MFMA row tiles per workgroup (16 rows: small and dma kernels; 32: rows kernel)
     int row_tiles;

@@ -253,7 +253,7 @@ __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
     const int tile = blk / g.ksplit;
     const int split = blk - tile * g.ksplit;
     const int col_tile = tile % g.col_tiles;
-    const int m0 = (tile / g.col_tiles) * BM;           // one or two row tiles
+    const int m0 = (tile / g.col_tiles) * BM;           // up to eight row tiles
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int w = t >> 6;

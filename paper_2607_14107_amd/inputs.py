@@ -91,10 +91,16 @@ def rng(config: int, subrun: int, stream: int) -> np.random.Generator:
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """float32 -> bf16 bit patterns, round to nearest, ties to even."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    bias = 0x7FFF + ((u >> 16) & 1)
-    return ((u + bias) >> 16).astype(np.uint16)
+    """float32 -> bf16 bit patterns, round to nearest, ties to even.  In 32-bit
+    integers: for every finite value (and the infinities) the sum below stays
+    under 2^32 (the largest, -FLT_MAX, gives 0xFF807FFF)."""
+    u = np.array(x, dtype=np.float32, copy=True).view(np.uint32)
+    lsb = u >> np.uint32(16)
+    lsb &= np.uint32(1)
+    u += np.uint32(0x7FFF)
+    u += lsb
+    u >>= np.uint32(16)
+    return u.astype(np.uint16)
 
 
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
@@ -205,19 +211,10 @@ def spike_rows(cfg: LayerConfig, subrun: int, fraction: float = 0.25) -> np.ndar
     return out
 
 
-def layer_inputs(cfg: LayerConfig, subrun: int = 0) -> dict:
-    """All inputs of one step of a single-layer workload.
-
-    For a chained configuration, sub-run s is step s: its h_prev is the h_cur
-    of step s-1 (step 0 starts from the base states)."""
-    h_prev = base_states(cfg)
-    steps = range(subrun + 1) if cfg.chained else [subrun]
-    for s in steps:
-        frac = cfg.heavy_fracs[s]
-        planted = (planted_runs if cfg.clustered else planted_uniform)(cfg, s, frac)
-        h_cur = perturb(cfg, h_prev, s, planted)
-        if s != steps[-1]:
-            h_prev = h_cur
+def _step_inputs(cfg: LayerConfig, subrun: int, h_prev: np.ndarray, w: dict) -> dict:
+    frac = cfg.heavy_fracs[subrun]
+    planted = (planted_runs if cfg.clustered else planted_uniform)(cfg, subrun, frac)
+    h_cur = perturb(cfg, h_prev, subrun, planted)
     bs, bl = cfg.block_start, cfg.block_len
     cached = np.ones(cfg.seq, dtype=bool)
     cached[bs:bs + bl] = False
@@ -226,7 +223,30 @@ def layer_inputs(cfg: LayerConfig, subrun: int = 0) -> dict:
                logits=logits(cfg, subrun), hist=history(cfg, subrun),
                hist_len=np.full(cfg.batch, cfg.hist_depth, dtype=np.int32),
                masked=np.ones((cfg.batch, cfg.block_len), dtype=np.uint8))
-    out.update(weights(cfg))
+    out.update(w)
+    return out
+
+
+def layer_inputs(cfg: LayerConfig, subrun: int = 0) -> dict:
+    """All inputs of one step of a single-layer workload.
+
+    For a chained configuration, sub-run s is step s: its h_prev is the h_cur
+    of step s-1 (step 0 starts from the base states)."""
+    if cfg.chained:
+        return chained_inputs(cfg, subrun)[-1]
+    return _step_inputs(cfg, subrun, base_states(cfg), weights(cfg))
+
+
+def chained_inputs(cfg: LayerConfig, last: int | None = None) -> list:
+    """Steps 0..last of a chained configuration in one pass (the same arrays
+    layer_inputs returns for each of them; weights shared)."""
+    last = len(cfg.heavy_fracs) - 1 if last is None else last
+    w = weights(cfg)
+    h_prev = base_states(cfg)
+    out = []
+    for s in range(last + 1):
+        out.append(_step_inputs(cfg, s, h_prev, w))
+        h_prev = out[-1]["h_cur"]
     return out
 
 

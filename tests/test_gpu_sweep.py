@@ -4,7 +4,7 @@ and K/V-refresh entry points, each checked against the CPU oracle.
 The shapes are drawn so that every launch plan gets exercised: per-head and
 grouped-head attention (4 or 8 waves, idle waves, one or many key splits,
 ragged key tiles and query groups), and the GEMM plans (small-M kernel, DMA
-kernel with one or two row tiles and 8 to 16 stages per split, row kernel)
+kernel with up to eight row tiles and 8 to 16 stages per split, row kernel)
 with ragged row tiles and refresh row counts.  Tolerances as in
 test_gpu_parity: fp32 1e-4, bf16 2e-2 relative per (row, head); rows the
 refresh does not touch byte-identical.
@@ -134,3 +134,34 @@ def test_refresh_random_shapes(P, case):
         vw = ref.project_rows(hdec[b], wvd, rows).reshape(rows.size, kvh, hd)
         assert_rows_close(ref.decode(kg[b, rows], dtype), kw, RTOL[dtype], f"K rows b{b} " + shape)
         assert_rows_close(ref.decode(vg[b, rows], dtype), vw, RTOL[dtype], f"V rows b{b} " + shape)
+
+
+@pytest.mark.parametrize("batch,seq,bs,bl,d,kvh,hd,k_max", [
+    (2, 700, 600, 32, 3584, 4, 128, 603),   # 1270 rows x 1024 columns: eight 159-row DMA tiles, four K splits
+    (1, 800, 400, 20, 640, 4, 128, 680),    # 700 rows x 1024 columns: five DMA tiles, K unsplit (5 steps)
+])
+def test_refresh_narrow_output_many_row_tiles(P, batch, seq, bs, bl, d, kvh, hd, k_max):
+    """Outputs of at most 1024 columns keep the DMA kernel up to eight row
+    tiles; every stale slot is filled, every refreshed row compared."""
+    g = np.random.default_rng(d + k_max)
+    dtype = "bf16"
+    cached = np.setdiff1d(np.arange(seq), np.arange(bs, bs + bl))
+    idx = np.stack([np.sort(g.choice(cached, size=k_max, replace=False)) for _ in range(batch)]).astype(np.int32)
+    cnt = np.full(batch, k_max, dtype=np.int32)
+    h = inputs.store(g.standard_normal((batch, seq, d), dtype=np.float32), dtype)
+    wk = inputs.store(0.05 * g.standard_normal((kvh * hd, d), dtype=np.float32), dtype)
+    wv = inputs.store(0.05 * g.standard_normal((kvh * hd, d), dtype=np.float32), dtype)
+    kc0 = inputs.store(g.standard_normal((batch, seq, kvh, hd), dtype=np.float32), dtype)
+    vc0 = inputs.store(g.standard_normal((batch, seq, kvh, hd), dtype=np.float32), dtype)
+    kc, vc = to_dev(kc0, dtype), to_dev(vc0, dtype)
+    P.refresh_kv(to_dev(h, dtype), _i32(idx), _i32(cnt), bs, bl, to_dev(wk, dtype), to_dev(wv, dtype), kc, vc)
+    kg, vg = from_dev(kc), from_dev(vc)
+    hdec, wkd, wvd = ref.decode(h, dtype), ref.decode(wk, dtype), ref.decode(wv, dtype)
+    for b in range(batch):
+        rows = np.asarray(sorted(set(idx[b].tolist()) | set(range(bs, bs + bl))), dtype=np.int64)
+        keep = np.setdiff1d(np.arange(seq), rows)
+        assert np.array_equal(kg[b, keep], kc0[b, keep]) and np.array_equal(vg[b, keep], vc0[b, keep])
+        kw = ref.project_rows(hdec[b], wkd, rows).reshape(rows.size, kvh, hd)
+        vw = ref.project_rows(hdec[b], wvd, rows).reshape(rows.size, kvh, hd)
+        assert_rows_close(ref.decode(kg[b, rows], dtype), kw, RTOL[dtype], f"K rows b{b}")
+        assert_rows_close(ref.decode(vg[b, rows], dtype), vw, RTOL[dtype], f"V rows b{b}")
