@@ -2,15 +2,16 @@
 // states (Sec. 3, eq. "drift"; the distribution of a token is the softmax of
 // its hidden state over the d channels).
 //
-// A row is spread over 64-256 threads (4 waves at d = 4096, two 16-byte
-// chunks of each row per lane): the two rows of the token are loaded once
+// A row is spread over one wave (batches of 2048 rows and more, d up to 4096
+// in bf16: eight 16-byte chunks of each row per lane) or 128-256 threads:
+// the two rows of the token are loaded once
 // with coalesced 16-byte loads into registers (an HBM-bound stream of 2*d
 // elements), both row maxima ma, mb are reduced (shuffles, then LDS across
 // the row's waves), then the thread accumulates in fp32, with reference
 // points ra = rb = max(ma, mb) when |ma - mb| <= 16, else ra = ma, rb = mb,
 // eb_c = exp(b_c - rb), ea_c = exp(a_c - ra) and dl_c = (a_c - b_c) - (ra - rb),
 //   Zb  = sum eb_c,   Za = sum ea_c,
-//   Sqe = sum (ea_c - eb_c)   (as eb_c * expm1(dl_c) when |dl_c| < 1/16),
+//   Sqe = sum (ea_c - eb_c)   (as eb_c * expm1(dl_c) when |dl_c| < 1/8),
 //   Spd = sum ea_c * dl_c
 // so that KL(softmax(a) || softmax(b)) = Spd / Za - log(Za / Zb), with
 // Za = Zb + Sqe and log(Za / Zb) = log1p(Sqe / Zb) while the two sums are
@@ -42,14 +43,12 @@ template <bool BF16>
 bool dispatch(int chunks, const void* hc, const void* hp, float* out, int rows, int d,
               hipStream_t s) {
     int tpr = 0, nch = 0;
-    if (!drift_config(chunks, tpr, nch)) return false;
+    if (!drift_config(chunks, rows, tpr, nch)) return false;
     switch (tpr * 16 + nch) {
-        case 64 * 16 + 1: launch<BF16, 64, 1>(hc, hp, out, rows, d, s); return true;
-        case 64 * 16 + 2: launch<BF16, 64, 2>(hc, hp, out, rows, d, s); return true;
-        case 128 * 16 + 2: launch<BF16, 128, 2>(hc, hp, out, rows, d, s); return true;
-        case 256 * 16 + 2: launch<BF16, 256, 2>(hc, hp, out, rows, d, s); return true;
-        case 256 * 16 + 4: launch<BF16, 256, 4>(hc, hp, out, rows, d, s); return true;
-        case 256 * 16 + 8: launch<BF16, 256, 8>(hc, hp, out, rows, d, s); return true;
+#define PS_CASE(TPR, NCH) \
+        case TPR * 16 + NCH: launch<BF16, TPR, NCH>(hc, hp, out, rows, d, s); return true;
+        PS_DRIFT_SHAPES(PS_CASE)
+#undef PS_CASE
         default: return false;
     }
 }

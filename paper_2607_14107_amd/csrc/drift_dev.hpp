@@ -12,11 +12,12 @@ namespace ps {
 namespace {
 
 constexpr int kDriftBlock = 256;
-constexpr float kSmall = 0.0625f;              // |dl| below this: series for expm1
+constexpr float kSmall = 0.125f;               // |dl| below this: expm1 from its series
 constexpr float kNear = 16.0f;                 // row maxima closer than this: one reference
+constexpr uint32_t kNeutral = 0xF149F149u;     // -1e30 in both bf16 halves (and as fp32): masked chunks
 
-// expm1 for |x| < 1/16 from its Taylor series; the first omitted term
-// x^6/720 is below 1.4e-9 relative there.
+// expm1 for |x| < 1/8 from its Taylor series to x^5/120; the first omitted
+// term x^6/720 is below 4.3e-8 relative there.
 __device__ __forceinline__ float expm1_small(float x) {
 #pragma clang fp contract(off)
     float p = fmaf(x, 1.0f / 120.0f, 1.0f / 24.0f);
@@ -65,9 +66,9 @@ __device__ __forceinline__ float drift_finish(float zb, float za, float sqe, flo
     return spd / za - logf(za / zb);
 }
 
-// One row of d elements per TPR threads (TPR = 64, 128 or 256); each thread
-// keeps NCH 16-byte chunks of both rows in registers.  Rows of a workgroup:
-// kDriftBlock / TPR.
+// One row of d elements per TPR threads (64, 128 or 256); each thread keeps
+// NCH 16-byte chunks of both rows in registers.
+// Rows of a workgroup: kDriftBlock / TPR.
 template <bool BF16, int TPR, int NCH>
 __device__ __forceinline__ void drift_body(const char* __restrict__ hc, const char* __restrict__ hp,
                                            float* __restrict__ out, int rows, int d, int blk) {
@@ -85,18 +86,24 @@ __device__ __forceinline__ void drift_body(const char* __restrict__ hc, const ch
     const int chunks = d / T::E;
 
     // Unconditional loads: chunks past the row end re-read chunk 0 and are
-    // masked out of the arithmetic.
+    // then set to -1e30 in both rows (no share of either maximum, zero
+    // exponentials, dl = 0 or the row shift: nothing added to any sum).
     uint4 ra[NCH], rb[NCH];
-    bool ok[NCH];
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         const int ch = c * TPR + tr;
-        ok[c] = ch < chunks;
-        const size_t off = base + static_cast<size_t>(ok[c] ? ch : 0) * 16;
+        const size_t off = base + static_cast<size_t>(ch < chunks ? ch : 0) * 16;
         ra[c] = ld16(hc + off);
         rb[c] = ld16(hp + off);
     }
     __builtin_amdgcn_sched_barrier(0);    // every load in flight before any use
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (c * TPR + tr >= chunks) {
+            ra[c] = make_uint4(kNeutral, kNeutral, kNeutral, kNeutral);
+            rb[c] = ra[c];
+        }
+    }
 
     // Pass 1: the maximum of each row (ma of the current, mb of the previous).
     float mx[2] = {-INFINITY, -INFINITY};
@@ -107,8 +114,8 @@ __device__ __forceinline__ void drift_body(const char* __restrict__ hc, const ch
         T::unpack(rb[c], b);
 #pragma unroll
         for (int j = 0; j < T::E; ++j) {
-            mx[0] = fmaxf(mx[0], ok[c] ? a[j] : -INFINITY);
-            mx[1] = fmaxf(mx[1], ok[c] ? b[j] : -INFINITY);
+            mx[0] = fmaxf(mx[0], a[j]);
+            mx[1] = fmaxf(mx[1], b[j]);
         }
     }
     row_reduce<TPR, 2, true>(mx, red);
@@ -122,27 +129,45 @@ __device__ __forceinline__ void drift_body(const char* __restrict__ hc, const ch
     const float shift = near ? 0.0f : mx[0] - mx[1];
     const float mal = (near ? m : mx[0]) * kLog2e, mbl = (near ? m : mx[1]) * kLog2e;
 
-    // Pass 2: the four sums (masked chunks contribute nothing).
+    // Pass 2: the four sums.  A chunk whose elements all move by less than
+    // 1/8 (every chunk of a lightly perturbed row) takes one exponential per
+    // element, ea = eb (1 + expm1(dl)); otherwise both exponentials are
+    // taken directly, and ea - eb still comes from the series where |dl| is
+    // small.
     float zb = 0.0f, za = 0.0f, sqe = 0.0f, spd = 0.0f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-        float a[T::E], b[T::E];
+        float a[T::E], b[T::E], dl[T::E], eb[T::E];
         T::unpack(ra[c], a);
         T::unpack(rb[c], b);
-        const float keep = ok[c] ? 1.0f : 0.0f;
+        bool big = false;
 #pragma unroll
         for (int j = 0; j < T::E; ++j) {
-            const float dl = (a[j] - b[j]) - shift;
-            const float eb = keep * fast_exp2(fmaf(b[j], kLog2e, -mbl));
-            const float ead = keep * fast_exp2(fmaf(a[j], kLog2e, -mal));
-            const float em = expm1_small(dl);
-            const bool small = fabsf(dl) < kSmall;
-            const float qe = small ? eb * em : ead - eb;
-            const float ea = small ? fmaf(eb, em, eb) : ead;
-            zb += eb;
-            za += ea;
-            sqe += qe;
-            spd = fmaf(ea, dl, spd);
+            dl[j] = (a[j] - b[j]) - shift;
+            big |= !(fabsf(dl[j]) < kSmall);
+            eb[j] = fast_exp2(fmaf(b[j], kLog2e, -mbl));
+        }
+        if (!big) {
+#pragma unroll
+            for (int j = 0; j < T::E; ++j) {
+                const float em = expm1_small(dl[j]);
+                const float ea = fmaf(eb[j], em, eb[j]);
+                sqe = fmaf(eb[j], em, sqe);
+                zb += eb[j];
+                za += ea;
+                spd = fmaf(ea, dl[j], spd);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < T::E; ++j) {
+                const float ead = fast_exp2(fmaf(a[j], kLog2e, -mal));
+                const float qs = eb[j] * expm1_small(dl[j]);
+                const float qe = fabsf(dl[j]) < kSmall ? qs : ead - eb[j];
+                sqe += qe;
+                zb += eb[j];
+                za += ead;
+                spd = fmaf(ead, dl[j], spd);
+            }
         }
     }
     float sums[4] = {zb, za, sqe, spd};
@@ -150,18 +175,31 @@ __device__ __forceinline__ void drift_body(const char* __restrict__ hc, const ch
     if (live && tr == 0) out[row] = drift_finish(sums[0], sums[1], sums[2], sums[3]);
 }
 
-// chunks per row -> (threads per row, chunks per thread); false above 2048
-// chunks (d above 16384 in bf16 / 8192 in fp32)
-inline bool drift_config(int chunks, int& tpr, int& nch) {
-    static const int cfg[6][3] = {{64, 64, 1}, {128, 64, 2}, {256, 128, 2}, {512, 256, 2}, {1024, 256, 4}, {2048, 256, 8}};
-    for (const auto& c : cfg)
-        if (chunks <= c[0]) {
-            tpr = c[1];
-            nch = c[2];
-            return true;
-        }
-    return false;
+// (chunks per row, rows) -> (threads per row, chunks per thread).  With at
+// least 2048 rows (eight waves per compute unit and more): one wave per row
+// up to 512 chunks (d = 4096 bf16, 2048 fp32), as many chunks per lane as it
+// takes (no idle lanes at d = 3584), reduced in shuffles alone; 128 threads
+// of 8 chunks up to 1024 chunks.  Fewer rows (or longer ones): 256 threads
+// per row, so that a batch-1 layer still spreads over every compute unit.
+// False above 2048 chunks (d above 16384 in bf16 / 8192 in fp32).
+// PS_DRIFT_SHAPES lists the shapes this can return, for the launch tables.
+inline bool drift_config(int chunks, long rows, int& tpr, int& nch) {
+    if (chunks <= 0 || chunks > 2048) return false;
+    if (rows >= 2048 && chunks <= 512) {
+        tpr = 64;
+        nch = (chunks + 63) / 64;
+    } else if (rows >= 2048 && chunks <= 1024) {
+        tpr = 128;
+        nch = 8;
+    } else {
+        tpr = 256;
+        const int need = (chunks + 255) / 256;
+        nch = need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : 8;
+    }
+    return true;
 }
+#define PS_DRIFT_SHAPES(X) X(64, 1) X(64, 2) X(64, 3) X(64, 4) X(64, 5) X(64, 6) X(64, 7) X(64, 8) \
+    X(128, 8) X(256, 1) X(256, 2) X(256, 4) X(256, 8)
 
 }  // namespace
 }  // namespace ps

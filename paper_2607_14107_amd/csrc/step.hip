@@ -151,12 +151,10 @@ void launch_lead1(dim3 grid, const LeadArgs& l, hipStream_t s) {
 template <bool BF16>
 bool launch_lead(int tpr, int nch, dim3 grid, const LeadArgs& l, hipStream_t s) {
     switch (tpr * 16 + nch) {
-        case 64 * 16 + 1: launch_lead1<BF16, 64, 1>(grid, l, s); return true;
-        case 64 * 16 + 2: launch_lead1<BF16, 64, 2>(grid, l, s); return true;
-        case 128 * 16 + 2: launch_lead1<BF16, 128, 2>(grid, l, s); return true;
-        case 256 * 16 + 2: launch_lead1<BF16, 256, 2>(grid, l, s); return true;
-        case 256 * 16 + 4: launch_lead1<BF16, 256, 4>(grid, l, s); return true;
-        case 256 * 16 + 8: launch_lead1<BF16, 256, 8>(grid, l, s); return true;
+#define PS_CASE(TPR, NCH) \
+        case TPR * 16 + NCH: launch_lead1<BF16, TPR, NCH>(grid, l, s); return true;
+        PS_DRIFT_SHAPES(PS_CASE)
+#undef PS_CASE
         default: return false;
     }
 }
@@ -253,7 +251,8 @@ StepLayout step_layout(const polestar_step_args& a) {
     L.ipt = select_ipt(a.seq);
     const bool q_dma = bf16 && L.qp.dma && L.qp.row_tiles == 1 && L.qp.mt >= 2 && L.qp.mt <= 4 &&
                        (2 * L.qp.steps_per_split == 8 || 2 * L.qp.steps_per_split == 16);
-    const bool drift_ok = drift_config(a.d / (bf16 ? 8 : 4), L.drift_tpr, L.drift_nch);
+    const bool drift_ok = drift_config(a.d / (bf16 ? 8 : 4), static_cast<long>(a.batch) * a.seq, L.drift_tpr,
+                                       L.drift_nch);
     const bool common = drift_ok && a.block_len <= kStepBlock && (a.head_dim == 64 || a.head_dim == 128);
     L.fused = common && L.ipt >= 1 && L.ipt <= 8 && (L.qp.small || q_dma);
     // more query rows than the front kernel takes (or a longer sequence):
