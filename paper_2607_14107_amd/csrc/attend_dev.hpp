@@ -429,36 +429,45 @@ __device__ __forceinline__ void merge_body(const AttArgs& a, int blk) {
 // read that group's K/V, so the workgroup is (sequence b, KV head, row block,
 // key split): its NW waves each own one (query head, 32-query group) pair of
 // the group and walk the same keys, which the whole workgroup stages once in
-// LDS -- K as [key][d] rows, V^T as attend_kernel lays it out, per 32 keys --
-// 64 keys per step, double-buffered with one barrier per step (the next
-// step's loads are in flight while the current one is computed).  A step
-// computes the scores of both 32-key halves before the softmax, so a wave has
-// eight independent MFMA chains in flight instead of four, and the online
-// softmax rescales once per 64 keys.  There is no wave merge: each wave
-// writes its own output (one split) or its (m, l, O) partial in the layout
-// the merge kernel reads.  Waves past the group's last pair help stage and
-// skip the arithmetic.
+// LDS -- K as [key][d] rows, V^T as [d][key slot] rows -- 64 keys per step,
+// double-buffered with one barrier per step (the next step's loads are in
+// flight while the current one is computed).  Both products run on
+// v_mfma_f32_32x32x16_bf16 (on gfx950 twice the rate of the 16x16x32 form):
+// S^T = K Q^T for 32 keys x the wave's 32 queries, then O^T += V^T P^T, 16
+// keys at a time.  A lane ends S^T with 16 scores of one query (query
+// lane % 32), which are exactly the eight-key slices of P^T that the second
+// product takes as its B operand -- keys 4h..4h+3 and 8+4h..8+4h+3 of each
+// 16-key block for lane half h -- so V^T is staged with the 4-key groups of a
+// block in slot order 0, 2, 1, 3 and the probabilities never leave the
+// registers.  There is no wave merge: each wave writes its own output (one
+// split) or its (m, l, O) partial in the layout the merge kernel reads.
+// Waves past the group's last pair help stage and skip the arithmetic.
 constexpr int kGKT = 64;   // keys per step of the grouped kernel
+
+// LDS slot of the first key of 4-key group kg (0..15) of a step in a V^T row.
+__device__ __forceinline__ int gslot(int kg) {
+    constexpr int kOrder[4] = {0, 8, 4, 12};
+    return 16 * (kg >> 2) + kOrder[kg & 3];
+}
 
 template <int HD, int NW>
 __global__ __launch_bounds__(64 * NW) void attend_group_kernel(AttArgs a) {
     constexpr int NT = 64 * NW;
-    constexpr int NC = HD * 2 / 64;          // 16-byte chunks of one lane's d-range
-    constexpr int DPL = HD / 4;              // d values per lane group
-    constexpr int DT = HD / 16;              // 16-row d tiles of O^T
-    constexpr int VP = 80;                   // V^T row: 32 keys x 2 B + 16 B pad
-    constexpr int KP = HD * 2 + 16;          // K row + 16 B pad: the 16 rows of a fragment read use distinct banks
+    constexpr int KS = HD / 16;              // 16-wide d steps of S^T = K Q^T
+    constexpr int DT = HD / 32;              // 32-row d tiles of O^T
+    constexpr int KP = HD * 2 + 16;          // K row + 16 B pad
+    constexpr int VP = kGKT * 2 + 16;        // V^T row: 64 key slots + 16 B pad (16-row reads on distinct banks)
     constexpr int KCH = kGKT * HD * 2 / 16;  // 16-byte chunks of a step's K
     constexpr int KI = (KCH + NT - 1) / NT;
-    constexpr int VU = 16 * HD / 2;          // V staging units: 4 keys x 2 d
+    constexpr int VU = (kGKT / 4) * (HD / 2);   // V staging units: 4 keys x 2 d
     constexpr int VI = (VU + NT - 1) / NT;
     __shared__ __align__(16) char ks[2][kGKT * KP];
-    __shared__ __align__(16) char vs[2][2][HD * VP];   // [buffer][32-key half]
+    __shared__ __align__(16) char vs[2][HD * VP];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
+    const int l32 = lane & 31, h32 = lane >> 5;
     const int w = tid >> 6;
-    const int g = lane >> 4;
     const int split = blockIdx.x;
     const int G = a.H / a.Hkv;
     const int qgroups = (a.nq + kQG - 1) / kQG;
@@ -476,21 +485,22 @@ __global__ __launch_bounds__(64 * NW) void attend_group_kernel(AttArgs a) {
     const char* kbase = a.k + (static_cast<size_t>(b) * a.seq * a.Hkv + kvh) * HD * 2;
     const char* vbase = a.v + (static_cast<size_t>(b) * a.seq * a.Hkv + kvh) * HD * 2;
 
-    // Q fragments (B operand of S^T), as in attend_kernel.
-    uint4 qf[2][NC];
+    // Q fragments (B operand of S^T: 16 d x 32 queries): query qg*32 + lane % 32,
+    // d = 16 kk + 8 h32 .. +8.  Queries past nq read the last row (never stored).
+    uint4 qf[KS];
+    {
+        const int q = min(qg * kQG + l32, a.nq - 1);
+        const char* qp = a.q + ((static_cast<size_t>(b) * a.nq + q) * a.H + h) * HD * 2 + h32 * 16;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const int q = min(qg * kQG + 16 * u + (lane & 15), a.nq - 1);
-        const char* qp = a.q + ((static_cast<size_t>(b) * a.nq + q) * a.H + h) * HD * 2 + g * DPL * 2;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) qf[u][c] = ld16(qp + 16 * c);
+        for (int kk = 0; kk < KS; ++kk) qf[kk] = ld16(qp + 32 * kk);
     }
 
-    floatx4 o[DT][2];
+    floatx16 o[DT];
 #pragma unroll
-    for (int i = 0; i < DT; ++i) o[i][0] = o[i][1] = floatx4{0.f, 0.f, 0.f, 0.f};
-    float mrun[2] = {-INFINITY, -INFINITY};
-    float lrun[2] = {0.f, 0.f};
+    for (int i = 0; i < DT; ++i)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) o[i][j] = 0.f;
+    float mrun = -INFINITY, lrun = 0.f;
 
     const int nsteps = (a.seq + kGKT - 1) / kGKT;
     const int s_begin = split * a.tiles_per_split;
@@ -530,138 +540,139 @@ __global__ __launch_bounds__(64 * NW) void attend_group_kernel(AttArgs a) {
             const int u = tid + i * NT;
             if (VU % NT == 0 || u < VU) {
                 const int dp = u % (HD / 2), kg = u / (HD / 2);
-                char* vt = vs[buf][kg >> 3];
-                const int slot = vslot(4 * (kg & 7));
+                const int slot = gslot(kg);
                 const uint2 lo = make_uint2((vr[i][0] & 0xffffu) | (vr[i][1] << 16),
                                             (vr[i][2] & 0xffffu) | (vr[i][3] << 16));
                 const uint2 hi = make_uint2((vr[i][0] >> 16) | (vr[i][1] & 0xffff0000u),
                                             (vr[i][2] >> 16) | (vr[i][3] & 0xffff0000u));
-                *reinterpret_cast<uint2*>(vt + (2 * dp) * VP + slot * 2) = lo;
-                *reinterpret_cast<uint2*>(vt + (2 * dp + 1) * VP + slot * 2) = hi;
+                *reinterpret_cast<uint2*>(vs[buf] + (2 * dp) * VP + slot * 2) = lo;
+                *reinterpret_cast<uint2*>(vs[buf] + (2 * dp + 1) * VP + slot * 2) = hi;
             }
         }
     };
     auto compute_step = [&](int buf, int step) {
         const int key0 = step * kGKT;
         const char* kb = ks[buf];
-        // S^T tiles st[t][u] = K_t Q_u^T for the four 16-key tiles t of the step.
-        floatx4 st[4][2];
+        const char* vb = vs[buf];
+        // S^T for the two 32-key tiles of the step; register j of st[kt] is key
+        // key0 + 32 kt + mfma32_row(lane, j) of query lane % 32.
+        floatx16 st[2];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            uint4 kf[NC];
+        for (int kt = 0; kt < 2; ++kt) {
+            floatx16 sacc;
 #pragma unroll
-            for (int c = 0; c < NC; ++c)
-                kf[c] = *reinterpret_cast<const uint4*>(kb + (16 * t + (lane & 15)) * KP + g * DPL * 2 + 16 * c);
+            for (int j = 0; j < 16; ++j) sacc[j] = 0.f;
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                floatx4 s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int c = 0; c < NC; ++c) s = mfma_bf16(kf[c], qf[u][c], s);
-                st[t][u] = s;
+            for (int kk = 0; kk < KS; ++kk) {
+                const uint4 kf = *reinterpret_cast<const uint4*>(kb + (32 * kt + l32) * KP + 32 * kk + 16 * h32);
+                sacc = Mma32<true>::step(kf, qf[kk], sacc);
             }
+            st[kt] = sacc;
         }
-        float p[4][2][4];   // [t][u][i]
+        float mx = -INFINITY;
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            float mx = -INFINITY;
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int key = key0 + 16 * t + 4 * g + i;
-                    const float s = key < a.seq ? st[t][u][i] * a.scale_log2 : -INFINITY;
-                    p[t][u][i] = s;
-                    mx = fmaxf(mx, s);
-                }
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float mnew = fmaxf(mrun[u], mx);
-            const float mref = mnew == -INFINITY ? 0.f : mnew;
-            const float alpha = fast_exp2(mrun[u] - mref);
-            float sum = 0.f;
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float e = fast_exp2(p[t][u][i] - mref);
-                    p[t][u][i] = e;
-                    sum += e;
-                }
-            sum += __shfl_xor(sum, 16);
-            sum += __shfl_xor(sum, 32);
-            lrun[u] = lrun[u] * alpha + sum;
-            mrun[u] = mnew;
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) o[dt][u] *= alpha;
-        }
-        // O^T += V^T P^T, one 32-key half at a time (tiles 2 hf and 2 hf + 1).
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-            const char* vb = vs[buf][hf];
-            uint4 pf[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
-                pf[u] = make_uint4(pack_bf16x2(p[2 * hf][u][0], p[2 * hf][u][1]),
-                                   pack_bf16x2(p[2 * hf][u][2], p[2 * hf][u][3]),
-                                   pack_bf16x2(p[2 * hf + 1][u][0], p[2 * hf + 1][u][1]),
-                                   pack_bf16x2(p[2 * hf + 1][u][2], p[2 * hf + 1][u][3]));
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                const uint4 va = *reinterpret_cast<const uint4*>(vb + (dt * 16 + (lane & 15)) * VP + g * 16);
-#pragma unroll
-                for (int u = 0; u < 2; ++u) o[dt][u] = mfma_bf16(va, pf[u], o[dt][u]);
+            for (int j = 0; j < 16; ++j) {
+                const int key = key0 + 32 * kt + mfma32_row(lane, j);
+                const float sv = key < a.seq ? st[kt][j] * a.scale_log2 : -INFINITY;
+                st[kt][j] = sv;
+                mx = fmaxf(mx, sv);
             }
-        }
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mnew = fmaxf(mrun, mx);
+        const float mref = mnew == -INFINITY ? 0.f : mnew;
+        const float alpha = fast_exp2(mrun - mref);
+        float sum = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const float e = fast_exp2(st[kt][j] - mref);
+                st[kt][j] = e;
+                sum += e;
+            }
+        sum += __shfl_xor(sum, 32);
+        lrun = lrun * alpha + sum;
+        mrun = mnew;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+        // O^T += V^T P^T over the four 16-key blocks: the B operand is
+        // registers 8 kb' .. 8 kb' + 7 of st[kt] (kb' = block within the tile).
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int kb2 = 0; kb2 < 2; ++kb2) {
+                const int r = 8 * kb2;
+                const uint4 pf = make_uint4(pack_bf16x2(st[kt][r + 0], st[kt][r + 1]),
+                                            pack_bf16x2(st[kt][r + 2], st[kt][r + 3]),
+                                            pack_bf16x2(st[kt][r + 4], st[kt][r + 5]),
+                                            pack_bf16x2(st[kt][r + 6], st[kt][r + 7]));
+                const int soff = (32 * kt + 16 * kb2 + 8 * h32) * 2;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+                    const uint4 va = *reinterpret_cast<const uint4*>(vb + (32 * dt + l32) * VP + soff);
+                    o[dt] = Mma32<true>::step(va, pf, o[dt]);
+                }
+            }
     };
 
-    // Two register sets: step i is stored to LDS buffer i % 2 while step i + 1
-    // is being loaded.  Buffer i % 2 is rewritten two steps after it was read;
-    // the barrier of the step in between orders every wave's reads before the
-    // rewrite.  The loop is unrolled by two so that the sets are fixed per
-    // position.
-    uint4 kr[2][KI];
-    uint32_t vr[2][VI][4];
+    // Three register sets: while step i is stored to LDS buffer i % 2, steps
+    // i + 1 and i + 2 are being loaded (one step of compute does not cover a
+    // global load's latency).  Buffer i % 2 is rewritten two steps after it
+    // was read; the barrier of the step in between orders every wave's reads
+    // before the rewrite.  The loop is unrolled by three so that the register
+    // sets are fixed per position.
+    constexpr int PD = 3;
+    uint4 kr[PD][KI];
+    uint32_t vr[PD][VI][4];
     const int n = s_end - s_begin;
-    if (n > 0) load_step(s_begin, kr[0], vr[0]);
-    for (int base = 0; base < n; base += 2) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < PD - 1; ++j)
+        if (j < n) load_step(s_begin + j, kr[j], vr[j]);
+    for (int base = 0; base < n; base += PD) {
+#pragma unroll
+        for (int j = 0; j < PD; ++j) {
             const int i = base + j;
             if (i < n) {
-                store_step(j, kr[j], vr[j]);
-                if (i + 1 < n) load_step(s_begin + i + 1, kr[j ^ 1], vr[j ^ 1]);
+                store_step(i & 1, kr[j], vr[j]);
+                if (i + PD - 1 < n) load_step(s_begin + i + PD - 1, kr[(j + PD - 1) % PD], vr[(j + PD - 1) % PD]);
                 __syncthreads();
-                if (active) compute_step(j, s_begin + i);
+                if (active) compute_step(i & 1, s_begin + i);
             }
         }
     }
     if (!active) return;
 
-    // Lane holds O^T[d = 16 dt + 4 g + i][q = 16 u + (lane & 15)].
+    // Register j of o[dt] is O^T[d = 32 dt + mfma32_row(lane, j)][query lane % 32]:
+    // groups of four consecutive d per lane.
+    const int q = qg * kQG + l32;
+    if (q >= a.nq) return;
+    const size_t row = (static_cast<size_t>(b) * a.nq + q) * a.H + h;   // [b][q][h]
+    if (a.splits == 1) {
+        const float inv = 1.f / lrun;
+        char* op = a.out + row * HD * 2;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const int q = qg * kQG + 16 * u + (lane & 15);
-        if (q >= a.nq) continue;
-        const size_t row = (static_cast<size_t>(b) * a.nq + q) * a.H + h;   // [b][q][h]
-        if (a.splits == 1) {
-            const float inv = 1.f / lrun[u];
-            char* op = a.out + row * HD * 2;
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-                *reinterpret_cast<uint2*>(op + (16 * dt + 4 * g) * 2) =
-                    make_uint2(pack_bf16x2(o[dt][u][0] * inv, o[dt][u][1] * inv),
-                               pack_bf16x2(o[dt][u][2] * inv, o[dt][u][3] * inv));
-            if (a.lse && g == 0)
-                a.lse[(static_cast<size_t>(b) * a.H + h) * a.nq + q] = (mrun[u] + __log2f(lrun[u])) * kLn2;
-        } else {
-            const size_t prow = ((static_cast<size_t>(b) * a.H + h) * a.nq + q) * a.splits + split;
-            float* po = a.part_o + prow * HD;
+            for (int g4 = 0; g4 < 4; ++g4)
+                *reinterpret_cast<uint2*>(op + (32 * dt + 8 * g4 + 4 * h32) * 2) =
+                    make_uint2(pack_bf16x2(o[dt][4 * g4] * inv, o[dt][4 * g4 + 1] * inv),
+                               pack_bf16x2(o[dt][4 * g4 + 2] * inv, o[dt][4 * g4 + 3] * inv));
+        if (a.lse && h32 == 0)
+            a.lse[(static_cast<size_t>(b) * a.H + h) * a.nq + q] = (mrun + __log2f(lrun)) * kLn2;
+    } else {
+        const size_t prow = ((static_cast<size_t>(b) * a.H + h) * a.nq + q) * a.splits + split;
+        float* po = a.part_o + prow * HD;
 #pragma unroll
-            for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<floatx4*>(po + 16 * dt + 4 * g) = o[dt][u];
-            if (g == 0) {
-                a.part_ml[prow * 2] = mrun[u];
-                a.part_ml[prow * 2 + 1] = lrun[u];
-            }
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4)
+                *reinterpret_cast<float4*>(po + 32 * dt + 8 * g4 + 4 * h32) =
+                    make_float4(o[dt][4 * g4], o[dt][4 * g4 + 1], o[dt][4 * g4 + 2], o[dt][4 * g4 + 3]);
+        if (h32 == 0) {
+            a.part_ml[prow * 2] = mrun;
+            a.part_ml[prow * 2 + 1] = lrun;
         }
     }
 }
@@ -670,20 +681,22 @@ struct AttPlan {
     int splits;
     int tiles_per_split;
     size_t part_bytes;   // partial O + (m, l)
-    int group_waves;     // 0: attend_kernel; 4 or 8: attend_group_kernel with that many waves
-                         // (its tiles_per_split then counts 64-key steps)
+    int group_waves;     // 0: attend_kernel; 8: attend_group_kernel (its tiles_per_split then counts
+                         // 64-key steps)
     int row_blocks;      // grouped: workgroups per (sequence, KV head, split)
 };
 
 // Plan of the attention launch.  Grouped heads (bf16, at least four (query
-// head, 32-query group) pairs per KV head) take attend_group_kernel with about
-// one workgroup per CU; everything else attend_kernel.
+// head, 32-query group) pairs per KV head) take attend_group_kernel: 8-wave
+// workgroups (two waves per SIMD), keys split so that about 256 workgroups
+// run (one round, one per CU); each split adds an fp32 (m, l, O) partial per
+// query row, so no more splits than that.  Everything else attend_kernel.
 inline AttPlan att_plan(bool bf16, int batch, int seq, int H, int Hkv, int nq, int hd) {
     AttPlan p{};
     const int ntiles = ceil_div(seq, kKT);
     const int npairs = (H / Hkv) * ceil_div(nq, kQG);
     if (bf16 && npairs >= 4 && static_cast<long>(batch) * Hkv <= 65535) {
-        p.group_waves = npairs >= 8 ? 8 : 4;
+        p.group_waves = 8;
         p.row_blocks = ceil_div(npairs, p.group_waves);
         const int nsteps = ceil_div(seq, kGKT);          // tiles_per_split counts 64-key steps
         const long base = static_cast<long>(batch) * Hkv * p.row_blocks;
@@ -719,10 +732,7 @@ void launch_att(const AttPlan& p, const AttArgs& a, hipStream_t s) {
     if constexpr (BF16) {
         if (p.group_waves > 0) {
             const dim3 grid(p.splits, p.row_blocks, a.batch * a.Hkv);
-            if (p.group_waves == 8)
-                hipLaunchKernelGGL((attend_group_kernel<HD, 8>), grid, dim3(512), 0, s, a);
-            else
-                hipLaunchKernelGGL((attend_group_kernel<HD, 4>), grid, dim3(256), 0, s, a);
+            hipLaunchKernelGGL((attend_group_kernel<HD, 8>), grid, dim3(512), 0, s, a);
             return;
         }
     }
