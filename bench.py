@@ -4,30 +4,41 @@
 
 A step is the whole hot path over one batch: drift -> select -> sparse K/V
 refresh -> Q projection of the active block -> bidirectional attention ->
-commit, one polestar_step call on one stream (six launches: drift beside
-the vocabulary scan, select beside the Q projection, the refresh GEMM, the
-refresh's split-K reduction beside the Q projection's, attention, and the
-attention merge beside the commit finalize).  The default workload is the LLaDA-8B-shaped layer (bf16,
+commit, one polestar_step call on one stream (its fused launches: drift
+beside the vocabulary scan, select beside the Q projection, the refresh
+GEMM, the split-K reductions, attention, and the attention merge beside the
+commit finalize).  The default workload is the LLaDA-8B-shaped layer (bf16,
 batch 1, d=4096, 32 heads of 128, sequence 768 = prompt 512 + 256 generated,
 active block 32, vocabulary 126464) with 15% of the positions heavily
 perturbed.  Inputs are seeded synthetic data, resident in HBM before timing.
 
 To measure HBM rather than the 256 MB Infinity Cache, every step reads one of
 R independent copies of all inputs and weights (R * working set > 256 MB),
-round robin.  After the warmup, an untimed diagnostic pass runs the six calls one
-by one with HIP events around each (the per-call breakdown, "calls_us"); in
-the timed region polestar_step records events on the launch stream around
-its refresh launches, the dominant kernels, which gives the roofline's launch
-duration.  One JSON line is printed.
+round robin.  The JSON line holds, beside the contract's keys:
+  - roofline: the dominant launch group (the refresh) from HIP events that
+    polestar_step records on its launch stream around those launches;
+  - step_us: median, p10 and p90 of per-step times over at least 50 steps
+    (HIP events around each step, after the timed region);
+  - calls_us: the six calls one by one (median over 50 passes), each with its
+    algorithmic bytes and flops, its fractions of HBM and MFMA peak and of its
+    attainable roofline max(bytes / HBM peak, flops / MFMA peak);
+  - copy_GB_s: a plain 1 GiB device copy, the achievable-bandwidth yardstick;
+  - extra_configs: the same step summary on the batch-8 LLaDA-8B layer (10%
+    stale, the middle of its three chained steps) and the Dream-7B GQA layer;
+  - cpu_baseline: the oracle, per step function, with all host cores and with
+    one thread.
 
-Counter summaries (HBM traffic of the dominant call):
+Counters (rocprofv3 --pmc) come from a separate pass:
 
-    python bench.py --copy-calibration      # a plain 1 GiB device copy, for the
-                                            # FETCH_SIZE / WRITE_SIZE scale factor
-    python bench.py --summarize-counters FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR
+    python bench.py --counter-pass --record-digest DIR/digest.json   # under rocprofv3 --pmc
+    python bench.py --copy-calibration                               # FETCH/WRITE scale factor
+    python bench.py --summarize-counters FETCH_DIR WRITE_DIR COPY_FETCH_DIR COPY_WRITE_DIR [--mfma-dir DIR]
 
-read rocprofv3 --pmc output directories and write
-profiles/<call>_<workload>_traffic.json.
+The counter pass runs each call (and the whole fused step) on its own,
+separated by one-element fill kernels, so every dispatch after the opening
+marker belongs to a known call; the summary (profiles/counters_<workload>.json)
+holds HBM bytes per call and per fused kernel, MFMA operation counts and busy
+cycles, and the source digest recorded when the counters were taken.
 """
 
 from __future__ import annotations
@@ -49,6 +60,9 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3
 CALLS = ("drift", "select", "refresh_kv", "project_q", "attend", "commit")
+COUNTER_CALLS = CALLS + ("gather", "scatter", "step")
+COPY_BYTES = 1 << 30
+MARKER_RUN = 3                 # back-to-back marker fills that open the counter pass
 
 
 def parse():
@@ -59,13 +73,20 @@ def parse():
     p.add_argument("--config", type=int, default=1)
     p.add_argument("--subrun", type=int, default=1)
     p.add_argument("--copies", type=int, default=0, help="input copies rotated (0: enough for 512 MB)")
+    p.add_argument("--stats-steps", type=int, default=100, help="steps timed one by one for the percentiles (>= 50)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-seconds", type=float, default=20.0)
+    p.add_argument("--no-extras", action="store_true", help="skip the batch-8 and Dream-7B summaries")
+    p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--copy-calibration", action="store_true",
                    help="run a plain 1 GiB device copy (counter scale factor) and exit")
+    p.add_argument("--counter-pass", action="store_true",
+                   help="run every call on its own between marker kernels (for rocprofv3 --pmc) and exit")
+    p.add_argument("--counter-rounds", type=int, default=12)
+    p.add_argument("--record-digest", default=None, metavar="PATH",
+                   help="write the digests of the sources the kernels are built from to PATH")
     p.add_argument("--summarize-counters", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH", "COPY_WRITE"),
-                   help="write the traffic summary of the dominant call from rocprofv3 --pmc output")
-    p.add_argument("--call", default="refresh_kv", help="call whose counters --summarize-counters reads")
+                   help="write profiles/counters_<workload>.json from rocprofv3 --pmc output of --counter-pass")
+    p.add_argument("--mfma-dir", default=None, help="--summarize-counters: directory of the MFMA counter pass")
     p.add_argument("--stack", type=int, default=None,
                    help="run the denoising loop of a whole layer stack (4: LLaDA-8B-shaped, 32 layers, batch 16) "
                         "once and print its tokens/s and tokens per forward instead of the layer-step benchmark")
@@ -74,6 +95,11 @@ def parse():
     p.add_argument("--codec", default=None, choices=("mxfp4", "mxfp8"),
                    help="--stack --flow packet: keep the window's cached inputs as quantized residuals")
     return p.parse_args()
+
+
+def workload_name(cfg, subrun):
+    frac = cfg.heavy_fracs[subrun]
+    return f"{cfg.name}-heavy{int(round(frac * 100)):02d}"
 
 
 def algorithmic_cost(cfg, k, es):
@@ -93,36 +119,39 @@ def algorithmic_cost(cfg, k, es):
         "commit": dict(bytes=b * B * V * es + b * B * (4 + 4 + 1 + 1) + 4 * b * (cfg.hist_depth + 1) * B,
                        flops=0),
     }
+    cost["step"] = dict(bytes=sum(c["bytes"] for c in cost.values()), flops=sum(c["flops"] for c in cost.values()))
     return cost
 
 
-# Kernels launched by each call, and the sources they are built from.
-CALL_KERNELS = {
-    # polestar_step's refresh: the GEMM, then reduce2_kernel (the split-K
-    # reduction, with the Q projection's beside it); the stand-alone call's
-    # reduction is gemm_reduce_kernel
-    "refresh_kv": ("gemm_dma_kernel", "gemm_reduce_kernel", "reduce2_kernel", "gemm_rows_kernel",
-                   "gemm_small_kernel"),
-    "project_q": ("gemm_dma_kernel", "gemm_small_kernel", "gemm_rows_kernel", "gemm_reduce_kernel"),
-    "attend": ("attend_kernel", "attend_merge_kernel"),
-    "drift": ("drift_kernel",),
-    "select": ("select_kernel",),
-    "commit": ("scan_kernel", "finalize_kernel"),
-}
+def roofline_numbers(nbytes, flops, us, dtype):
+    """Rates and fractions of one call: HBM and MFMA fractions of peak and
+    the fraction of its attainable roofline max(bytes / HBM, flops / MFMA)."""
+    t = us * 1e-6
+    peak_t = BF16_PEAK_TFLOPS if dtype == "bf16" else FP32_PEAK_TFLOPS
+    roof_us = max(nbytes / (HBM_PEAK_GBS * 1e9), flops / (peak_t * 1e12)) * 1e6
+    return {"us": round(us, 3), "bytes": int(nbytes), "flops": int(flops),
+            "GB_s": round(nbytes / t / 1e9, 1), "hbm_frac": round(nbytes / t / 1e9 / HBM_PEAK_GBS, 4),
+            "TFLOP_s": round(flops / t / 1e12, 3), "mfma_frac": round(flops / t / 1e12 / peak_t, 4),
+            "roofline_us": round(roof_us, 3), "roofline_frac": round(roof_us / us, 4),
+            "bound": "mfma" if flops / (peak_t * 1e12) > nbytes / (HBM_PEAK_GBS * 1e9) else "hbm"}
+
+
+# Sources each call's kernels are built from (a change retires its counters).
 CALL_SOURCES = {
     "refresh_kv": ("gemm.hip", "gemm.hpp", "gemm_dev.hpp", "step.hip"),
     "project_q": ("attend.hip", "gemm.hip", "gemm.hpp", "gemm_dev.hpp"),
-    "attend": ("attend.hip",),
+    "attend": ("attend.hip", "attend_dev.hpp"),
     "drift": ("drift.hip", "drift_dev.hpp"),
-    "select": ("select.hip",),
-    "commit": ("commit.hip",),
+    "select": ("select.hip", "select_dev.hpp"),
+    "commit": ("commit.hip", "commit_dev.hpp"),
+    "gather": ("model.hip",),
+    "scatter": ("model.hip",),
+    "step": ("step.hip", "drift_dev.hpp", "select_dev.hpp", "gemm_dev.hpp", "gemm.hip", "attend_dev.hpp",
+             "commit_dev.hpp"),
 }
-COPY_BYTES = 1 << 30
 
 
 def source_digest(call):
-    """Digest of the sources a call's kernels are built from (changes when the
-    kernels do, which retires a counter summary)."""
     h = hashlib.sha256()
     for f in CALL_SOURCES[call] + ("common.hpp", "host_common.hpp"):
         with open(os.path.join(ROOT, "paper_2607_14107_amd", "csrc", f), "rb") as fh:
@@ -130,21 +159,45 @@ def source_digest(call):
     return h.hexdigest()[:16]
 
 
-def traffic_path(call, workload):
-    return os.path.join(ROOT, "profiles", f"{call}_{workload}_traffic.json")
+def source_digests():
+    return {c: source_digest(c) for c in COUNTER_CALLS}
 
 
-def traffic_for(call, workload):
-    """HBM bytes per launch of `call` from the committed counter summary, or
-    None when there is none or the kernels changed since it was taken."""
-    path = traffic_path(call, workload)
+def counters_path(workload):
+    return os.path.join(ROOT, "profiles", f"counters_{workload}.json")
+
+
+def traffic_for(call_key, workload):
+    """Counted HBM bytes per launch of `call_key` ("refresh_kv" in the fused
+    step: its GEMM and reduction launches) from the committed counter summary,
+    or None when there is none or the sources changed since it was taken."""
+    path = counters_path(workload)
     if not os.path.exists(path):
         return None
     with open(path) as f:
         t = json.load(f)
-    if t.get("source_digest") != source_digest(call):
+    if t.get("source_digests", {}).get("step") != source_digest("step"):
         return None
-    return t.get("bytes_per_launch")
+    return t.get("step_kernels", {}).get(call_key, {}).get("bytes")
+
+
+def copy_bandwidth(torch, reps=10):
+    """A plain device copy of COPY_BYTES, median of `reps` (read + write bytes
+    per second): the bandwidth a streaming kernel achieves on this GPU."""
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    dst.copy_(src)
+    times = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e-3)
+    del src, dst
+    return round(2 * COPY_BYTES / float(np.median(times)) / 1e9, 1)
 
 
 def copy_calibration():
@@ -161,9 +214,13 @@ def copy_calibration():
     return 0
 
 
+# ---------------------------------------------------------------------------
+# Counter summaries
+# ---------------------------------------------------------------------------
+
 def _counter_rows(directory, counter):
-    """(dispatch id, kernel name, value) per dispatch from the counter CSVs
-    rocprofv3 --pmc wrote under `directory`."""
+    """(dispatch id, kernel name, value) per dispatch, in dispatch order, from
+    the counter CSVs rocprofv3 --pmc wrote under `directory`."""
     import csv
     import glob
     out = {}
@@ -179,70 +236,316 @@ def _counter_rows(directory, counter):
     return sorted((k, v[0], v[1]) for k, v in out.items())
 
 
-def _call_launch_kib(rows, call):
-    """Counter KiB per launch of `call`: the dispatches of its most frequent
-    leading kernel, each with the dispatches of the same call that follow it."""
-    names = CALL_KERNELS[call]
-    lead = [n for _, n, _ in rows if names[0] in n]
-    if not lead:
-        lead = [n for _, n, _ in rows if any(k in n for k in names)]
-    from collections import Counter
-    main = Counter(lead).most_common(1)[0][0]
-    per_launch = []
-    i = 0
-    while i < len(rows):
-        _, name, v = rows[i]
-        if name == main:
-            tot = v
-            j = i + 1
-            while j < len(rows) and rows[j][1] != main and any(k in rows[j][1] for k in names[1:]):
-                tot += rows[j][2]
-                j += 1
-            per_launch.append(tot)
-            i = j
-        else:
-            i += 1
-    return main, per_launch
+def _is_marker(name):
+    # the counter pass's markers fill a float64 tensor; nothing else in the
+    # process runs a float64 fill
+    return "FillFunctor<double>" in name
 
 
-def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, call, workload):
+def _segments(rows):
+    """Split the dispatches after the opening run of markers into per-call
+    segments: [(call, [(name, value), ...]), ...] in COUNTER_CALLS order."""
+    start = None
+    for i in range(len(rows) - MARKER_RUN + 1):
+        if all(_is_marker(rows[i + j][1]) for j in range(MARKER_RUN)):
+            start = i + MARKER_RUN
+            break
+    if start is None:
+        raise SystemExit("no opening marker run: was the run made with --counter-pass?")
+    while start < len(rows) and _is_marker(rows[start][1]):
+        start += 1                    # the whole run; its last marker opens the first call
+    start -= 1
+    segs, cur = [], None
+    for _, name, v in rows[start:]:
+        if _is_marker(name):
+            if cur is not None:
+                segs.append(cur)
+            cur = []
+        elif cur is not None:
+            cur.append((name, v))
+    if cur:
+        segs.append(cur)
+    return [(COUNTER_CALLS[i % len(COUNTER_CALLS)], s) for i, s in enumerate(segs)]
+
+
+# roles of the fused step's kernels, by name
+STEP_ROLES = (("lead", ("lead_kernel",)), ("front", ("front_kernel", "front_dma_kernel", "select_kernel")),
+              ("refresh_kv", ("gemm_", "reduce2_kernel")), ("attend", ("attend_",)), ("back", ("back_kernel",)))
+
+
+def _step_role(name):
+    for role, pats in STEP_ROLES:
+        if any(p in name for p in pats):
+            return role
+    return "other"
+
+
+def _per_call(segs):
+    """Median over rounds of the summed value per call, and per role of the
+    fused step's kernels."""
+    calls, roles = {}, {}
+    for call, seg in segs:
+        calls.setdefault(call, []).append(sum(v for _, v in seg))
+        if call == "step":
+            per = {}
+            for name, v in seg:
+                per[_step_role(name)] = per.get(_step_role(name), 0.0) + v
+            for r, v in per.items():
+                roles.setdefault(r, []).append(v)
+    med = lambda xs: float(np.median(xs))
+    return {c: med(v) for c, v in calls.items()}, {r: med(v) for r, v in roles.items()}
+
+
+def summarize_counters(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, mfma_dir, cfg, subrun):
+    from paper_2607_14107_amd import inputs
+    x = inputs.layer_inputs(cfg, subrun)
+    k = int(x["k"])
+    cost = algorithmic_cost(cfg, k, 2 if cfg.dtype == "bf16" else 4)
+    workload = workload_name(cfg, subrun)
+
     def copy_kib(d, counter):
         vals = [v for _, n, v in _counter_rows(d, counter) if "copy" in n.lower()]
         if not vals:
             raise SystemExit(f"no copy dispatch with {counter} under {d}")
         return float(np.median(vals))
+
+    def digest_of(d):
+        with open(os.path.join(d, "digest.json")) as f:
+            return json.load(f)
+
+    rec = digest_of(fetch_dir)
+    if digest_of(write_dir)["source_digests"] != rec["source_digests"]:
+        raise SystemExit("FETCH and WRITE passes ran on different sources")
     f_fetch = COPY_BYTES / (copy_kib(copy_fetch_dir, "FETCH_SIZE") * 1024)
     f_write = COPY_BYTES / (copy_kib(copy_write_dir, "WRITE_SIZE") * 1024)
-    main, fetch = _call_launch_kib(_counter_rows(fetch_dir, "FETCH_SIZE"), call)
-    _, write = _call_launch_kib(_counter_rows(write_dir, "WRITE_SIZE"), call)
-    fetch_kib, write_kib = float(np.median(fetch)), float(np.median(write))
-    t = {
-        "call": call, "workload": workload, "lead_kernel": main,
-        "launches_counted": [len(fetch), len(write)],
-        "fetch_kib_per_launch": round(fetch_kib, 1), "write_kib_per_launch": round(write_kib, 1),
-        "copy_scale_fetch": round(f_fetch, 4), "copy_scale_write": round(f_write, 4),
-        "bytes_per_launch": int(fetch_kib * 1024 * f_fetch + write_kib * 1024 * f_write),
-        "source_digest": source_digest(call),
-        "commands": [
-            "cd /tmp && export TMPDIR=/tmp",
-            "rocprofv3 --pmc FETCH_SIZE -f csv -d $OUT/pmc_fetch -o c -- "
-            "python3 $R/bench.py --no-cpu-baseline --steps 20 --warmup 2",
-            "rocprofv3 --pmc WRITE_SIZE -f csv -d $OUT/pmc_write -o c -- "
-            "python3 $R/bench.py --no-cpu-baseline --steps 20 --warmup 2",
-            "rocprofv3 --pmc FETCH_SIZE -f csv -d $OUT/pmc_cfetch -o c -- python3 $R/bench.py --copy-calibration",
-            "rocprofv3 --pmc WRITE_SIZE -f csv -d $OUT/pmc_cwrite -o c -- python3 $R/bench.py --copy-calibration",
-            f"python3 $R/bench.py --summarize-counters $OUT/pmc_fetch $OUT/pmc_write "
-            f"$OUT/pmc_cfetch $OUT/pmc_cwrite --call {call}",
-        ],
-        "note": "counter KiB per launch summed over the call's kernels (median over launches); "
-                "bytes = KiB * 1024 * (copy bytes / copy counter bytes) for FETCH and WRITE; "
-                "$R is the repository, $OUT any output directory",
-    }
-    with open(traffic_path(call, workload), "w") as f:
+    fetch, fetch_roles = _per_call(_segments(_counter_rows(fetch_dir, "FETCH_SIZE")))
+    write, write_roles = _per_call(_segments(_counter_rows(write_dir, "WRITE_SIZE")))
+    calls = {}
+    for c in COUNTER_CALLS:
+        if c not in fetch:
+            continue
+        nb = fetch[c] * 1024 * f_fetch + write[c] * 1024 * f_write
+        calls[c] = {"fetch_bytes": int(fetch[c] * 1024 * f_fetch), "write_bytes": int(write[c] * 1024 * f_write),
+                    "bytes": int(nb)}
+        if c in cost:
+            calls[c]["algorithmic_bytes"] = int(cost[c]["bytes"])
+            calls[c]["ratio"] = round(nb / cost[c]["bytes"], 3)
+    step_kernels = {r: {"fetch_bytes": int(fetch_roles[r] * 1024 * f_fetch),
+                        "write_bytes": int(write_roles.get(r, 0.0) * 1024 * f_write),
+                        "bytes": int(fetch_roles[r] * 1024 * f_fetch + write_roles.get(r, 0.0) * 1024 * f_write)}
+                    for r in fetch_roles}
+    t = {"workload": workload, "stale_rows": k, "calls": calls, "step_kernels": step_kernels,
+         "copy_scale_fetch": round(f_fetch, 4), "copy_scale_write": round(f_write, 4),
+         "source_digests": rec["source_digests"]}
+    if mfma_dir:
+        if digest_of(mfma_dir)["source_digests"] != rec["source_digests"]:
+            raise SystemExit("the MFMA pass ran on different sources")
+        mops, mops_roles = _per_call(_segments(_counter_rows(mfma_dir, "SQ_INSTS_VALU_MFMA_MOPS_BF16")))
+        busy, busy_roles = _per_call(_segments(_counter_rows(mfma_dir, "SQ_VALU_MFMA_BUSY_CYCLES")))
+        gui, gui_roles = _per_call(_segments(_counter_rows(mfma_dir, "GRBM_GUI_ACTIVE")))
+        mf = {}
+        for c in COUNTER_CALLS:
+            if c in mops and mops[c] > 0:
+                mf[c] = {"mfma_flops": int(mops[c] * 512), "mfma_busy_cycles": int(busy.get(c, 0)),
+                         "gui_active_cycles": int(gui.get(c, 0))}
+                if c in cost and cost[c]["flops"]:
+                    mf[c]["algorithmic_flops"] = int(cost[c]["flops"])
+        t["mfma"] = mf
+        t["mfma_step_kernels"] = {r: {"mfma_flops": int(mops_roles[r] * 512),
+                                      "mfma_busy_cycles": int(busy_roles.get(r, 0)),
+                                      "gui_active_cycles": int(gui_roles.get(r, 0))}
+                                  for r in mops_roles if mops_roles[r] > 0}
+    t["commands"] = [
+        "cd /tmp && export TMPDIR=/tmp",
+        f"rocprofv3 --pmc FETCH_SIZE -f csv -d $OUT/f -o c -- python3 $R/bench.py --config {cfg.index} "
+        f"--subrun {subrun} --counter-pass --record-digest $OUT/f/digest.json",
+        f"rocprofv3 --pmc WRITE_SIZE -f csv -d $OUT/w -o c -- python3 $R/bench.py --config {cfg.index} "
+        f"--subrun {subrun} --counter-pass --record-digest $OUT/w/digest.json",
+        f"rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE -f csv -d $OUT/m "
+        f"-o c -- python3 $R/bench.py --config {cfg.index} --subrun {subrun} --counter-pass "
+        f"--record-digest $OUT/m/digest.json",
+        "rocprofv3 --pmc FETCH_SIZE -f csv -d $OUT/cf -o c -- python3 $R/bench.py --copy-calibration",
+        "rocprofv3 --pmc WRITE_SIZE -f csv -d $OUT/cw -o c -- python3 $R/bench.py --copy-calibration",
+        f"python3 $R/bench.py --config {cfg.index} --subrun {subrun} --summarize-counters $OUT/f $OUT/w "
+        f"$OUT/cf $OUT/cw --mfma-dir $OUT/m",
+    ]
+    t["note"] = ("per call: median over the counter pass's rounds of the counter summed over the call's "
+                 "dispatches (between marker fills); bytes = KiB * 1024 * (copy bytes / copy counter bytes); "
+                 "mfma_flops = SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512; $R is the repository, $OUT any directory")
+    with open(counters_path(workload), "w") as f:
         json.dump(t, f, indent=1)
         f.write("\n")
     print(json.dumps(t))
     return 0
+
+
+# ---------------------------------------------------------------------------
+# One layer workload on the GPU
+# ---------------------------------------------------------------------------
+
+class Layer:
+    """Inputs of one workload in HBM (R rotated copies), the Step buffers
+    and the prepared polestar_step arguments of every copy."""
+
+    def __init__(self, P, torch, cfg, subrun, copies=0):
+        from paper_2607_14107_amd import inputs
+        self.P, self.torch, self.cfg, self.subrun = P, torch, cfg, subrun
+        x = inputs.layer_inputs(cfg, subrun)
+        self.x = x
+        self.k = k = int(x["k"])
+        self.dt = dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+        self.es = es = 2 if cfg.dtype == "bf16" else 4
+        dev = torch.device("cuda", 0)
+
+        def up(a):
+            if cfg.dtype == "bf16":
+                return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+        # working set of one copy; enough copies to exceed the Infinity Cache twice
+        ws_bytes = sum(x[n].nbytes for n in ("h_cur", "h_prev", "w_q", "w_k", "w_v", "logits")) \
+            + 2 * cfg.batch * cfg.seq * cfg.n_kv_heads * cfg.head_dim * es
+        self.copies = copies or max(1, -(-512 * 2 ** 20 // ws_bytes))
+        self.sets = []
+        for _ in range(self.copies):
+            s = {n: up(x[n]) for n in ("h_cur", "h_prev", "w_q", "w_k", "w_v", "logits")}
+            s["k_cache"] = torch.empty((cfg.batch, cfg.seq, cfg.n_kv_heads, cfg.head_dim), dtype=dt, device=dev)
+            s["v_cache"] = torch.empty_like(s["k_cache"])
+            # prior cache = projection of the previous states (setup, untimed)
+            all_idx = torch.arange(cfg.seq, dtype=torch.int32, device=dev).repeat(cfg.batch, 1).contiguous()
+            all_cnt = torch.full((cfg.batch,), cfg.seq, dtype=torch.int32, device=dev)
+            P.refresh_kv(s["h_prev"], all_idx, all_cnt, cfg.block_start, 0, s["w_k"], s["w_v"],
+                         s["k_cache"], s["v_cache"])
+            s["masked"] = torch.from_numpy(x["masked"]).to(dev)
+            s["hist"] = torch.from_numpy(x["hist"].copy()).to(dev)
+            s["hist_len"] = torch.from_numpy(x["hist_len"].copy()).to(dev)
+            self.sets.append(s)
+        self.step = P.Step(batch=cfg.batch, seq=cfg.seq, d=cfg.d, n_heads=cfg.n_heads, n_kv_heads=cfg.n_kv_heads,
+                           head_dim=cfg.head_dim, block_start=cfg.block_start, block_len=cfg.block_len,
+                           vocab=cfg.vocab, k=k, dtype=dt, device=dev)
+        self.prepared = [self.step.prepare(c["h_cur"], c["h_prev"], c["w_q"], c["w_k"], c["w_v"], c["k_cache"],
+                                           c["v_cache"], c["logits"], c["masked"], c["hist"], c["hist_len"],
+                                           tau_s=cfg.tau_s, alpha=cfg.alpha) for c in self.sets]
+        self.stream = torch.cuda.current_stream()
+        self.cost = algorithmic_cost(cfg, k, es)
+        if k > 0:   # packet buffers of the gather / scatter calls
+            kvd = cfg.n_kv_heads * cfg.head_dim
+            self.packet = torch.empty((cfg.batch, k, cfg.d), dtype=dt, device=dev)
+            self.krows = [torch.zeros((cfg.batch, k, kvd), dtype=dt, device=dev) for _ in self.sets]
+        torch.cuda.synchronize()
+
+    def call(self, name, i):
+        """One stand-alone call on input copy i % copies."""
+        P, st, cfg, k = self.P, self.step, self.cfg, self.k
+        s = self.sets[i % self.copies]
+        sh = st.shape
+        if name == "drift":
+            P.drift(s["h_cur"], s["h_prev"], out=st.drift)
+        elif name == "select":
+            if k > 0:
+                P.select(st.drift, k, sh["block_start"], sh["block_len"], None, st.stale_idx, st.stale_count)
+        elif name == "refresh_kv":
+            P.refresh_kv(s["h_cur"], st.stale_idx, st.stale_count, sh["block_start"], sh["block_len"],
+                         s["w_k"], s["w_v"], s["k_cache"], s["v_cache"], workspace=st.ws_refresh)
+        elif name == "project_q":
+            P.project_q(s["h_cur"], s["w_q"], sh["block_start"], sh["block_len"], sh["n_heads"],
+                        out=st.q_buf, workspace=st.ws_q)
+        elif name == "attend":
+            P.attend(None, None, s["k_cache"], s["v_cache"], sh["block_start"], sh["block_len"],
+                     sh["n_heads"], q_buf=st.q_buf, out=st.out, lse=st.lse, workspace=st.ws_attend)
+        elif name == "commit":
+            P.commit(s["logits"], s["masked"], st.drift, sh["block_start"], s["hist"], s["hist_len"], -1,
+                     cfg.tau_s, cfg.alpha, False, st.token, st.conf, st.commit, workspace=st.ws_commit)
+        elif name == "gather":
+            if k > 0:
+                P.gather_rows(s["h_cur"], st.stale_idx, st.stale_count, self.packet)
+        elif name == "scatter":
+            if k > 0:
+                kvd = cfg.n_kv_heads * cfg.head_dim
+                P.scatter_rows(self.krows[i % self.copies], st.stale_idx, st.stale_count,
+                               s["k_cache"].view(cfg.batch, cfg.seq, kvd))
+        elif name == "step":
+            self.run_step(i)
+        else:
+            raise ValueError(name)
+
+    def run_step(self, i, ev=None):
+        self.step.launch(self.prepared[i % self.copies], ev)
+
+    def _spin(self):
+        # a device-side spin ahead of a batch of launches lets the host queue
+        # them all before the GPU starts, so events time the kernels back to
+        # back rather than the Python launch path
+        self.torch.cuda.synchronize()
+        self.torch.cuda._sleep(100_000_000)
+
+    def calls_us(self, n=50):
+        """The six calls one by one with events around each: median µs."""
+        torch = self.torch
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)] for _ in range(n)]
+        self._spin()
+        for i in range(n):
+            for j, name in enumerate(CALLS):
+                ev[i][j].record(self.stream)
+                self.call(name, i)
+            ev[i][len(CALLS)].record(self.stream)
+        torch.cuda.synchronize()
+        return {c: float(np.median([e[j].elapsed_time(e[j + 1]) * 1e3 for e in ev])) for j, c in enumerate(CALLS)}
+
+    def step_stats(self, n, first=0):
+        """Per-step times (µs) of n consecutive steps, events between steps."""
+        torch = self.torch
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        self._spin()
+        ev[0].record(self.stream)
+        for i in range(n):
+            self.run_step(first + i)
+            ev[i + 1].record(self.stream)
+        torch.cuda.synchronize()
+        t = np.array([ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(n)])
+        return {"n": n, "median": round(float(np.median(t)), 3), "p10": round(float(np.percentile(t, 10)), 3),
+                "p90": round(float(np.percentile(t, 90)), 3), "mean": round(float(t.mean()), 3)}
+
+    def calls_report(self, call_us):
+        return {c: roofline_numbers(self.cost[c]["bytes"], self.cost[c]["flops"], call_us[c], self.cfg.dtype)
+                for c in CALLS}
+
+    def counter_pass(self, rounds):
+        """Every call of COUNTER_CALLS on its own, `rounds` times, each preceded
+        by a one-element float64 fill (the marker the counter summary splits
+        on); the pass opens with MARKER_RUN fills back to back."""
+        torch = self.torch
+        marker = torch.zeros(1, dtype=torch.float64, device="cuda")
+        torch.cuda.synchronize()
+        for j in range(MARKER_RUN):
+            marker.fill_(float(j))
+        for r in range(rounds):
+            for c in COUNTER_CALLS:
+                marker.fill_(float(r))
+                self.call(c, r)
+        marker.fill_(-1.0)
+        torch.cuda.synchronize()
+
+
+def layer_summary(P, torch, cfg_index, subrun, n_steps=60):
+    """The step of another workload: per-step percentiles and the calls
+    against their rooflines (an extra key of the bench line)."""
+    from paper_2607_14107_amd import inputs
+    cfg = inputs.CONFIGS[cfg_index]
+    L = Layer(P, torch, cfg, subrun)
+    for i in range(5):
+        L.run_step(i)
+    stats = L.step_stats(n_steps, 5)
+    calls = L.calls_report(L.calls_us(30))
+    tokens = cfg.batch * cfg.block_len
+    out = {"workload": workload_name(cfg, subrun),
+           "shape": f"batch {cfg.batch}, seq {cfg.seq}, block {cfg.block_len}, d {cfg.d}, heads "
+                    f"{cfg.n_heads}/{cfg.n_kv_heads}x{cfg.head_dim}, vocab {cfg.vocab}, {L.k} stale rows per sequence",
+           "tokens_per_s": round(tokens / (stats["median"] * 1e-6), 1), "step_us": stats, "calls_us": calls}
+    del L
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
 
 
 def measure_gather_scatter(P, torch, cfg, sets, idx, cnt, es, reps=50):
@@ -323,37 +626,74 @@ def measure_proxy(P, torch, cfg, s, stream, es, n_clusters=8, k_top=4, reps=50):
 
 
 def cpu_baseline(cfg, x, k, budget_s):
-    """The oracle as it stands, timed on the host on whole steps of the same
-    workload until about budget_s seconds of CPU work are done."""
+    """The oracle as it stands, timed on the host per step function on the
+    benchmarked workload: median of at least 3 runs each, with the BLAS pool
+    at every core this process may use and again with one thread; tokens/s
+    = tokens of one step / the summed medians."""
     from oracle import polestar_ref as ref
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = len(os.sched_getaffinity(0))
+    cores = len(os.sched_getaffinity(0))
     dec = {n: ref.decode(x[n], cfg.dtype) for n in ("h_cur", "h_prev", "w_q", "w_k", "w_v")}
     shape = (cfg.batch, cfg.seq, cfg.n_kv_heads, cfg.head_dim)
     kc = ref.round_to((dec["h_prev"] @ dec["w_k"].T).reshape(shape), cfg.dtype)
     vc = ref.round_to((dec["h_prev"] @ dec["w_v"].T).reshape(shape), cfg.dtype)
     logits = ref.decode(x["logits"], cfg.dtype)
-    steps, t_total = 0, 0.0
-    while t_total < budget_s and steps < 50:
-        t0 = time.perf_counter()
-        r = ref.layer_step(dec["h_cur"], dec["h_prev"], dec["w_q"], dec["w_k"], dec["w_v"], kc, vc,
-                           k=k, block_start=cfg.block_start, block_len=cfg.block_len,
-                           n_heads=cfg.n_heads, n_kv_heads=cfg.n_kv_heads, head_dim=cfg.head_dim,
-                           cache_dtype=cfg.dtype)
-        token, conf = ref.confidence(logits, -1)
-        delta = r["drift"][:, cfg.block_start:cfg.block_start + cfg.block_len].astype(np.float32)
-        ref.commit_rule(conf.astype(np.float32), delta, x["masked"].astype(bool), x["hist"],
-                        x["hist_len"], cfg.hist_depth, cfg.tau_s, cfg.alpha, False)
-        t_total += time.perf_counter() - t0
-        steps += 1
+    bs, bl = cfg.block_start, cfg.block_len
+    st = {}
+
+    def f_drift():
+        st["d"] = ref.drift(dec["h_cur"], dec["h_prev"])
+
+    def f_select():
+        st["idx"], st["cnt"] = ref.select(st["d"], k, bs, bl)
+
+    def f_refresh():
+        kn, vn, _ = ref.refresh_kv(dec["h_cur"], dec["w_k"], dec["w_v"], kc, vc, st["idx"], st["cnt"], bs, bl)
+        st["k"], st["v"] = ref.round_to(kn, cfg.dtype), ref.round_to(vn, cfg.dtype)
+
+    def f_q():
+        st["q"] = ref.q_project(dec["h_cur"], dec["w_q"], bs, bl, cfg.n_heads, cfg.head_dim)
+
+    def f_attend():
+        ref.attend(ref.round_to(st["q"], cfg.dtype), st["k"], st["v"])
+
+    def f_commit():
+        _, conf = ref.confidence(logits, -1)
+        delta = st["d"][:, bs:bs + bl].astype(np.float32)
+        ref.commit_rule(conf.astype(np.float32), delta, x["masked"].astype(bool), x["hist"], x["hist_len"],
+                        cfg.hist_depth, cfg.tau_s, cfg.alpha, False)
+
+    fns = (("drift", f_drift), ("select", f_select), ("refresh_kv", f_refresh), ("project_q", f_q),
+           ("attend", f_attend), ("commit", f_commit))
+
+    def run_all(per_fn_s):
+        times = {n: [] for n, _ in fns}
+        spent = 0.0
+        while True:
+            for n, f in fns:       # in step order: each function consumes the one before
+                t0 = time.perf_counter()
+                f()
+                dt = time.perf_counter() - t0
+                times[n].append(dt)
+                spent += dt
+            reps = len(times["drift"])
+            if reps >= 3 and (spent >= per_fn_s * len(fns) or reps >= 50):
+                break
+        med = {n: float(np.median(v)) for n, v in times.items()}
+        return med, reps, spent
+
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=cores):
+        multi, reps_m, spent_m = run_all(budget_s / len(fns) / 2)
+    with threadpool_limits(limits=1):
+        single, reps_s, spent_s = run_all(budget_s / len(fns) / 2)
     tok = cfg.batch * cfg.block_len
-    return {"value": round(tok * steps / t_total, 3), "unit": "tokens/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"{steps} whole oracle layer steps (drift, select, refresh, Q projection, "
-                      f"attention, commit) of the benchmarked workload, {t_total:.1f} s"}
+    return {"value": round(tok / sum(multi.values()), 3), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{reps_m} oracle layer steps of the benchmarked workload timed per step function "
+                      f"(drift, select, refresh, Q projection, attention, commit; median per function), "
+                      f"{spent_m:.1f} s with {cores} BLAS threads; single-thread: {reps_s} steps, {spent_s:.1f} s",
+            "per_call_s": {n: round(v, 5) for n, v in multi.items()},
+            "single_thread": {"value": round(tok / sum(single.values()), 3), "cores": 1,
+                              "per_call_s": {n: round(v, 5) for n, v in single.items()}}}
 
 
 def stack_bench(index, P, torch, flow="window", codec=None):
@@ -417,9 +757,13 @@ def stack_bench(index, P, torch, flow="window", codec=None):
 
 def main():
     args = parse()
+    from paper_2607_14107_amd import inputs
     if args.summarize_counters:
-        from paper_2607_14107_amd import inputs
-        return summarize_counters(*args.summarize_counters, args.call, inputs.CONFIGS[args.config].name)
+        return summarize_counters(*args.summarize_counters, args.mfma_dir, inputs.CONFIGS[args.config], args.subrun)
+    if args.record_digest:
+        os.makedirs(os.path.dirname(os.path.abspath(args.record_digest)), exist_ok=True)
+        with open(args.record_digest, "w") as f:
+            json.dump({"source_digests": source_digests(), "config": args.config, "subrun": args.subrun}, f)
     if args.copy_calibration:
         return copy_calibration()
     if args.gpus != 1:
@@ -428,7 +772,6 @@ def main():
         return 2
 
     import torch
-    from paper_2607_14107_amd import inputs
     from paper_2607_14107_amd import polestar as P
 
     if not torch.cuda.is_available():
@@ -438,103 +781,26 @@ def main():
         from paper_2607_14107_amd import build
         build.build(verbose=False)
     P.lib()
+    torch.cuda.set_device(torch.device("cuda", 0))
     if args.stack is not None:
         return stack_bench(args.stack, P, torch, args.flow, args.codec)
 
     cfg = inputs.CONFIGS[args.config]
-    x = inputs.layer_inputs(cfg, args.subrun)
-    k = int(x["k"])
-    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
-    es = 2 if cfg.dtype == "bf16" else 4
-    dev = torch.device("cuda", 0)
-    torch.cuda.set_device(dev)
-
-    def up(a):
-        if cfg.dtype == "bf16":
-            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
-        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
-
-    # working set of one copy; enough copies to exceed the Infinity Cache twice
-    ws_bytes = sum(x[n].nbytes for n in ("h_cur", "h_prev", "w_q", "w_k", "w_v", "logits")) \
-        + 2 * cfg.batch * cfg.seq * cfg.n_kv_heads * cfg.head_dim * es
-    copies = args.copies or max(1, -(-512 * 2 ** 20 // ws_bytes))
-    sets = []
-    for c in range(copies):
-        s = {n: up(x[n]) for n in ("h_cur", "h_prev", "w_q", "w_k", "w_v", "logits")}
-        s["k_cache"] = torch.empty((cfg.batch, cfg.seq, cfg.n_kv_heads, cfg.head_dim), dtype=dt, device=dev)
-        s["v_cache"] = torch.empty_like(s["k_cache"])
-        # prior cache = projection of the previous states (setup, untimed)
-        all_idx = torch.arange(cfg.seq, dtype=torch.int32, device=dev).repeat(cfg.batch, 1).contiguous()
-        all_cnt = torch.full((cfg.batch,), cfg.seq, dtype=torch.int32, device=dev)
-        P.refresh_kv(s["h_prev"], all_idx, all_cnt, cfg.block_start, 0, s["w_k"], s["w_v"],
-                     s["k_cache"], s["v_cache"])
-        s["masked"] = torch.from_numpy(x["masked"]).to(dev)
-        s["hist"] = torch.from_numpy(x["hist"].copy()).to(dev)
-        s["hist_len"] = torch.from_numpy(x["hist_len"].copy()).to(dev)
-        sets.append(s)
-    step = P.Step(batch=cfg.batch, seq=cfg.seq, d=cfg.d, n_heads=cfg.n_heads, n_kv_heads=cfg.n_kv_heads,
-                  head_dim=cfg.head_dim, block_start=cfg.block_start, block_len=cfg.block_len,
-                  vocab=cfg.vocab, k=k, dtype=dt, device=dev)
-    torch.cuda.synchronize()
-
-    stream = torch.cuda.current_stream()
-
-    def call(name, s):
-        sh = step.shape
-        if name == "drift":
-            P.drift(s["h_cur"], s["h_prev"], out=step.drift)
-        elif name == "select":
-            if k > 0:
-                P.select(step.drift, k, sh["block_start"], sh["block_len"], None, step.stale_idx, step.stale_count)
-        elif name == "refresh_kv":
-            P.refresh_kv(s["h_cur"], step.stale_idx, step.stale_count, sh["block_start"], sh["block_len"],
-                         s["w_k"], s["w_v"], s["k_cache"], s["v_cache"], workspace=step.ws_refresh)
-        elif name == "project_q":
-            P.project_q(s["h_cur"], s["w_q"], sh["block_start"], sh["block_len"], sh["n_heads"],
-                        out=step.q_buf, workspace=step.ws_q)
-        elif name == "attend":
-            P.attend(None, None, s["k_cache"], s["v_cache"], sh["block_start"], sh["block_len"],
-                     sh["n_heads"], q_buf=step.q_buf, out=step.out, lse=step.lse, workspace=step.ws_attend)
-        else:
-            P.commit(s["logits"], s["masked"], step.drift, sh["block_start"], s["hist"], s["hist_len"], -1,
-                     cfg.tau_s, cfg.alpha, False, step.token, step.conf, step.commit, workspace=step.ws_commit)
-
-    def run_serial(i, ev):
-        """One step with every call on the launch stream and events around
-        each (the per-call breakdown)."""
-        s = sets[i % copies]
-        for j, name in enumerate(CALLS):
-            ev[j].record(stream)
-            call(name, s)
-        ev[len(CALLS)].record(stream)
-
-    # the step as it runs in the timed region: polestar_step, with its
-    # arguments built once per input copy
-    prepared = [step.prepare(c["h_cur"], c["h_prev"], c["w_q"], c["w_k"], c["w_v"], c["k_cache"],
-                             c["v_cache"], c["logits"], c["masked"], c["hist"], c["hist_len"],
-                             tau_s=cfg.tau_s, alpha=cfg.alpha) for c in sets]
-
-    def run_step(i, ev=None):
-        step.launch(prepared[i % copies], ev)
+    L = Layer(P, torch, cfg, args.subrun, args.copies)
+    if args.counter_pass:
+        for i in range(3):
+            L.run_step(i)
+        L.counter_pass(args.counter_rounds)
+        print(json.dumps({"counter_pass": workload_name(cfg, args.subrun), "rounds": args.counter_rounds}))
+        return 0
+    k, es, stream = L.k, L.es, L.stream
 
     for i in range(args.warmup):
-        run_step(i)
+        L.run_step(i)
     torch.cuda.synchronize()
 
-    # diagnostic pass (untimed): the six calls one by one with events around
-    # each give the per-call breakdown
-    # each give the per-call breakdown.  A device-side spin enqueued first
-    # lets the host queue the whole pass ahead of the GPU, so the events time
-    # the kernels back to back rather than the Python launch path.
-    ndiag = max(1, min(args.steps, 50))
-    dev_events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(CALLS) + 1)] for _ in range(ndiag)]
-    torch.cuda.synchronize()
-    torch.cuda._sleep(100_000_000)
-    for i in range(ndiag):
-        run_serial(i, dev_events[i])
-    torch.cuda.synchronize()
-    call_us = {c: float(np.mean([ev[j].elapsed_time(ev[j + 1]) * 1e3 for ev in dev_events]))
-               for j, c in enumerate(CALLS)}
+    # per-call breakdown (untimed for the headline)
+    call_us = L.calls_us(max(1, min(args.steps, 50)))
     dom = "refresh_kv"   # the step's dominant launch group; polestar_step brackets it with events
 
     # timed region: K whole steps through polestar_step; its refresh launches
@@ -547,18 +813,18 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        run_step(args.warmup + i, events[i])
+        L.run_step(args.warmup + i, events[i])
     enqueued = time.perf_counter() - t0
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     dom_us = float(np.mean([ev[0].elapsed_time(ev[1]) * 1e3 for ev in events]))
 
-    proxy = measure_proxy(P, torch, cfg, sets[0], stream, es)
+    # per-step percentiles over at least 50 steps (after the timed region)
+    stats = L.step_stats(max(50, args.stats_steps), args.warmup + args.steps)
 
     tokens = cfg.batch * cfg.block_len
     value = tokens * args.steps / elapsed
-    cost = algorithmic_cost(cfg, k, es)
-    c = cost[dom]
+    c = L.cost[dom]
     flops_rate = c["flops"] / (dom_us * 1e-6) / 1e12
     bytes_rate = c["bytes"] / (dom_us * 1e-6) / 1e9
     peak_t = BF16_PEAK_TFLOPS if cfg.dtype == "bf16" else FP32_PEAK_TFLOPS
@@ -571,16 +837,7 @@ def main():
                 "frac": round(bytes_rate / HBM_PEAK_GBS, 4)}
     roof["kernel"] = dom
     roof["launch_us"] = round(dom_us, 3)
-    roof["traffic"] = traffic_for(dom, cfg.name)
-
-    calls = {}
-    for name in CALLS:
-        cc = cost[name]
-        t = call_us[name] * 1e-6
-        calls[name] = {"us": round(call_us[name], 3), "bytes": int(cc["bytes"]), "flops": int(cc["flops"]),
-                       "GB_s": round(cc["bytes"] / t / 1e9, 1),
-                       "hbm_frac": round(cc["bytes"] / t / 1e9 / HBM_PEAK_GBS, 4),
-                       "TFLOP_s": round(cc["flops"] / t / 1e12, 3)}
+    roof["traffic"] = traffic_for(dom, workload_name(cfg, args.subrun))
 
     out = {
         "metric": METRIC,
@@ -595,18 +852,28 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: single {'LLaDA-8B' if cfg.n_heads == cfg.n_kv_heads else 'Dream-7B'}"
+        "config": {"workload": f"{workload_name(cfg, args.subrun)}: single "
+                               f"{'LLaDA-8B' if cfg.n_heads == cfg.n_kv_heads else 'Dream-7B'}"
                                f"-shaped layer step, batch {cfg.batch}, seq {cfg.seq}, block {cfg.block_len}, "
                                f"d {cfg.d}, heads {cfg.n_heads}/{cfg.n_kv_heads}x{cfg.head_dim}, vocab {cfg.vocab}, "
                                f"{k} stale rows per sequence",
                    "global_batch": cfg.batch, "seq_len": cfg.seq, "block": cfg.block_len,
-                   "stale_rows": k, "input_copies": copies},
+                   "stale_rows": k, "input_copies": L.copies},
         "roofline": roof,
-        "proxy_drift": proxy,
+        "step_us": stats,
+        "tokens_per_s_median_step": round(tokens / (stats["median"] * 1e-6), 1),
         "host_enqueue_us_per_step": round(enqueued / args.steps * 1e6, 2),
-        "calls_us": calls,
+        "calls_us": L.calls_report(call_us),
     }
-    out["gather_scatter"] = measure_gather_scatter(P, torch, cfg, sets, step.stale_idx, step.stale_count, es)
+    out["proxy_drift"] = measure_proxy(P, torch, cfg, L.sets[0], stream, es)
+    out["gather_scatter"] = measure_gather_scatter(P, torch, cfg, L.sets, L.step.stale_idx, L.step.stale_count, es)
+    x = L.x
+    del L
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    out["copy_GB_s"] = copy_bandwidth(torch)
+    if not args.no_extras and args.config == 1:
+        out["extra_configs"] = {"llada8b_b8": layer_summary(P, torch, 2, 1), "dream7b_b4": layer_summary(P, torch, 3, 0)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, x, k, args.cpu_seconds)
     print(json.dumps(out))

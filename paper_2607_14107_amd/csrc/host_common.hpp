@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <cstring>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -12,7 +13,15 @@ namespace ps {
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-inline bool dtype_ok(polestar_dtype dt) { return dt == POLESTAR_FP32 || dt == POLESTAR_BF16; }
+// Whether a caller's dtype argument names a supported type.  Taken by
+// reference and read as an int: a C caller may pass any int, and in C++
+// loading an enum object that holds a value outside the enumerators' range is
+// undefined, so the value is checked before any enum-typed use.
+inline bool dtype_ok(const polestar_dtype& dt) {
+    int v;
+    std::memcpy(&v, &dt, sizeof v);
+    return v == POLESTAR_FP32 || v == POLESTAR_BF16;
+}
 
 inline size_t elem_bytes(polestar_dtype dt) { return dt == POLESTAR_BF16 ? 2 : 4; }
 

@@ -18,7 +18,9 @@ import os
 import torch
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libpolestar.so")
+# POLESTAR_LIB selects another build of the library (the host-sanitized one
+# of the CPU tests); by default the in-tree libpolestar.so.
+LIB_PATH = os.environ.get("POLESTAR_LIB") or os.path.join(PKG, "libpolestar.so")
 
 OK = 0
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "launch failed", 4: "workspace too small"}
