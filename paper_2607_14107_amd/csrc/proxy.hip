@@ -284,7 +284,9 @@ __global__ __launch_bounds__(kKmBlock) void kmeans_kernel(const char* __restrict
 //   |sum_{j in M} u_j|^2 = sum_{j, l in M} u_j . u_l.
 // kmeans_gram_kernel, one workgroup per sequence:
 //   1. G = (h_i . h_j) with MFMAs, the window rows staged in LDS 256 bytes of
-//      each row at a time (upper-triangle tiles, mirrored);
+//      each row at a time (upper-triangle tiles); G is symmetric and only its
+//      upper triangle is kept (row i holds j = i .. n-1), so windows of up to
+//      224 positions fit in LDS;
 //   2. the rounds on G_ij / (|h_i| |h_j|) and C, all in LDS: the cosines are
 //      G C^T and a new centroid's squared norm is the sum of G over its
 //      member pairs, both as small fp32 MFMA products (fixed order:
@@ -298,15 +300,14 @@ __global__ __launch_bounds__(kKmBlock) void kmeans_kernel(const char* __restrict
 
 constexpr int kGramBlock = 512;                 // 8 waves
 constexpr int kGramWaves = kGramBlock / kWave;
-constexpr int kGramMaxWin = 176;                // 11 row tiles: G fits in LDS
+constexpr int kGramMaxWin = 224;                // 14 row tiles: the upper triangle of G fits in LDS
 constexpr int kGramTiles = kGramMaxWin / 16;
 constexpr int kGramPairs = kGramTiles * (kGramTiles + 1) / 2;
 constexpr int kGramPairsPerWave = (kGramPairs + kGramWaves - 1) / kGramWaves;
 constexpr int kGramLda = 272;                   // staged row pitch (bytes): conflict-free fragments
-constexpr int kGramPitch = kGramMaxWin + 4;     // G row pitch (floats; 16-byte rows)
 constexpr int kGramRowsPerThread = (kGramMaxWin * 16 + kGramBlock - 1) / kGramBlock;
 constexpr int kGramStageBytes = 2 * kGramMaxWin * kGramLda;
-constexpr int kGramBytes = kGramMaxWin * kGramPitch * 4;
+constexpr int kGramBytes = kGramMaxWin * (kGramMaxWin + 1) / 2 * 4;   // upper triangle of G, fp32
 constexpr int kGramUnionBytes = kGramStageBytes > kGramBytes ? kGramStageBytes : kGramBytes;
 
 template <bool BF16>
@@ -332,6 +333,11 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
     const char* hb = h + static_cast<size_t>(b) * seq * d * ES;
     const int32_t* wi = win_idx + static_cast<size_t>(b) * n;
     float* G = reinterpret_cast<float*>(un);
+    // G[i][j] of the upper triangle (the pair ordered so that i <= j)
+    auto gidx = [n](int i, int j) {
+        const int lo = min(i, j), hi = max(i, j);
+        return lo * n - (lo * (lo - 1)) / 2 + (hi - lo);
+    };
     const int nt = (n + 15) / 16;
     const int npairs = nt * (nt + 1) / 2;
 
@@ -420,8 +426,7 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int gi = pti[r] * 16 + 4 * (lane >> 4) + i, gj = ptj[r] * 16 + (lane & 15);
-                G[gi * kGramPitch + gj] = acc[r][i];
-                if (pti[r] != ptj[r]) G[gj * kGramPitch + gi] = acc[r][i];   // a diagonal tile holds both halves
+                if (gi <= gj && gj < n) G[gidx(gi, gj)] = acc[r][i];   // a diagonal tile holds both halves
             }
         }
     }
@@ -429,13 +434,13 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
 
     // 2. rounds on the cosine Gram matrix
     for (int i = t; i < n; i += kGramBlock) {
-        const float g = G[i * kGramPitch + i];
+        const float g = G[gidx(i, i)];
         invn[i] = g > 0.f ? 1.0f / sqrtf(g) : 0.f;
     }
     __syncthreads();
     for (int e = t; e < n * n; e += kGramBlock) {
         const int i = e / n, j = e - i * n;
-        G[i * kGramPitch + j] = G[i * kGramPitch + j] * invn[i] * invn[j];
+        if (i <= j) G[gidx(i, j)] = G[gidx(i, j)] * invn[i] * invn[j];
     }
     // centroid k starts at the point of window rank floor(k n / K); C (all 16
     // rows) and the labels are padded with zeros / -1 to n4 = n rounded up to 4
@@ -455,7 +460,12 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
     auto gram_product = [&](int mode) {
         for (int tile = w; tile < nt; tile += kGramWaves) {
             const int i0 = tile * 16;
-            const float* gi = G + (i0 + (lane & 15)) * kGramPitch + (lane >> 4);
+            const int ia = i0 + (lane & 15);
+            // G[ia][j], zero past the window (padded rows and columns)
+            auto gi = [&](int j0) {
+                const int j = j0 + (lane >> 4);
+                return ia < n && j < n ? G[gidx(ia, j)] : 0.f;
+            };
             const int col = lane & 15;
             auto bval = [&](int j0) {
                 const int j = j0 + (lane >> 4);
@@ -465,11 +475,11 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
             floatx4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
             int j0 = 0;
             for (; j0 + 8 <= n4; j0 += 8) {
-                const float a0 = gi[j0], b0 = bval(j0), a1 = gi[j0 + 4], b1 = bval(j0 + 4);
+                const float a0 = gi(j0), b0 = bval(j0), a1 = gi(j0 + 4), b1 = bval(j0 + 4);
                 c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0, c0, 0, 0, 0);
                 c1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1, c1, 0, 0, 0);
             }
-            if (j0 < n4) c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(gi[j0], bval(j0), c0, 0, 0, 0);
+            if (j0 < n4) c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(gi(j0), bval(j0), c0, 0, 0, 0);
             const floatx4 c = c0 + c1;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {

@@ -81,11 +81,12 @@ def test_cluster_matches_oracle(P, dtype, batch, seq, d, K, block_start):
         np.testing.assert_allclose(z_g[b], z_o, rtol=0, atol=1e-5)
 
 
-@pytest.mark.parametrize("n_win", [150, 176, 177])
+@pytest.mark.parametrize("n_win", [150, 176, 177, 192, 224, 225])
 def test_cluster_window_sizes_match_oracle(P, n_win):
-    """Windows of up to 176 positions run the K-means on the window's Gram
-    matrix, longer ones directly on the rows; both match the oracle (ragged
-    tile counts, the largest Gram window, the first direct one)."""
+    """Windows of up to 224 positions run the K-means on the window's Gram
+    matrix (its upper triangle in LDS), longer ones directly on the rows; both
+    match the oracle (ragged tile counts, the largest Gram window, the first
+    direct one)."""
     torch = _torch()
     seq, d, K = 400, 512, 12
     g = np.random.default_rng(n_win)
@@ -96,6 +97,27 @@ def test_cluster_window_sizes_match_oracle(P, n_win):
     h = ref.decode(hs, "bf16")
     lab_g, sums_g, cnt_g, z_g = from_dev(labels), from_dev(sums), from_dev(counts), from_dev(cents)
     for b in range(2):
+        lab_o, z_o = pr.spherical_kmeans(h[b, win], K, iters=10)
+        s_o, c_o = pr.cluster_sums(h[b, win], lab_o, K)
+        assert np.array_equal(lab_g[b], pr.labels_by_position(win, lab_o, seq))
+        assert np.array_equal(cnt_g[b], c_o)
+        np.testing.assert_allclose(sums_g[b], s_o, rtol=1e-5, atol=1e-5 * np.abs(s_o).max())
+        np.testing.assert_allclose(z_g[b], z_o, rtol=0, atol=1e-5)
+
+
+def test_cluster_dream_shape_window_matches_oracle(P):
+    """The Dream-7B layer's block entry: batch 4, d 3584, K 8 over the window
+    of 2B = 128 positions before the 64-position block and B after (192)."""
+    torch = _torch()
+    seq, d, K, bs, bl = 2048, 3584, 8, 1536, 64
+    win = P.window_positions(seq, bs, bl, 2 * bl, bl)
+    assert len(win) == 192
+    hs, _ = planted_window(4, seq, d, win, K, "bf16", seed=77)
+    widx = torch.tensor([win] * 4, dtype=torch.int32, device="cuda")
+    labels, sums, counts, cents = P.cluster(to_dev(hs, "bf16"), widx, K, iters=10)
+    h = ref.decode(hs, "bf16")
+    lab_g, sums_g, cnt_g, z_g = from_dev(labels), from_dev(sums), from_dev(counts), from_dev(cents)
+    for b in range(4):
         lab_o, z_o = pr.spherical_kmeans(h[b, win], K, iters=10)
         s_o, c_o = pr.cluster_sums(h[b, win], lab_o, K)
         assert np.array_equal(lab_g[b], pr.labels_by_position(win, lab_o, seq))
