@@ -28,6 +28,7 @@ namespace {
 constexpr int kAttBlock = 256;   // 4 waves
 constexpr int kQG = 32;          // queries per workgroup
 constexpr int kKT = 32;          // keys per tile
+constexpr float kLazy = 8.f;     // log2 headroom of the lazy softmax reference
 
 struct AttArgs {
     const char* q;       // [batch][nq][H][hd]
@@ -189,12 +190,11 @@ __global__ __launch_bounds__(kAttBlock, 2) void attend_kernel(AttArgs a) {
                     const int slot = vslot(4 * kg);
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
-                        const int sh = (e & 1) * 16;
-                        const uint32_t k0 = (x0[e >> 1] >> sh) & 0xffffu;
-                        const uint32_t k1 = (x1[e >> 1] >> sh) & 0xffffu;
-                        const uint32_t k2 = (x2[e >> 1] >> sh) & 0xffffu;
-                        const uint32_t k3 = (x3[e >> 1] >> sh) & 0xffffu;
-                        uint2 pk = make_uint2(k0 | (k1 << 16), k2 | (k3 << 16));
+                        // d = 8 dc + e of the 4 keys: the low (e even) or high
+                        // (e odd) halves of word e / 2, two keys per byte permute
+                        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+                        const uint2 pk = make_uint2(__builtin_amdgcn_perm(x1[e >> 1], x0[e >> 1], sel),
+                                                    __builtin_amdgcn_perm(x3[e >> 1], x2[e >> 1], sel));
                         *reinterpret_cast<uint2*>(myvt + vrow(dc * 8 + e) * VP + slot * 2) = pk;
                     }
                 }
@@ -228,6 +228,20 @@ __global__ __launch_bounds__(kAttBlock, 2) void attend_kernel(AttArgs a) {
             if constexpr (BF16) {
                 if (tile + 4 < t_end) load_tile(tile + 4);
             }
+            // Keys past seq exist only in a partial last tile.
+            if (__builtin_expect(key0 + kKT > a.seq, 0)) {
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int u = 0; u < 2; ++u)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            if (key0 + 16 * t + 4 * g + i >= a.seq) st[t][u][i] = -INFINITY;
+            }
+            // Online softmax in base-2 units with a lazy exponent reference:
+            // the reference moves (and O, l are rescaled) only when some
+            // query's maximum exceeds it by more than kLazy, so exponents stay
+            // below 2^kLazy; (m, l, O) are exact for any reference.
             float p[2][2][4];   // [t][u][i]
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
@@ -235,40 +249,38 @@ __global__ __launch_bounds__(kAttBlock, 2) void attend_kernel(AttArgs a) {
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int key = key0 + 16 * t + 4 * g + i;
-                        const float s = key < a.seq ? st[t][u][i] * a.scale_log2 : -INFINITY;
-                        p[t][u][i] = s;
-                        mx = fmaxf(mx, s);
-                    }
+                    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, st[t][u][i]);
                 mx = fmaxf(mx, __shfl_xor(mx, 16));
                 mx = fmaxf(mx, __shfl_xor(mx, 32));
-                const float mnew = fmaxf(mrun[u], mx);
-                const float mref = mnew == -INFINITY ? 0.f : mnew;
-                const float alpha = fast_exp2(mrun[u] - mref);
+                const float mcand = fmaxf(mrun[u], mx * a.scale_log2);
+                const bool any = __builtin_amdgcn_ballot_w64(mcand > mrun[u] + kLazy) != 0;
+                const float alpha = any ? fast_exp2(mrun[u] - (mcand == -INFINITY ? 0.f : mcand)) : 1.f;
+                if (any) mrun[u] = mcand;
+                const float mref = mrun[u] == -INFINITY ? 0.f : mrun[u];
                 float sum = 0.f;
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const float e = fast_exp2(p[t][u][i] - mref);
+                        const float e = fast_exp2(fmaf(st[t][u][i], a.scale_log2, -mref));
                         p[t][u][i] = e;
                         sum += e;
                     }
                 sum += __shfl_xor(sum, 16);
                 sum += __shfl_xor(sum, 32);
-                lrun[u] = lrun[u] * alpha + sum;
-                mrun[u] = mnew;
+                lrun[u] = fmaf(lrun[u], alpha, sum);
+                if (any) {
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) o[dt][u] *= alpha;
+                    for (int dt = 0; dt < DT; ++dt) o[dt][u] *= alpha;
+                }
             }
             // O^T += V^T P^T
             if constexpr (BF16) {
                 uint4 pf[2];
 #pragma unroll
                 for (int u = 0; u < 2; ++u)
-                    pf[u] = make_uint4(pack_bf16x2(p[0][u][0], p[0][u][1]), pack_bf16x2(p[0][u][2], p[0][u][3]),
-                                       pack_bf16x2(p[1][u][0], p[1][u][1]), pack_bf16x2(p[1][u][2], p[1][u][3]));
+                    pf[u] = make_uint4(cvt_pk_bf16(p[0][u][0], p[0][u][1]), cvt_pk_bf16(p[0][u][2], p[0][u][3]),
+                                       cvt_pk_bf16(p[1][u][0], p[1][u][1]), cvt_pk_bf16(p[1][u][2], p[1][u][3]));
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) {
                     const uint4 va = *reinterpret_cast<const uint4*>(myvt + vrow(dt * 16 + (lane & 15)) * VP + g * 16);
@@ -507,10 +519,36 @@ __global__ __launch_bounds__(64 * NW) void attend_group_kernel(AttArgs a) {
     const int s_end = min(nsteps, s_begin + a.tiles_per_split);
 
     // Staging registers of one step: K chunks (16 B) and V units (4 keys x 2 d).
-    // Indices past the step are clamped on load and skipped on store; keys past
-    // seq read the last row (their scores are masked).
+    // Each thread's offsets inside a step are fixed: a step wholly inside the
+    // sequence loads from the step's first row plus them; the last step of a
+    // sequence whose length is not a multiple of 64 clamps its keys to the
+    // last row (their scores are masked).  Indices past the step are clamped
+    // on load and skipped on store.
+    uint32_t koff[KI], voff[VI];
+#pragma unroll
+    for (int i = 0; i < KI; ++i) {
+        const int c = min(tid + i * NT, KCH - 1);
+        koff[i] = static_cast<uint32_t>((c / (HD / 8)) * krow + (c % (HD / 8)) * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < VI; ++i) {
+        const int u = min(tid + i * NT, VU - 1);
+        voff[i] = static_cast<uint32_t>(4 * (u / (HD / 2)) * krow + (u % (HD / 2)) * 4);
+    }
     auto load_step = [&](int step, uint4 (&kr)[KI], uint32_t (&vr)[VI][4]) {
         const int key0 = step * kGKT;
+        if (key0 + kGKT <= a.seq) {
+            const char* kp = kbase + static_cast<size_t>(key0) * krow;
+            const char* vp = vbase + static_cast<size_t>(key0) * krow;
+#pragma unroll
+            for (int i = 0; i < KI; ++i) kr[i] = ld16(kp + koff[i]);
+#pragma unroll
+            for (int i = 0; i < VI; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    vr[i][j] = *reinterpret_cast<const uint32_t*>((vp + j * krow) + voff[i]);
+            return;
+        }
 #pragma unroll
         for (int i = 0; i < KI; ++i) {
             const int c = min(tid + i * NT, KCH - 1);
@@ -520,7 +558,7 @@ __global__ __launch_bounds__(64 * NW) void attend_group_kernel(AttArgs a) {
 #pragma unroll
         for (int i = 0; i < VI; ++i) {
             const int u = min(tid + i * NT, VU - 1);
-            const int dp = u % (HD / 2), kg = u / (HD / 2);   // kg: 4-key group 0..15
+            const int dp = u % (HD / 2), kg = u / (HD / 2);
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int key = min(key0 + 4 * kg + j, a.seq - 1);
@@ -541,10 +579,11 @@ __global__ __launch_bounds__(64 * NW) void attend_group_kernel(AttArgs a) {
             if (VU % NT == 0 || u < VU) {
                 const int dp = u % (HD / 2), kg = u / (HD / 2);
                 const int slot = gslot(kg);
-                const uint2 lo = make_uint2((vr[i][0] & 0xffffu) | (vr[i][1] << 16),
-                                            (vr[i][2] & 0xffffu) | (vr[i][3] << 16));
-                const uint2 hi = make_uint2((vr[i][0] >> 16) | (vr[i][1] & 0xffff0000u),
-                                            (vr[i][2] >> 16) | (vr[i][3] & 0xffff0000u));
+                // low halves (d = 2 dp) and high halves (d = 2 dp + 1) of the 4 keys
+                const uint2 lo = make_uint2(__builtin_amdgcn_perm(vr[i][1], vr[i][0], 0x05040100u),
+                                            __builtin_amdgcn_perm(vr[i][3], vr[i][2], 0x05040100u));
+                const uint2 hi = make_uint2(__builtin_amdgcn_perm(vr[i][1], vr[i][0], 0x07060302u),
+                                            __builtin_amdgcn_perm(vr[i][3], vr[i][2], 0x07060302u));
                 *reinterpret_cast<uint2*>(vs[buf] + (2 * dp) * VP + slot * 2) = lo;
                 *reinterpret_cast<uint2*>(vs[buf] + (2 * dp + 1) * VP + slot * 2) = hi;
             }
@@ -569,34 +608,43 @@ __global__ __launch_bounds__(64 * NW) void attend_group_kernel(AttArgs a) {
             }
             st[kt] = sacc;
         }
+        // Keys past seq exist only in a partial last step.
+        if (__builtin_expect(key0 + kGKT > a.seq, 0)) {
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                    if (key0 + 32 * kt + mfma32_row(lane, j) >= a.seq) st[kt][j] = -INFINITY;
+        }
+        // Online softmax in base-2 units: the maximum of the raw scores times
+        // the positive scale is the maximum of the scaled scores, and each
+        // exponent is one fma of the raw score.
         float mx = -INFINITY;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const int key = key0 + 32 * kt + mfma32_row(lane, j);
-                const float sv = key < a.seq ? st[kt][j] * a.scale_log2 : -INFINITY;
-                st[kt][j] = sv;
-                mx = fmaxf(mx, sv);
-            }
+            for (int j = 0; j < 16; ++j) mx = fmaxf(mx, st[kt][j]);
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mnew = fmaxf(mrun, mx);
-        const float mref = mnew == -INFINITY ? 0.f : mnew;
-        const float alpha = fast_exp2(mrun - mref);
+        const float mcand = fmaxf(mrun, mx * a.scale_log2);
+        const bool any = __builtin_amdgcn_ballot_w64(mcand > mrun + kLazy) != 0;
+        const float alpha = any ? fast_exp2(mrun - (mcand == -INFINITY ? 0.f : mcand)) : 1.f;
+        if (any) mrun = mcand;
+        const float mref = mrun == -INFINITY ? 0.f : mrun;
         float sum = 0.f;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
-                const float e = fast_exp2(st[kt][j] - mref);
+                const float e = fast_exp2(fmaf(st[kt][j], a.scale_log2, -mref));
                 st[kt][j] = e;
                 sum += e;
             }
         sum += __shfl_xor(sum, 32);
-        lrun = lrun * alpha + sum;
-        mrun = mnew;
+        lrun = fmaf(lrun, alpha, sum);
+        if (any) {
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+            for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+        }
         // O^T += V^T P^T over the four 16-key blocks: the B operand is
         // registers 8 kb' .. 8 kb' + 7 of st[kt] (kb' = block within the tile).
 #pragma unroll
@@ -604,10 +652,10 @@ __global__ __launch_bounds__(64 * NW) void attend_group_kernel(AttArgs a) {
 #pragma unroll
             for (int kb2 = 0; kb2 < 2; ++kb2) {
                 const int r = 8 * kb2;
-                const uint4 pf = make_uint4(pack_bf16x2(st[kt][r + 0], st[kt][r + 1]),
-                                            pack_bf16x2(st[kt][r + 2], st[kt][r + 3]),
-                                            pack_bf16x2(st[kt][r + 4], st[kt][r + 5]),
-                                            pack_bf16x2(st[kt][r + 6], st[kt][r + 7]));
+                const uint4 pf = make_uint4(cvt_pk_bf16(st[kt][r + 0], st[kt][r + 1]),
+                                            cvt_pk_bf16(st[kt][r + 2], st[kt][r + 3]),
+                                            cvt_pk_bf16(st[kt][r + 4], st[kt][r + 5]),
+                                            cvt_pk_bf16(st[kt][r + 6], st[kt][r + 7]));
                 const int soff = (32 * kt + 16 * kb2 + 8 * h32) * 2;
 #pragma unroll
                 for (int dt = 0; dt < DT; ++dt) {

@@ -34,6 +34,15 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
 }
 
+// Two finite floats to packed bf16 in one v_cvt_pk_bf16_f32 (round to nearest
+// even, the same bits as pack_bf16x2 for every non-NaN input; NaN keeps its
+// sign and payload instead of becoming 0x7fc0).
+typedef __bf16 bf16x2_hw __attribute__((ext_vector_type(2)));
+typedef float float2_hw __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((float2_hw){lo, hi}, bf16x2_hw));
+}
+
 // Storage traits: E = element count of one 16-byte chunk.
 template <bool BF16> struct Elem;
 template <> struct Elem<true> {

@@ -382,6 +382,44 @@ def test_attend_small_shapes_with_given_queries(P, dtype, batch, seq, bs, bl, H,
         assert_rows_close(ref.decode(from_dev(out), dtype), want, RTOL[dtype], "single key")
 
 
+@pytest.mark.parametrize("dtype,batch,seq,bl,H,Hkv,hd", [
+    ("bf16", 2, 700, 32, 4, 4, 128),     # one (head, query group) pair per KV head: attend_kernel
+    ("bf16", 2, 700, 64, 8, 2, 128),     # grouped-head kernel, 8 pairs per KV head
+    ("bf16", 1, 2100, 32, 6, 1, 64),     # grouped, many key splits
+    ("fp32", 1, 300, 20, 2, 1, 64),
+])
+def test_attend_late_dominant_keys(P, dtype, batch, seq, bl, H, Hkv, hd):
+    """Keys late in the sequence whose scores exceed everything before them:
+    one by about 4 nats (below the kernels' lazy rescale threshold of 8 in
+    log2 units, so probabilities above 1 are accumulated against the old
+    reference) and one by about 40 nats (the output and l are rescaled to a
+    new reference).  Queries share one direction per head so that every
+    query sees both jumps."""
+    g = np.random.default_rng(seq + 31 * H + hd)
+    u = g.standard_normal((batch, 1, H, hd)).astype(np.float32)
+    u /= np.linalg.norm(u, axis=-1, keepdims=True)
+    qf = 3.0 * u + 0.05 * g.standard_normal((batch, bl, H, hd)).astype(np.float32)
+    kf = 0.2 * g.standard_normal((batch, seq, Hkv, hd)).astype(np.float32)
+    vf = g.standard_normal((batch, seq, Hkv, hd)).astype(np.float32)
+    G = H // Hkv
+    ukv = u[:, 0].reshape(batch, Hkv, G, hd).mean(axis=2)             # the group's shared direction
+    ukv /= np.linalg.norm(ukv, axis=-1, keepdims=True)
+    # score = q.k / sqrt(hd) with |q| ~ 3: a key c * ukv scores about 3 c / sqrt(hd) * cos
+    mid, late = int(seq * 0.4), int(seq * 0.85)
+    kf[:, mid] = (4.0 * math.sqrt(hd) / 3.0) * ukv
+    kf[:, late] = (40.0 * math.sqrt(hd) / 3.0) * ukv
+    q, kc, vc = (inputs.store(a, dtype) for a in (qf, kf, vf))
+    torch = _torch()
+    lse = torch.empty((batch, H, bl), dtype=torch.float32, device="cuda")
+    out, _ = P.attend(None, None, to_dev(kc, dtype), to_dev(vc, dtype), 0, bl, H, q_buf=to_dev(q, dtype), lse=lse)
+    o_want, lse_want = ref.attend(ref.decode(q, dtype), ref.decode(kc, dtype), ref.decode(vc, dtype))
+    assert_rows_close(ref.decode(from_dev(out), dtype), o_want, RTOL[dtype], "output")
+    np.testing.assert_allclose(from_dev(lse), lse_want, rtol=RTOL[dtype], atol=RTOL[dtype])
+    # the dominant key carries almost all of the weight
+    vl = ref.decode(vc, dtype)[:, late][:, None, np.arange(H) // G]
+    assert np.abs(o_want - vl).max() < 0.1 * np.abs(vl).max()
+
+
 def test_attend_key_order_and_uniform_scores(P):
     torch = _torch()
     L = layer(1)
