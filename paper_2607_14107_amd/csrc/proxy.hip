@@ -310,15 +310,19 @@ constexpr int kGramStageBytes = 2 * kGramMaxWin * kGramLda;
 constexpr int kGramBytes = kGramMaxWin * (kGramMaxWin + 1) / 2 * 4;   // upper triangle of G, fp32
 constexpr int kGramUnionBytes = kGramStageBytes > kGramBytes ? kGramStageBytes : kGramBytes;
 
+// gin: G of every sequence already computed by kmeans_gram_tiles_kernel
+// (packed upper triangle, gstride floats apart), else null and phase 1 below
+// computes it.
 template <bool BF16>
 __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __restrict__ h, int seq, int d,
                                                                  const int32_t* __restrict__ win_idx, int n,
                                                                  int K, int iters, int32_t* __restrict__ labels_out,
                                                                  float* __restrict__ sums,
                                                                  int32_t* __restrict__ counts,
-                                                                 float* __restrict__ centroids) {
+                                                                 const float* __restrict__ gin, size_t gstride) {
     __shared__ __align__(16) char un[kGramUnionBytes];   // staging (phase 1), then G
-    __shared__ __align__(16) float cf[kMaxClusters][kGramMaxWin];   // C
+    // C; rows padded by four floats so that a 16-row column read hits 16 banks
+    __shared__ __align__(16) float cf[kMaxClusters][kGramMaxWin + 4];
     __shared__ float cosv[kGramMaxWin][kMaxClusters + 1];
     __shared__ float invn[kGramMaxWin];
     __shared__ float tsum[kGramMaxWin];
@@ -346,6 +350,10 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
     __syncthreads();
 
     // 1. Gram matrix.  Wave w owns the upper-triangle tile pairs w, w + 8, ...
+    if (gin) {
+        const float* gs = gin + static_cast<size_t>(b) * gstride;
+        for (int e = t; e < n * (n + 1) / 2; e += kGramBlock) G[e] = gs[e];
+    } else {
     int pti[kGramPairsPerWave], ptj[kGramPairsPerWave];
 #pragma unroll
     for (int r = 0; r < kGramPairsPerWave; ++r) {
@@ -430,6 +438,7 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
             }
         }
     }
+    }   // phase 1
     __syncthreads();
 
     // 2. rounds on the cosine Gram matrix
@@ -437,11 +446,8 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
         const float g = G[gidx(i, i)];
         invn[i] = g > 0.f ? 1.0f / sqrtf(g) : 0.f;
     }
-    __syncthreads();
-    for (int e = t; e < n * n; e += kGramBlock) {
-        const int i = e / n, j = e - i * n;
-        if (i <= j) G[gidx(i, j)] = G[gidx(i, j)] * invn[i] * invn[j];
-    }
+    // (the cosines G_ij / (|h_i| |h_j|) are formed as the rounds' registers are
+    // loaded below)
     // centroid k starts at the point of window rank floor(k n / K); C (all 16
     // rows) and the labels are padded with zeros / -1 to n4 = n rounded up to 4
     const int n4 = (n + 3) & ~3;
@@ -457,33 +463,64 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
     // the result of points i0 + 4 (l/16) + r, column l%16.
     //   mode 0: column k = C[k][.]            -> cosines of the points
     //   mode 1: column k = (label == k)        -> sum of G over the point's cluster
+    // The rounds never change G, so each wave keeps its tiles' A operands in
+    // registers (ga[tt][s] = cosine of points i0 + l%16 and 4 s + l/16, zero
+    // past the window) and every round reads only the columns from LDS.
+    constexpr int kWaveTiles = (kGramTiles + kGramWaves - 1) / kGramWaves;
+    constexpr int kSteps = kGramMaxWin / 4;        // four-column steps of a row
+    float ga[kWaveTiles][kSteps];
+#pragma unroll
+    for (int tt = 0; tt < kWaveTiles; ++tt) {
+        const int ia = (w + kGramWaves * tt) * 16 + (lane & 15);
+#pragma unroll
+        for (int st = 0; st < kSteps; ++st) {
+            const int j = 4 * st + (lane >> 4);
+            const int lo = min(ia, j), hi = max(ia, j);
+            ga[tt][st] = ia < n && j < n ? G[gidx(lo, hi)] * invn[lo] * invn[hi] : 0.f;
+        }
+    }
+    // Columns go in chunks of eight four-column steps: a chunk's eight LDS
+    // reads are issued together (addresses stay inside the arrays; steps past
+    // n4 read zero), then its MFMAs run on every tile of the wave.  Steps past
+    // the window multiply zeros, so the sums are those of the steps up to n4.
+    constexpr int kChunk = 8;
+    static_assert(kSteps % kChunk == 0, "whole chunks");
     auto gram_product = [&](int mode) {
-        for (int tile = w; tile < nt; tile += kGramWaves) {
-            const int i0 = tile * 16;
-            const int ia = i0 + (lane & 15);
-            // G[ia][j], zero past the window (padded rows and columns)
-            auto gi = [&](int j0) {
-                const int j = j0 + (lane >> 4);
-                return ia < n && j < n ? G[gidx(ia, j)] : 0.f;
-            };
-            const int col = lane & 15;
-            auto bval = [&](int j0) {
-                const int j = j0 + (lane >> 4);
-                return mode == 0 ? cf[col][j] : (lab[j] == col ? 1.f : 0.f);
-            };
-            // two interleaved chains (j0 = 0, 8, 16, ... and 4, 12, ...), then summed
-            floatx4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
-            int j0 = 0;
-            for (; j0 + 8 <= n4; j0 += 8) {
-                const float a0 = gi(j0), b0 = bval(j0), a1 = gi(j0 + 4), b1 = bval(j0 + 4);
-                c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0, b0, c0, 0, 0, 0);
-                c1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1, b1, c1, 0, 0, 0);
+        const int col = lane & 15;
+        // two interleaved chains per tile (even steps: j0 = 0, 8, 16, ...; odd
+        // steps: 4, 12, ...), then summed
+        floatx4 c0[kWaveTiles], c1[kWaveTiles];
+#pragma unroll
+        for (int tt = 0; tt < kWaveTiles; ++tt) c0[tt] = c1[tt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ch = 0; ch < kSteps / kChunk; ++ch) {
+            if (4 * kChunk * ch >= n4) break;
+            float bv[kChunk];
+#pragma unroll
+            for (int q = 0; q < kChunk; ++q) {
+                const int j = 4 * (kChunk * ch + q) + (lane >> 4);
+                const float v = mode == 0 ? cf[col][j] : (lab[j] == col ? 1.f : 0.f);
+                bv[q] = j < n4 ? v : 0.f;
             }
-            if (j0 < n4) c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(gi(j0), bval(j0), c0, 0, 0, 0);
-            const floatx4 c = c0 + c1;
+#pragma unroll
+            for (int tt = 0; tt < kWaveTiles; ++tt) {
+                if (w + kGramWaves * tt >= nt) break;
+#pragma unroll
+                for (int q = 0; q < kChunk; q += 2) {
+                    c0[tt] = __builtin_amdgcn_mfma_f32_16x16x4f32(ga[tt][kChunk * ch + q], bv[q], c0[tt], 0, 0, 0);
+                    c1[tt] = __builtin_amdgcn_mfma_f32_16x16x4f32(ga[tt][kChunk * ch + q + 1], bv[q + 1], c1[tt],
+                                                                  0, 0, 0);
+                }
+            }
+        }
+#pragma unroll
+        for (int tt = 0; tt < kWaveTiles; ++tt) {
+            const int tile = w + kGramWaves * tt;
+            if (tile >= nt) break;
+            const floatx4 c = c0[tt] + c1[tt];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int i = i0 + 4 * (lane >> 4) + r;
+                const int i = tile * 16 + 4 * (lane >> 4) + r;
                 if (i >= n || col >= K) continue;
                 if (mode == 0) cosv[i][col] = c[r];
                 else if (lab[i] == col) tsum[i] = c[r];
@@ -504,15 +541,23 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
         if (t < kMaxClusters) cnt_s[t] = 0;
         __syncthreads();
         if (it == iters) break;                          // the last round only assigns
-        // update: |sum of the members' directions|^2 = sum over member pairs of G
-        for (int i = t; i < n; i += kGramBlock) atomicAdd(&cnt_s[lab[i]], 1);
+        // update: |sum of the members' directions|^2 = sum over member pairs of
+        // G; a cluster's wave also counts its members
         gram_product(1);
         __syncthreads();
         for (int k = w; k < K; k += kGramWaves) {
             float s2 = 0.f;
-            for (int j = lane; j < n; j += kWave) s2 += lab[j] == k ? tsum[j] : 0.f;
+            int c = 0;
+            for (int j = lane; j < n; j += kWave) {
+                const bool m = lab[j] == k;
+                s2 += m ? tsum[j] : 0.f;
+                c += __popcll(__ballot(m));
+            }
             s2 = wave_sum(s2);
-            if (lane == 0) nrm[k] = s2;
+            if (lane == 0) {
+                nrm[k] = s2;
+                cnt_s[k] = c;
+            }
         }
         __syncthreads();
         // clusters with no member keep their centroid
@@ -538,6 +583,97 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
         stash[e] = cf[k][j];
     }
     for (int i = t; i < n; i += kGramBlock) stash[K * n + i] = invn[i];
+}
+
+// The Gram matrix of a window over many workgroups: one 32 x 32 block (bi,
+// bj), bi <= bj, of G per workgroup, its four waves one 16 x 16 tile each.
+// Every tile runs the MFMA chain of kmeans_gram_kernel's phase 1 (the same
+// staged fragments, stages and k order), so G is bit-identical; it is written
+// in the kernel's packed upper-triangle layout for kmeans_gram_kernel to load.
+constexpr int kGtBlock = 256;
+
+template <bool BF16>
+__global__ __launch_bounds__(kGtBlock) void kmeans_gram_tiles_kernel(const char* __restrict__ h, int seq, int d,
+                                                                     const int32_t* __restrict__ win_idx, int n,
+                                                                     float* __restrict__ gout, size_t gstride) {
+    using T = Elem<BF16>;
+    constexpr int ES = T::kBytes;
+    __shared__ __align__(16) char sa[2][64 * kGramLda];   // staged rows: 0..31 block bi, 32..63 block bj
+    const int b = blockIdx.y;
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const int nb = (n + 31) / 32;
+    int q = blockIdx.x, bi = 0;
+    while (q >= nb - bi) {
+        q -= nb - bi;
+        ++bi;
+    }
+    const int bj = bi + q;
+    const char* hb = h + static_cast<size_t>(b) * seq * d * ES;
+    const int32_t* wi = win_idx + static_cast<size_t>(b) * n;
+    // thread t moves 16-byte chunk t%16 of staged rows t/16 + 16 r; points
+    // past the window read the first window row and are stored as zeros
+    const char* srow[4];
+    bool live[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int sr = (t >> 4) + 16 * r;
+        const int pt = sr < 32 ? 32 * bi + sr : 32 * bj + sr - 32;
+        live[r] = pt < n;
+        const int pos = min(max(wi[live[r] ? pt : 0], 0), seq - 1);
+        srow[r] = hb + static_cast<size_t>(pos) * d * ES + (t & 15) * 16;
+    }
+    const int nstages = d * ES / 256;
+    auto load_stage = [&](int st, uint4 (&ra)[4]) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ra[r] = ld16(srow[r] + min(st, nstages - 1) * 256);
+    };
+    auto store_stage = [&](int buf, const uint4 (&ra)[4]) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+            st16(sa[buf] + ((t >> 4) + 16 * r) * kGramLda + (t & 15) * 16, live[r] ? ra[r] : zero16());
+    };
+    // wave w: rows 16 (w / 2) .. of block bi against rows 16 (w % 2) .. of block bj
+    const int frag = (lane & 15) * kGramLda + (lane >> 4) * 16;
+    const int aoff = 16 * (w >> 1) * kGramLda + frag, boff = (32 + 16 * (w & 1)) * kGramLda + frag;
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](int buf) {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            const uint4 a = *reinterpret_cast<const uint4*>(sa[buf] + aoff + 64 * p);
+            const uint4 bb = *reinterpret_cast<const uint4*>(sa[buf] + boff + 64 * p);
+            acc = Mma<BF16>::step(a, bb, acc);
+        }
+    };
+    uint4 q0[4], q1[4], q2[4];
+    load_stage(0, q0);
+    load_stage(1, q1);
+    load_stage(2, q2);
+    store_stage(0, q0);
+    __syncthreads();
+#define PS_GT_STEP(ST, Q_STORE, Q_LOAD)                                     \
+    {                                                                       \
+        const int st_ = (ST);                                               \
+        compute(st_ & 1);                                                   \
+        if (st_ + 1 < nstages) store_stage((st_ + 1) & 1, Q_STORE);         \
+        __syncthreads();                                                    \
+        load_stage(st_ + 3, Q_LOAD);                                        \
+    }
+    int sc = 0;
+    for (; sc + 3 <= nstages; sc += 3) {   // stage st sits in q(st % 3)
+        PS_GT_STEP(sc, q1, q0)
+        PS_GT_STEP(sc + 1, q2, q1)
+        PS_GT_STEP(sc + 2, q0, q2)
+    }
+    if (sc < nstages) PS_GT_STEP(sc, q1, q0)
+    if (sc + 1 < nstages) PS_GT_STEP(sc + 1, q2, q1)
+#undef PS_GT_STEP
+    // lane l holds G[gi0 + 4 (l/16) + i][gj0 + l%16]
+    float* gs = gout + static_cast<size_t>(b) * gstride;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int gi = 32 * bi + 16 * (w >> 1) + 4 * (lane >> 4) + i, gj = 32 * bj + 16 * (w & 1) + (lane & 15);
+        if (gi <= gj && gj < n) gs[gi * n - (gi * (gi - 1)) / 2 + (gj - gi)] = acc[i];
+    }
 }
 
 constexpr int kKmOutBlock = 64;                // output kernels: one wave, thread per 4 channels (many workgroups)
@@ -1020,16 +1156,29 @@ extern "C" polestar_status polestar_cluster(polestar_dtype dtype, int batch, int
     if (n_win <= kGramMaxWin && static_cast<long>(n_clusters) * d >= static_cast<long>(n_clusters + 1) * n_win) {
         const char* hc = static_cast<const char*>(h);
         const dim3 out_grid(ceil_div(d, 4 * kKmOutBlock), batch);
+        // windows longer than 64: G over many workgroups, held in the centroid
+        // output (free until kmeans_centroid_kernel) when it fits there
+        const size_t gstride = static_cast<size_t>(n_clusters) * d;
+        const bool tiles = n_win > 64 && gstride >= static_cast<size_t>(n_win) * (n_win + 1) / 2;
+        const float* gin = tiles ? centroids : nullptr;
+        const int nb = ceil_div(n_win, 32);
+        const dim3 tgrid(nb * (nb + 1) / 2, batch);
         if (dtype == POLESTAR_BF16) {
+            if (tiles)
+                hipLaunchKernelGGL((kmeans_gram_tiles_kernel<true>), tgrid, dim3(kGtBlock), 0, stream, hc, seq, d,
+                                   win_idx, n_win, centroids, gstride);
             hipLaunchKernelGGL((kmeans_gram_kernel<true>), dim3(batch), dim3(kGramBlock), 0, stream, hc, seq, d,
-                               win_idx, n_win, n_clusters, iters, labels, sums, counts, centroids);
+                               win_idx, n_win, n_clusters, iters, labels, sums, counts, gin, gstride);
             hipLaunchKernelGGL((kmeans_centroid_kernel<true>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq,
                                d, win_idx, n_win, n_clusters, sums, centroids);
             hipLaunchKernelGGL((kmeans_sum_kernel<true>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq, d,
                                win_idx, n_win, n_clusters, labels, sums);
         } else {
+            if (tiles)
+                hipLaunchKernelGGL((kmeans_gram_tiles_kernel<false>), tgrid, dim3(kGtBlock), 0, stream, hc, seq, d,
+                                   win_idx, n_win, centroids, gstride);
             hipLaunchKernelGGL((kmeans_gram_kernel<false>), dim3(batch), dim3(kGramBlock), 0, stream, hc, seq, d,
-                               win_idx, n_win, n_clusters, iters, labels, sums, counts, centroids);
+                               win_idx, n_win, n_clusters, iters, labels, sums, counts, gin, gstride);
             hipLaunchKernelGGL((kmeans_centroid_kernel<false>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq,
                                d, win_idx, n_win, n_clusters, sums, centroids);
             hipLaunchKernelGGL((kmeans_sum_kernel<false>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq, d,
