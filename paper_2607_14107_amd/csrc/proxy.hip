@@ -292,10 +292,11 @@ __global__ __launch_bounds__(kKmBlock) void kmeans_kernel(const char* __restrict
 //      member pairs, both as small fp32 MFMA products (fixed order:
 //      deterministic);
 //   3. labels and counts.
-// Then, over many workgroups (channel ranges), kmeans_centroid_kernel writes
-// the unit centroids sum_j C[k][j] u_j and kmeans_sum_kernel the raw sums
-// (points in order, as the direct kernel).  The rows are read three times
-// instead of twice per round.
+// Then, over many workgroups (channel ranges), kmeans_out_kernel writes
+// the unit centroids sum_j C[k][j] u_j and then the raw sums.  Windows of
+// more than 64 positions compute G itself over many workgroups first
+// (kmeans_gram_tiles_kernel, 32 x 32 blocks) and phase 1 only loads it.  The
+// rows are read a fixed number of times instead of twice per round.
 // ---------------------------------------------------------------------------
 
 constexpr int kGramBlock = 512;                 // 8 waves
@@ -575,7 +576,7 @@ __global__ __launch_bounds__(kGramBlock) void kmeans_gram_kernel(const char* __r
     for (int i = t; i < n; i += kGramBlock) labels_out[static_cast<size_t>(b) * seq + posw[i]] = lab[i];
     if (t < K) counts[static_cast<size_t>(b) * K + t] = cnt_s[t];
     // the final C and 1/|h_i| go to the caller's sums array (K*n + n <= K*d
-    // floats) for kmeans_centroid_kernel, which kmeans_sum_kernel then
+    // floats) for the centroid launch of kmeans_out_kernel, which its sum launch then
     // overwrites with the raw sums
     float* stash = sums + static_cast<size_t>(b) * K * d;
     for (int e = t; e < K * n; e += kGramBlock) {
@@ -676,46 +677,63 @@ __global__ __launch_bounds__(kGtBlock) void kmeans_gram_tiles_kernel(const char*
     }
 }
 
-constexpr int kKmOutBlock = 64;                // output kernels: one wave, thread per 4 channels (many workgroups)
 
-// Unit centroids z_k = sum_i C[k][i] h_i / |h_i| (points in order) from the
-// stash kmeans_gram_kernel leaves in the sums array.
-template <bool BF16>
-__global__ __launch_bounds__(kKmOutBlock) void kmeans_centroid_kernel(const char* __restrict__ h, int seq, int d,
-                                                                      const int32_t* __restrict__ win_idx, int n,
-                                                                      int K, const float* __restrict__ stash_all,
-                                                                      float* __restrict__ centroids) {
-    __shared__ float w_s[kMaxClusters][kGramMaxWin];   // C[k][i] / |h_i|
+// Per-cluster weighted sums of the window rows, 256 channels per workgroup
+// (a lane's four channels), for the Gram path's outputs:
+//   UNITC: the unit centroids z_k = sum_i C[k][i] h_i / |h_i|, from the stash
+//          kmeans_gram_kernel leaves in the sums array;
+//   else:  the raw sums of the final clusters (one-hot labels), written over
+//          the sums array (after the centroid launch has read the stash).
+// Wave w takes points w, w + 8, ... in order (loads of eight points issued
+// before any is used); the eight waves' sums are then added in wave order.
+constexpr int kKmOutWaves = 8;
+constexpr int kKmOutThreads = kKmOutWaves * 64;
+
+template <bool BF16, bool UNITC>
+__global__ __launch_bounds__(kKmOutThreads) void kmeans_out_kernel(const char* __restrict__ h, int seq, int d,
+                                                                  const int32_t* __restrict__ win_idx, int n, int K,
+                                                                  const float* __restrict__ stash_all,
+                                                                  const int32_t* __restrict__ labels,
+                                                                  float* __restrict__ out) {
+    __shared__ float w_s[UNITC ? kMaxClusters : 1][kGramMaxWin];   // C[k][i] / |h_i|
+    __shared__ int lab_s[kGramMaxWin];
     __shared__ int pos_s[kGramMaxWin];
+    __shared__ float4 red[kKmOutWaves - 1][kMaxClusters][64];
     constexpr int ES = Elem<BF16>::kBytes;
     const int b = blockIdx.y;
-    const int t = threadIdx.x;
-    const float* stash = stash_all + static_cast<size_t>(b) * K * d;
-    for (int e = t; e < K * n; e += kKmOutBlock) {
-        const int k = e / n, i = e - k * n;
-        w_s[k][i] = stash[e] * stash[K * n + i];
-    }
-    for (int i = t; i < n; i += kKmOutBlock)
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    for (int i = t; i < n; i += kKmOutThreads) {
         pos_s[i] = min(max(win_idx[static_cast<size_t>(b) * n + i], 0), seq - 1);
+        if (!UNITC) lab_s[i] = labels[static_cast<size_t>(b) * seq + pos_s[i]];
+    }
+    if constexpr (UNITC) {
+        const float* stash = stash_all + static_cast<size_t>(b) * K * d;
+        for (int e = t; e < K * n; e += kKmOutThreads) {
+            const int k = e / n, i = e - k * n;
+            w_s[k][i] = stash[e] * stash[K * n + i];
+        }
+    }
     __syncthreads();
-    const int c = (blockIdx.x * kKmOutBlock + t) * 4;
-    if (c >= d) return;
+    const int c = min((blockIdx.x * 64 + lane) * 4, d - 4);   // lanes past d repeat the last quad, never stored
     const char* hb = h + static_cast<size_t>(b) * seq * d * ES;
     float4 acc[kMaxClusters];
 #pragma unroll
     for (int k = 0; k < kMaxClusters; ++k) acc[k] = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int i0 = 0; i0 < n; i0 += 16) {     // loads of 16 points issued before any is used
-        float4 v[16];
+    constexpr int kBatch = 8;
+    for (int i0 = w; i0 < n; i0 += kBatch * kKmOutWaves) {
+        float4 v[kBatch];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = load4<BF16>(hb + static_cast<size_t>(pos_s[min(i0 + u, n - 1)]) * d * ES, c);
+        for (int u = 0; u < kBatch; ++u)
+            v[u] = load4<BF16>(hb + static_cast<size_t>(pos_s[min(i0 + kKmOutWaves * u, n - 1)]) * d * ES, c);
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const int i = i0 + u;
+        for (int u = 0; u < kBatch; ++u) {
+            const int i = i0 + kKmOutWaves * u;
             if (i >= n) break;
+            const int li = UNITC ? 0 : lab_s[i];
 #pragma unroll
             for (int k = 0; k < kMaxClusters; ++k) {
                 if (k < K) {
-                    const float wk = w_s[k][i];
+                    const float wk = UNITC ? w_s[k][i] : (li == k ? 1.f : 0.f);
                     acc[k].x = fmaf(v[u].x, wk, acc[k].x);
                     acc[k].y = fmaf(v[u].y, wk, acc[k].y);
                     acc[k].z = fmaf(v[u].z, wk, acc[k].z);
@@ -724,36 +742,27 @@ __global__ __launch_bounds__(kKmOutBlock) void kmeans_centroid_kernel(const char
             }
         }
     }
+    if (w > 0) {
 #pragma unroll
-    for (int k = 0; k < kMaxClusters; ++k)
-        if (k < K) *reinterpret_cast<float4*>(centroids + (static_cast<size_t>(b) * K + k) * d + c) = acc[k];
-}
-
-// Raw sums of the final clusters (points in order, as the direct kernel).
-template <bool BF16>
-__global__ __launch_bounds__(kKmOutBlock) void kmeans_sum_kernel(const char* __restrict__ h, int seq, int d,
-                                                                 const int32_t* __restrict__ win_idx, int n, int K,
-                                                                 const int32_t* __restrict__ labels,
-                                                                 float* __restrict__ sums) {
-    __shared__ int lab_s[kGramMaxWin];
-    __shared__ int32_t pos_s[kGramMaxWin];
-    __shared__ float inv_unused[1];
-    const int b = blockIdx.y;
-    const int t = threadIdx.x;
-    const int32_t* wi = win_idx + static_cast<size_t>(b) * n;
-    for (int i = t; i < n; i += kKmOutBlock) {
-        pos_s[i] = min(max(wi[i], 0), seq - 1);
-        lab_s[i] = labels[static_cast<size_t>(b) * seq + pos_s[i]];
+        for (int k = 0; k < kMaxClusters; ++k)
+            if (k < K) red[w - 1][k][lane] = acc[k];
     }
     __syncthreads();
-    const int c = (blockIdx.x * kKmOutBlock + t) * 4;
-    if (c >= d) return;
-    float4 acc[kMaxClusters];
-    quad_sums<BF16, false>(h + static_cast<size_t>(b) * seq * d * Elem<BF16>::kBytes, pos_s, seq, n, d, c,
-                           inv_unused, lab_s, acc);
+    if (w > 0 || (blockIdx.x * 64 + lane) * 4 >= d) return;
 #pragma unroll
-    for (int k = 0; k < kMaxClusters; ++k)
-        if (k < K) *reinterpret_cast<float4*>(sums + (static_cast<size_t>(b) * K + k) * d + c) = acc[k];
+    for (int k = 0; k < kMaxClusters; ++k) {
+        if (k >= K) continue;
+        float4 s = acc[k];
+#pragma unroll
+        for (int ww = 0; ww < kKmOutWaves - 1; ++ww) {
+            const float4 r = red[ww][k][lane];
+            s.x += r.x;
+            s.y += r.y;
+            s.z += r.z;
+            s.w += r.w;
+        }
+        *reinterpret_cast<float4*>(out + (static_cast<size_t>(b) * K + k) * d + c) = s;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1155,9 +1164,9 @@ extern "C" polestar_status polestar_cluster(polestar_dtype dtype, int batch, int
     // the Gram path stashes (K + 1) * n_win floats in each sequence's K * d sums
     if (n_win <= kGramMaxWin && static_cast<long>(n_clusters) * d >= static_cast<long>(n_clusters + 1) * n_win) {
         const char* hc = static_cast<const char*>(h);
-        const dim3 out_grid(ceil_div(d, 4 * kKmOutBlock), batch);
+        const dim3 out_grid(ceil_div(d, 256), batch);
         // windows longer than 64: G over many workgroups, held in the centroid
-        // output (free until kmeans_centroid_kernel) when it fits there
+        // output (free until the centroid launch) when it fits there
         const size_t gstride = static_cast<size_t>(n_clusters) * d;
         const bool tiles = n_win > 64 && gstride >= static_cast<size_t>(n_win) * (n_win + 1) / 2;
         const float* gin = tiles ? centroids : nullptr;
@@ -1169,20 +1178,20 @@ extern "C" polestar_status polestar_cluster(polestar_dtype dtype, int batch, int
                                    win_idx, n_win, centroids, gstride);
             hipLaunchKernelGGL((kmeans_gram_kernel<true>), dim3(batch), dim3(kGramBlock), 0, stream, hc, seq, d,
                                win_idx, n_win, n_clusters, iters, labels, sums, counts, gin, gstride);
-            hipLaunchKernelGGL((kmeans_centroid_kernel<true>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq,
-                               d, win_idx, n_win, n_clusters, sums, centroids);
-            hipLaunchKernelGGL((kmeans_sum_kernel<true>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq, d,
-                               win_idx, n_win, n_clusters, labels, sums);
+            hipLaunchKernelGGL((kmeans_out_kernel<true, true>), out_grid, dim3(kKmOutThreads), 0, stream, hc,
+                               seq, d, win_idx, n_win, n_clusters, sums, labels, centroids);
+            hipLaunchKernelGGL((kmeans_out_kernel<true, false>), out_grid, dim3(kKmOutThreads), 0, stream, hc,
+                               seq, d, win_idx, n_win, n_clusters, sums, labels, sums);
         } else {
             if (tiles)
                 hipLaunchKernelGGL((kmeans_gram_tiles_kernel<false>), tgrid, dim3(kGtBlock), 0, stream, hc, seq, d,
                                    win_idx, n_win, centroids, gstride);
             hipLaunchKernelGGL((kmeans_gram_kernel<false>), dim3(batch), dim3(kGramBlock), 0, stream, hc, seq, d,
                                win_idx, n_win, n_clusters, iters, labels, sums, counts, gin, gstride);
-            hipLaunchKernelGGL((kmeans_centroid_kernel<false>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq,
-                               d, win_idx, n_win, n_clusters, sums, centroids);
-            hipLaunchKernelGGL((kmeans_sum_kernel<false>), out_grid, dim3(kKmOutBlock), 0, stream, hc, seq, d,
-                               win_idx, n_win, n_clusters, labels, sums);
+            hipLaunchKernelGGL((kmeans_out_kernel<false, true>), out_grid, dim3(kKmOutThreads), 0, stream, hc,
+                               seq, d, win_idx, n_win, n_clusters, sums, labels, centroids);
+            hipLaunchKernelGGL((kmeans_out_kernel<false, false>), out_grid, dim3(kKmOutThreads), 0, stream, hc,
+                               seq, d, win_idx, n_win, n_clusters, sums, labels, sums);
         }
         return launch_status();
     }
