@@ -80,7 +80,7 @@ __device__ __forceinline__ void scan_body(const char* __restrict__ logits, int v
         for (int gq = 0; gq < G; ++gq) {
             const int c = c0 + gq * kScanBlock + threadIdx.x;
             ok[gq] = c < nchunks;
-            r[gq] = ld16(row + static_cast<size_t>(v0 + (ok[gq] ? c : 0) * T::E) * ES);
+            r[gq] = ld16_nt(row + static_cast<size_t>(v0 + (ok[gq] ? c : 0) * T::E) * ES);   // read once
         }
         __builtin_amdgcn_sched_barrier(0);   // all G loads in flight before any use
         float lm = -INFINITY;

@@ -69,6 +69,14 @@ template <> struct Elem<false> {
 __device__ __forceinline__ uint4 ld16(const void* p) {
     return *reinterpret_cast<const uint4*>(p);
 }
+// A 16-byte load of data read once per call (weights of a single row tile,
+// previous hidden states, logits): marked non-temporal so that the stream
+// does not push the caches and the rows the step reuses out of L2 and the
+// Infinity Cache.
+typedef unsigned int u32x4_nt __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld16_nt(const void* p) {
+    return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4_nt*>(p)));
+}
 __device__ __forceinline__ void st16(void* p, const uint4& v) {
     *reinterpret_cast<uint4*>(p) = v;
 }

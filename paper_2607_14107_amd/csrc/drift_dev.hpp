@@ -93,8 +93,8 @@ __device__ __forceinline__ void drift_body(const char* __restrict__ hc, const ch
     for (int c = 0; c < NCH; ++c) {
         const int ch = c * TPR + tr;
         const size_t off = base + static_cast<size_t>(ch < chunks ? ch : 0) * 16;
-        ra[c] = ld16(hc + off);
-        rb[c] = ld16(hp + off);
+        ra[c] = ld16_nt(hc + off);   // both rows are read once per call
+        rb[c] = ld16_nt(hp + off);
     }
     __builtin_amdgcn_sched_barrier(0);    // every load in flight before any use
 #pragma unroll

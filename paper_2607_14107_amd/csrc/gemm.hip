@@ -243,9 +243,9 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_rows_kernel(GemmArgs g) {
 // gemm_dma_kernel: the DMA-staged body of gemm_dev.hpp (dma_body).
 // ---------------------------------------------------------------------------
 
-template <bool BF16, int MT, int NST>
+template <bool BF16, int MT, int NST, bool NTW>
 __global__ __launch_bounds__(kGemmBlock) void gemm_dma_kernel(GemmArgs g) {
-    dma_body<BF16, MT, NST>(g, blockIdx.x);
+    dma_body<BF16, MT, NST, 4, NTW>(g, blockIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -515,19 +515,19 @@ bool dispatch_rows(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
     }
 }
 
-template <bool BF16, int NST>
+template <bool BF16, int NST, bool NTW>
 bool dispatch_dma_mt(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
     const dim3 grid(p.grid), block(kGemmBlock);
     switch (p.mt) {   // 16-row tiles
-        case 2: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 2, NST>), grid, block, 0, s, g); return true;
-        case 3: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 3, NST>), grid, block, 0, s, g); return true;
-        case 4: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 4, NST>), grid, block, 0, s, g); return true;
-        case 5: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 5, NST>), grid, block, 0, s, g); return true;
-        case 6: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 6, NST>), grid, block, 0, s, g); return true;
-        case 7: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 7, NST>), grid, block, 0, s, g); return true;
-        case 8: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 8, NST>), grid, block, 0, s, g); return true;
-        case 9: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 9, NST>), grid, block, 0, s, g); return true;
-        case 10: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 10, NST>), grid, block, 0, s, g); return true;
+        case 2: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 2, NST, NTW>), grid, block, 0, s, g); return true;
+        case 3: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 3, NST, NTW>), grid, block, 0, s, g); return true;
+        case 4: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 4, NST, NTW>), grid, block, 0, s, g); return true;
+        case 5: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 5, NST, NTW>), grid, block, 0, s, g); return true;
+        case 6: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 6, NST, NTW>), grid, block, 0, s, g); return true;
+        case 7: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 7, NST, NTW>), grid, block, 0, s, g); return true;
+        case 8: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 8, NST, NTW>), grid, block, 0, s, g); return true;
+        case 9: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 9, NST, NTW>), grid, block, 0, s, g); return true;
+        case 10: hipLaunchKernelGGL((gemm_dma_kernel<BF16, 10, NST, NTW>), grid, block, 0, s, g); return true;
         default: return false;
     }
 }
@@ -535,12 +535,23 @@ bool dispatch_dma_mt(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
 template <bool BF16>
 bool dispatch_dma(const GemmPlan& p, const GemmArgs& g, hipStream_t s) {
     static_assert(kDmaMaxRowTiles == 10, "dispatch covers 2..kDmaMaxRowTiles");
-    switch (2 * p.steps_per_split) {   // 128-byte stages per split
-        case 8: return dispatch_dma_mt<BF16, 8>(p, g, s);
-        case 10: return dispatch_dma_mt<BF16, 10>(p, g, s);
-        case 12: return dispatch_dma_mt<BF16, 12>(p, g, s);
-        case 14: return dispatch_dma_mt<BF16, 14>(p, g, s);
-        case 16: return dispatch_dma_mt<BF16, 16>(p, g, s);
+    // one row tile reads every weight byte once: non-temporal weight stream
+    if (p.row_tiles == 1) {
+        switch (2 * p.steps_per_split) {   // 128-byte stages per split
+            case 8: return dispatch_dma_mt<BF16, 8, true>(p, g, s);
+            case 10: return dispatch_dma_mt<BF16, 10, true>(p, g, s);
+            case 12: return dispatch_dma_mt<BF16, 12, true>(p, g, s);
+            case 14: return dispatch_dma_mt<BF16, 14, true>(p, g, s);
+            case 16: return dispatch_dma_mt<BF16, 16, true>(p, g, s);
+            default: return false;
+        }
+    }
+    switch (2 * p.steps_per_split) {
+        case 8: return dispatch_dma_mt<BF16, 8, false>(p, g, s);
+        case 10: return dispatch_dma_mt<BF16, 10, false>(p, g, s);
+        case 12: return dispatch_dma_mt<BF16, 12, false>(p, g, s);
+        case 14: return dispatch_dma_mt<BF16, 14, false>(p, g, s);
+        case 16: return dispatch_dma_mt<BF16, 16, false>(p, g, s);
         default: return false;
     }
 }

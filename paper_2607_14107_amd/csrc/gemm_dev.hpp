@@ -220,6 +220,11 @@ constexpr int kDmaMaxRowTiles = 10;          // 160 rows
 __device__ __forceinline__ void dma16(const void* src, void* lds_base) {
     __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
 }
+// The same transfer marked non-temporal (cache policy nt): for weights that a
+// single row tile reads once.
+__device__ __forceinline__ void dma16_nt(const void* src, void* lds_base) {
+    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 2);
+}
 
 // s_waitcnt immediates (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt
 // 6:4, lgkmcnt 11:8): wait until at most n vector-memory operations of this
@@ -231,8 +236,11 @@ constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
 __device__ __forceinline__ int dma_swz(int r, int c) { return r * kDmaStage + ((c ^ ((r >> 1) & 7)) << 4); }
 
 // NS: LDS slots per operand (4: three stages in flight; 3: two, for a
-// workgroup that must share its compute unit).
-template <bool BF16, int MT, int NST, int NS = 4>
+// workgroup that must share its compute unit).  NTW: the plan has one row
+// tile, so every weight byte is read once and its DMA is marked non-temporal
+// (a compile-time choice: a branch inside the unrolled stage loop costs more
+// than the hint saves).
+template <bool BF16, int MT, int NST, int NS = 4, bool NTW = false>
 __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
     static_assert(NS == 3 || NS == 4, "three or four LDS slots");
     using T = Elem<BF16>;
@@ -272,8 +280,10 @@ __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
     auto issue_b = [&](int st, char* buf) {
         const int off = min(st, nst_here - 1) * kDmaStage;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            dma16(bsrc[i] + off, buf + (32 * w + 8 * i) * kDmaStage);
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (NTW) dma16_nt(bsrc[i] + off, buf + (32 * w + 8 * i) * kDmaStage);
+            else dma16(bsrc[i] + off, buf + (32 * w + 8 * i) * kDmaStage);
+        }
     };
     // Row bookkeeping (one load per row); the first workgroup publishes the
     // map for the split-K reduction.

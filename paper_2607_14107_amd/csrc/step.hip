@@ -96,7 +96,9 @@ __global__ __launch_bounds__(kStepBlock) void front_dma_kernel(FrontArgs f) {
         select_body<IPT>(f.drift, f.elig, f.seq, f.bs, f.bl, f.k, f.idx, f.cnt, vb);
         return;
     }
-    dma_body<true, MT, NST, 3>(f.q, vb - f.n_sel);   // three slots: the select workgroup shares a CU
+    // three slots: the select workgroup shares a CU; one row tile, so the
+    // weight stream is non-temporal
+    dma_body<true, MT, NST, 3, true>(f.q, vb - f.n_sel);
 }
 
 struct ReduceArgs {
