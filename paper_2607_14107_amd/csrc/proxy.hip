@@ -859,6 +859,9 @@ __global__ __launch_bounds__(kQkBlock) void qkl_kernel(QklArgs a) {
     const int t1 = min(ntiles, t0 + a.tiles_per_split);
     const size_t krow = static_cast<size_t>(a.Hkv) * HD * ES;
     const char* kbase = a.kc + (static_cast<size_t>(b) * a.S * a.Hkv + kvh) * HD * ES;
+    // with S a multiple of 16 (and 16-byte aligned scores) every tile is whole
+    // and the lane's four scores load and store as one float4
+    const bool full = (a.S & 15) == 0 && (reinterpret_cast<uintptr_t>(a.scores) & 15) == 0;
     for (int tb = t0 + w; tb < t1; tb += kQkWaves * TB) {
         // every load of this round first: key fragments of TB tiles and the
         // previous scores the lane will fold in (clamped, unused when invalid)
@@ -874,8 +877,16 @@ __global__ __launch_bounds__(kQkBlock) void qkl_kernel(QklArgs a) {
             for (int rt = 0; rt < RT; ++rt) {
                 const int r = min(16 * rt + li, a.R - 1);
                 const float* srow = a.scores + ((static_cast<size_t>(b) * a.R + r) * a.H + h) * a.S;
+                if (full) {   // the lane's four scores in one 16-byte load
+                    const float4 v = *reinterpret_cast<const float4*>(srow + tile * 16 + 4 * g);
+                    sp[u][rt][0] = v.x;
+                    sp[u][rt][1] = v.y;
+                    sp[u][rt][2] = v.z;
+                    sp[u][rt][3] = v.w;
+                } else {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) sp[u][rt][i] = srow[min(tile * 16 + 4 * g + i, a.S - 1)];
+                    for (int i = 0; i < 4; ++i) sp[u][rt][i] = srow[min(tile * 16 + 4 * g + i, a.S - 1)];
+                }
             }
         }
 #pragma unroll
@@ -908,9 +919,11 @@ __global__ __launch_bounds__(kQkBlock) void qkl_kernel(QklArgs a) {
                             const float e = __expf(sv[i] - mx);
                             z += e;
                             ww = fmaf(e, sv[i] - sp[u][rt][i], ww);
-                            srow[tile * 16 + 4 * g + i] = sv[i];
+                            if (!full) srow[tile * 16 + 4 * g + i] = sv[i];
                         }
                     }
+                    if (full && r < a.R)
+                        *reinterpret_cast<float4*>(srow + tile * 16 + 4 * g) = make_float4(sv[0], sv[1], sv[2], sv[3]);
                     pm[rt] = mx;
                     pz[rt] = z;
                     pw[rt] = ww;
