@@ -105,6 +105,31 @@ def test_cluster_window_sizes_match_oracle(P, n_win):
         np.testing.assert_allclose(z_g[b], z_o, rtol=0, atol=1e-5)
 
 
+@pytest.mark.parametrize("n_win", [48, 65, 97, 177, 224])
+def test_cluster_gram_over_workgroups_matches_oracle(P, n_win):
+    """Windows longer than 64 positions whose packed Gram matrix fits the
+    centroid output (K d >= n (n + 1) / 2) compute G over many workgroups in
+    32 x 32 blocks (ragged last block row and column); 48 positions stay on
+    the single-workgroup product."""
+    torch = _torch()
+    seq, d, K = 600, 2048, 16
+    assert K * d >= n_win * (n_win + 1) // 2
+    g = np.random.default_rng(1000 + n_win)
+    win = sorted(g.choice(seq, size=n_win, replace=False).tolist())
+    hs, _ = planted_window(2, seq, d, win, K, "bf16", seed=2000 + n_win)
+    widx = torch.tensor([win, win], dtype=torch.int32, device="cuda")
+    labels, sums, counts, cents = P.cluster(to_dev(hs, "bf16"), widx, K, iters=10)
+    h = ref.decode(hs, "bf16")
+    lab_g, sums_g, cnt_g, z_g = from_dev(labels), from_dev(sums), from_dev(counts), from_dev(cents)
+    for b in range(2):
+        lab_o, z_o = pr.spherical_kmeans(h[b, win], K, iters=10)
+        s_o, c_o = pr.cluster_sums(h[b, win], lab_o, K)
+        assert np.array_equal(lab_g[b], pr.labels_by_position(win, lab_o, seq))
+        assert np.array_equal(cnt_g[b], c_o)
+        np.testing.assert_allclose(sums_g[b], s_o, rtol=1e-5, atol=1e-5 * np.abs(s_o).max())
+        np.testing.assert_allclose(z_g[b], z_o, rtol=0, atol=1e-5)
+
+
 def test_cluster_dream_shape_window_matches_oracle(P):
     """The Dream-7B layer's block entry: batch 4, d 3584, K 8 over the window
     of 2B = 128 positions before the 64-position block and B after (192)."""
