@@ -15,9 +15,11 @@
 // Six launches instead of eleven kernels on their own.  Workgroups of a
 // fused launch take their role from their block index; each role is the
 // device body the stand-alone kernel runs, so results are bit-identical to
-// calling the six entry points in order.  With more than 64 query rows or
-// more than 2048 positions, select and the Q projection run as two launches
-// of their own (seven in all); shapes outside the other fused kernels
+// calling the six entry points in order.  With more than 2048 positions, or
+// a Q projection other than one DMA row tile of up to 64 rows or two of 128
+// whose grid leaves room for select's workgroups in one round, select and
+// the Q projection run as two launches of their own (seven in all); shapes
+// outside the other fused kernels
 // (blocks longer than 256, head_dim other than 64/128, rows above the
 // drift kernel's) run exactly the sequence of entry points instead.
 #include "attend_dev.hpp"
@@ -31,6 +33,7 @@ namespace ps {
 namespace {
 
 constexpr int kStepBlock = 256;
+constexpr long kCus = 256;   // compute units of MI355X: one round of one workgroup each
 static_assert(kSelBlock == kStepBlock && kSmallBlock == kStepBlock && kScanBlock == kStepBlock &&
                   kAttBlock == kStepBlock && kDriftBlock == kStepBlock && kGemmBlock == kStepBlock,
               "fused roles share one workgroup size");
@@ -86,19 +89,20 @@ __global__ __launch_bounds__(kStepBlock) void front_kernel(FrontArgs f) {
 }
 
 // select | Q projection on the DMA-staged kernel (bf16; split-K partials
-// reduced in launch 4).  With three LDS slots two workgroups fit per
-// compute unit, so the select workgroups do not push the Q projection's
-// one-per-CU grid into a second round.
-template <int IPT, int MT, int NST>
+// reduced in launch 4).  With three LDS slots two workgroups of up to four
+// 16-row tiles fit per compute unit, so the select workgroups do not push the
+// Q projection's one-per-CU grid into a second round; the 256-row block
+// projections (two row tiles of eight) run one workgroup per CU and are fused
+// only when the whole grid fits one round.  NTW: one row tile, so the weight
+// stream is non-temporal.
+template <int IPT, int MT, int NST, bool NTW>
 __global__ __launch_bounds__(kStepBlock) void front_dma_kernel(FrontArgs f) {
     const int vb = blockIdx.x;
     if (vb < f.n_sel) {
         select_body<IPT>(f.drift, f.elig, f.seq, f.bs, f.bl, f.k, f.idx, f.cnt, vb);
         return;
     }
-    // three slots: the select workgroup shares a CU; one row tile, so the
-    // weight stream is non-temporal
-    dma_body<true, MT, NST, 3, true>(f.q, vb - f.n_sel);
+    dma_body<true, MT, NST, 3, NTW>(f.q, vb - f.n_sel);
 }
 
 struct ReduceArgs {
@@ -172,12 +176,15 @@ bool launch_front_mt(int mt, dim3 grid, const FrontArgs& f, hipStream_t s) {
     }
 }
 
+// one row tile of 2..4 16-row tiles (NST 8 or 16, non-temporal weights), or
+// two row tiles of 8 (NST 8, 14 or 16)
 template <int IPT, int NST>
 bool launch_front_dma_mt(int mt, dim3 grid, const FrontArgs& f, hipStream_t s) {
     switch (mt) {
-        case 2: hipLaunchKernelGGL((front_dma_kernel<IPT, 2, NST>), grid, dim3(kStepBlock), 0, s, f); return true;
-        case 3: hipLaunchKernelGGL((front_dma_kernel<IPT, 3, NST>), grid, dim3(kStepBlock), 0, s, f); return true;
-        case 4: hipLaunchKernelGGL((front_dma_kernel<IPT, 4, NST>), grid, dim3(kStepBlock), 0, s, f); return true;
+        case 2: hipLaunchKernelGGL((front_dma_kernel<IPT, 2, NST, true>), grid, dim3(kStepBlock), 0, s, f); return true;
+        case 3: hipLaunchKernelGGL((front_dma_kernel<IPT, 3, NST, true>), grid, dim3(kStepBlock), 0, s, f); return true;
+        case 4: hipLaunchKernelGGL((front_dma_kernel<IPT, 4, NST, true>), grid, dim3(kStepBlock), 0, s, f); return true;
+        case 8: hipLaunchKernelGGL((front_dma_kernel<IPT, 8, NST, false>), grid, dim3(kStepBlock), 0, s, f); return true;
         default: return false;
     }
 }
@@ -186,6 +193,10 @@ template <int IPT>
 bool launch_front_dma_nst(int nst, int mt, dim3 grid, const FrontArgs& f, hipStream_t s) {
     if (nst == 8) return launch_front_dma_mt<IPT, 8>(mt, grid, f, s);
     if (nst == 16) return launch_front_dma_mt<IPT, 16>(mt, grid, f, s);
+    if (nst == 14 && mt == 8) {
+        hipLaunchKernelGGL((front_dma_kernel<IPT, 8, 14, false>), grid, dim3(kStepBlock), 0, s, f);
+        return true;
+    }
     return false;
 }
 
@@ -251,8 +262,16 @@ StepLayout step_layout(const polestar_step_args& a) {
     L.ap = att_plan(bf16, a.batch, a.seq, a.n_heads, a.n_kv_heads, a.block_len, a.head_dim);
     L.cp = commit_plan(bf16, a.batch, a.block_len, a.vocab);
     L.ipt = select_ipt(a.seq);
-    const bool q_dma = bf16 && L.qp.dma && L.qp.row_tiles == 1 && L.qp.mt >= 2 && L.qp.mt <= 4 &&
-                       (2 * L.qp.steps_per_split == 8 || 2 * L.qp.steps_per_split == 16);
+    const int qnst = 2 * L.qp.steps_per_split;
+    const bool q_dma1 = bf16 && L.qp.dma && L.qp.row_tiles == 1 && L.qp.mt >= 2 && L.qp.mt <= 4 &&
+                        (qnst == 8 || qnst == 16);
+    // the 256-row block projections (two row tiles of eight 16-row tiles):
+    // one workgroup per CU, so fused only when select's workgroups and the
+    // projection's fit one round
+    const bool q_dma2 = bf16 && L.qp.dma && L.qp.row_tiles == 2 && L.qp.mt == 8 &&
+                        (qnst == 8 || qnst == 14 || qnst == 16) &&
+                        static_cast<long>(L.qp.grid) + a.batch <= kCus;
+    const bool q_dma = q_dma1 || q_dma2;
     const bool drift_ok = drift_config(a.d / (bf16 ? 8 : 4), static_cast<long>(a.batch) * a.seq, L.drift_tpr,
                                        L.drift_nch);
     const bool common = drift_ok && a.block_len <= kStepBlock && (a.head_dim == 64 || a.head_dim == 128);
