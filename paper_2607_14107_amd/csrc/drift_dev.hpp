@@ -176,21 +176,21 @@ __device__ __forceinline__ void drift_body(const char* __restrict__ hc, const ch
 }
 
 // (chunks per row, rows) -> (threads per row, chunks per thread).  With at
-// least 2048 rows (eight waves per compute unit and more): one wave per row
-// up to 512 chunks (d = 4096 bf16, 2048 fp32), as many chunks per lane as it
-// takes (no idle lanes at d = 3584), reduced in shuffles alone; 128 threads
-// of 8 chunks up to 1024 chunks.  Fewer rows (or longer ones): 256 threads
-// per row, so that a batch-1 layer still spreads over every compute unit.
+// least 2048 rows: 128 threads per row of up to 8 chunks each (two rows per
+// workgroup) up to 1024 chunks (d = 8192 bf16); one wave per row with as many
+// chunks per lane as d needs ran 2-7 us slower on the batch-8 and Dream-7B
+// layer steps, because the fused launch that also runs the vocabulary scan
+// takes the register count of its largest role (149 registers for 7 chunks
+// per lane against 87 for 4).  Fewer rows (or longer ones): 256 threads per
+// row, so that a batch-1 layer still spreads over every compute unit.
 // False above 2048 chunks (d above 16384 in bf16 / 8192 in fp32).
 // PS_DRIFT_SHAPES lists the shapes this can return, for the launch tables.
 inline bool drift_config(int chunks, long rows, int& tpr, int& nch) {
     if (chunks <= 0 || chunks > 2048) return false;
-    if (rows >= 2048 && chunks <= 512) {
-        tpr = 64;
-        nch = (chunks + 63) / 64;
-    } else if (rows >= 2048 && chunks <= 1024) {
+    if (rows >= 2048 && chunks <= 1024) {
         tpr = 128;
-        nch = 8;
+        const int need = (chunks + 127) / 128;
+        nch = need <= 4 ? need : 8;
     } else {
         tpr = 256;
         const int need = (chunks + 255) / 256;
@@ -198,8 +198,8 @@ inline bool drift_config(int chunks, long rows, int& tpr, int& nch) {
     }
     return true;
 }
-#define PS_DRIFT_SHAPES(X) X(64, 1) X(64, 2) X(64, 3) X(64, 4) X(64, 5) X(64, 6) X(64, 7) X(64, 8) \
-    X(128, 8) X(256, 1) X(256, 2) X(256, 4) X(256, 8)
+#define PS_DRIFT_SHAPES(X) X(128, 1) X(128, 2) X(128, 3) X(128, 4) X(128, 8) \
+    X(256, 1) X(256, 2) X(256, 4) X(256, 8)
 
 }  // namespace
 }  // namespace ps
