@@ -68,10 +68,13 @@ __device__ __forceinline__ void scan_body(const char* __restrict__ logits, int v
     // Straight-line loads: chunks past the slice re-read chunk 0 and count as
     // -inf (no exp contribution, never the argmax); the mask id takes part in
     // the softmax but not in the argmax.  A thread visits its elements in
-    // increasing id order, so once it holds a candidate an element can only
-    // replace it by being strictly larger: each chunk's maximum is compared
-    // with the running best, and only a chunk that beats it (or any chunk
-    // before the first candidate) is searched element by element.
+    // increasing id order, so the lowest id of the largest value is the first
+    // element equal to the largest chunk maximum in the first chunk that
+    // reaches it.  Each round therefore keeps only that chunk (its maximum
+    // over ids other than the mask id, and its data, by selects) and searches
+    // it once at the end of the round; an element-wise search of every chunk
+    // that might hold a new best ran for almost every chunk, since some lane
+    // of the wave nearly always needed it.
     const int nchunks = (v1 - v0) / T::E;
     for (int c0 = 0; c0 < nchunks; c0 += kScanBlock * G) {
         uint4 r[G];
@@ -84,7 +87,11 @@ __device__ __forceinline__ void scan_body(const char* __restrict__ logits, int v
         }
         __builtin_amdgcn_sched_barrier(0);   // all G loads in flight before any use
         float lm = -INFINITY;
-        float cmx[G];
+        // the round's candidate chunk: maximum rbv (mask id excluded), data rdat, first id rvb
+        float rbv = -INFINITY;
+        bool rhave = false;
+        uint4 rdat = r[0];
+        int rvb = 0;
 #pragma unroll
         for (int gq = 0; gq < G; ++gq) {
             float f[T::E];
@@ -92,19 +99,47 @@ __device__ __forceinline__ void scan_body(const char* __restrict__ logits, int v
             float cm = f[0];
 #pragma unroll
             for (int e = 1; e < T::E; ++e) cm = fmaxf(cm, f[e]);
-            cmx[gq] = ok[gq] ? cm : -INFINITY;
-            lm = fmaxf(lm, cmx[gq]);
-        }
-#pragma unroll
-        for (int gq = 0; gq < G; ++gq) {
+            lm = fmaxf(lm, ok[gq] ? cm : -INFINITY);
             const int vb = v0 + (c0 + gq * kScanBlock + threadIdx.x) * T::E;
-            if (ok[gq] && (cmx[gq] > bv || bi == 0x7fffffff)) {
-                float f[T::E];
-                T::unpack(r[gq], f);
+            float ca = cm;
+            if (__builtin_expect(static_cast<unsigned>(mask_id - vb) < static_cast<unsigned>(T::E), 0)) {
+                ca = -INFINITY;
 #pragma unroll
-                for (int e = 0; e < T::E; ++e) better(bv, bi, f[e], vb + e, vb + e != mask_id);
+                for (int e = 0; e < T::E; ++e) ca = vb + e != mask_id ? fmaxf(ca, f[e]) : ca;
             }
+            // a later chunk replaces the candidate only with a strictly larger
+            // maximum; the first valid chunk is taken even at -inf (a NaN
+            // maximum, from a chunk of NaNs, never is)
+            const bool take = ok[gq] & ((ca > rbv) | (!rhave & (ca == ca)));
+            rbv = take ? ca : rbv;
+            rdat.x = take ? r[gq].x : rdat.x;
+            rdat.y = take ? r[gq].y : rdat.y;
+            rdat.z = take ? r[gq].z : rdat.z;
+            rdat.w = take ? r[gq].w : rdat.w;
+            rvb = take ? vb : rvb;
+            rhave |= take;
         }
+        if (rhave) {
+            // the candidate's first element equal to its maximum (mask id
+            // excluded), merged into the running best: earlier rounds hold
+            // lower ids, so on a tie the running best stays
+            float f[T::E];
+            T::unpack(rdat, f);
+            int ie = -1;
+            float fv = rbv;
+#pragma unroll
+            for (int e = T::E - 1; e >= 0; --e) {
+                const bool hit = (f[e] == rbv) & (rvb + e != mask_id);
+                ie = hit ? e : ie;
+                fv = hit ? f[e] : fv;
+            }
+            if (ie >= 0) better(bv, bi, fv, rvb + ie);
+        }
+        // The exponentials unpack the chunks again: keeping every chunk's
+        // floats live from the first pass took 123 registers against 65 (the
+        // fused launch that runs this beside the drift takes the larger count).
+#pragma unroll
+        for (int gq = 0; gq < G; ++gq) asm volatile("" : "+v"(r[gq].x), "+v"(r[gq].y), "+v"(r[gq].z), "+v"(r[gq].w));
         const float mn = fmaxf(m, lm);
         const float mref = mn == -INFINITY ? 0.f : mn;
         const float mnl = mref * kLog2e;

@@ -568,7 +568,9 @@ def test_commit_argmax_edges(P, cfg_index):
     (the lowest id wins, within one vocabulary slice and across slices), the
     [MASK] id holding the strict maximum, long -inf runs (so that a lane's
     and a slice's first elements are -inf), a row that is -inf except for its
-    last element, and -inf rows with a tie among their few finite entries."""
+    last element, -inf rows with a tie among their few finite entries, a
+    maximum reached twice by one lane (16-byte chunks 256 apart), the [MASK]
+    id tied with its neighbour, and a row that is -inf but for [MASK]."""
     L = layer(cfg_index)
     cfg, x = L["cfg"], L["x"]
     lg = x["logits"].copy()
@@ -590,8 +592,15 @@ def test_commit_argmax_edges(P, cfg_index):
     lg[0, 5, :] = val(-np.inf)                                                  # tie among three finite ids
     for pos in (V // 7, V // 2, V - 3):
         lg[0, 5, pos] = val(1.0)
+    E = 8 if bf16 else 4                                                        # ids per 16-byte chunk
+    lg[0, 6, 16] = val(55.0)                                                    # one lane, chunks 0 and 256 of it
+    if 16 + 256 * E < V:
+        lg[0, 6, 16 + 256 * E] = val(55.0)
+    lg[0, 7, mask_id] = lg[0, 7, mask_id + 1] = val(80.0)                       # [MASK] tied with the next id
+    lg[0, 8, :] = val(-np.inf)                                                  # only [MASK] finite
+    lg[0, 8, mask_id] = val(3.0)
     token, conf = ref.confidence(ref.decode(lg, cfg.dtype), mask_id)
-    assert token[0, :6].tolist() == [3, V // 3, V // 2, V - 7, V - 1, V // 7]
+    assert token[0, :9].tolist() == [3, V // 3, V // 2, V - 7, V - 1, V // 7, 16, mask_id + 1, 0]
     gt, gc, _, _, _ = _run_commit(P, cfg, lg, None, None, None, x["masked"], False, mask_id)
     assert np.array_equal(gt, token)
     np.testing.assert_allclose(gc, conf, rtol=1e-4)
