@@ -627,9 +627,12 @@ def cluster_update(h_new: torch.Tensor, h_old: torch.Tensor, labels: torch.Tenso
 
 
 def _event_handle(ev) -> int | None:
-    """Raw hipEvent_t of a torch.cuda.Event (created by recording it once)."""
+    """Raw hipEvent_t of a torch.cuda.Event (created by recording it once), or
+    an int that already is one (an event created through the HIP runtime)."""
     if ev is None:
         return None
+    if isinstance(ev, int):
+        return ev
     if not ev.cuda_event:
         ev.record()
     return ev.cuda_event
@@ -676,7 +679,8 @@ def step_workspace_size(args: StepArgs) -> int:
 
 def step(args: StepArgs, workspace: torch.Tensor, refresh_events=None, stream=None) -> None:
     """polestar_step: the whole layer step; refresh_events = (begin, end)
-    torch.cuda.Event pair recorded around the K/V refresh, or None."""
+    pair of torch.cuda.Event or raw hipEvent_t recorded around the K/V
+    refresh, or None."""
     ev0, ev1 = refresh_events if refresh_events is not None else (None, None)
     nbytes = workspace.numel() * workspace.element_size()
     _check("polestar_step", lib().polestar_step(ctypes.byref(args), _ptr(workspace), nbytes,
