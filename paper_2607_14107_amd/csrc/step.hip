@@ -17,8 +17,9 @@
 // device body the stand-alone kernel runs, so results are bit-identical to
 // calling the six entry points in order.  With more than 2048 positions, or
 // a Q projection other than one DMA row tile of up to 64 rows or two of 128
-// whose grid leaves room for select's workgroups in one round, select and
-// the Q projection run as two launches of their own (seven in all); shapes
+// whose grid and select's workgroups overflow one round by at most 16,
+// select and the Q projection run as two launches of their own (seven in
+// all); shapes
 // outside the other fused kernels
 // (blocks longer than 256, head_dim other than 64/128, rows above the
 // drift kernel's) run exactly the sequence of entry points instead.
@@ -266,11 +267,14 @@ StepLayout step_layout(const polestar_step_args& a) {
     const bool q_dma1 = bf16 && L.qp.dma && L.qp.row_tiles == 1 && L.qp.mt >= 2 && L.qp.mt <= 4 &&
                         (qnst == 8 || qnst == 16);
     // the 256-row block projections (two row tiles of eight 16-row tiles):
-    // one workgroup per CU, so fused only when select's workgroups and the
-    // projection's fit one round
+    // one workgroup per CU, so fused when select's workgroups and the
+    // projection's fit one round, or overflow it by at most 16: the select
+    // workgroups go first and are short, so the projection's last few start
+    // when they end (batch-8 LLaDA-8B layer, 256 + 8 workgroups: 202-380 us
+    // per step against 207-385 us with select launched on its own)
     const bool q_dma2 = bf16 && L.qp.dma && L.qp.row_tiles == 2 && L.qp.mt == 8 &&
                         (qnst == 8 || qnst == 14 || qnst == 16) &&
-                        static_cast<long>(L.qp.grid) + a.batch <= kCus;
+                        static_cast<long>(L.qp.grid) + a.batch <= kCus + 16;
     const bool q_dma = q_dma1 || q_dma2;
     const bool drift_ok = drift_config(a.d / (bf16 ? 8 : 4), static_cast<long>(a.batch) * a.seq, L.drift_tpr,
                                        L.drift_nch);
