@@ -239,8 +239,11 @@ __device__ __forceinline__ int dma_swz(int r, int c) { return r * kDmaStage + ((
 // workgroup that must share its compute unit).  NTW: the plan has one row
 // tile, so every weight byte is read once and its DMA is marked non-temporal
 // (a compile-time choice: a branch inside the unrolled stage loop costs more
-// than the hint saves).
-template <bool BF16, int MT, int NST, int NS = 4, bool NTW = false>
+// than the hint saves).  REG: the operands go through registers instead of
+// global -> LDS transfers (below); taken for row tiles of at most 64 rows,
+// where it made the batch-1 Q projection 13.8 -> 13.3 us, while the 144- and
+// 160-row refreshes ran 27.5 -> 31.1 and 25.4 -> 28.0 us with it.
+template <bool BF16, int MT, int NST, int NS = 4, bool NTW = false, bool REG = (MT <= 4)>
 __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
     static_assert(NS == 3 || NS == 4, "three or four LDS slots");
     using T = Elem<BF16>;
@@ -253,8 +256,8 @@ __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
     constexpr int NDMA = 4 + AIW;                       // DMA instructions per wave per stage
     static_assert(2 * NDMA <= 63, "outstanding DMA must fit the vmcnt counter");
     // one LDS object per slot and operand: the compiler can tell them apart
-    __shared__ __align__(16) char sa0[ASZ], sa1[ASZ], sa2[ASZ], sa3[NS == 4 ? ASZ : 16];
-    __shared__ __align__(16) char sb0[BSZ], sb1[BSZ], sb2[BSZ], sb3[NS == 4 ? BSZ : 16];
+    __shared__ __align__(16) char sa0[ASZ], sa1[ASZ], sa2[REG ? 16 : ASZ], sa3[NS == 4 && !REG ? ASZ : 16];
+    __shared__ __align__(16) char sb0[BSZ], sb1[BSZ], sb2[REG ? 16 : BSZ], sb3[NS == 4 && !REG ? BSZ : 16];
     __shared__ __align__(16) int rowb[BM];
     __shared__ int rowp[BM];
 
@@ -312,15 +315,6 @@ __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
         for (int i = 0; i < AIW; ++i)
             dma16(asrc[i] + off, buf + 8 * min(w + 4 * i, AG - 1) * kDmaStage);
     };
-    issue_b(0, sb0);
-    issue_a(0, sa0);
-    issue_b(1, sb1);
-    issue_a(1, sa1);
-    if constexpr (NS == 4) {
-        issue_b(2, sb2);
-        issue_a(2, sa2);
-    }
-
     floatx4 acc[2][MT];
 #pragma unroll
     for (int c = 0; c < 2; ++c)
@@ -342,31 +336,90 @@ __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
             }
         }
     };
-    // Stage s: wait for this wave's DMA of stage s and its own earlier LDS
-    // reads; barrier (stage s is in LDS for every wave, and the slot of stage
-    // s-1 is free); issue stage s+NS-1 into that slot; compute stage s.
-    // Issue order (NS = 4) B0 A0 B1 A1 B2 A2 | B3 A3 | ...: the wait leaves
-    // exactly the NS-2 newer stages outstanding.  Stages past the split
-    // re-read its last stage, so every stage issues the same DMA count.
-#define PS_DMA_STEP(S, WAIT, AUSE, BUSE, ANEXT, BNEXT)                      \
-    {                                                                       \
-        __builtin_amdgcn_s_waitcnt(WAIT);                                   \
-        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);                             \
-        __builtin_amdgcn_s_barrier();                                       \
-        issue_b((S) + NS - 1, BNEXT);                                       \
-        issue_a((S) + NS - 1, ANEXT);                                       \
-        compute(AUSE, BUSE);                                                \
-    }
-    constexpr int WS = wait_vm((NS - 2) * NDMA);        // after stage s: stages s+1 .. s+NS-2
-    char* const sa[4] = {sa0, sa1, sa2, sa3};
-    char* const sb[4] = {sb0, sb1, sb2, sb3};
-    // fully unrolled: every slot index is a constant and the compiler sees the
-    // whole issue order (a loop would make it drain the DMA at the loop head)
+    if constexpr (!REG) {
+        issue_b(0, sb0);
+        issue_a(0, sa0);
+        issue_b(1, sb1);
+        issue_a(1, sa1);
+        if constexpr (NS == 4) {
+            issue_b(2, sb2);
+            issue_a(2, sa2);
+        }
+
+        // Stage s: wait for this wave's DMA of stage s and its own earlier LDS
+        // reads; barrier (stage s is in LDS for every wave, and the slot of stage
+        // s-1 is free); issue stage s+NS-1 into that slot; compute stage s.
+        // Issue order (NS = 4) B0 A0 B1 A1 B2 A2 | B3 A3 | ...: the wait leaves
+        // exactly the NS-2 newer stages outstanding.  Stages past the split
+        // re-read its last stage, so every stage issues the same DMA count.
+    #define PS_DMA_STEP(S, WAIT, AUSE, BUSE, ANEXT, BNEXT)                      \
+        {                                                                       \
+            __builtin_amdgcn_s_waitcnt(WAIT);                                   \
+            __builtin_amdgcn_s_waitcnt(kWaitLgkm0);                             \
+            __builtin_amdgcn_s_barrier();                                       \
+            issue_b((S) + NS - 1, BNEXT);                                       \
+            issue_a((S) + NS - 1, ANEXT);                                       \
+            compute(AUSE, BUSE);                                                \
+        }
+        constexpr int WS = wait_vm((NS - 2) * NDMA);        // after stage s: stages s+1 .. s+NS-2
+        char* const sa[4] = {sa0, sa1, sa2, sa3};
+        char* const sb[4] = {sb0, sb1, sb2, sb3};
+        // fully unrolled: every slot index is a constant and the compiler sees the
+        // whole issue order (a loop would make it drain the DMA at the loop head)
+    #pragma unroll
+        for (int st = 0; st < NST; ++st)
+            PS_DMA_STEP(st, WS, sa[st % NS], sb[st % NS], sa[(st + NS - 1) % NS], sb[(st + NS - 1) % NS])
+    #undef PS_DMA_STEP
+        __builtin_amdgcn_s_waitcnt(0);                      // the re-read tail DMA lands before the workgroup ends
+    } else {
+        // Register staging: each stage's chunks are loaded into registers P
+        // stages ahead and written to the same LDS positions the DMA fills
+        // (lane l of an instruction at base + 16 l), into two LDS slots.
+        // Plain loads stream faster than global -> LDS transfers (a probe
+        // with the batch-8 Q projection's addresses and no arithmetic: 14.4
+        // against 18.4 us, 9.1 against 13.4 us when the data is in L2), but
+        // the stores to LDS cost the large tiles more than that.  Iteration
+        // s: compute slot s%2; wait for stage s+1's registers, write them to
+        // slot (s+1)%2 (computed an iteration back), load stage s+1+P into
+        // the freed set; barrier.  Stages past the split re-read its last
+        // stage, so every iteration issues the same load count.
+        constexpr int P = 3;
+        static_assert(P * NDMA <= 63, "outstanding loads must fit the vmcnt counter");
+        uint4 rs[P][NDMA];
+        auto load_stage = [&](int st, uint4 (&r)[NDMA]) {
+            const int off = min(st, nst_here - 1) * kDmaStage;
 #pragma unroll
-    for (int st = 0; st < NST; ++st)
-        PS_DMA_STEP(st, WS, sa[st % NS], sb[st % NS], sa[(st + NS - 1) % NS], sb[(st + NS - 1) % NS])
-#undef PS_DMA_STEP
-    __builtin_amdgcn_s_waitcnt(0);                      // the re-read tail DMA lands before the workgroup ends
+            for (int i = 0; i < 4; ++i) r[i] = NTW ? ld16_nt(bsrc[i] + off) : ld16(bsrc[i] + off);
+#pragma unroll
+            for (int i = 0; i < AIW; ++i) r[4 + i] = ld16(asrc[i] + off);
+        };
+        auto store_stage = [&](const uint4 (&r)[NDMA], char* abuf, char* bbuf) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) st16(bbuf + (32 * w + 8 * i) * kDmaStage + 16 * lane, r[i]);
+#pragma unroll
+            for (int i = 0; i < AIW; ++i)
+                if (AG % 4 == 0 || w + 4 * i < AG)   // surplus instructions repeat the last group: no store
+                    st16(abuf + 8 * (w + 4 * i) * kDmaStage + 16 * lane, r[4 + i]);
+        };
+#pragma unroll
+        for (int j = 0; j < P; ++j) load_stage(j, rs[j]);
+        __builtin_amdgcn_s_waitcnt(wait_vm((P - 1) * NDMA));
+        store_stage(rs[0], sa0, sb0);
+        load_stage(P, rs[0]);
+        __syncthreads();
+        constexpr int WR = wait_vm((P - 1) * NDMA);     // stages s+2 .. s+P stay in flight
+#pragma unroll
+        for (int st = 0; st < NST; ++st) {
+            compute(st % 2 ? sa1 : sa0, st % 2 ? sb1 : sb0);
+            if (st + 1 < NST) {
+                __builtin_amdgcn_s_waitcnt(WR);
+                store_stage(rs[(st + 1) % P], (st + 1) % 2 ? sa1 : sa0, (st + 1) % 2 ? sb1 : sb0);
+                load_stage(st + 1 + P, rs[(st + 1) % P]);
+            }
+            __syncthreads();
+        }
+        __builtin_amdgcn_s_waitcnt(0);                  // the re-read tail loads land before the workgroup ends
+    }
 
     // results straight from registers: register i of acc[c][mt] is row
     // 16mt + 4(l/16) + i, column 32w + 16c + l%16.  Split K (the usual case):
