@@ -458,6 +458,241 @@ __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
 }
 
 
+// ---------------------------------------------------------------------------
+// tile_body (gemm_tile_kernel, and the fused step's refresh): 256 x 256
+// outputs per workgroup for row sets of more than
+// one DMA tile (the refresh of a whole batch, the dense rows of a stack).
+// The four waves form a 2 x 2 grid of 128 x 128 blocks, each 4 x 4 tiles of
+// v_mfma_f32_32x32x16_bf16, so every fragment read from LDS feeds four MFMAs
+// (the row kernels of gemm.hip read one A fragment per MFMA).
+// Both operands arrive by DMA in stages of 64 bytes (32 bf16) of each row,
+// four LDS slots, three stages in flight; the DMA wait and barrier for stage
+// s+1 sit between the two halves of stage s, so the first fragments of s+1
+// are read while the second half's MFMAs run.
+// ---------------------------------------------------------------------------
+
+constexpr int kTileStage = 64;                 // bytes of each row per stage
+constexpr int kTileDim = 256;                  // rows and columns per workgroup
+constexpr int kTileGroupRows = 4;              // row tiles per band of the launch order
+constexpr int kTileSlot = kTileDim * kTileStage;
+
+// LDS offset of 16-byte chunk c (0..3) of row r in a stage: the chunk is
+// XOR-ed with (r/4) % 4.  Measured on gfx950, fragment reads (lane l: row
+// l%32, chunk l/32) with this layout run at the full ds_read_b128 rate;
+// ((r/2) ^ (r/8)) % 4 or (r/2) % 4 reach half of it.
+__device__ __forceinline__ int tile_sw(int r) { return (r >> 2) & 3; }
+
+// Workgroup blk -> (split, row tile, column tile).  Consecutive workgroups go
+// to different XCDs, so the ids are first regrouped per XCD; each XCD then
+// walks bands of kTileGroupRows row tiles column by column, which keeps the
+// input rows and weight rows its compute units share in its own L2.  (The
+// tile workgroups must be the first ones of their launch.)
+__device__ __forceinline__ void tile_coords(const GemmArgs& g, int blk, int& split, int& rt, int& ct) {
+    const int ntc = (g.N + kTileDim - 1) / kTileDim;
+    const int ntiles = g.row_tiles * ntc;
+    const int nb = ntiles * g.ksplit;
+    int bid = blk;
+    if (nb % 8 == 0) bid = (bid % 8) * (nb / 8) + bid / 8;
+    split = bid / ntiles;
+    const int tl = bid - split * ntiles;
+    const int band = tl / (kTileGroupRows * ntc);
+    const int rows_here = min(kTileGroupRows, g.row_tiles - band * kTileGroupRows);
+    const int in = tl - band * kTileGroupRows * ntc;
+    ct = in / rows_here;
+    rt = band * kTileGroupRows + (in - ct * rows_here);
+}
+
+constexpr int kTileThreads = 256;             // four waves, one per SIMD
+
+__device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
+    constexpr int ES = 2;                                // bf16 operands
+    constexpr int NDMA = 8;                              // DMA instructions per wave per stage (4 A, 4 B)
+    __shared__ __align__(16) char sa0[kTileSlot], sa1[kTileSlot], sa2[kTileSlot], sa3[kTileSlot];
+    __shared__ __align__(16) char sb0[kTileSlot], sb1[kTileSlot], sb2[kTileSlot], sb3[kTileSlot];
+    __shared__ int rowb[kTileDim], rowp[kTileDim];
+
+    int split, rt, ct;
+    tile_coords(g, blk, split, rt, ct);
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int w = t >> 6;
+    const int wm = w & 1, wn = w >> 1;
+    const int m0 = rt * kTileDim;
+    const int n0 = ct * kTileDim;
+    const int nss = g.steps_per_split;                   // stages of this split (a multiple of 4)
+    const size_t k0b = static_cast<size_t>(split) * nss * kTileStage;
+
+    // Row bookkeeping: thread t maps row m0 + t; the first workgroup of each
+    // row tile publishes the map for the split-K reduction.
+    int rb_ = -1, rp_ = 0;
+    map_row(g, m0 + t, rb_, rp_);
+    rowb[t] = rb_;
+    rowp[t] = rp_;
+    if (g.ksplit > 1 && split == 0 && ct == 0 && m0 + t < g.m_max)
+        *reinterpret_cast<int2*>(g.rowmap + 2 * (m0 + t)) = make_int2(rb_, rp_);
+    if (!__syncthreads_or(rb_ >= 0)) return;             // no row of this tile maps anywhere (uniform)
+
+    // DMA sources: instruction i of wave w moves rows 16(w + 4i) .. +15 of a
+    // slot; lane l fills chunk l%4 of row 16(w + 4i) + l/4, i.e. logical
+    // chunk (l%4) ^ swizzle(row).  Rows that map to nothing read row 0 of the
+    // input, columns past N weight row 0; neither is stored.
+    const char* asrc[4];
+    const char* bsrc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = 16 * (w + 4 * i) + (lane >> 2);
+        const int chunk = ((lane & 3) ^ tile_sw(r)) << 4;
+        const int b = rowb[r];
+        const char* arow = b >= 0 ? g.x + (static_cast<size_t>(b) * g.seq + rowp[r]) * g.K * ES : g.x;
+        asrc[i] = arow + k0b + chunk;
+        const char* brow = weight_row(g, n0 + r, ES);
+        bsrc[i] = (brow ? brow : g.w0) + k0b + chunk;
+    }
+    auto issue = [&](int st, char* abuf, char* bbuf) {
+        const int off = min(st, nss - 1) * kTileStage;   // past the split: re-read its last stage
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dma16(bsrc[i] + off, bbuf + 16 * (w + 4 * i) * kTileStage);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dma16(asrc[i] + off, abuf + 16 * (w + 4 * i) * kTileStage);
+    };
+
+    // Fragment offsets: lane l reads row 32i + l%32 of its wave's block at
+    // k-group l/32 of half kk; the swizzle depends on l%32 only.
+    const int fr = lane & 31;
+    const int fsw = tile_sw(fr);                         // = tile_sw(32i + fr)
+    const int h = lane >> 5;
+    const int aoff0 = (128 * wm + fr) * kTileStage + (((0 + h) ^ fsw) << 4);
+    const int aoff1 = (128 * wm + fr) * kTileStage + (((2 + h) ^ fsw) << 4);
+    const int boff0 = (128 * wn + fr) * kTileStage + (((0 + h) ^ fsw) << 4);
+    const int boff1 = (128 * wn + fr) * kTileStage + (((2 + h) ^ fsw) << 4);
+
+    floatx16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    uint4 fa0[4], fb0[4], fa1[4], fb1[4];                // fragments of half 0 / half 1
+    auto read_half = [&](const char* abuf, const char* bbuf, int aoff, int boff, uint4 (&fa)[4], uint4 (&fb)[4]) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) fa[i] = *reinterpret_cast<const uint4*>(abuf + aoff + i * 32 * kTileStage);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) fb[j] = *reinterpret_cast<const uint4*>(bbuf + boff + j * 32 * kTileStage);
+    };
+    auto mfma_half = [&](const uint4 (&fa)[4], const uint4 (&fb)[4]) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = Mma32<true>::step(fa[i], fb[j], acc[i][j]);
+    };
+    // Instruction order of a half: the 8 fragment reads for the next half
+    // go out behind the first two MFMAs (so they land well before the next
+    // half starts), the DMA instructions (second half only) behind the next
+    // four, then the remaining MFMAs.
+    auto interleave = [&](bool with_dma) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+        if (with_dma) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 10, 0);
+        } else {
+            __builtin_amdgcn_sched_group_barrier(0x008, 14, 0);
+        }
+    };
+
+    constexpr int WS = wait_vm(2 * NDMA);                // two newer stages stay in flight
+    issue(0, sa0, sb0);
+    issue(1, sa1, sb1);
+    issue(2, sa2, sb2);
+    issue(3, sa3, sb3);
+    __builtin_amdgcn_s_waitcnt(wait_vm(3 * NDMA));
+    __builtin_amdgcn_s_barrier();
+    read_half(sa0, sb0, aoff0, boff0, fa0, fb0);
+
+    // Stage S in slot S%4: half 1 of S is read while half 0's MFMAs run;
+    // then (own reads done, stage S+1 landed for this wave) a barrier makes
+    // S+1 visible to all waves and frees slot S%4, which takes stage S+4;
+    // half 0 of S+1 is read while half 1's MFMAs run.
+#define PS_TILE_STEP(S, AU, BU, AX, BX)                                     \
+    {                                                                       \
+        __builtin_amdgcn_sched_barrier(0);                                  \
+        read_half(AU, BU, aoff1, boff1, fa1, fb1);                          \
+        mfma_half(fa0, fb0);                                                \
+        interleave(false);                                                  \
+        __builtin_amdgcn_sched_barrier(0);                                  \
+        __builtin_amdgcn_s_waitcnt(WS);                                     \
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);                             \
+        __builtin_amdgcn_s_barrier();                                       \
+        __builtin_amdgcn_sched_barrier(0);                                  \
+        issue((S) + 4, AU, BU);                                             \
+        read_half(AX, BX, aoff0, boff0, fa0, fb0);                          \
+        mfma_half(fa1, fb1);                                                \
+        interleave(true);                                                   \
+        __builtin_amdgcn_sched_barrier(0);                                  \
+    }
+    for (int st = 0; st < nss; st += 4) {
+        PS_TILE_STEP(st + 0, sa0, sb0, sa1, sb1)
+        PS_TILE_STEP(st + 1, sa1, sb1, sa2, sb2)
+        PS_TILE_STEP(st + 2, sa2, sb2, sa3, sb3)
+        PS_TILE_STEP(st + 3, sa3, sb3, sa0, sb0)
+    }
+#undef PS_TILE_STEP
+    __builtin_amdgcn_s_waitcnt(0);                       // every DMA (the re-read tail too) has landed
+    __syncthreads();                                     // and every wave is done with the slots
+
+    // Epilogue through LDS, per wave, 16 rows at a time: register e of
+    // acc[i][j] is row 32i + 8(e/4) + 4(l/32) + e%4, column 32j + l%32 of the
+    // wave's block; each lane then moves 8 consecutive columns of a row.
+    constexpr int EP = 132;                              // fp32 pitch of a staged row
+    float* ep = reinterpret_cast<float*>(w == 0 ? sa0 : w == 1 ? sa1 : w == 2 ? sa2 : sa3);
+    const int cbase = n0 + 128 * wn;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int ee = 8 * hh + e;
+                    const int r = 8 * (e >> 2) + 4 * h + (e & 3);
+                    ep[r * EP + 32 * j + fr] = acc[i][j][ee];
+                }
+            __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int idx = 64 * q + lane;           // 16 rows x 16 chunks of 8 columns
+                const int r = idx >> 4, c = (idx & 15) * 8;
+                const int lr = 128 * wm + 32 * i + 16 * hh + r;   // row within the tile
+                const int b = rowb[lr];
+                const int n = cbase + c;
+                const float* v = ep + r * EP + c;
+                if (b >= 0 && n < g.N) {
+                    if (g.ksplit == 1) {
+                        store8<true>(out_ptr<true>(g, b, rowp[lr], m0 + lr, n), v);
+                    } else {
+                        float* dst = g.ws + ((static_cast<size_t>(split) * g.col_tiles + (n >> 7)) * g.m_max +
+                                             (m0 + lr)) * 128 + (n & 127);
+                        *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+                        *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+                    }
+                }
+            }
+            __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
+}
+
 // Split-K reduction: thread = (column tile, row, 8 columns); sums the splits
 // in order and stores the row through the published row map.  One
 // kGemmBlock workgroup per 16 rows of a column tile.

@@ -9,6 +9,8 @@
 //      inputs, so it fills the GPU while select runs.
 //   3. refresh GEMM: gather -> MFMA -> split-K partials (needs 2)
 //   4. reduce: refresh split-K reduce + scatter | Q split-K reduce
+//      (an unsplit refresh on the tile kernel takes the Q reduce into its
+//      own launch instead: five launches)
 //   5. attention over the refreshed cache (needs 2, 3, 4)
 //   6. back: attention merge | commit finalize (needs 5, and 1-2)
 //
@@ -111,6 +113,27 @@ struct ReduceArgs {
     GemmArgs q;    // Q projection
     int n_r;
 };
+
+// refresh on the 256 x 256 tile kernel, unsplit | Q split-K reduce: the tile
+// workgroups come first (tile_body's XCD-aware order counts from id 0), the
+// reduction's after them on the compute units the tiles leave free (192 tiles
+// on 256 CUs at the batch-8 LLaDA-8B layer's 10% stale), so the Q reduce
+// needs no launch of its own (bf16 only, as the tile kernel).
+struct TileQArgs {
+    GemmArgs r;    // refresh (n_tile workgroups, first)
+    GemmArgs q;    // Q projection
+    int n_tile;
+};
+
+static_assert(kTileThreads == kGemmBlock, "the tile and reduce roles share one workgroup size");
+
+__global__ __launch_bounds__(kTileThreads) void tile_qred_kernel(TileQArgs k) {
+    if (static_cast<int>(blockIdx.x) < k.n_tile) {
+        tile_body(k.r, blockIdx.x);
+        return;
+    }
+    reduce_body<true>(k.q, blockIdx.x - k.n_tile);
+}
 
 template <bool BF16>
 __global__ __launch_bounds__(kStepBlock) void reduce2_kernel(ReduceArgs k) {
@@ -428,17 +451,29 @@ extern "C" polestar_status polestar_step(const polestar_step_args* a, void* work
     GemmArgs rg = refresh_gemm_args(a->batch, a->seq, a->d, a->n_kv_heads * a->head_dim, a->h_cur, a->stale_idx,
                                     a->stale_count, a->k, a->block_start, a->block_len, a->w_k, a->w_v,
                                     a->k_cache, a->v_cache, ws);
-    st = gemm_run(bf16, L.rp, rg, stream, &rk.r);
-    if (st != POLESTAR_OK) return st;
-    gemm_finalize_args(L.rp, rg);
-    rk.n_r = gemm_reduce_blocks(L.rp, rg);
-    rk.q = f.q;
-    const int n_red = rk.n_r + gemm_reduce_blocks(L.qp, f.q);
-    if (n_red > 0) {
-        if (bf16) hipLaunchKernelGGL(reduce2_kernel<true>, dim3(n_red), dim3(kStepBlock), 0, stream, rk);
-        else hipLaunchKernelGGL(reduce2_kernel<false>, dim3(n_red), dim3(kStepBlock), 0, stream, rk);
+    const int n_qred = gemm_reduce_blocks(L.qp, f.q);
+    if (bf16 && L.rp.tile && L.rp.ksplit == 1 && L.rp.steps_per_split % 4 == 0 && n_qred > 0) {
+        TileQArgs tq{};
+        gemm_finalize_args(L.rp, rg);
+        tq.r = rg;
+        tq.q = f.q;
+        tq.n_tile = L.rp.grid;
+        hipLaunchKernelGGL(tile_qred_kernel, dim3(L.rp.grid + n_qred), dim3(kTileThreads), 0, stream, tq);
         st = launch_status();
         if (st != POLESTAR_OK) return st;
+    } else {
+        st = gemm_run(bf16, L.rp, rg, stream, &rk.r);
+        if (st != POLESTAR_OK) return st;
+        gemm_finalize_args(L.rp, rg);
+        rk.n_r = gemm_reduce_blocks(L.rp, rg);
+        rk.q = f.q;
+        const int n_red = rk.n_r + n_qred;
+        if (n_red > 0) {
+            if (bf16) hipLaunchKernelGGL(reduce2_kernel<true>, dim3(n_red), dim3(kStepBlock), 0, stream, rk);
+            else hipLaunchKernelGGL(reduce2_kernel<false>, dim3(n_red), dim3(kStepBlock), 0, stream, rk);
+            st = launch_status();
+            if (st != POLESTAR_OK) return st;
+        }
     }
     if (refresh_end && hipEventRecord(refresh_end, stream) != hipSuccess) return POLESTAR_ERR_LAUNCH;
 
