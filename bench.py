@@ -854,21 +854,16 @@ def main():
         return 0
     k, es, stream = L.k, L.es, L.stream
 
-    for i in range(args.warmup):
-        L.run_step(i)
-    torch.cuda.synchronize()
-
-    # per-call breakdown (untimed for the headline)
-    call_us = L.calls_us(max(1, min(args.steps, 50)))
     dom = "refresh_kv"   # the step's dominant launch group; polestar_step brackets it with events
-
-    # timed region: K whole steps through polestar_step, each bracketing its
-    # refresh launches with the two timing events it is given (recorded on
-    # its launch stream; without the system-scope fence they cost no
-    # measurable step time: 60.6 against 60.3 us per step at config 1 with
-    # events on every fifth step)
+    # timed region: K whole steps through polestar_step right after the W
+    # warm-up steps, each bracketing its refresh launches with the two timing
+    # events it is given (recorded on its launch stream; without the
+    # system-scope fence they cost no measurable step time: 60.6 against
+    # 60.3 us per step at config 1 with events on every fifth step)
     te = L.events
     events = [(te.new(), te.new()) for _ in range(args.steps)]
+    for i in range(args.warmup):
+        L.run_step(i)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -878,6 +873,9 @@ def main():
     elapsed = time.perf_counter() - t0
     dom_us = float(np.mean([te.us(e0, e1) for e0, e1 in events]))
     te.close()
+
+    # per-call breakdown (untimed for the headline)
+    call_us = L.calls_us(max(1, min(args.steps, 50)))
 
     # per-step percentiles over at least 50 steps (after the timed region)
     stats = L.step_stats(max(50, args.stats_steps), args.warmup + args.steps)
