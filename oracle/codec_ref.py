@@ -8,7 +8,7 @@ The paper caches the local window's hidden states as residuals to their
 cluster's centroid, quantized along the channels in a 4-bit float format with
 block scales (Sec. 4.1 "Cluster and Quantize Hidden States"; App. C
 "Quantization Format"; the format ablation of App. D finds microscaling FP4
-and FP8 residuals as accurate as the paper's choice).  This build uses the
+and FP8 residuals as accurate as the paper's choice).  The codec here uses the
 OCP microscaling formats that MI355X supports natively:
 
   MXFP4: blocks of 32 consecutive channels share one E8M0 scale 2^e
