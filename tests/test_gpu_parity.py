@@ -731,11 +731,13 @@ def _assert_same(a, b):
                               b[n].view(np.uint8) if b[n].dtype != np.uint8 else b[n]), f"fused step differs in {n}"
 
 
-@pytest.mark.parametrize("cfg_index,subrun", [(0, 0), (1, 1), (2, 0), (3, 0)])
+@pytest.mark.parametrize("cfg_index,subrun", [(0, 0), (1, 1), (2, 0), (2, 1), (3, 0)])
 def test_step_fused_equals_calls_on_configs(P, cfg_index, subrun):
-    """Configs 0-1 take the six fused launches, 2-3 (more than 64 query rows)
-    the seven with select and the Q projection on their own; either way the
-    results equal the six calls bit for bit."""
+    """Configs 0-1 take the six fused launches with a Q projection of up to
+    64 rows; 2-3 the front with two 128-row projection tiles (config 2's
+    eight select workgroups overflow one round); config 2 at 10% stale also
+    puts the Q reduction into its unsplit tile-kernel refresh (five launches).
+    Either way the results equal the six calls bit for bit."""
     L = layer(cfg_index, subrun)
     a, b = _run_both(P, L["cfg"], L["x"], L["kc"], L["vc"], int(L["x"]["k"]))
     _assert_same(a, b)
