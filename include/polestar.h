@@ -563,13 +563,17 @@ polestar_status polestar_scatter_rows(int batch, int seq, int row_bytes, const v
  *
  * Work that does not depend on the previous launch shares launches: the
  * drift beside the vocabulary scan, the per-sequence select beside the Q
- * projection, the refresh's split-K reduction beside the Q projection's, and
- * the attention's split merge beside the commit's finalize step, so the
- * latency-bound pieces overlap bandwidth-bound ones.  With seq > 2048 or
- * batch * block_len > 64, select and the Q projection run as launches of
- * their own and the rest stays fused; shapes outside the other fused
- * kernels (block_len > 256, d above the drift kernel's rows) run the six
- * calls one after another.  The results are the same on every path.
+ * projection, the refresh's split-K reduction beside the Q projection's (or,
+ * for a refresh large enough to run unsplit on 256 x 256 tiles, the Q
+ * projection's reduction inside the refresh launch), and the attention's
+ * split merge beside the commit's finalize step, so the latency-bound pieces
+ * overlap bandwidth-bound ones.  With seq > 2048, or a Q projection that is
+ * neither one row tile of up to 64 rows nor two of 128 whose workgroups and
+ * select's overflow one round of the 256 compute units by at most 16, select
+ * and the Q projection run as launches of their own and the rest stays
+ * fused; shapes outside the other fused kernels (block_len > 256, d above
+ * the drift kernel's rows) run the six calls one after another.  The results
+ * are the same on every path.
  *
  * All fields of polestar_step_args keep the meaning, layout and
  * requirements they have in the stand-alone calls above; eligible may be
@@ -579,8 +583,9 @@ polestar_status polestar_scatter_rows(int batch, int seq, int row_bytes, const v
  *   refresh_begin, refresh_end : optional events (NULL: none) recorded on the
  *       stream right before and right after the refresh launches, so that a
  *       caller can time the K/V refresh inside the step (on the fused path
- *       the second of them, the split-K reduction, also reduces the Q
- *       projection's partials when its plan splits K).
+ *       these launches also reduce the Q projection's partials when its plan
+ *       splits K).  Events created with hipEventDisableSystemFence time the
+ *       launches without the cache write-back a default event performs.
  * Returns the first non-OK status of the pieces; as with the stand-alone
  * calls, argument errors are found on the host before anything is enqueued
  * (for the fused path: every check of every piece).
