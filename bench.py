@@ -325,7 +325,8 @@ def _segments(rows):
 
 # roles of the fused step's kernels, by name
 STEP_ROLES = (("lead", ("lead_kernel",)), ("front", ("front_kernel", "front_dma_kernel", "select_kernel")),
-              ("refresh_kv", ("gemm_", "reduce2_kernel")), ("attend", ("attend_",)), ("back", ("back_kernel",)))
+              ("refresh_kv", ("gemm_", "reduce2_kernel", "tile_qred_kernel")), ("attend", ("attend_",)),
+              ("back", ("back_kernel",)))
 
 
 def _step_role(name):
