@@ -564,7 +564,7 @@ polestar_status polestar_scatter_rows(int batch, int seq, int row_bytes, const v
  * Work that does not depend on the previous launch shares launches: the
  * drift beside the vocabulary scan, the per-sequence select beside the Q
  * projection, the refresh's split-K reduction beside the Q projection's (or,
- * for a refresh large enough to run unsplit on 256 x 256 tiles, the Q
+ * for a refresh large enough to run unsplit on the tile GEMM, the Q
  * projection's reduction inside the refresh launch), and the attention's
  * split merge beside the commit's finalize step, so the latency-bound pieces
  * overlap bandwidth-bound ones.  With seq > 2048, or a Q projection that is

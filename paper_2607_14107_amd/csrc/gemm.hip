@@ -63,6 +63,14 @@ namespace {
 
 constexpr int kLda = 272;         // LDS row pitch (bytes) of the staged input rows
 constexpr int kTargetWgs = 256;   // one workgroup per compute unit on MI355X
+// Per-CU rate of a 192-row tile relative to a 256-row one in the plan's
+// estimate.  Unsplit, the batch-8 LLaDA-8B refresh (1488 x 8192 x 4096 in
+// one round) measures 0.86 (256 tiles of 192 rows 112.9 us against 192 of
+// 256 rows 130 us); 0.95 is the value whose choices matched the faster
+// plan on every shape measured through polestar_linear (with 0.86 the
+// 1250 x 2512 x 2048 product takes 256-row tiles in four splits, 45.4 us,
+// against 43.8 us for 192-row tiles in two).
+constexpr double kTile192Rate = 0.95;
 
 // ---------------------------------------------------------------------------
 // gemm_rows_kernel: BM = 32*MT rows x 128 columns per workgroup; wave w owns
@@ -248,7 +256,8 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_dma_kernel(GemmArgs g) {
     dma_body<BF16, MT, NST, 4, NTW>(g, blockIdx.x);
 }
 
-__global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmArgs g) { tile_body(g, blockIdx.x); }
+template <int MI>
+__global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmArgs g) { tile_body<MI>(g, blockIdx.x); }
 
 // Sum of the split-K partials, in split order (deterministic): thread ->
 // (column tile, row, 8 columns) so that consecutive threads read consecutive
@@ -384,7 +393,7 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     }
     p.small = false;
     p.col_tiles = ceil_div(N, 128);                     // split-K partials: 128-column tiles
-    // Tile kernel: more rows than one DMA tile; 256 x 256 tiles, K split
+    // Tile kernel: more rows than one DMA tile; 256- or 192-row x 256-column tiles, K split
     // while the tiles alone leave compute units idle.  Measured against the
     // other kernels it wins when it launches at least 128 workgroups and at
     // most four splits fill the chip, each split still runs 48 stages or
@@ -403,30 +412,41 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     const bool narrow_dma = bf16 && dma_k && N <= 4 * kTileDim && m_max <= 8L * 16 * kDmaMaxRowTiles;
     if (bf16 && m_max > 16L * kDmaMaxRowTiles && K % kTileStage == 0 && !narrow_dma) {
         const int nstage = K / (kTileStage / 2);
-        p.row_tiles = ceil_div(m_max, kTileDim);
-        const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, kTileDim);
-        // The split with the least estimated time: ceil(tiles * k / 256)
-        // rounds of one workgroup per CU, each 1/k of a tile's work (a whole
-        // 256 x 256 x K tile at the ~1 PFLOP/s this kernel sustains: 3.9
-        // GFLOP/ms per CU), plus the fp32 partials of a split run written
-        // and read back (8 k M N bytes at ~5 TB/s).  Measured on the
-        // batch-8 LLaDA-8B refresh: 192 tiles (10% stale) unsplit in one
-        // round 130 us, in two splits (384 workgroups, a round and a half,
-        // 98 MB of partials) 159 us; 64 tiles (2%) best in four splits;
-        // 20 tiles (the Dream-7B refresh) in seven.  Every split runs a whole
-        // number of 4-stage loop trips and at least 16 stages.
-        const double tile_us = 256.0 * 256.0 * 2.0 * K / 3.9e6;
-        int ksplit = 1;
+        // The tile height and split with the least estimated time: ceil(tiles
+        // * k / 256) rounds of one workgroup per CU, each 1/k of a tile's
+        // work (a whole 256 x 256 x K tile at the ~1 PFLOP/s this kernel
+        // sustains: 3.9 GFLOP/ms per CU; a 192-row tile at kTile192Rate of
+        // that rate), plus the fp32 partials of a split run written and read
+        // back (8 k M N bytes at ~5 TB/s); ties keep the 256-row tile.
+        // Measured on the batch-8 LLaDA-8B refresh: 192 tiles of 256 rows
+        // (10% stale) unsplit in one round 130 us, in two splits (384
+        // workgroups, a round and a half, 98 MB of partials) 159 us, as 256
+        // tiles of 192 rows 112.9 us; 64 tiles (2%) best in four splits; 20
+        // tiles (the Dream-7B refresh) in seven.  Through polestar_linear the
+        // 192-row plans it picks ran 3-15% faster than the best 256-row ones
+        // (512 x 4096 x 4096: 47.6 against 50.9 us; 1264 x 8192 x 4096: 95.1
+        // against 110.3 us).  Every split runs a whole number of 4-stage loop
+        // trips and at least 16 stages.
+        int ksplit = 1, mi = 4;
         double best = 1e30;
-        for (int k = 1; k <= kMaxSplit; ++k) {
-            if (nstage % (4 * k) != 0 || nstage / k < 16) continue;
-            const double rounds = static_cast<double>((tiles * k + kTargetWgs - 1) / kTargetWgs);
-            const double cost = rounds * tile_us / k + (k > 1 ? 8.0 * k * m_max * N / 5e6 : 0.0);
-            if (cost < best) {
-                best = cost;
-                ksplit = k;
+        for (int cand = 4; cand >= 3; --cand) {
+            const int rows = 64 * cand;
+            const long tiles = static_cast<long>(ceil_div(m_max, rows)) * ceil_div(N, kTileDim);
+            const double tile_us = rows * 256.0 * 2.0 * K / (3.9e6 * (cand == 4 ? 1.0 : kTile192Rate));
+            for (int k = 1; k <= kMaxSplit; ++k) {
+                if (nstage % (4 * k) != 0 || nstage / k < 16) continue;
+                const double rounds = static_cast<double>((tiles * k + kTargetWgs - 1) / kTargetWgs);
+                const double cost = rounds * tile_us / k + (k > 1 ? 8.0 * k * m_max * N / 5e6 : 0.0);
+                if (cost < best) {
+                    best = cost;
+                    ksplit = k;
+                    mi = cand;
+                }
             }
         }
+        p.tile_mi = mi;
+        p.row_tiles = ceil_div(m_max, 64 * mi);
+        const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, kTileDim);
         p.tile = tiles * ksplit >= kTargetWgs / 2 &&
                  (ksplit <= 4 || nstage / ksplit >= 48 || p.row_tiles >= 4);
         p.ksplit = ksplit;
@@ -436,7 +456,7 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
         const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, kTileDim);
         const int ksplit = p.ksplit;
         p.steps_per_split = nstage / ksplit;
-        p.mt = kTileDim / 32;
+        p.mt = 2 * p.tile_mi;
         p.grid = static_cast<int>(tiles * ksplit);
         if (p.ksplit > 1)
             p.ws_bytes = partial_bytes(p, m_max) + align_up(static_cast<size_t>(m_max) * 2 * sizeof(int), 256);
@@ -522,7 +542,10 @@ polestar_status gemm_run(bool bf16, const GemmPlan& p, GemmArgs g, hipStream_t s
     if (p.small) ok = bf16 ? dispatch_small<true>(p, g, stream) : dispatch_small<false>(p, g, stream);
     else if (p.tile) {
         ok = bf16 && p.steps_per_split % 4 == 0;
-        if (ok) hipLaunchKernelGGL(gemm_tile_kernel, dim3(p.grid), dim3(kTileThreads), 0, stream, g);
+        if (ok && p.tile_mi == 3)
+            hipLaunchKernelGGL(gemm_tile_kernel<3>, dim3(p.grid), dim3(kTileThreads), 0, stream, g);
+        else if (ok)
+            hipLaunchKernelGGL(gemm_tile_kernel<4>, dim3(p.grid), dim3(kTileThreads), 0, stream, g);
     } else if (p.dma) ok = bf16 && dispatch_dma<true>(p, g, stream);
     else ok = bf16 ? dispatch_rows<true>(p, g, stream) : dispatch_rows<false>(p, g, stream);
     if (!ok) return POLESTAR_ERR_UNSUPPORTED;

@@ -459,12 +459,14 @@ __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
 
 
 // ---------------------------------------------------------------------------
-// tile_body (gemm_tile_kernel, and the fused step's refresh): 256 x 256
-// outputs per workgroup for row sets of more than
-// one DMA tile (the refresh of a whole batch, the dense rows of a stack).
-// The four waves form a 2 x 2 grid of 128 x 128 blocks, each 4 x 4 tiles of
-// v_mfma_f32_32x32x16_bf16, so every fragment read from LDS feeds four MFMAs
-// (the row kernels of gemm.hip read one A fragment per MFMA).
+// tile_body (gemm_tile_kernel, and the fused step's refresh): 256 x 256 or
+// 192 x 256 outputs per workgroup for row sets of more than one DMA tile
+// (the refresh of a whole batch, the dense rows of a stack).  The four waves
+// form a 2 x 2 grid of 128 x 128 (or 96 x 128) blocks, each 4 x 4 (3 x 4)
+// tiles of v_mfma_f32_32x32x16_bf16, so every fragment read from LDS feeds
+// three or four MFMAs (the row kernels of gemm.hip read one A fragment per
+// MFMA).  The plan takes 192-row tiles where 256-row ones would leave compute
+// units idle (1488 rows x 8192 columns: 256 tiles instead of 192).
 // Both operands arrive by DMA in stages of 64 bytes (32 bf16) of each row,
 // four LDS slots, three stages in flight; the DMA wait and barrier for stage
 // s+1 sit between the two halves of stage s, so the first fragments of s+1
@@ -472,7 +474,7 @@ __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
 // ---------------------------------------------------------------------------
 
 constexpr int kTileStage = 64;                 // bytes of each row per stage
-constexpr int kTileDim = 256;                  // rows and columns per workgroup
+constexpr int kTileDim = 256;                  // columns (and at most rows) per workgroup
 constexpr int kTileGroupRows = 4;              // row tiles per band of the launch order
 constexpr int kTileSlot = kTileDim * kTileStage;
 
@@ -504,10 +506,17 @@ __device__ __forceinline__ void tile_coords(const GemmArgs& g, int blk, int& spl
 
 constexpr int kTileThreads = 256;             // four waves, one per SIMD
 
+// MI: 32-row MFMA tiles per wave down the rows: 4 (256-row tiles) or 3
+// (192-row tiles, for row counts where 256-row tiles would leave compute
+// units idle; the columns stay 256 wide).
+template <int MI>
 __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
+    static_assert(MI == 3 || MI == 4, "192- or 256-row tiles");
     constexpr int ES = 2;                                // bf16 operands
-    constexpr int NDMA = 8;                              // DMA instructions per wave per stage (4 A, 4 B)
-    __shared__ __align__(16) char sa0[kTileSlot], sa1[kTileSlot], sa2[kTileSlot], sa3[kTileSlot];
+    constexpr int BMT = 64 * MI;                         // rows per tile (two waves down, MI tiles each)
+    constexpr int ASLOT = BMT * kTileStage;
+    constexpr int NDMA = MI + 4;                         // DMA instructions per wave per stage (MI A, 4 B)
+    __shared__ __align__(16) char sa0[ASLOT], sa1[ASLOT], sa2[ASLOT], sa3[ASLOT];
     __shared__ __align__(16) char sb0[kTileSlot], sb1[kTileSlot], sb2[kTileSlot], sb3[kTileSlot];
     __shared__ int rowb[kTileDim], rowp[kTileDim];
 
@@ -517,34 +526,37 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
     const int lane = t & 63;
     const int w = t >> 6;
     const int wm = w & 1, wn = w >> 1;
-    const int m0 = rt * kTileDim;
+    const int m0 = rt * BMT;
     const int n0 = ct * kTileDim;
     const int nss = g.steps_per_split;                   // stages of this split (a multiple of 4)
     const size_t k0b = static_cast<size_t>(split) * nss * kTileStage;
 
-    // Row bookkeeping: thread t maps row m0 + t; the first workgroup of each
-    // row tile publishes the map for the split-K reduction.
+    // Row bookkeeping: thread t < BMT maps row m0 + t; the first workgroup of
+    // each row tile publishes the map for the split-K reduction.
     int rb_ = -1, rp_ = 0;
-    map_row(g, m0 + t, rb_, rp_);
+    if (t < BMT) map_row(g, m0 + t, rb_, rp_);
     rowb[t] = rb_;
     rowp[t] = rp_;
-    if (g.ksplit > 1 && split == 0 && ct == 0 && m0 + t < g.m_max)
+    if (g.ksplit > 1 && split == 0 && ct == 0 && t < BMT && m0 + t < g.m_max)
         *reinterpret_cast<int2*>(g.rowmap + 2 * (m0 + t)) = make_int2(rb_, rp_);
     if (!__syncthreads_or(rb_ >= 0)) return;             // no row of this tile maps anywhere (uniform)
 
     // DMA sources: instruction i of wave w moves rows 16(w + 4i) .. +15 of a
-    // slot; lane l fills chunk l%4 of row 16(w + 4i) + l/4, i.e. logical
-    // chunk (l%4) ^ swizzle(row).  Rows that map to nothing read row 0 of the
+    // slot (i < MI for the input rows, i < 4 for the 256 weight rows); lane l
+    // fills chunk l%4 of row 16(w + 4i) + l/4, i.e. logical chunk
+    // (l%4) ^ swizzle(row).  Rows that map to nothing read row 0 of the
     // input, columns past N weight row 0; neither is stored.
-    const char* asrc[4];
+    const char* asrc[MI];
     const char* bsrc[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int r = 16 * (w + 4 * i) + (lane >> 2);
         const int chunk = ((lane & 3) ^ tile_sw(r)) << 4;
-        const int b = rowb[r];
-        const char* arow = b >= 0 ? g.x + (static_cast<size_t>(b) * g.seq + rowp[r]) * g.K * ES : g.x;
-        asrc[i] = arow + k0b + chunk;
+        if (i < MI) {
+            const int b = rowb[r];
+            const char* arow = b >= 0 ? g.x + (static_cast<size_t>(b) * g.seq + rowp[r]) * g.K * ES : g.x;
+            asrc[i] = arow + k0b + chunk;
+        }
         const char* brow = weight_row(g, n0 + r, ES);
         bsrc[i] = (brow ? brow : g.w0) + k0b + chunk;
     }
@@ -553,7 +565,7 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) dma16(bsrc[i] + off, bbuf + 16 * (w + 4 * i) * kTileStage);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) dma16(asrc[i] + off, abuf + 16 * (w + 4 * i) * kTileStage);
+        for (int i = 0; i < MI; ++i) dma16(asrc[i] + off, abuf + 16 * (w + 4 * i) * kTileStage);
     };
 
     // Fragment offsets: lane l reads row 32i + l%32 of its wave's block at
@@ -561,50 +573,54 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
     const int fr = lane & 31;
     const int fsw = tile_sw(fr);                         // = tile_sw(32i + fr)
     const int h = lane >> 5;
-    const int aoff0 = (128 * wm + fr) * kTileStage + (((0 + h) ^ fsw) << 4);
-    const int aoff1 = (128 * wm + fr) * kTileStage + (((2 + h) ^ fsw) << 4);
+    const int aoff0 = (32 * MI * wm + fr) * kTileStage + (((0 + h) ^ fsw) << 4);
+    const int aoff1 = (32 * MI * wm + fr) * kTileStage + (((2 + h) ^ fsw) << 4);
     const int boff0 = (128 * wn + fr) * kTileStage + (((0 + h) ^ fsw) << 4);
     const int boff1 = (128 * wn + fr) * kTileStage + (((2 + h) ^ fsw) << 4);
 
-    floatx16 acc[4][4];
+    floatx16 acc[MI][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    uint4 fa0[4], fb0[4], fa1[4], fb1[4];                // fragments of half 0 / half 1
-    auto read_half = [&](const char* abuf, const char* bbuf, int aoff, int boff, uint4 (&fa)[4], uint4 (&fb)[4]) {
+    uint4 fa0[MI], fb0[4], fa1[MI], fb1[4];              // fragments of half 0 / half 1
+    auto read_half = [&](const char* abuf, const char* bbuf, int aoff, int boff, uint4 (&fa)[MI], uint4 (&fb)[4]) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) fa[i] = *reinterpret_cast<const uint4*>(abuf + aoff + i * 32 * kTileStage);
+        for (int i = 0; i < MI; ++i) fa[i] = *reinterpret_cast<const uint4*>(abuf + aoff + i * 32 * kTileStage);
 #pragma unroll
         for (int j = 0; j < 4; ++j) fb[j] = *reinterpret_cast<const uint4*>(bbuf + boff + j * 32 * kTileStage);
     };
-    auto mfma_half = [&](const uint4 (&fa)[4], const uint4 (&fb)[4]) {
+    auto mfma_half = [&](const uint4 (&fa)[MI], const uint4 (&fb)[4]) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < MI; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc[i][j] = Mma32<true>::step(fa[i], fb[j], acc[i][j]);
     };
-    // Instruction order of a half: the 8 fragment reads for the next half
-    // go out behind the first two MFMAs (so they land well before the next
-    // half starts), the DMA instructions (second half only) behind the next
-    // four, then the remaining MFMAs.
+    // Instruction order of a half: the MI + 4 fragment reads for the next
+    // half go out behind the first two MFMAs (so they land well before the
+    // next half starts), the NDMA DMA instructions (second half only) two
+    // behind each of the next MFMAs, then the remaining MFMAs.
     auto interleave = [&](bool with_dma) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, MI, 0);
         if (with_dma) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
+            for (int q = 0; q < NDMA / 2; ++q) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, 10, 0);
+            if constexpr (NDMA % 2) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 4 * MI - 2 - (NDMA + 1) / 2, 0);
         } else {
-            __builtin_amdgcn_sched_group_barrier(0x008, 14, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 4 * MI - 2, 0);
         }
     };
 
@@ -652,10 +668,11 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
     // acc[i][j] is row 32i + 8(e/4) + 4(l/32) + e%4, column 32j + l%32 of the
     // wave's block; each lane then moves 8 consecutive columns of a row.
     constexpr int EP = 132;                              // fp32 pitch of a staged row
+    static_assert(16 * EP * 4 <= ASLOT, "a wave's 16 staged rows fit its input slot");
     float* ep = reinterpret_cast<float*>(w == 0 ? sa0 : w == 1 ? sa1 : w == 2 ? sa2 : sa3);
     const int cbase = n0 + 128 * wn;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < MI; ++i) {
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
 #pragma unroll
@@ -672,7 +689,7 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
             for (int q = 0; q < 4; ++q) {
                 const int idx = 64 * q + lane;           // 16 rows x 16 chunks of 8 columns
                 const int r = idx >> 4, c = (idx & 15) * 8;
-                const int lr = 128 * wm + 32 * i + 16 * hh + r;   // row within the tile
+                const int lr = 32 * MI * wm + 32 * i + 16 * hh + r;   // row within the tile
                 const int b = rowb[lr];
                 const int n = cbase + c;
                 const float* v = ep + r * EP + c;

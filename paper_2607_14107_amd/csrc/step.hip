@@ -114,11 +114,11 @@ struct ReduceArgs {
     int n_r;
 };
 
-// refresh on the 256 x 256 tile kernel, unsplit | Q split-K reduce: the tile
+// refresh on the tile kernel, unsplit | Q split-K reduce: the tile
 // workgroups come first (tile_body's XCD-aware order counts from id 0), the
-// reduction's after them on the compute units the tiles leave free (192 tiles
-// on 256 CUs at the batch-8 LLaDA-8B layer's 10% stale), so the Q reduce
-// needs no launch of its own (bf16 only, as the tile kernel).
+// reduction's after them, on compute units the tiles leave free or as a short
+// tail, so the Q reduce needs no launch of its own (bf16 only, as the tile
+// kernel).
 struct TileQArgs {
     GemmArgs r;    // refresh (n_tile workgroups, first)
     GemmArgs q;    // Q projection
@@ -127,9 +127,10 @@ struct TileQArgs {
 
 static_assert(kTileThreads == kGemmBlock, "the tile and reduce roles share one workgroup size");
 
+template <int MI>
 __global__ __launch_bounds__(kTileThreads) void tile_qred_kernel(TileQArgs k) {
     if (static_cast<int>(blockIdx.x) < k.n_tile) {
-        tile_body(k.r, blockIdx.x);
+        tile_body<MI>(k.r, blockIdx.x);
         return;
     }
     reduce_body<true>(k.q, blockIdx.x - k.n_tile);
@@ -458,7 +459,10 @@ extern "C" polestar_status polestar_step(const polestar_step_args* a, void* work
         tq.r = rg;
         tq.q = f.q;
         tq.n_tile = L.rp.grid;
-        hipLaunchKernelGGL(tile_qred_kernel, dim3(L.rp.grid + n_qred), dim3(kTileThreads), 0, stream, tq);
+        if (L.rp.tile_mi == 3)
+            hipLaunchKernelGGL(tile_qred_kernel<3>, dim3(L.rp.grid + n_qred), dim3(kTileThreads), 0, stream, tq);
+        else
+            hipLaunchKernelGGL(tile_qred_kernel<4>, dim3(L.rp.grid + n_qred), dim3(kTileThreads), 0, stream, tq);
         st = launch_status();
         if (st != POLESTAR_OK) return st;
     } else {

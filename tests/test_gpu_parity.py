@@ -261,7 +261,8 @@ def test_refresh_large_configs_sampled(P, cfg_index, subrun):
 def test_refresh_row_counts_around_one_tile(P, counts, k_max):
     """Refresh row sets on the LLaDA-8B-shaped weights: 65..160 rows (one row
     tile, the DMA-staged GEMM), the first two-tile case, and 352..1264 rows
-    (256 x 256 tiles with a ragged last row tile, K split in 2 or 4); slots
+    (192 x 256 tiles, unsplit or K split in 2 or 4, the last row tile
+    ragged); slots
     past a sequence's count and an out-of-range index refresh nothing."""
     torch = _torch()
     L = layer(1)

@@ -69,14 +69,24 @@ def test_noalloc_matches_refresh_kv_twice(P):
 
 
 def test_noalloc_refuses_shapes_beyond_its_array(P):
-    c = _case(73, 24, 96, 4096, 32, 128, 64, 32, 60)
-    assert P.refresh_kv_workspace_size(P.BF16, 24, 4096, 32, 128, 60, 32) > P.refresh_kv_noalloc_max_bytes()
+    # 8 sequences x (100 stale + 32 block) rows onto 64 x 128 K and V columns
+    # from d = 8192: the plan splits K, and its partials (132 MiB) exceed the
+    # array.  The call is refused before anything is enqueued, so the inputs
+    # are never read (uninitialised device tensors).
     import torch
-    h, w_k, w_v = (to_dev(c[k], "bf16") for k in ("h", "w_k", "w_v"))
-    k2, v2 = to_dev(c["kc"], "bf16"), to_dev(c["vc"], "bf16")
+    batch, seq, d, kvh, hd, bs, bl, k_max = 8, 160, 8192, 64, 128, 128, 32, 100
+    assert P.refresh_kv_workspace_size(P.BF16, batch, d, kvh, hd, k_max, bl) > P.refresh_kv_noalloc_max_bytes()
+    g = np.random.default_rng(73)
+    idx = np.stack([np.sort(g.choice(bs, size=k_max, replace=False)) for _ in range(batch)]).astype(np.int32)
+    cnt = np.full(batch, k_max, dtype=np.int32)
+    h = torch.empty((batch, seq, d), dtype=torch.bfloat16, device="cuda")
+    w_k = torch.empty((kvh * hd, d), dtype=torch.bfloat16, device="cuda")
+    w_v = torch.empty((kvh * hd, d), dtype=torch.bfloat16, device="cuda")
+    k2 = torch.randn((batch, seq, kvh, hd), device="cuda").to(torch.bfloat16)
+    v2 = torch.randn((batch, seq, kvh, hd), device="cuda").to(torch.bfloat16)
+    k0, v0 = k2.clone(), v2.clone()
     with pytest.raises(P.PolestarError) as e:
-        P.refresh_kv_noalloc(h, torch.from_numpy(c["idx"]).cuda(), torch.from_numpy(c["cnt"]).cuda(),
-                             c["bs"], c["bl"], w_k, w_v, k2, v2)
+        P.refresh_kv_noalloc(h, torch.from_numpy(idx).cuda(), torch.from_numpy(cnt).cuda(), bs, bl, w_k, w_v, k2, v2)
     assert e.value.status == 4       # POLESTAR_ERR_WORKSPACE, nothing enqueued
     torch.cuda.synchronize()
-    assert np.array_equal(from_dev(k2), c["kc"])
+    assert torch.equal(k2, k0) and torch.equal(v2, v0)
