@@ -256,8 +256,8 @@ __global__ __launch_bounds__(kGemmBlock) void gemm_dma_kernel(GemmArgs g) {
     dma_body<BF16, MT, NST, 4, NTW>(g, blockIdx.x);
 }
 
-template <int MI>
-__global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmArgs g) { tile_body<MI>(g, blockIdx.x); }
+template <int MI, int NJ>
+__global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(GemmArgs g) { tile_body<MI, NJ>(g, blockIdx.x); }
 
 // Sum of the split-K partials, in split order (deterministic): thread ->
 // (column tile, row, 8 columns) so that consecutive threads read consecutive
@@ -393,7 +393,7 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     }
     p.small = false;
     p.col_tiles = ceil_div(N, 128);                     // split-K partials: 128-column tiles
-    // Tile kernel: more rows than one DMA tile; 256- or 192-row x 256-column tiles, K split
+    // Tile kernel: more rows than one DMA tile; 256- or 192-row x 256- or 192-column tiles, K split
     // while the tiles alone leave compute units idle.  Measured against the
     // other kernels it wins when it launches at least 128 workgroups and at
     // most four splits fill the chip, each split still runs 48 stages or
@@ -412,12 +412,13 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
     const bool narrow_dma = bf16 && dma_k && N <= 4 * kTileDim && m_max <= 8L * 16 * kDmaMaxRowTiles;
     if (bf16 && m_max > 16L * kDmaMaxRowTiles && K % kTileStage == 0 && !narrow_dma) {
         const int nstage = K / (kTileStage / 2);
-        // The tile height and split with the least estimated time: ceil(tiles
+        // The tile shape and split with the least estimated time: ceil(tiles
         // * k / 256) rounds of one workgroup per CU, each 1/k of a tile's
         // work (a whole 256 x 256 x K tile at the ~1 PFLOP/s this kernel
-        // sustains: 3.9 GFLOP/ms per CU; a 192-row tile at kTile192Rate of
-        // that rate), plus the fp32 partials of a split run written and read
-        // back (8 k M N bytes at ~5 TB/s); ties keep the 256-row tile.
+        // sustains: 3.9 GFLOP/ms per CU; a 192-row or 192-column tile at
+        // kTile192Rate of that rate, 192 x 192 at its square), plus the fp32
+        // partials of a split run written and read back (8 k M N bytes at
+        // ~5 TB/s); ties keep the larger tile, rows before columns.
         // Measured on the batch-8 LLaDA-8B refresh: 192 tiles of 256 rows
         // (10% stale) unsplit in one round 130 us, in two splits (384
         // workgroups, a round and a half, 98 MB of partials) 159 us, as 256
@@ -426,34 +427,42 @@ GemmPlan gemm_plan(bool bf16, long m_max, int N, int K) {
         // 192-row plans it picks ran 3-15% faster than the best 256-row ones
         // (512 x 4096 x 4096: 47.6 against 50.9 us; 1264 x 8192 x 4096: 95.1
         // against 110.3 us).  Every split runs a whole number of 4-stage loop
-        // trips and at least 16 stages.
-        int ksplit = 1, mi = 4;
+        // trips and at least 16 stages.  192-column tiles moved the 512-row
+        // projections of a 32-layer stack's block-only forwards (12288 and
+        // 24576 columns) from 192 to 256 workgroups: those forwards 13.9 ->
+        // 13.4 ms.
+        int ksplit = 1, mi = 4, nj = 4;
         double best = 1e30;
-        for (int cand = 4; cand >= 3; --cand) {
-            const int rows = 64 * cand;
-            const long tiles = static_cast<long>(ceil_div(m_max, rows)) * ceil_div(N, kTileDim);
-            const double tile_us = rows * 256.0 * 2.0 * K / (3.9e6 * (cand == 4 ? 1.0 : kTile192Rate));
-            for (int k = 1; k <= kMaxSplit; ++k) {
-                if (nstage % (4 * k) != 0 || nstage / k < 16) continue;
-                const double rounds = static_cast<double>((tiles * k + kTargetWgs - 1) / kTargetWgs);
-                const double cost = rounds * tile_us / k + (k > 1 ? 8.0 * k * m_max * N / 5e6 : 0.0);
-                if (cost < best) {
-                    best = cost;
-                    ksplit = k;
-                    mi = cand;
+        for (int cm = 4; cm >= 3; --cm) {
+            for (int cn = 4; cn >= 3; --cn) {
+                const int rows = 64 * cm, cols = 64 * cn;
+                const long tiles = static_cast<long>(ceil_div(m_max, rows)) * ceil_div(N, cols);
+                const double rate = (cm == 4 ? 1.0 : kTile192Rate) * (cn == 4 ? 1.0 : kTile192Rate);
+                const double tile_us = static_cast<double>(rows) * cols * 2.0 * K / (3.9e6 * rate);
+                for (int k = 1; k <= kMaxSplit; ++k) {
+                    if (nstage % (4 * k) != 0 || nstage / k < 16) continue;
+                    const double rounds = static_cast<double>((tiles * k + kTargetWgs - 1) / kTargetWgs);
+                    const double cost = rounds * tile_us / k + (k > 1 ? 8.0 * k * m_max * N / 5e6 : 0.0);
+                    if (cost < best) {
+                        best = cost;
+                        ksplit = k;
+                        mi = cm;
+                        nj = cn;
+                    }
                 }
             }
         }
         p.tile_mi = mi;
+        p.tile_nj = nj;
         p.row_tiles = ceil_div(m_max, 64 * mi);
-        const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, kTileDim);
+        const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, 64 * nj);
         p.tile = tiles * ksplit >= kTargetWgs / 2 &&
                  (ksplit <= 4 || nstage / ksplit >= 48 || p.row_tiles >= 4);
         p.ksplit = ksplit;
     }
     if (p.tile) {
         const int nstage = K / (kTileStage / 2);
-        const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, kTileDim);
+        const long tiles = static_cast<long>(p.row_tiles) * ceil_div(N, 64 * p.tile_nj);
         const int ksplit = p.ksplit;
         p.steps_per_split = nstage / ksplit;
         p.mt = 2 * p.tile_mi;
@@ -536,16 +545,25 @@ int gemm_reduce_blocks(const GemmPlan& p, const GemmArgs& g) {
     return ceil_div(static_cast<long>(p.col_tiles) * g.m_max * 16, kGemmBlock);
 }
 
+// The tile kernel of the plan's tile shape (false for a shape not instantiated).
+static bool launch_tile(const GemmPlan& p, const GemmArgs& g, hipStream_t stream) {
+    const dim3 grid(p.grid), block(kTileThreads);
+    switch (10 * p.tile_mi + p.tile_nj) {
+        case 44: hipLaunchKernelGGL((gemm_tile_kernel<4, 4>), grid, block, 0, stream, g); return true;
+        case 43: hipLaunchKernelGGL((gemm_tile_kernel<4, 3>), grid, block, 0, stream, g); return true;
+        case 34: hipLaunchKernelGGL((gemm_tile_kernel<3, 4>), grid, block, 0, stream, g); return true;
+        case 33: hipLaunchKernelGGL((gemm_tile_kernel<3, 3>), grid, block, 0, stream, g); return true;
+        default: return false;
+    }
+}
+
 polestar_status gemm_run(bool bf16, const GemmPlan& p, GemmArgs g, hipStream_t stream, GemmArgs* deferred) {
     gemm_finalize_args(p, g);
     bool ok;
     if (p.small) ok = bf16 ? dispatch_small<true>(p, g, stream) : dispatch_small<false>(p, g, stream);
     else if (p.tile) {
         ok = bf16 && p.steps_per_split % 4 == 0;
-        if (ok && p.tile_mi == 3)
-            hipLaunchKernelGGL(gemm_tile_kernel<3>, dim3(p.grid), dim3(kTileThreads), 0, stream, g);
-        else if (ok)
-            hipLaunchKernelGGL(gemm_tile_kernel<4>, dim3(p.grid), dim3(kTileThreads), 0, stream, g);
+        if (ok) ok = launch_tile(p, g, stream);
     } else if (p.dma) ok = bf16 && dispatch_dma<true>(p, g, stream);
     else ok = bf16 ? dispatch_rows<true>(p, g, stream) : dispatch_rows<false>(p, g, stream);
     if (!ok) return POLESTAR_ERR_UNSUPPORTED;

@@ -40,8 +40,9 @@ struct GemmPlan {
     bool small;         // gemm_small_kernel (<= 64 rows) instead of gemm_rows_kernel
     bool dma;           // gemm_dma_kernel (17..320 rows in up to two row tiles, up to 1280 in eight for
                         // outputs of <= 1024 columns; operands DMA'd into LDS)
-    bool tile;          // gemm_tile_kernel (bf16, more than 160 rows: 256- or 192-row x 256-column tiles)
+    bool tile;          // gemm_tile_kernel (bf16, more than 160 rows: 256- or 192-row x 256- or 192-column tiles)
     int tile_mi;        // tile kernel: 32-row MFMA tiles per wave down the rows (4: 256-row tiles, 3: 192)
+    int tile_nj;        // tile kernel: 32-column MFMA tiles per wave across (4: 256-column tiles, 3: 192)
     int mt;             // MFMA row tiles per workgroup (16 rows: small and dma kernels; 32: rows and tile kernels)
     int row_tiles;
     int col_tiles;

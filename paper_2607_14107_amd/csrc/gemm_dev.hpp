@@ -459,14 +459,16 @@ __device__ __forceinline__ void dma_body(const GemmArgs& g, int blk) {
 
 
 // ---------------------------------------------------------------------------
-// tile_body (gemm_tile_kernel, and the fused step's refresh): 256 x 256 or
-// 192 x 256 outputs per workgroup for row sets of more than one DMA tile
-// (the refresh of a whole batch, the dense rows of a stack).  The four waves
-// form a 2 x 2 grid of 128 x 128 (or 96 x 128) blocks, each 4 x 4 (3 x 4)
-// tiles of v_mfma_f32_32x32x16_bf16, so every fragment read from LDS feeds
-// three or four MFMAs (the row kernels of gemm.hip read one A fragment per
-// MFMA).  The plan takes 192-row tiles where 256-row ones would leave compute
-// units idle (1488 rows x 8192 columns: 256 tiles instead of 192).
+// tile_body (gemm_tile_kernel, and the fused step's refresh): 256 or 192
+// rows x 256 or 192 columns of outputs per workgroup for row sets of more
+// than one DMA tile (the refresh of a whole batch, the dense rows of a
+// stack).  The four waves form a 2 x 2 grid of blocks of MI x NJ tiles of
+// v_mfma_f32_32x32x16_bf16 (MI, NJ = 4 or 3), so every fragment read from LDS
+// feeds three or four MFMAs (the row kernels of gemm.hip read one A fragment
+// per MFMA).  The plan takes 192-row or 192-column tiles where 256 x 256 ones
+// would leave compute units idle (1488 rows x 8192 columns: 256 tiles of 192
+// rows instead of 192 tiles; 512 rows x 12288: 128 tiles of 192 columns in
+// two splits instead of 96).
 // Both operands arrive by DMA in stages of 64 bytes (32 bf16) of each row,
 // four LDS slots, three stages in flight; the DMA wait and barrier for stage
 // s+1 sit between the two halves of stage s, so the first fragments of s+1
@@ -489,8 +491,8 @@ __device__ __forceinline__ int tile_sw(int r) { return (r >> 2) & 3; }
 // walks bands of kTileGroupRows row tiles column by column, which keeps the
 // input rows and weight rows its compute units share in its own L2.  (The
 // tile workgroups must be the first ones of their launch.)
-__device__ __forceinline__ void tile_coords(const GemmArgs& g, int blk, int& split, int& rt, int& ct) {
-    const int ntc = (g.N + kTileDim - 1) / kTileDim;
+__device__ __forceinline__ void tile_coords(const GemmArgs& g, int bn, int blk, int& split, int& rt, int& ct) {
+    const int ntc = (g.N + bn - 1) / bn;
     const int ntiles = g.row_tiles * ntc;
     const int nb = ntiles * g.ksplit;
     int bid = blk;
@@ -506,28 +508,30 @@ __device__ __forceinline__ void tile_coords(const GemmArgs& g, int blk, int& spl
 
 constexpr int kTileThreads = 256;             // four waves, one per SIMD
 
-// MI: 32-row MFMA tiles per wave down the rows: 4 (256-row tiles) or 3
-// (192-row tiles, for row counts where 256-row tiles would leave compute
-// units idle; the columns stay 256 wide).
-template <int MI>
+// MI / NJ: 32-row / 32-column MFMA tiles per wave: 4 (256-row or -column
+// tiles) or 3 (192), for shapes where 256 x 256 tiles would leave compute
+// units idle.
+template <int MI, int NJ>
 __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
-    static_assert(MI == 3 || MI == 4, "192- or 256-row tiles");
+    static_assert((MI == 3 || MI == 4) && (NJ == 3 || NJ == 4), "192- or 256-row and -column tiles");
     constexpr int ES = 2;                                // bf16 operands
     constexpr int BMT = 64 * MI;                         // rows per tile (two waves down, MI tiles each)
+    constexpr int BNT = 64 * NJ;                         // columns per tile (two waves across, NJ tiles each)
     constexpr int ASLOT = BMT * kTileStage;
-    constexpr int NDMA = MI + 4;                         // DMA instructions per wave per stage (MI A, 4 B)
+    constexpr int BSLOT = BNT * kTileStage;
+    constexpr int NDMA = MI + NJ;                        // DMA instructions per wave per stage (MI A, NJ B)
     __shared__ __align__(16) char sa0[ASLOT], sa1[ASLOT], sa2[ASLOT], sa3[ASLOT];
-    __shared__ __align__(16) char sb0[kTileSlot], sb1[kTileSlot], sb2[kTileSlot], sb3[kTileSlot];
+    __shared__ __align__(16) char sb0[BSLOT], sb1[BSLOT], sb2[BSLOT], sb3[BSLOT];
     __shared__ int rowb[kTileDim], rowp[kTileDim];
 
     int split, rt, ct;
-    tile_coords(g, blk, split, rt, ct);
+    tile_coords(g, BNT, blk, split, rt, ct);
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int w = t >> 6;
     const int wm = w & 1, wn = w >> 1;
     const int m0 = rt * BMT;
-    const int n0 = ct * kTileDim;
+    const int n0 = ct * BNT;
     const int nss = g.steps_per_split;                   // stages of this split (a multiple of 4)
     const size_t k0b = static_cast<size_t>(split) * nss * kTileStage;
 
@@ -542,12 +546,12 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
     if (!__syncthreads_or(rb_ >= 0)) return;             // no row of this tile maps anywhere (uniform)
 
     // DMA sources: instruction i of wave w moves rows 16(w + 4i) .. +15 of a
-    // slot (i < MI for the input rows, i < 4 for the 256 weight rows); lane l
+    // slot (i < MI for the input rows, i < NJ for the weight rows); lane l
     // fills chunk l%4 of row 16(w + 4i) + l/4, i.e. logical chunk
     // (l%4) ^ swizzle(row).  Rows that map to nothing read row 0 of the
     // input, columns past N weight row 0; neither is stored.
     const char* asrc[MI];
-    const char* bsrc[4];
+    const char* bsrc[NJ];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int r = 16 * (w + 4 * i) + (lane >> 2);
@@ -557,13 +561,15 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
             const char* arow = b >= 0 ? g.x + (static_cast<size_t>(b) * g.seq + rowp[r]) * g.K * ES : g.x;
             asrc[i] = arow + k0b + chunk;
         }
-        const char* brow = weight_row(g, n0 + r, ES);
-        bsrc[i] = (brow ? brow : g.w0) + k0b + chunk;
+        if (i < NJ) {
+            const char* brow = weight_row(g, n0 + r, ES);
+            bsrc[i] = (brow ? brow : g.w0) + k0b + chunk;
+        }
     }
     auto issue = [&](int st, char* abuf, char* bbuf) {
         const int off = min(st, nss - 1) * kTileStage;   // past the split: re-read its last stage
 #pragma unroll
-        for (int i = 0; i < 4; ++i) dma16(bsrc[i] + off, bbuf + 16 * (w + 4 * i) * kTileStage);
+        for (int i = 0; i < NJ; ++i) dma16(bsrc[i] + off, bbuf + 16 * (w + 4 * i) * kTileStage);
 #pragma unroll
         for (int i = 0; i < MI; ++i) dma16(asrc[i] + off, abuf + 16 * (w + 4 * i) * kTileStage);
     };
@@ -575,37 +581,37 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
     const int h = lane >> 5;
     const int aoff0 = (32 * MI * wm + fr) * kTileStage + (((0 + h) ^ fsw) << 4);
     const int aoff1 = (32 * MI * wm + fr) * kTileStage + (((2 + h) ^ fsw) << 4);
-    const int boff0 = (128 * wn + fr) * kTileStage + (((0 + h) ^ fsw) << 4);
-    const int boff1 = (128 * wn + fr) * kTileStage + (((2 + h) ^ fsw) << 4);
+    const int boff0 = (32 * NJ * wn + fr) * kTileStage + (((0 + h) ^ fsw) << 4);
+    const int boff1 = (32 * NJ * wn + fr) * kTileStage + (((2 + h) ^ fsw) << 4);
 
-    floatx16 acc[MI][4];
+    floatx16 acc[MI][NJ];
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < NJ; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    uint4 fa0[MI], fb0[4], fa1[MI], fb1[4];              // fragments of half 0 / half 1
-    auto read_half = [&](const char* abuf, const char* bbuf, int aoff, int boff, uint4 (&fa)[MI], uint4 (&fb)[4]) {
+    uint4 fa0[MI], fb0[NJ], fa1[MI], fb1[NJ];            // fragments of half 0 / half 1
+    auto read_half = [&](const char* abuf, const char* bbuf, int aoff, int boff, uint4 (&fa)[MI], uint4 (&fb)[NJ]) {
 #pragma unroll
         for (int i = 0; i < MI; ++i) fa[i] = *reinterpret_cast<const uint4*>(abuf + aoff + i * 32 * kTileStage);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) fb[j] = *reinterpret_cast<const uint4*>(bbuf + boff + j * 32 * kTileStage);
+        for (int j = 0; j < NJ; ++j) fb[j] = *reinterpret_cast<const uint4*>(bbuf + boff + j * 32 * kTileStage);
     };
-    auto mfma_half = [&](const uint4 (&fa)[MI], const uint4 (&fb)[4]) {
+    auto mfma_half = [&](const uint4 (&fa)[MI], const uint4 (&fb)[NJ]) {
 #pragma unroll
         for (int i = 0; i < MI; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = Mma32<true>::step(fa[i], fb[j], acc[i][j]);
+            for (int j = 0; j < NJ; ++j) acc[i][j] = Mma32<true>::step(fa[i], fb[j], acc[i][j]);
     };
-    // Instruction order of a half: the MI + 4 fragment reads for the next
+    // Instruction order of a half: the MI + NJ fragment reads for the next
     // half go out behind the first two MFMAs (so they land well before the
     // next half starts), the NDMA DMA instructions (second half only) two
     // behind each of the next MFMAs, then the remaining MFMAs.
     auto interleave = [&](bool with_dma) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, NJ, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, MI, 0);
         if (with_dma) {
@@ -618,9 +624,9 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
                 __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, 4 * MI - 2 - (NDMA + 1) / 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, NJ * MI - 2 - (NDMA + 1) / 2, 0);
         } else {
-            __builtin_amdgcn_sched_group_barrier(0x008, 4 * MI - 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, NJ * MI - 2, 0);
         }
     };
 
@@ -670,13 +676,13 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
     constexpr int EP = 132;                              // fp32 pitch of a staged row
     static_assert(16 * EP * 4 <= ASLOT, "a wave's 16 staged rows fit its input slot");
     float* ep = reinterpret_cast<float*>(w == 0 ? sa0 : w == 1 ? sa1 : w == 2 ? sa2 : sa3);
-    const int cbase = n0 + 128 * wn;
+    const int cbase = n0 + 32 * NJ * wn;
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < NJ; ++j)
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const int ee = 8 * hh + e;
@@ -686,9 +692,9 @@ __device__ __forceinline__ void tile_body(const GemmArgs& g, int blk) {
             __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
             __builtin_amdgcn_wave_barrier();
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int idx = 64 * q + lane;           // 16 rows x 16 chunks of 8 columns
-                const int r = idx >> 4, c = (idx & 15) * 8;
+            for (int q = 0; q < NJ; ++q) {
+                const int idx = 64 * q + lane;           // 16 rows x 4 NJ chunks of 8 columns
+                const int r = idx / (4 * NJ), c = (idx % (4 * NJ)) * 8;
                 const int lr = 32 * MI * wm + 32 * i + 16 * hh + r;   // row within the tile
                 const int b = rowb[lr];
                 const int n = cbase + c;

@@ -127,10 +127,10 @@ struct TileQArgs {
 
 static_assert(kTileThreads == kGemmBlock, "the tile and reduce roles share one workgroup size");
 
-template <int MI>
+template <int MI, int NJ>
 __global__ __launch_bounds__(kTileThreads) void tile_qred_kernel(TileQArgs k) {
     if (static_cast<int>(blockIdx.x) < k.n_tile) {
-        tile_body<MI>(k.r, blockIdx.x);
+        tile_body<MI, NJ>(k.r, blockIdx.x);
         return;
     }
     reduce_body<true>(k.q, blockIdx.x - k.n_tile);
@@ -459,10 +459,14 @@ extern "C" polestar_status polestar_step(const polestar_step_args* a, void* work
         tq.r = rg;
         tq.q = f.q;
         tq.n_tile = L.rp.grid;
-        if (L.rp.tile_mi == 3)
-            hipLaunchKernelGGL(tile_qred_kernel<3>, dim3(L.rp.grid + n_qred), dim3(kTileThreads), 0, stream, tq);
-        else
-            hipLaunchKernelGGL(tile_qred_kernel<4>, dim3(L.rp.grid + n_qred), dim3(kTileThreads), 0, stream, tq);
+        const dim3 grid(L.rp.grid + n_qred), block(kTileThreads);
+        switch (10 * L.rp.tile_mi + L.rp.tile_nj) {
+            case 44: hipLaunchKernelGGL((tile_qred_kernel<4, 4>), grid, block, 0, stream, tq); break;
+            case 43: hipLaunchKernelGGL((tile_qred_kernel<4, 3>), grid, block, 0, stream, tq); break;
+            case 34: hipLaunchKernelGGL((tile_qred_kernel<3, 4>), grid, block, 0, stream, tq); break;
+            case 33: hipLaunchKernelGGL((tile_qred_kernel<3, 3>), grid, block, 0, stream, tq); break;
+            default: return POLESTAR_ERR_UNSUPPORTED;
+        }
         st = launch_status();
         if (st != POLESTAR_OK) return st;
     } else {

@@ -85,9 +85,12 @@ def test_embed_rmsnorm_swiglu_residual(P, dtype):
     ("bf16", 2, 300, 10, 261, 256, 400),     # rows kernel, split K, ragged tiles
     ("fp32", 2, 90, 0, 90, 320, 144),
     ("bf16", 1, 700, 0, 700, 512, 1536),     # rows kernel, several row tiles
-    ("bf16", 2, 1100, 30, 1000, 4096, 2000),  # 256x256-tile kernel: ragged rows and columns, K split 4
-    ("bf16", 1, 1300, 20, 1250, 2048, 2512),  # 192x256-tile kernel: ragged rows and columns, K split 2
-    ("bf16", 3, 320, 10, 300, 4096, 3008),    # 192x256-tile kernel: 900 rows of three sequences, K split 4
+    ("bf16", 1, 400, 10, 385, 4096, 6480),    # 256x256-tile kernel: ragged rows and columns, K split 4
+    ("bf16", 2, 1100, 30, 1000, 4096, 2000),  # 192x192-tile kernel: ragged rows and columns, K split 2
+    ("bf16", 1, 1300, 20, 1250, 2048, 2512),  # 192x192-tile kernel: ragged rows and columns, K split 2
+    ("bf16", 3, 320, 10, 300, 4096, 3008),    # 256x192-tile kernel: 900 rows of three sequences, K split 4
+    ("bf16", 1, 460, 5, 450, 2048, 16736),    # 256x192-tile kernel, unsplit, ragged last column tile
+    ("bf16", 2, 210, 3, 200, 4096, 2800),     # rows kernel, K split 6 (too short a split for two tile rows)
     ("bf16", 1, 4000, 0, 4000, 1024, 8000),   # tile kernel, no K split, ragged last column tile
     ("bf16", 1, 1100, 0, 1052, 3584, 1024),   # tile kernel, K split 7 (16 stages each)
     ("bf16", 2, 200, 20, 150, 4096, 1008),    # DMA kernel, two row tiles, ragged columns
