@@ -79,9 +79,10 @@ def test_refresh_noalloc_validation_and_limit(L):
     assert f(*a) == UNSUPPORTED                               # head_dim
     a = list(args); a[15] = MISALIGNED
     assert f(*a) == UNSUPPORTED
-    # 24 sequences x (60 stale + 32 block rows) at LLaDA-8B width: 138 MiB of partials
-    assert ps.refresh_kv_workspace_size(ps.BF16, 24, 4096, 32, 128, 60, 32) > limit
-    big = [1, 24, 768, 4096, 32, 128, FAKE, FAKE, FAKE, 60, 512, 32, FAKE, FAKE, FAKE, FAKE, None]
+    # 8 sequences x (100 stale + 32 block rows) onto 64 x 128 K and V columns
+    # from d = 8192: the plan splits K, 132 MiB of partials
+    assert ps.refresh_kv_workspace_size(ps.BF16, 8, 8192, 64, 128, 100, 32) > limit
+    big = [1, 8, 160, 8192, 64, 128, FAKE, FAKE, FAKE, 100, 128, 32, FAKE, FAKE, FAKE, FAKE, None]
     assert f(*big) == WORKSPACE
 
 
