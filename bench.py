@@ -195,14 +195,14 @@ def roofline_numbers(nbytes, flops, us, dtype):
 CALL_SOURCES = {
     "refresh_kv": ("gemm.hip", "gemm.hpp", "gemm_dev.hpp", "step.hip"),
     "project_q": ("attend.hip", "gemm.hip", "gemm.hpp", "gemm_dev.hpp"),
-    "attend": ("attend.hip", "attend_dev.hpp"),
+    "attend": ("attend.hip", "attend_dev.hpp", "attend_ring.hip"),
     "drift": ("drift.hip", "drift_dev.hpp"),
     "select": ("select.hip", "select_dev.hpp"),
     "commit": ("commit.hip", "commit_dev.hpp"),
     "gather": ("model.hip",),
     "scatter": ("model.hip",),
     "step": ("step.hip", "drift_dev.hpp", "select_dev.hpp", "gemm_dev.hpp", "gemm.hip", "attend_dev.hpp",
-             "commit_dev.hpp"),
+             "attend_ring.hip", "commit_dev.hpp"),
 }
 
 

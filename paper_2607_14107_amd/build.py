@@ -21,7 +21,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpolestar.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "drift.hip", "select.hip", "gemm.hip", "attend.hip", "commit.hip", "step.hip",
+SOURCES = ["api.hip", "drift.hip", "select.hip", "gemm.hip", "attend.hip", "attend_ring.hip", "commit.hip", "step.hip",
            "proxy.hip", "model.hip", "codec.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

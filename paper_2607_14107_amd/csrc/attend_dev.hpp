@@ -30,6 +30,10 @@ constexpr int kQG = 32;          // queries per workgroup
 constexpr int kKT = 32;          // keys per tile
 constexpr float kLazy = 8.f;     // log2 headroom of the lazy softmax reference
 
+}  // namespace
+
+// Outside the anonymous namespace: the ring kernel (attend_ring.hip) is
+// launched from the other files through launch_att_ring.
 struct AttArgs {
     const char* q;       // [batch][nq][H][hd]
     const char* k;       // [batch][seq][Hkv][hd]
@@ -42,6 +46,11 @@ struct AttArgs {
     int splits, tiles_per_split;
     float scale_log2;    // scale * log2(e)
 };
+
+// attend_ring_kernel<hd> over `grid` (attend_ring.hip; hd 64 or 128, bf16).
+void launch_att_ring(int hd, dim3 grid, const AttArgs& a, hipStream_t s);
+
+namespace {
 
 // Position of key kk (0..31) of a tile in the LDS row of V^T: lane group g
 // reads slots 8g..8g+7 = keys 4g..4g+3 and 16+4g..16+4g+3 (bf16 path).
@@ -732,13 +741,16 @@ struct AttPlan {
     int group_waves;     // 0: attend_kernel; 8: attend_group_kernel (its tiles_per_split then counts
                          // 64-key steps)
     int row_blocks;      // grouped: workgroups per (sequence, KV head, split)
+    bool ring;           // attend_ring_kernel (attend_ring.hip): one workgroup per CU, three tiles in flight per wave
 };
 
 // Plan of the attention launch.  Grouped heads (bf16, at least four (query
 // head, 32-query group) pairs per KV head) take attend_group_kernel: 8-wave
 // workgroups (two waves per SIMD), keys split so that about 256 workgroups
 // run (one round, one per CU); each split adds an fp32 (m, l, O) partial per
-// query row, so no more splits than that.  Everything else attend_kernel.
+// query row, so no more splits than that.  bf16 with at least four tiles per
+// wave at about 256 workgroups: attend_ring_kernel.  Everything else
+// attend_kernel.
 inline AttPlan att_plan(bool bf16, int batch, int seq, int H, int Hkv, int nq, int hd) {
     AttPlan p{};
     const int ntiles = ceil_div(seq, kKT);
@@ -760,10 +772,32 @@ inline AttPlan att_plan(bool bf16, int batch, int seq, int H, int Hkv, int nq, i
         return p;
     }
     const long base = static_cast<long>(batch) * H * ceil_div(nq, kQG);
+    const int max_splits = ceil_div(ntiles, 4);      // at least one tile per wave
+    // bf16 with long key ranges: the ring kernel, about 256 workgroups (one
+    // per CU, one round), while every wave still walks at least 4 tiles (the
+    // batch-8 LLaDA-8B layer: one split, 12 tiles per wave, attention + merge
+    // 50.2 -> 45.2 us; at batch 1 the six splits leave one tile per wave and
+    // the plain kernel stays; more than 256 (sequence, head, query group)
+    // rows, as in a batch-16 stack, keep the plain kernel's one round)
+    if (bf16 && base <= 256) {
+        int rs = static_cast<int>(256 / base);
+        if (rs > max_splits) rs = max_splits;
+        if (rs < 1) rs = 1;
+        const int tps = ceil_div(ntiles, rs);
+        if (tps >= 16) {
+            p.ring = true;
+            p.tiles_per_split = tps;
+            p.splits = ceil_div(ntiles, tps);
+            if (p.splits > 1) {
+                const size_t rows = static_cast<size_t>(batch) * H * nq * p.splits;
+                p.part_bytes = align_up(rows * hd * sizeof(float), 256) + align_up(rows * 2 * sizeof(float), 256);
+            }
+            return p;
+        }
+    }
     // about 512 workgroups, rounded down: two fit per CU, so a grid of at most
     // 512 runs in one round without a partial second one
     int splits = static_cast<int>(512 / base);
-    const int max_splits = ceil_div(ntiles, 4);      // at least one tile per wave
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
     p.tiles_per_split = ceil_div(ntiles, splits);
@@ -785,6 +819,12 @@ void launch_att(const AttPlan& p, const AttArgs& a, hipStream_t s) {
         }
     }
     dim3 grid(p.splits, a.H * ceil_div(a.nq, kQG), a.batch);
+    if constexpr (BF16) {
+        if (p.ring) {
+            launch_att_ring(HD, grid, a, s);
+            return;
+        }
+    }
     hipLaunchKernelGGL((attend_kernel<BF16, HD>), grid, dim3(kAttBlock), 0, s, a);
 }
 

@@ -65,6 +65,30 @@ def test_attend_random_shapes(P, case):
     np.testing.assert_allclose(from_dev(lse), lse_want, rtol=RTOL[dtype], atol=RTOL[dtype], err_msg=shape)
 
 
+@pytest.mark.parametrize("batch,seq,nq,H,Hkv,hd", [
+    (4, 2100, 32, 16, 16, 64),     # 66 key tiles (the last ragged) in 4 splits of 17: head_dim 64
+    (4, 1600, 20, 24, 12, 128),    # two query heads per KV head, 20 queries, 2 splits of 25 tiles
+    (1, 4200, 32, 64, 64, 128),    # 132 key tiles in 4 splits of 33: long walks per wave
+])
+def test_attend_ring_kernel_shapes(P, batch, seq, nq, H, Hkv, hd):
+    """bf16 shapes whose plan takes the ring kernel (one workgroup per CU,
+    at least four key tiles per wave), against the oracle."""
+    dtype = "bf16"
+    g = np.random.default_rng(seq + nq + H)
+    bs = seq // 3
+    q = inputs.store(g.standard_normal((batch, nq, H, hd), dtype=np.float32), dtype)
+    kc = inputs.store(g.standard_normal((batch, seq, Hkv, hd), dtype=np.float32), dtype)
+    vc = inputs.store(g.standard_normal((batch, seq, Hkv, hd), dtype=np.float32), dtype)
+    torch = pytest.importorskip("torch")
+    lse = torch.empty((batch, H, nq), dtype=torch.float32, device="cuda")
+    out, _ = P.attend(None, None, to_dev(kc, dtype), to_dev(vc, dtype), bs, nq, H,
+                      q_buf=to_dev(q, dtype), lse=lse)
+    o_want, lse_want = ref.attend(ref.decode(q, dtype), ref.decode(kc, dtype), ref.decode(vc, dtype))
+    shape = f"b{batch} seq{seq} nq{nq} H{H}/{Hkv} hd{hd}"
+    assert_rows_close(ref.decode(from_dev(out), dtype), o_want, RTOL[dtype], "output " + shape)
+    np.testing.assert_allclose(from_dev(lse), lse_want, rtol=RTOL[dtype], atol=RTOL[dtype], err_msg=shape)
+
+
 def _gemm_dims(g, dtype):
     # d: K split into 8..16 stages per split for the DMA kernel at several of these
     d = int(g.choice([128, 256, 640, 1280, 1536, 1792, 2048])) if dtype == "bf16" else int(g.choice([128, 256, 512]))
