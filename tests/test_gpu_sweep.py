@@ -3,9 +3,11 @@ and K/V-refresh entry points, each checked against the CPU oracle.
 
 The shapes are drawn so that every launch plan gets exercised: per-head and
 grouped-head attention (4 or 8 waves, idle waves, one or many key splits,
-ragged key tiles and query groups), and the GEMM plans (small-M kernel, DMA
-kernel with up to eight row tiles and 8 to 16 stages per split, row kernel)
-with ragged row tiles and refresh row counts.  Tolerances as in
+ragged key tiles and query groups; the ring kernel for long key ranges), and
+the GEMM plans (small-M kernel, DMA kernel with up to eight row tiles and 8
+to 16 stages per split, row kernel, and through polestar_linear the tile
+kernel's 256- or 192-row by 256- or 192-column tiles) with ragged row tiles
+and refresh row counts.  Tolerances as in
 test_gpu_parity: fp32 1e-4, bf16 2e-2 relative per (row, head); rows the
 refresh does not touch byte-identical.
 """
@@ -94,6 +96,28 @@ def _gemm_dims(g, dtype):
     d = int(g.choice([128, 256, 640, 1280, 1536, 1792, 2048])) if dtype == "bf16" else int(g.choice([128, 256, 512]))
     hd = int(g.choice([64, 128]))
     return d, hd
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_linear_random_tile_shapes(P, case):
+    """Row counts and widths where the tile kernel's plans compete (256- or
+    192-row by 256- or 192-column tiles, unsplit or split K), ragged in both
+    directions, bf16."""
+    torch = pytest.importorskip("torch")
+    g = np.random.default_rng(17000 + case)
+    batch = int(g.integers(1, 4))
+    n = int(g.integers(200, 1600)) // batch
+    rs = int(g.integers(0, 40))
+    seq = n + rs + int(g.integers(0, 30))
+    K = int(g.choice([1024, 2048, 3072, 4096]))
+    N = 16 * int(g.integers(16, 376))                      # 256 .. 6000 columns
+    x = inputs.store(g.standard_normal((batch, seq, K)).astype(np.float32), "bf16")
+    w = inputs.store((g.standard_normal((N, K)) * 0.05).astype(np.float32), "bf16")
+    y = torch.empty((batch, n, N), dtype=torch.bfloat16, device="cuda")
+    P.linear(to_dev(x, "bf16"), rs, n, to_dev(w, "bf16"), y)
+    want = ref.decode(x, "bf16")[:, rs:rs + n] @ ref.decode(w, "bf16").T
+    assert_rows_close(ref.decode(from_dev(y), "bf16"), want, RTOL["bf16"],
+                      f"linear {batch}x{n} rows x {N} x K {K}")
 
 
 @pytest.mark.parametrize("case", range(16))
