@@ -753,6 +753,7 @@ def test_step_fused_equals_calls_on_configs(P, cfg_index, subrun):
     # select and the Q projection as their own launches, the rest fused:
     (2, 3000, 100, 40, 256, 2, 1, 64, 1000, 50),    # 3000 positions (12 keys per thread), 80 query rows
     (1, 300, 10, 100, 256, 4, 2, 64, 512, 20),      # 100 query rows, grouped KV heads
+    (2, 2048, 1500, 32, 256, 64, 64, 64, 512, 100),  # the ring attention kernel, head_dim 64, 2 key splits
 ])
 def test_step_fused_equals_calls_small_shapes(P, dtype, batch, seq, bs, bl, d, H, Hkv, hd, vocab, k):
     from types import SimpleNamespace
