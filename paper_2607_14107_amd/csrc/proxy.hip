@@ -996,11 +996,17 @@ struct QklPlan {
     size_t part_bytes;
 };
 
+// Key splits: at least about 256 workgroups, and at most 16 key tiles per
+// workgroup, so that a wave's tiles (four at a time for bf16 rows of up to
+// 32 query rows at head_dim 128) are loaded in one round instead of several
+// dependent ones: the batch-8 LLaDA-8B shape (8 x 32 heads, 96 tiles) went
+// from one split to six, the Dream-7B one (4 x 28 heads, 128 tiles) from
+// three to eight.  Several workgroups fit per CU.
 QklPlan qkl_plan(int batch, int seq, int R, int H) {
     QklPlan p{};
     const int ntiles = ceil_div(seq, 16);
     const long base = static_cast<long>(batch) * H;
-    int splits = static_cast<int>((256 + base - 1) / base);
+    int splits = max(static_cast<int>((256 + base - 1) / base), ceil_div(ntiles, 16));
     splits = min(splits, max(1, ntiles / kQkWaves));
     splits = max(1, min(splits, kQkMaxSplits));
     p.tiles_per_split = ceil_div(ntiles, splits);
