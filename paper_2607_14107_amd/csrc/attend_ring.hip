@@ -121,120 +121,114 @@ __global__ __launch_bounds__(kAttBlock, 1) void attend_ring_kernel(AttArgs a) {
     // the loop, so the waves' trip counts may differ); tile t_begin + w + 4i
     // goes through register set i % PF.
     auto step = [&](int tile, uint4 (&kf_)[2][NC], uint4 (&vv_)[ITV][4]) {
+        const int key0 = tile * kKT;
+        floatx4 st[2][2];
+        // V tile (loaded into vv) -> LDS, transposed to [d][key slot].
         {
-            const int key0 = tile * kKT;
-            floatx4 st[2][2];
-            // V tile (loaded into vv) -> LDS, transposed to [d][key slot].
-            {
-                // 8 groups of 4 keys x HD/8 chunks of 8 d; item pr = lane + 64 it
-                constexpr int DC = HD / 8;
-                constexpr int IT = DC * 8 / 64;
+            // 8 groups of 4 keys x HD/8 chunks of 8 d; item pr = lane + 64 it
+            constexpr int DC = HD / 8;
+            constexpr int IT = DC * 8 / 64;
 #pragma unroll
-                for (int it = 0; it < IT; ++it) {
-                    int dc, kg;
-                    vitem(it, dc, kg);
-                    const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vv_[it][0]);
-                    const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vv_[it][1]);
-                    const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vv_[it][2]);
-                    const uint32_t* x3 = reinterpret_cast<const uint32_t*>(&vv_[it][3]);
-                    const int slot = vslot(4 * kg);
+            for (int it = 0; it < IT; ++it) {
+                int dc, kg;
+                vitem(it, dc, kg);
+                const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vv_[it][0]);
+                const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vv_[it][1]);
+                const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vv_[it][2]);
+                const uint32_t* x3 = reinterpret_cast<const uint32_t*>(&vv_[it][3]);
+                const int slot = vslot(4 * kg);
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        // d = 8 dc + e of the 4 keys: the low (e even) or high
-                        // (e odd) halves of word e / 2, two keys per byte permute
-                        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-                        const uint2 pk = make_uint2(__builtin_amdgcn_perm(x1[e >> 1], x0[e >> 1], sel),
-                                                    __builtin_amdgcn_perm(x3[e >> 1], x2[e >> 1], sel));
-                        *reinterpret_cast<uint2*>(myvt + vrow(dc * 8 + e) * VP + slot * 2) = pk;
-                    }
+                for (int e = 0; e < 8; ++e) {
+                    // d = 8 dc + e of the 4 keys: the low (e even) or high
+                    // (e odd) halves of word e / 2, two keys per byte permute
+                    const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+                    const uint2 pk = make_uint2(__builtin_amdgcn_perm(x1[e >> 1], x0[e >> 1], sel),
+                                                __builtin_amdgcn_perm(x3[e >> 1], x2[e >> 1], sel));
+                    *reinterpret_cast<uint2*>(myvt + vrow(dc * 8 + e) * VP + slot * 2) = pk;
                 }
             }
-            // S^T tiles: st[t][u] = K_t Q_u^T.
+        }
+        // S^T tiles: st[t][u] = K_t Q_u^T.
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                floatx4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int c = 0; c < NC; ++c) s = Mma<true>::step(kf_[t][c], qf[u][c], s);
+                st[t][u] = s;
+            }
+        if (tile + 4 * PF < t_end) load_tile(tile + 4 * PF, kf_, vv_);
+        // Keys past seq exist only in a partial last tile.
+        if (__builtin_expect(key0 + kKT > a.seq, 0)) {
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    floatx4 s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int c = 0; c < NC; ++c) s = Mma<true>::step(kf_[t][c], qf[u][c], s);
-                    st[t][u] = s;
-                }
-            {
-                if (tile + 4 * PF < t_end) load_tile(tile + 4 * PF, kf_, vv_);
-            }
-            // Keys past seq exist only in a partial last tile.
-            if (__builtin_expect(key0 + kKT > a.seq, 0)) {
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int u = 0; u < 2; ++u)
-#pragma unroll
-                        for (int i = 0; i < 4; ++i)
-                            if (key0 + 16 * t + 4 * g + i >= a.seq) st[t][u][i] = -INFINITY;
-            }
-            // Online softmax in base-2 units with a lazy exponent reference:
-            // the reference moves (and O, l are rescaled) only when some
-            // query's maximum exceeds it by more than kLazy, so exponents stay
-            // below 2^kLazy; (m, l, O) are exact for any reference.
-            float p[2][2][4];   // [t][u][i]
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                float mx = -INFINITY;
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) mx = fmaxf(mx, st[t][u][i]);
-                mx = fmaxf(mx, __shfl_xor(mx, 16));
-                mx = fmaxf(mx, __shfl_xor(mx, 32));
-                const float mcand = fmaxf(mrun[u], mx * a.scale_log2);
-                const bool any = __builtin_amdgcn_ballot_w64(mcand > mrun[u] + kLazy) != 0;
-                const float alpha = any ? fast_exp2(mrun[u] - (mcand == -INFINITY ? 0.f : mcand)) : 1.f;
-                if (any) mrun[u] = mcand;
-                const float mref = mrun[u] == -INFINITY ? 0.f : mrun[u];
-                float sum = 0.f;
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const float e = fast_exp2(fmaf(st[t][u][i], a.scale_log2, -mref));
-                        p[t][u][i] = e;
-                        sum += e;
-                    }
-                sum += __shfl_xor(sum, 16);
-                sum += __shfl_xor(sum, 32);
-                lrun[u] = fmaf(lrun[u], alpha, sum);
-                if (any) {
-#pragma unroll
-                    for (int dt = 0; dt < DT; ++dt) o[dt][u] *= alpha;
-                }
-            }
-            // O^T += V^T P^T
-            {
-                uint4 pf[2];
-#pragma unroll
                 for (int u = 0; u < 2; ++u)
-                    pf[u] = make_uint4(cvt_pk_bf16(p[0][u][0], p[0][u][1]), cvt_pk_bf16(p[0][u][2], p[0][u][3]),
-                                       cvt_pk_bf16(p[1][u][0], p[1][u][1]), cvt_pk_bf16(p[1][u][2], p[1][u][3]));
 #pragma unroll
-                for (int dt = 0; dt < DT; ++dt) {
-                    const uint4 va = *reinterpret_cast<const uint4*>(myvt + vrow(dt * 16 + (lane & 15)) * VP + g * 16);
+                    for (int i = 0; i < 4; ++i)
+                        if (key0 + 16 * t + 4 * g + i >= a.seq) st[t][u][i] = -INFINITY;
+        }
+        // Online softmax in base-2 units with a lazy exponent reference:
+        // the reference moves (and O, l are rescaled) only when some
+        // query's maximum exceeds it by more than kLazy, so exponents stay
+        // below 2^kLazy; (m, l, O) are exact for any reference.
+        float p[2][2][4];   // [t][u][i]
 #pragma unroll
-                    for (int u = 0; u < 2; ++u) o[dt][u] = mfma_bf16(va, pf[u], o[dt][u]);
+        for (int u = 0; u < 2; ++u) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) mx = fmaxf(mx, st[t][u][i]);
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float mcand = fmaxf(mrun[u], mx * a.scale_log2);
+            const bool any = __builtin_amdgcn_ballot_w64(mcand > mrun[u] + kLazy) != 0;
+            const float alpha = any ? fast_exp2(mrun[u] - (mcand == -INFINITY ? 0.f : mcand)) : 1.f;
+            if (any) mrun[u] = mcand;
+            const float mref = mrun[u] == -INFINITY ? 0.f : mrun[u];
+            float sum = 0.f;
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float e = fast_exp2(fmaf(st[t][u][i], a.scale_log2, -mref));
+                    p[t][u][i] = e;
+                    sum += e;
                 }
+            sum += __shfl_xor(sum, 16);
+            sum += __shfl_xor(sum, 32);
+            lrun[u] = fmaf(lrun[u], alpha, sum);
+            if (any) {
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) o[dt][u] *= alpha;
+            }
+        }
+        // O^T += V^T P^T
+        {
+            uint4 pf[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                pf[u] = make_uint4(cvt_pk_bf16(p[0][u][0], p[0][u][1]), cvt_pk_bf16(p[0][u][2], p[0][u][3]),
+                                   cvt_pk_bf16(p[1][u][0], p[1][u][1]), cvt_pk_bf16(p[1][u][2], p[1][u][3]));
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const uint4 va = *reinterpret_cast<const uint4*>(myvt + vrow(dt * 16 + (lane & 15)) * VP + g * 16);
+#pragma unroll
+                for (int u = 0; u < 2; ++u) o[dt][u] = mfma_bf16(va, pf[u], o[dt][u]);
             }
         }
     };
     const int t0 = t_begin + wu;
-    {
 #pragma unroll
-        for (int j = 0; j < PF; ++j)
-            if (t0 + 4 * j < t_end) load_tile(t0 + 4 * j, kf[j], vv[j]);
-        for (int base = t0; base < t_end; base += 4 * PF) {
+    for (int j = 0; j < PF; ++j)
+        if (t0 + 4 * j < t_end) load_tile(t0 + 4 * j, kf[j], vv[j]);
+    for (int base = t0; base < t_end; base += 4 * PF) {
 #pragma unroll
-            for (int j = 0; j < PF; ++j) {
-                const int tile = base + 4 * j;
-                if (tile < t_end) step(tile, kf[j], vv[j]);
-            }
+        for (int j = 0; j < PF; ++j) {
+            const int tile = base + 4 * j;
+            if (tile < t_end) step(tile, kf[j], vv[j]);
         }
     }
 
@@ -286,14 +280,11 @@ __global__ __launch_bounds__(kAttBlock, 1) void attend_ring_kernel(AttArgs a) {
         const float inv = 1.f / L;
         char* op = a.out + (row * HD + d0) * ES;
 #pragma unroll
-        for (int j = 0; j < PER; j += 8) {
-            {
-                st16(op + 2 * j, make_uint4(pack_bf16x2(acc[j] * inv, acc[j + 1] * inv),
-                                            pack_bf16x2(acc[j + 2] * inv, acc[j + 3] * inv),
-                                            pack_bf16x2(acc[j + 4] * inv, acc[j + 5] * inv),
-                                            pack_bf16x2(acc[j + 6] * inv, acc[j + 7] * inv)));
-            }
-        }
+        for (int j = 0; j < PER; j += 8)
+            st16(op + 2 * j, make_uint4(pack_bf16x2(acc[j] * inv, acc[j + 1] * inv),
+                                        pack_bf16x2(acc[j + 2] * inv, acc[j + 3] * inv),
+                                        pack_bf16x2(acc[j + 4] * inv, acc[j + 5] * inv),
+                                        pack_bf16x2(acc[j + 6] * inv, acc[j + 7] * inv)));
         if (a.lse && d0 == 0)
             a.lse[(static_cast<size_t>(b) * a.H + h) * a.nq + q] = (M + __log2f(L)) * kLn2;
     } else {
